@@ -1,0 +1,161 @@
+"""Seeded synthetic workloads for the GSPN line scan.
+
+Shared by the tests, the benchmark and the smoke check.  Nothing here computes
+any part of the scan: it only describes workload shapes and draws the numbers
+(see ``gen.c`` for the counter-based generator).  Both the CPU oracle and the
+GPU library read the arrays returned by :func:`make_inputs`.
+
+Direction bits follow the library's convention: 1 = top-to-bottom,
+2 = bottom-to-top, 4 = left-to-right, 8 = right-to-left.  Per-direction
+tensors are stacked along a leading axis in increasing bit order.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, replace
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libgspn_inputs.so")
+
+T2B, B2T, L2R, R2L = 1, 2, 4, 8
+ALL_DIRS = 15
+DIR_BITS = (T2B, B2T, L2R, R2L)
+
+# tensor ids of the counter-based streams
+_TID_X, _TID_LOGIT, _TID_LAM, _TID_U, _TID_DY = 0, 1, 2, 3, 4
+
+
+@dataclass(frozen=True)
+class Workload:
+    """One synthetic workload: shapes, storage dtype and value recipe."""
+    name: str
+    B: int
+    C: int
+    G: int
+    H: int
+    W: int
+    dtype: str            # "f32" or "bf16" storage; arithmetic is fp32 on the GPU
+    dirs: int             # direction bitmask
+    backward: bool        # whether the workload includes the backward pass
+    gate: str             # "normal": lambda, u ~ N(0,1); "sigmoid": sigmoid(N(0,1))
+    logit_sigma: float    # std-dev of the neighbour logits
+    seed: int
+
+    @property
+    def ndirs(self) -> int:
+        return bin(self.dirs).count("1")
+
+    @property
+    def pixels_channels(self) -> int:
+        return self.B * self.C * self.H * self.W
+
+    def with_(self, **kw) -> "Workload":
+        return replace(self, **kw)
+
+
+# The five workloads: a tiny fp32 case the oracle checks in full, three ViT /
+# hierarchical-encoder stages and one extreme-resolution inference case.
+WORKLOADS = [
+    Workload("tiny-16x16-c8-f32", 1, 8, 1, 16, 16, "f32", T2B, False, "normal", 1.0, 0),
+    Workload("vit-s-14x14-b32-c384", 32, 384, 12, 14, 14, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 1),
+    Workload("hier-56x56-b64-c96", 64, 96, 8, 56, 56, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 2),
+    Workload("hires-64x64-b8-c768", 8, 768, 24, 64, 64, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 3),
+    Workload("xres-256x256-b1-c1024", 1, 1024, 32, 256, 256, "bf16", ALL_DIRS, False, "sigmoid", 2.0, 4),
+]
+
+
+def workload(name_or_index) -> Workload:
+    if isinstance(name_or_index, int):
+        return WORKLOADS[name_or_index]
+    for w in WORKLOADS:
+        if w.name == name_or_index:
+            return w
+    raise KeyError(name_or_index)
+
+
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(
+                f"{_LIB_PATH} is missing; build it with python -m gspn_inputs.build")
+        lib = ctypes.CDLL(_LIB_PATH)
+        lib.gspn_gen_normal.argtypes = [
+            ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int,
+            ctypes.c_int, ctypes.c_double, ctypes.c_double, ctypes.c_int, ctypes.c_int]
+        lib.gspn_gen_normal.restype = None
+        lib.gspn_gen_taps.argtypes = [
+            ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+            ctypes.c_int, ctypes.c_uint64, ctypes.c_int, ctypes.c_int, ctypes.c_double,
+            ctypes.c_int]
+        lib.gspn_gen_taps.restype = None
+        _lib = lib
+    return _lib
+
+
+def _normal(shape, seed, tid, slot, mean, sigma, transform, bf16):
+    out = np.empty(shape, dtype=np.float32)
+    _load().gspn_gen_normal(out.ctypes.data, out.size, seed, tid, slot, mean, sigma,
+                            transform, int(bf16))
+    return out
+
+
+def make_inputs(wl: Workload, with_dy: bool | None = None) -> dict:
+    """Draw every input of ``wl`` as float32 arrays.
+
+    When ``wl.dtype == "bf16"`` every value is already bf16-representable, so
+    :func:`to_bf16_bits` is exact.  Returns x [B,C,H,W], w [D,B,G,3,H,W],
+    lam and u [D,B,C,H,W] and, for backward workloads, dy [B,C,H,W].
+    """
+    bf16 = wl.dtype == "bf16"
+    B, C, G, H, W = wl.B, wl.C, wl.G, wl.H, wl.W
+    D = wl.ndirs
+    gate = 1 if wl.gate == "sigmoid" else 0
+    x = _normal((B, C, H, W), wl.seed, _TID_X, 0, 0.0, 1.0, 0, bf16)
+    w = np.empty((D, B, G, 3, H, W), dtype=np.float32)
+    lam = np.empty((D, B, C, H, W), dtype=np.float32)
+    u = np.empty((D, B, C, H, W), dtype=np.float32)
+    s = 0
+    for bit in DIR_BITS:
+        if not wl.dirs & bit:
+            continue
+        vertical = 1 if bit in (T2B, B2T) else 0
+        _load().gspn_gen_taps(w[s].ctypes.data, B, G, H, W, vertical, wl.seed,
+                              _TID_LOGIT, bit, wl.logit_sigma, int(bf16))
+        lam[s] = _normal((B, C, H, W), wl.seed, _TID_LAM, bit, 0.0, 1.0, gate, bf16)
+        u[s] = _normal((B, C, H, W), wl.seed, _TID_U, bit, 0.0, 1.0, gate, bf16)
+        s += 1
+    out = {"x": x, "w": w, "lam": lam, "u": u}
+    if with_dy is None:
+        with_dy = wl.backward
+    if with_dy:
+        out["dy"] = _normal((B, C, H, W), wl.seed, _TID_DY, 0, 0.0, 1.0, 0, bf16)
+    return out
+
+
+def to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Exact view of bf16-representable float32 values as bf16 bit patterns."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    bits = a.view(np.uint32)
+    if np.any(bits & 0xFFFF):
+        raise ValueError("values are not bf16-representable")
+    return (bits >> 16).astype(np.uint16)
+
+
+def from_bf16_bits(b: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> float32 values (exact)."""
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def round_to_bf16(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bf16 (ties to even), as float32."""
+    bits = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    lsb = (bits >> 16) & 1
+    bits = ((bits + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
+    return bits.view(np.float32)

@@ -1,0 +1,107 @@
+"""CPU oracle for the GSPN line scan -- TEST INFRASTRUCTURE ONLY.
+
+Python front end (ctypes + numpy, float64) of ``gspn_oracle.c``.  Only the
+tests, the smoke check and the benchmark's CPU-baseline leg use it; the GPU
+library never imports it and shares no code with it.
+
+Follows Sec. 3, Eqs. (gspn_recurrence), (gspn_output) and (row_stochastic_norm)
+and Sec. 4.2, Eq. (2dsp) of the paper; the readings taken where the paper is
+silent are listed in ``gspn_oracle.c``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} is missing; build it with python -m oracle.build")
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        lib.oracle_scan_fwd.argtypes = [P, P, P, P, P, I, I, I, I, I, I]
+        lib.oracle_scan_fwd.restype = None
+        lib.oracle_scan_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I, I, I, I, I, I]
+        lib.oracle_scan_bwd.restype = None
+        _lib = lib
+    return _lib
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _ndirs(dirs):
+    return bin(dirs & 15).count("1")
+
+
+def _check(x, w, lam, u, dirs, G):
+    B, C, H, W = x.shape
+    D = _ndirs(dirs)
+    if not 1 <= dirs <= 15:
+        raise ValueError("direction mask must be in [1, 15]")
+    if C % G:
+        raise ValueError("C must be a multiple of G")
+    if w.shape != (D, B, G, 3, H, W):
+        raise ValueError(f"w shape {w.shape} != {(D, B, G, 3, H, W)}")
+    if lam.shape != (D, B, C, H, W) or u.shape != (D, B, C, H, W):
+        raise ValueError("lam/u shape mismatch")
+    return B, C, H, W
+
+
+def scan_fwd(x, w, lam, u, dirs: int) -> np.ndarray:
+    """y [B,C,H,W] = sum_d u_d * h_d, in float64."""
+    x, w, lam, u = map(_f64, (x, w, lam, u))
+    G = w.shape[2]
+    B, C, H, W = _check(x, w, lam, u, dirs, G)
+    y = np.empty((B, C, H, W), dtype=np.float64)
+    _load().oracle_scan_fwd(x.ctypes.data, w.ctypes.data, lam.ctypes.data, u.ctypes.data,
+                            y.ctypes.data, dirs, B, C, G, H, W)
+    return y
+
+
+def scan_bwd(x, w, lam, u, dy, dirs: int) -> dict:
+    """Gradients {dx, dw, dlam, du} of <y, dy>, in float64."""
+    x, w, lam, u, dy = map(_f64, (x, w, lam, u, dy))
+    G = w.shape[2]
+    B, C, H, W = _check(x, w, lam, u, dirs, G)
+    if dy.shape != x.shape:
+        raise ValueError("dy shape mismatch")
+    dx = np.empty_like(x)
+    dw = np.empty_like(w)
+    dlam = np.empty_like(lam)
+    du = np.empty_like(u)
+    _load().oracle_scan_bwd(x.ctypes.data, w.ctypes.data, lam.ctypes.data, u.ctypes.data,
+                            dy.ctypes.data, dx.ctypes.data, dw.ctypes.data, dlam.ctypes.data,
+                            du.ctypes.data, dirs, B, C, G, H, W)
+    return {"dx": dx, "dw": dw, "dlam": dlam, "du": du}
+
+
+def slice_group(inputs: dict, b: int, g: int, G: int) -> dict:
+    """Inputs of one (batch b, weight group g) unit as a B=1, G=1 problem.
+
+    Every output of that unit depends only on these slices, so the oracle can
+    check sampled units of a full-size workload one at a time.
+    """
+    x = inputs["x"]
+    C = x.shape[1]
+    cpg = C // G
+    cs = slice(g * cpg, (g + 1) * cpg)
+    out = {
+        "x": x[b:b + 1, cs],
+        "w": inputs["w"][:, b:b + 1, g:g + 1],
+        "lam": inputs["lam"][:, b:b + 1, cs],
+        "u": inputs["u"][:, b:b + 1, cs],
+    }
+    if "dy" in inputs:
+        out["dy"] = inputs["dy"][b:b + 1, cs]
+    return out
