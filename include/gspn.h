@@ -1,0 +1,132 @@
+/*
+ * libgspn -- GSPN 2D line-scan propagation on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Sec. 3 of "Scaling Parallel Sequence Models to
+ * Foundation-Scale Vision Encoders", Eqs. (gspn_recurrence), (gspn_output),
+ * (row_stochastic_norm); channel-shared weights as in Sec. 4.2, Eq. (2dsp)):
+ *
+ *   for every direction d in the mask, batch b and channel c (group g = c/(C/G)),
+ *   scanning the lines i = 0..L-1 of the grid in direction d:
+ *
+ *     h_i[j] = sum_{k=0..2} w_d[b,g,k @ (i,j)] * h_{i-1}[j+k-1]
+ *              + lam_d[b,c @ (i,j)] * x[b,c @ (i,j)]          (h_{-1} = 0)
+ *     y[b,c @ (i,j)] = sum_d u_d[b,c @ (i,j)] * h_i[j]
+ *
+ *   "@ (i,j)" is the pixel at step i, line position j of direction d:
+ *     top-to-bottom (i, j)   bottom-to-top (H-1-i, j)
+ *     left-to-right (j, i)   right-to-left (j, W-1-i)     as (row, col).
+ *   Tap k at a pixel reads the previous line at perpendicular offset k-1
+ *   (column offset for vertical scans, row offset for horizontal ones), i.e.
+ *   the "top-left, top-center, top-right" neighbours of Sec. 3.  Taps that
+ *   leave the grid and all taps on the first scanned line are ignored (any
+ *   value, NaN included); their gradients are written as 0.
+ *
+ * Storage and arithmetic: every tensor of one call has the same storage type
+ * (fp32 or bf16); arithmetic is fp32 and results are rounded to the storage
+ * type (round to nearest even) once, when stored.
+ *
+ * Layouts (contiguous, row-major), D = number of directions in the mask,
+ * per-direction tensors stacked in increasing direction-bit order:
+ *   x, y, dy, dx           [B][C][H][W]
+ *   w, dw                  [D][B][G][3][H][W]
+ *   lam, u, dlam, du       [D][B][C][H][W]
+ *
+ * Ownership and threading: all pointers are device pointers owned by the
+ * caller; the library keeps none of them after a call returns.  Outputs are
+ * fully overwritten (never accumulated into); inputs are never written.
+ * Buffers of one call must not overlap.  Every base pointer must be 16-byte
+ * aligned.  Calls are asynchronous on `stream` (a hipStream_t; NULL is the
+ * null stream) and never synchronise the device.  gspn_scan_bwd may take
+ * stream-ordered scratch memory from the device's default memory pool; it
+ * is released on the same stream.  Calls are thread-safe.
+ *
+ * Errors: every argument check runs on the host before any HIP call, so an
+ * invalid call has no effect on the device.  A failed HIP call returns
+ * GSPN_ERR_HIP (see gspn_last_hip_error).  No C++ exception crosses the ABI.
+ */
+#ifndef GSPN_H
+#define GSPN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Scan directions (bitmask). */
+#define GSPN_T2B 1
+#define GSPN_B2T 2
+#define GSPN_L2R 4
+#define GSPN_R2L 8
+#define GSPN_ALL 15
+
+/* Storage types. */
+#define GSPN_F32 0
+#define GSPN_BF16 1
+
+/* Status codes. */
+#define GSPN_OK 0
+#define GSPN_ERR_NULL (-1)        /* a required pointer is NULL                 */
+#define GSPN_ERR_DIM (-2)         /* a size < 1, or C not a multiple of G       */
+#define GSPN_ERR_DIRECTION (-3)   /* direction mask outside [1, 15]             */
+#define GSPN_ERR_DTYPE (-4)       /* unknown storage type                       */
+#define GSPN_ERR_ALIGN (-5)       /* a base pointer is not 16-byte aligned      */
+#define GSPN_ERR_ALIAS (-6)       /* two buffers of the call overlap            */
+#define GSPN_ERR_UNSUPPORTED (-7) /* H or W > GSPN_MAX_SIDE, or too many elements */
+#define GSPN_ERR_HIP (-8)         /* a HIP runtime call or launch failed        */
+
+/* Largest supported H and W, and largest B*C*H*W and B*G*H*W*3*D. */
+#define GSPN_MAX_SIDE 4096
+#define GSPN_MAX_ELEMS (((int64_t)1) << 40)
+
+/*
+ * Forward pass (Sec. 3, Eqs. (gspn_recurrence) and (gspn_output)).
+ *   x    [B][C][H][W]        input feature map
+ *   w    [D][B][G][3][H][W]  neighbour weights (normalised, e.g. row-stochastic)
+ *   lam  [D][B][C][H][W]     input scaling lambda_d
+ *   u    [D][B][C][H][W]     output gate u_d
+ *   y    [B][C][H][W]        out: sum over directions of u_d * h_d
+ *   direction  bitmask of GSPN_T2B | GSPN_B2T | GSPN_L2R | GSPN_R2L
+ *   G          weight groups; channel c uses group c / (C/G); C % G == 0
+ *   dtype      GSPN_F32 or GSPN_BF16 (all tensors)
+ *   stream     hipStream_t to launch on
+ * Returns GSPN_OK or a negative status.
+ */
+int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u,
+                  void *y, int direction, int B, int C, int G, int H, int W,
+                  int dtype, void *stream);
+
+/*
+ * Backward pass: gradients of a loss l(y) given dy = dl/dy.  The backward of
+ * the recurrence is not printed in the paper (which reports only its run
+ * time); with the adjoint a_i = dl/dh_i it is
+ *   a_i[j]  = u_i[j] dy_i[j] + sum_k w_{i+1}[j-k+1, k] a_{i+1}[j-k+1],  a_L = 0
+ *   du_i    = dy_i * h_i,   dlam_i = a_i * x_i,   dx = sum_d a_d * lam_d,
+ *   dw_i[j,k] = sum_{c in group} a_i[j] h_{i-1}[j+k-1]   (0 on ignored taps).
+ * h is recomputed on the GPU; nothing is saved by the forward pass.
+ *   dy   [B][C][H][W]        in: gradient of the merged output y
+ *   dx   [B][C][H][W]        out
+ *   dw   [D][B][G][3][H][W]  out
+ *   dlam [D][B][C][H][W]     out
+ *   du   [D][B][C][H][W]     out
+ * Other arguments as in gspn_scan_fwd.
+ */
+int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
+                  const void *dy, void *dx, void *dw, void *dlam, void *du,
+                  int direction, int B, int C, int G, int H, int W, int dtype,
+                  void *stream);
+
+/* Static description of a status code (never NULL). */
+const char *gspn_strerror(int status);
+
+/* hipError_t of the most recent GSPN_ERR_HIP on the calling thread (0 if none). */
+int gspn_last_hip_error(void);
+
+/* Library version as 10000*major + 100*minor + patch. */
+int gspn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSPN_H */

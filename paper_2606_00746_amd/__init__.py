@@ -1,0 +1,14 @@
+"""MI355X-native GSPN line-scan propagation (libgspn).
+
+The 2D line-scan recurrence of Generalized Spatial Propagation Networks,
+h_i = w_i h_{i-1} + lambda_i * x_i with output y = sum_d u_d * h_d over four
+scan directions, forward and backward, as hand-written HIP kernels for gfx950
+behind a C ABI (``include/gspn.h``).  This package is the ctypes binding.
+"""
+from ._native import (ALL, B2T, BF16, F32, L2R, LIB_PATH, R2L, T2B, GspnError, gspn_last_hip_error,
+                      gspn_scan_bwd, gspn_scan_fwd, gspn_strerror, gspn_version, load, scan_bwd,
+                      scan_fwd)
+
+__all__ = ["ALL", "B2T", "BF16", "F32", "L2R", "LIB_PATH", "R2L", "T2B", "GspnError",
+           "gspn_last_hip_error", "gspn_scan_bwd", "gspn_scan_fwd", "gspn_strerror",
+           "gspn_version", "load", "scan_bwd", "scan_fwd"]

@@ -1,0 +1,152 @@
+"""ctypes binding of libgspn (argument marshalling only).
+
+The raw functions keep the C names and signatures of ``include/gspn.h``.
+``scan_fwd`` / ``scan_bwd`` take torch tensors, derive the sizes from their
+shapes, and raise :class:`GspnError` on a non-zero status.  Every step of the
+scan runs in the library's HIP kernels; there is no other code path, and
+loading fails loudly when the library is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgspn.so")
+
+T2B, B2T, L2R, R2L, ALL = 1, 2, 4, 8, 15
+F32, BF16 = 0, 1
+OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUPPORTED, ERR_HIP = (
+    0, -1, -2, -3, -4, -5, -6, -7, -8)
+MAX_SIDE = 4096
+
+EXPORTED = ("gspn_scan_fwd", "gspn_scan_bwd", "gspn_strerror", "gspn_last_hip_error",
+            "gspn_version")
+
+_lib = None
+
+
+class GspnError(RuntimeError):
+    def __init__(self, status: int, hip_error: int = 0):
+        msg = f"libgspn status {status}: {gspn_strerror(status)}"
+        if status == ERR_HIP:
+            msg += f" (hipError_t {hip_error})"
+        super().__init__(msg)
+        self.status = status
+        self.hip_error = hip_error
+
+
+def load() -> ctypes.CDLL:
+    """Load libgspn.so (built in place by ``paper_2606_00746_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2606_00746_amd.build` "
+                "(there is no fallback implementation)")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i = ctypes.c_void_p, ctypes.c_int
+        lib.gspn_scan_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+        lib.gspn_scan_fwd.restype = i
+        lib.gspn_scan_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+        lib.gspn_scan_bwd.restype = i
+        lib.gspn_strerror.argtypes = [i]
+        lib.gspn_strerror.restype = ctypes.c_char_p
+        lib.gspn_last_hip_error.argtypes = []
+        lib.gspn_last_hip_error.restype = i
+        lib.gspn_version.argtypes = []
+        lib.gspn_version.restype = i
+        _lib = lib
+    return _lib
+
+
+# ---------------------------------------------------------------------------
+# raw C entry points (pointers as ints, sizes as ints)
+# ---------------------------------------------------------------------------
+
+def gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, stream) -> int:
+    return load().gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, stream)
+
+
+def gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
+                  stream) -> int:
+    return load().gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W,
+                                dtype, stream)
+
+
+def gspn_strerror(status: int) -> str:
+    return load().gspn_strerror(status).decode()
+
+
+def gspn_last_hip_error() -> int:
+    return load().gspn_last_hip_error()
+
+
+def gspn_version() -> int:
+    return load().gspn_version()
+
+
+# ---------------------------------------------------------------------------
+# torch-tensor front end (sizes from shapes, current stream)
+# ---------------------------------------------------------------------------
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _stream_handle(t, stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(t.device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _check_raise(status):
+    if status != OK:
+        raise GspnError(status, gspn_last_hip_error() if status == ERR_HIP else 0)
+
+
+def _sizes(x, w, direction):
+    if x.dim() != 4 or w.dim() != 6:
+        raise ValueError("x must be [B,C,H,W] and w [D,B,G,3,H,W]")
+    B, C, H, W = x.shape
+    G = w.shape[2]
+    return B, C, G, H, W
+
+
+def _ptrs(*ts):
+    for t in ts:
+        if not t.is_contiguous():
+            raise ValueError("all tensors must be contiguous")
+    return [t.data_ptr() for t in ts]
+
+
+def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None):
+    """y = sum_d u_d * h_d for device tensors (see include/gspn.h)."""
+    import torch
+    B, C, G, H, W = _sizes(x, w, direction)
+    if y is None:
+        y = torch.empty_like(x)
+    status = gspn_scan_fwd(*_ptrs(x, w, lam, u, y), direction, B, C, G, H, W, _dtype_code(x),
+                           _stream_handle(x, stream))
+    _check_raise(status)
+    return y
+
+
+def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
+    """Gradients (dx, dw, dlam, du) of <y, dy> for device tensors."""
+    import torch
+    B, C, G, H, W = _sizes(x, w, direction)
+    if out is None:
+        out = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
+               torch.empty_like(u))
+    dx, dw, dlam, du = out
+    status = gspn_scan_bwd(*_ptrs(x, w, lam, u, dy, dx, dw, dlam, du), direction, B, C, G, H, W,
+                           _dtype_code(x), _stream_handle(x, stream))
+    _check_raise(status)
+    return dx, dw, dlam, du

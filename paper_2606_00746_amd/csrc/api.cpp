@@ -1,0 +1,153 @@
+// C ABI of libgspn: argument checks (host only, before any HIP call),
+// dispatch to the kernel variants, error mapping.
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+
+#include "../../include/gspn.h"
+#include "launch.hpp"
+
+namespace gspn {
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+struct Buf {
+    const void *p;
+    int64_t bytes;
+    bool output;
+};
+
+int check_common(int direction, int B, int C, int G, int H, int W, int dtype)
+{
+    if (dtype != GSPN_F32 && dtype != GSPN_BF16)
+        return GSPN_ERR_DTYPE;
+    if (direction < 1 || direction > 15)
+        return GSPN_ERR_DIRECTION;
+    if (B < 1 || C < 1 || G < 1 || H < 1 || W < 1 || C % G != 0)
+        return GSPN_ERR_DIM;
+    if (H > GSPN_MAX_SIDE || W > GSPN_MAX_SIDE)
+        return GSPN_ERR_UNSUPPORTED;
+    const int64_t HW = (int64_t)H * W;
+    const int64_t D = __builtin_popcount(direction);
+    if ((int64_t)B * C > GSPN_MAX_ELEMS / HW || D * B * C > GSPN_MAX_ELEMS / HW ||
+        D * B * G * 3 > GSPN_MAX_ELEMS / HW)
+        return GSPN_ERR_UNSUPPORTED;
+    return GSPN_OK;
+}
+
+int check_buffers(const Buf *bufs, int n)
+{
+    for (int i = 0; i < n; ++i)
+        if (bufs[i].p == nullptr)
+            return GSPN_ERR_NULL;
+    for (int i = 0; i < n; ++i)
+        if (reinterpret_cast<uintptr_t>(bufs[i].p) % 16 != 0)
+            return GSPN_ERR_ALIGN;
+    for (int i = 0; i < n; ++i) {
+        if (!bufs[i].output)
+            continue;
+        const uintptr_t a0 = reinterpret_cast<uintptr_t>(bufs[i].p);
+        const uintptr_t a1 = a0 + (uintptr_t)bufs[i].bytes;
+        for (int k = 0; k < n; ++k) {
+            if (k == i)
+                continue;
+            const uintptr_t b0 = reinterpret_cast<uintptr_t>(bufs[k].p);
+            const uintptr_t b1 = b0 + (uintptr_t)bufs[k].bytes;
+            if (a0 < b1 && b0 < a1)
+                return GSPN_ERR_ALIAS;
+        }
+    }
+    return GSPN_OK;
+}
+
+int hip_status(hipError_t e)
+{
+    if (e == hipSuccess)
+        return GSPN_OK;
+    g_last_hip_error = (int)e;
+    return GSPN_ERR_HIP;
+}
+
+}  // namespace
+
+hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s)
+{
+    return hipMallocAsync(ptr, bytes, s);
+}
+
+hipError_t scratch_free(void *ptr, hipStream_t s) { return hipFreeAsync(ptr, s); }
+
+}  // namespace gspn
+
+using namespace gspn;
+
+extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u, void *y,
+                             int direction, int B, int C, int G, int H, int W, int dtype,
+                             void *stream)
+{
+    int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t n = (int64_t)B * C * H * W;
+    const int64_t nw = D * B * G * 3 * H * W;
+    const Buf bufs[] = {{x, n * es, false},      {w, nw * es, false}, {lam, D * n * es, false},
+                        {u, D * n * es, false},  {y, n * es, true}};
+    st = check_buffers(bufs, 5);
+    if (st != GSPN_OK)
+        return st;
+    Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
+              direction, B, C, G, H, W, dtype};
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (H <= kSmallSide && W <= kSmallSide)
+        return hip_status(launch_fwd_small(p, s));
+    return hip_status(launch_fwd_general(p, s));
+}
+
+extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
+                             const void *dy, void *dx, void *dw, void *dlam, void *du,
+                             int direction, int B, int C, int G, int H, int W, int dtype,
+                             void *stream)
+{
+    int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t n = (int64_t)B * C * H * W;
+    const int64_t nw = D * B * G * 3 * H * W;
+    const Buf bufs[] = {{x, n * es, false},      {w, nw * es, false},      {lam, D * n * es, false},
+                        {u, D * n * es, false},  {dy, n * es, false},      {dx, n * es, true},
+                        {dw, nw * es, true},     {dlam, D * n * es, true}, {du, D * n * es, true}};
+    st = check_buffers(bufs, 9);
+    if (st != GSPN_OK)
+        return st;
+    Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (H <= kSmallSide && W <= kSmallSide)
+        return hip_status(launch_bwd_small(p, s));
+    return hip_status(launch_bwd_general(p, s));
+}
+
+extern "C" const char *gspn_strerror(int status)
+{
+    switch (status) {
+    case GSPN_OK: return "success";
+    case GSPN_ERR_NULL: return "a required pointer is NULL";
+    case GSPN_ERR_DIM: return "a size is < 1 or C is not a multiple of G";
+    case GSPN_ERR_DIRECTION: return "direction mask outside [1, 15]";
+    case GSPN_ERR_DTYPE: return "unknown storage type";
+    case GSPN_ERR_ALIGN: return "a base pointer is not 16-byte aligned";
+    case GSPN_ERR_ALIAS: return "two buffers of the call overlap";
+    case GSPN_ERR_UNSUPPORTED: return "shape beyond the supported limits";
+    case GSPN_ERR_HIP: return "a HIP runtime call or kernel launch failed";
+    default: return "unknown status";
+    }
+}
+
+extern "C" int gspn_last_hip_error(void) { return g_last_hip_error; }
+
+extern "C" int gspn_version(void) { return 100; }

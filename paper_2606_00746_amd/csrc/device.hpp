@@ -1,0 +1,74 @@
+// Device-side helpers shared by the libgspn kernels (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gspn {
+
+// Storage types: fp32 is stored as float, bf16 as its 16-bit pattern.
+using bf16_t = uint16_t;
+
+__device__ __forceinline__ float load_f(const float *p) { return *p; }
+__device__ __forceinline__ float load_f(const bf16_t *p)
+{
+    // bf16 -> fp32 is exact: the pattern becomes the high half of the float.
+    return __uint_as_float(static_cast<uint32_t>(*p) << 16);
+}
+
+__device__ __forceinline__ void store_f(float *p, float v) { *p = v; }
+__device__ __forceinline__ void store_f(bf16_t *p, float v)
+{
+    // fp32 -> bf16, round to nearest even (v_cvt_pk_bf16_f32 on gfx950).
+    __bf16 b = static_cast<__bf16>(v);
+    *p = __builtin_bit_cast(bf16_t, b);
+}
+
+// DPP lane shifts along a line of T lanes (T = 16, 32 or 64).  from_left(v)
+// returns v of lane-1 and from_right(v) v of lane+1; lanes without a source
+// read 0 (bound_ctrl).  For T = 16 the shift stays inside each 16-lane row,
+// so every row is one line.  For T = 32 the whole-wave shift crosses from one
+// 32-lane line into the next; callers zero the weights that would read across.
+template <int T>
+__device__ __forceinline__ float from_left(float v)
+{
+    constexpr int ctrl = (T == 16) ? 0x111 /* row_shr:1 */ : 0x138 /* wave_shr:1 */;
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xf, 0xf, true));
+}
+
+template <int T>
+__device__ __forceinline__ float from_right(float v)
+{
+    constexpr int ctrl = (T == 16) ? 0x101 /* row_shl:1 */ : 0x130 /* wave_shl:1 */;
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xf, 0xf, true));
+}
+
+// Direction index d (direction bit 1 << d): the pixel at frame (step i, line
+// position j) sits at e0 + i * es in an H x W plane whose rows are `pitch`
+// elements apart (pitch = W in global memory, padded in LDS).
+struct Frame {
+    int L;        // scan length
+    int P;        // line length
+    int e0;       // offset of (0, j)
+    int es;       // offset change per step
+};
+
+__device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitch)
+{
+    Frame f;
+    switch (d) {
+    case 0:  f.L = H; f.P = W; f.e0 = j;                           f.es = pitch;  break; // T2B
+    case 1:  f.L = H; f.P = W; f.e0 = (H - 1) * pitch + j;         f.es = -pitch; break; // B2T
+    case 2:  f.L = W; f.P = H; f.e0 = j * pitch;                   f.es = 1;      break; // L2R
+    default: f.L = W; f.P = H; f.e0 = j * pitch + (W - 1);         f.es = -1;     break; // R2L
+    }
+    return f;
+}
+
+__device__ __forceinline__ int scan_len(int d, int H, int W) { return d < 2 ? H : W; }
+__device__ __forceinline__ int line_len(int d, int H, int W) { return d < 2 ? W : H; }
+
+// Slot of direction bit `bit` in the stacked per-direction tensors.
+__device__ __forceinline__ int dir_slot(int mask, int bit) { return __popc(mask & (bit - 1)); }
+
+}  // namespace gspn

@@ -1,0 +1,27 @@
+// Host-side kernel launchers of libgspn (internal; not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gspn {
+
+struct Problem {
+    const void *x, *w, *lam, *u, *dy;
+    void *y, *dx, *dw, *dlam, *du;
+    int mask, B, C, G, H, W, dtype;
+};
+
+// Planes whose sides are both <= kSmallSide run on the register-resident path.
+constexpr int kSmallSide = 64;
+
+hipError_t launch_fwd_small(const Problem &p, hipStream_t s);
+hipError_t launch_bwd_small(const Problem &p, hipStream_t s);
+hipError_t launch_fwd_general(const Problem &p, hipStream_t s);
+hipError_t launch_bwd_general(const Problem &p, hipStream_t s);
+
+// Stream-ordered scratch from the device's default pool.
+hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s);
+hipError_t scratch_free(void *ptr, hipStream_t s);
+
+}  // namespace gspn

@@ -1,0 +1,134 @@
+"""GPU parity: libgspn (through the C ABI) against the fp64 CPU oracle.
+
+Both sides read the same seeded inputs.  Tolerances (normwise max error per
+output tensor): 1e-5 for fp32 storage, 2e-2 for bf16 storage with fp32
+accumulation.  Taps the operator ignores must get exactly zero gradient, and
+garbage (NaN) in them must not change any result.
+"""
+import numpy as np
+import pytest
+
+import gspn_inputs as gi
+import oracle
+import paper_2606_00746_amd as gspn
+from gpu_util import ignored_taps, normwise_err, require_gpu, to_host, tolerance, upload
+
+pytestmark = pytest.mark.gpu
+
+GRAD_KEYS = ("dx", "dw", "dlam", "du")
+
+
+def run_gpu(inputs, wl, backward):
+    torch = require_gpu()
+    t = upload(inputs, wl.dtype)
+    y = gspn.scan_fwd(t["x"], t["w"], t["lam"], t["u"], wl.dirs)
+    out = {"y": y}
+    if backward:
+        dx, dw, dlam, du = gspn.scan_bwd(t["x"], t["w"], t["lam"], t["u"], t["dy"], wl.dirs)
+        out.update(dx=dx, dw=dw, dlam=dlam, du=du)
+    torch.cuda.synchronize()
+    return {k: to_host(v) for k, v in out.items()}
+
+
+def check_against_oracle(inputs, got, wl, backward, tag=""):
+    tol = tolerance(wl.dtype)
+    ref_y = oracle.scan_fwd(inputs["x"], inputs["w"], inputs["lam"], inputs["u"], wl.dirs)
+    err = normwise_err(got["y"], ref_y)
+    assert err <= tol, f"{tag} y err {err:.3g} > {tol}"
+    if backward:
+        ref = oracle.scan_bwd(inputs["x"], inputs["w"], inputs["lam"], inputs["u"], inputs["dy"],
+                              wl.dirs)
+        for k in GRAD_KEYS:
+            err = normwise_err(got[k], ref[k])
+            assert err <= tol, f"{tag} {k} err {err:.3g} > {tol}"
+        ign = ignored_taps(wl.dirs, wl.H, wl.W)          # [D,3,H,W]
+        dw = got["dw"]                                    # [D,B,G,3,H,W]
+        mask = np.broadcast_to(ign[:, None, None], dw.shape)
+        assert np.all(dw[mask] == 0.0), f"{tag} dw not zero on ignored taps"
+
+
+def case(name, B, C, G, H, W, dirs=15, dtype="bf16", backward=True, gate="sigmoid", sigma=1.0,
+         seed=5):
+    return gi.Workload(name, B, C, G, H, W, dtype, dirs, backward, gate, sigma, seed)
+
+
+# reduced-batch versions of the five workloads: the oracle checks every output
+REDUCED = [
+    gi.workload(0),
+    gi.workload(0).with_(name="tiny-f32-bwd", backward=True),
+    gi.workload(1).with_(B=2),
+    gi.workload(2).with_(B=2),
+    gi.workload(3).with_(B=1, C=64, G=2),
+    gi.workload(4).with_(C=8, G=2),
+]
+
+EDGE = [
+    case("1x1", 1, 3, 3, 1, 1),
+    case("row", 2, 5, 1, 1, 7),
+    case("column", 1, 6, 2, 9, 1),
+    case("13x7-G=C", 1, 4, 4, 13, 7),
+    case("17x33-ragged-channels", 3, 7, 7, 17, 33),
+    case("31x20-dirs5", 1, 10, 5, 31, 20, dirs=5),
+    case("64x63-dirs10", 2, 12, 3, 64, 63, dirs=10),
+    case("16x16-cpg64", 1, 128, 2, 16, 16),
+    case("f32-40x24", 2, 6, 3, 40, 24, dtype="f32", gate="normal"),
+    case("f32-9x12-R2L", 1, 5, 1, 9, 12, dirs=8, dtype="f32", gate="normal"),
+    case("general-65x3", 1, 2, 1, 65, 3),
+    case("general-70x100", 1, 4, 2, 70, 100),
+    case("general-f32-3x130", 1, 3, 1, 3, 130, dtype="f32", gate="normal"),
+    case("peaky-48x48", 1, 8, 2, 48, 48, sigma=2.0),
+]
+
+
+@pytest.mark.parametrize("wl", REDUCED + EDGE, ids=lambda w: w.name)
+def test_parity_against_oracle(wl):
+    inputs = gi.make_inputs(wl, with_dy=wl.backward)
+    got = run_gpu(inputs, wl, wl.backward)
+    check_against_oracle(inputs, got, wl, wl.backward, wl.name)
+
+
+@pytest.mark.parametrize("wl", [case("nan-taps-14x14", 2, 8, 2, 14, 14),
+                                case("nan-taps-64x64", 1, 4, 1, 64, 64),
+                                case("nan-taps-general", 1, 2, 1, 3, 80)], ids=lambda w: w.name)
+def test_ignored_taps_may_hold_nan(wl):
+    inputs = gi.make_inputs(wl, with_dy=True)
+    clean = run_gpu(inputs, wl, True)
+    dirty = dict(inputs)
+    w = inputs["w"].copy()
+    ign = ignored_taps(wl.dirs, wl.H, wl.W)
+    w[np.broadcast_to(ign[:, None, None], w.shape)] = np.nan
+    dirty["w"] = w
+    got = run_gpu(dirty, wl, True)
+    for k in ("y",) + GRAD_KEYS:
+        assert np.array_equal(got[k], clean[k]), k
+
+
+def test_deterministic_bitwise():
+    wl = gi.workload(3).with_(B=1, C=64, G=2)
+    inputs = gi.make_inputs(wl)
+    a = run_gpu(inputs, wl, True)
+    b = run_gpu(inputs, wl, True)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+# full-size workloads: every output computed on the GPU, sampled
+# (batch, group) units checked against the oracle
+@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+def test_full_size_sampled_units(idx):
+    wl = gi.workload(idx)
+    inputs = gi.make_inputs(wl)
+    got = run_gpu(inputs, wl, wl.backward)
+    rng = np.random.default_rng(idx)
+    units = {(0, 0), (wl.B - 1, wl.G - 1), (int(rng.integers(wl.B)), int(rng.integers(wl.G)))}
+    cpg = wl.C // wl.G
+    for b, g in sorted(units):
+        sl = oracle.slice_group(inputs, b, g, wl.G)
+        cs = slice(g * cpg, (g + 1) * cpg)
+        part = {"y": got["y"][b:b + 1, cs]}
+        if wl.backward:
+            part.update(dx=got["dx"][b:b + 1, cs], dw=got["dw"][:, b:b + 1, g:g + 1],
+                        dlam=got["dlam"][:, b:b + 1, cs], du=got["du"][:, b:b + 1, cs])
+        unit_wl = wl.with_(B=1, C=cpg, G=1)
+        check_against_oracle(sl, part, unit_wl, wl.backward, f"{wl.name} unit b={b} g={g}")
+    assert np.all(np.isfinite(got["y"]))
