@@ -1,0 +1,205 @@
+#!/usr/bin/env python3
+"""Benchmark of the 4-direction GSPN line scan (forward + backward) on one MI355X.
+
+One step = gspn_scan_fwd + gspn_scan_bwd over one batch of the workload, with
+every input already resident in HBM.  Prints ONE JSON line on stdout:
+throughput in G pixel-channels per second (B*C*H*W per step), the roofline
+of the dominant kernel (algorithmic bytes / average launch time, from HIP
+events on the launch stream) and the CPU oracle timed on a bounded sample of
+the same workload.  Diagnostics go to stderr.
+
+    python bench.py [--steps K] [--warmup W] [--workload IDX|NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+import gspn_inputs as gi  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published peak
+METRIC = "GSPN scan fwd+bwd Gpix·ch/s at 1 MI355X; achieved HBM GB/s vs peak"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(wl: gi.Workload) -> dict:
+    """Compulsory HBM bytes: each input read once, each output written once.
+
+    forward  : x, lam_d, u_d, w_d in; y out           s*N*[C(2+2D) + 3GD]
+    backward : x, dy, lam_d, u_d, w_d in;
+               dx, dlam_d, du_d, dw_d out            s*N*[C(3+4D) + 6GD]
+    with N = B*H*W, D directions, s bytes per stored element.
+    """
+    s = 4 if wl.dtype == "f32" else 2
+    N = wl.B * wl.H * wl.W
+    D = wl.ndirs
+    fwd = s * N * (wl.C * (2 + 2 * D) + 3 * wl.G * D)
+    bwd = s * N * (wl.C * (3 + 4 * D) + 6 * wl.G * D)
+    return {"fwd": fwd, "bwd": bwd if wl.backward else 0}
+
+
+def to_device(a, dtype, torch):
+    if dtype == "bf16":
+        return torch.from_numpy(gi.to_bf16_bits(a).view(np.int16)).to("cuda").view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
+
+
+def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float) -> dict:
+    """The fp64 oracle, single thread, on (batch, group) units of the workload.
+
+    Units run in a fixed order until `min_seconds` have passed or the whole
+    workload is done; a workload shorter than that is run again (whole passes
+    only) so the timed region reaches about `min_seconds`.
+    """
+    import oracle
+    cpg = wl.C // wl.G
+    order = [(b, g) for g in range(wl.G) for b in range(wl.B)]
+    done = 0
+    passes = 0
+    t0 = time.perf_counter()
+    while True:
+        for b, g in order:
+            sl = oracle.slice_group(inputs, b, g, wl.G)
+            oracle.scan_fwd(sl["x"], sl["w"], sl["lam"], sl["u"], wl.dirs)
+            if wl.backward:
+                oracle.scan_bwd(sl["x"], sl["w"], sl["lam"], sl["u"], sl["dy"], wl.dirs)
+            done += 1
+            if passes == 0 and time.perf_counter() - t0 >= min_seconds:
+                break
+        passes += 1
+        if time.perf_counter() - t0 >= min_seconds:
+            break
+    dt = time.perf_counter() - t0
+    pixch = done * cpg * wl.H * wl.W
+    return {"value": round(pixch / dt / 1e9, 6), "unit": "Gpix·ch/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{done} (batch, group) units of {wl.name} ({wl.B * wl.G} per step; "
+                      f"{done * cpg} channel planes, {'fwd+bwd' if wl.backward else 'fwd'}, "
+                      f"fp64, single thread), {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="3", help="index or name of the workload")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time of the oracle baseline")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the scan needs no communication, and each GPU "
+              "of a data-parallel job runs this kernel on its own batch shard. Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2606_00746_amd as gspn
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    gspn.load()
+
+    key = args.workload
+    wl = gi.workload(int(key) if key.isdigit() else key)
+    log(f"workload {wl}")
+    t0 = time.perf_counter()
+    inputs = gi.make_inputs(wl, with_dy=wl.backward)
+    log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
+    dev = {k: to_device(v, wl.dtype, torch) for k, v in inputs.items()}
+    x, w, lam, u = dev["x"], dev["w"], dev["lam"], dev["u"]
+    y = torch.empty_like(x)
+    if wl.backward:
+        dy = dev["dy"]
+        grads = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
+                 torch.empty_like(u))
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        gspn.scan_fwd(x, w, lam, u, wl.dirs, y=y, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        if wl.backward:
+            gspn.scan_bwd(x, w, lam, u, dy, wl.dirs, out=grads, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
+    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events])) if wl.backward else 0.0
+    ms_per_step = elapsed * 1e3 / args.steps
+    pixch = wl.pixels_channels
+    value = pixch / (elapsed / args.steps) / 1e9
+    nbytes = algorithmic_bytes(wl)
+    step_gbs = (nbytes["fwd"] + nbytes["bwd"]) / (ms_per_step * 1e-3) / 1e9
+    log(f"fwd {fwd_ms:.4f} ms  bwd {bwd_ms:.4f} ms  step {ms_per_step:.4f} ms  "
+        f"{value:.2f} Gpix.ch/s  step algorithmic {step_gbs:.0f} GB/s "
+        f"({step_gbs / HBM_PEAK_GBS:.1%} of peak)")
+
+    if bwd_ms > fwd_ms:
+        dom, dom_ms, dom_bytes = "gspn_scan_bwd", bwd_ms, nbytes["bwd"]
+    else:
+        dom, dom_ms, dom_bytes = "gspn_scan_fwd", fwd_ms, nbytes["fwd"]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": dom, "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "Gpix·ch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "B": wl.B, "C": wl.C, "G": wl.G, "H": wl.H, "W": wl.W,
+                   "directions": wl.ndirs, "pass": "fwd+bwd" if wl.backward else "fwd",
+                   "storage": wl.dtype, "parallelism": "single GPU"},
+        "fwd_ms": round(fwd_ms, 5),
+        "bwd_ms": round(bwd_ms, 5),
+        "step_hbm_gbs_algorithmic": round(step_gbs, 1),
+        "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
