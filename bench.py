@@ -120,7 +120,8 @@ def main() -> int:
     t0 = time.perf_counter()
     inputs = gi.make_inputs(wl, with_dy=wl.backward)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
-    dev = {k: to_device(v, wl.dtype, torch) for k, v in inputs.items()}
+    dev = {k: to_device(v, wl.dtype, torch)
+           for k, v in gi.inputs_line_major(inputs, wl.dirs).items()}
     x, w, lam, u = dev["x"], dev["w"], dev["lam"], dev["u"]
     y = torch.empty_like(x)
     if wl.backward:

@@ -159,3 +159,45 @@ def round_to_bf16(a: np.ndarray) -> np.ndarray:
     lsb = (bits >> 16) & 1
     bits = ((bits + 0x7FFF + lsb) & 0xFFFF0000).astype(np.uint32)
     return bits.view(np.float32)
+
+
+def direction_bits(dirs: int) -> list:
+    """Direction bits of a mask in slot order."""
+    return [bit for bit in DIR_BITS if dirs & bit]
+
+
+def to_line_major(a: np.ndarray, dirs: int) -> np.ndarray:
+    """Pixel-major per-direction tensor [D, ..., H, W] -> line-major [D, ..., H*W].
+
+    Line-major stores every line a direction scans contiguously: planes of
+    vertical directions are unchanged, planes of horizontal directions are
+    transposed ([W][H]).  This is the library's layout for lam, u, w and
+    their gradients.
+    """
+    a = np.asarray(a)
+    H, W = a.shape[-2:]
+    out = np.empty(a.shape[:-2] + (H * W,), dtype=a.dtype)
+    for s, bit in enumerate(direction_bits(dirs)):
+        plane = a[s] if bit in (T2B, B2T) else np.swapaxes(a[s], -1, -2)
+        out[s] = np.ascontiguousarray(plane).reshape(a.shape[1:-2] + (H * W,))
+    return out
+
+
+def from_line_major(a: np.ndarray, dirs: int, H: int, W: int) -> np.ndarray:
+    """Inverse of :func:`to_line_major`: [D, ..., H*W] -> [D, ..., H, W]."""
+    a = np.asarray(a)
+    out = np.empty(a.shape[:-1] + (H, W), dtype=a.dtype)
+    for s, bit in enumerate(direction_bits(dirs)):
+        if bit in (T2B, B2T):
+            out[s] = a[s].reshape(a.shape[1:-1] + (H, W))
+        else:
+            out[s] = np.swapaxes(a[s].reshape(a.shape[1:-1] + (W, H)), -1, -2)
+    return out
+
+
+PER_DIRECTION = ("lam", "u", "w", "dlam", "du", "dw")
+
+
+def inputs_line_major(inputs: dict, dirs: int) -> dict:
+    """Copy of a pixel-major input dict with the per-direction tensors line-major."""
+    return {k: (to_line_major(v, dirs) if k in PER_DIRECTION else v) for k, v in inputs.items()}

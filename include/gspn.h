@@ -25,11 +25,20 @@
  * (fp32 or bf16); arithmetic is fp32 and results are rounded to the storage
  * type (round to nearest even) once, when stored.
  *
- * Layouts (contiguous, row-major), D = number of directions in the mask,
- * per-direction tensors stacked in increasing direction-bit order:
- *   x, y, dy, dx           [B][C][H][W]
- *   w, dw                  [D][B][G][3][H][W]
- *   lam, u, dlam, du       [D][B][C][H][W]
+ * Layouts.  D = number of directions in the mask; per-direction tensors are
+ * stacked in increasing direction-bit order.  Shared tensors are pixel-major:
+ *   x, y, dy, dx           [B][C][H][W]          element (r, c) at r*W + c
+ * Per-direction tensors are line-major: every line scanned by the direction
+ * is contiguous, so the scan reads whole lines (rows for vertical scans,
+ * columns for horizontal ones):
+ *   lam, u, dlam, du       [D][B][C][plane]
+ *   w, dw                  [D][B][G][3][plane]
+ *   plane of a vertical direction (T2B, B2T):    element (r, c) at r*W + c
+ *   plane of a horizontal direction (L2R, R2L):  element (r, c) at c*H + r
+ * i.e. horizontal-direction planes are stored transposed ([W][H]).  A
+ * producer (for instance the 1x1 convolutions that predict lam, u and w)
+ * can write this layout directly; it costs nothing compared with the
+ * pixel-major one.
  *
  * Ownership and threading: all pointers are device pointers owned by the
  * caller; the library keeps none of them after a call returns.  Outputs are
@@ -82,9 +91,9 @@ extern "C" {
 /*
  * Forward pass (Sec. 3, Eqs. (gspn_recurrence) and (gspn_output)).
  *   x    [B][C][H][W]        input feature map
- *   w    [D][B][G][3][H][W]  neighbour weights (normalised, e.g. row-stochastic)
- *   lam  [D][B][C][H][W]     input scaling lambda_d
- *   u    [D][B][C][H][W]     output gate u_d
+ *   w    [D][B][G][3][plane] neighbour weights (normalised, e.g. row-stochastic)
+ *   lam  [D][B][C][plane]    input scaling lambda_d
+ *   u    [D][B][C][plane]    output gate u_d
  *   y    [B][C][H][W]        out: sum over directions of u_d * h_d
  *   direction  bitmask of GSPN_T2B | GSPN_B2T | GSPN_L2R | GSPN_R2L
  *   G          weight groups; channel c uses group c / (C/G); C % G == 0
@@ -106,9 +115,9 @@ int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u,
  * h is recomputed on the GPU; nothing is saved by the forward pass.
  *   dy   [B][C][H][W]        in: gradient of the merged output y
  *   dx   [B][C][H][W]        out
- *   dw   [D][B][G][3][H][W]  out
- *   dlam [D][B][C][H][W]     out
- *   du   [D][B][C][H][W]     out
+ *   dw   [D][B][G][3][plane] out
+ *   dlam [D][B][C][plane]    out
+ *   du   [D][B][C][plane]    out
  * Other arguments as in gspn_scan_fwd.
  */
 int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,

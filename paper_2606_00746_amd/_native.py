@@ -111,11 +111,17 @@ def _check_raise(status):
         raise GspnError(status, gspn_last_hip_error() if status == ERR_HIP else 0)
 
 
-def _sizes(x, w, direction):
-    if x.dim() != 4 or w.dim() != 6:
-        raise ValueError("x must be [B,C,H,W] and w [D,B,G,3,H,W]")
+def _sizes(x, w, lam, u, direction):
+    """(B, C, G, H, W) from x [B,C,H,W] and w [D,B,G,3,...] (line-major planes)."""
+    if x.dim() != 4 or w.dim() < 3:
+        raise ValueError("x must be [B,C,H,W] and w [D,B,G,3,plane]")
     B, C, H, W = x.shape
     G = w.shape[2]
+    D = bin(direction & 15).count("1")
+    if w.numel() != D * B * G * 3 * H * W:
+        raise ValueError("w must hold D*B*G*3*H*W elements")
+    if lam.numel() != D * B * C * H * W or u.numel() != D * B * C * H * W:
+        raise ValueError("lam and u must hold D*B*C*H*W elements")
     return B, C, G, H, W
 
 
@@ -127,9 +133,13 @@ def _ptrs(*ts):
 
 
 def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None):
-    """y = sum_d u_d * h_d for device tensors (see include/gspn.h)."""
+    """y = sum_d u_d * h_d for device tensors (see include/gspn.h).
+
+    x is pixel-major [B,C,H,W]; lam, u and w are line-major per direction
+    (horizontal-direction planes transposed), e.g. from :func:`to_line_major`.
+    """
     import torch
-    B, C, G, H, W = _sizes(x, w, direction)
+    B, C, G, H, W = _sizes(x, w, lam, u, direction)
     if y is None:
         y = torch.empty_like(x)
     status = gspn_scan_fwd(*_ptrs(x, w, lam, u, y), direction, B, C, G, H, W, _dtype_code(x),
@@ -141,7 +151,7 @@ def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None):
 def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
     """Gradients (dx, dw, dlam, du) of <y, dy> for device tensors."""
     import torch
-    B, C, G, H, W = _sizes(x, w, direction)
+    B, C, G, H, W = _sizes(x, w, lam, u, direction)
     if out is None:
         out = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                torch.empty_like(u))
@@ -150,3 +160,32 @@ def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
                            _dtype_code(x), _stream_handle(x, stream))
     _check_raise(status)
     return dx, dw, dlam, du
+
+
+def to_line_major(t, direction: int):
+    """Pixel-major per-direction tensor [D, ..., H, W] -> line-major [D, ..., H*W].
+
+    Planes of horizontal directions are transposed so that every scanned
+    line is contiguous (a layout a producer can also write directly).
+    """
+    import torch
+    bits = [b for b in (T2B, B2T, L2R, R2L) if direction & b]
+    H, W = t.shape[-2:]
+    out = []
+    for s, b in enumerate(bits):
+        p = t[s] if b in (T2B, B2T) else t[s].transpose(-1, -2)
+        out.append(p.contiguous().reshape(*t.shape[1:-2], H * W))
+    return torch.stack(out)
+
+
+def from_line_major(t, direction: int, H: int, W: int):
+    """Inverse of :func:`to_line_major`."""
+    import torch
+    bits = [b for b in (T2B, B2T, L2R, R2L) if direction & b]
+    out = []
+    for s, b in enumerate(bits):
+        if b in (T2B, B2T):
+            out.append(t[s].reshape(*t.shape[1:-1], H, W))
+        else:
+            out.append(t[s].reshape(*t.shape[1:-1], W, H).transpose(-1, -2))
+    return torch.stack(out).contiguous()

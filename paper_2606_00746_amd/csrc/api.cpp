@@ -102,6 +102,8 @@ extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, cons
     Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
               direction, B, C, G, H, W, dtype};
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (med_supported(p))
+        return hip_status(launch_fwd_med(p, s));
     if (H <= kSmallSide && W <= kSmallSide)
         return hip_status(launch_fwd_small(p, s));
     return hip_status(launch_fwd_general(p, s));
@@ -127,6 +129,8 @@ extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, cons
         return st;
     Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
     hipStream_t s = static_cast<hipStream_t>(stream);
+    if (med_supported(p))
+        return hip_status(launch_bwd_med(p, s));
     if (H <= kSmallSide && W <= kSmallSide)
         return hip_status(launch_bwd_small(p, s));
     return hip_status(launch_bwd_general(p, s));

@@ -43,24 +43,34 @@ __device__ __forceinline__ float from_right(float v)
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xf, 0xf, true));
 }
 
-// Direction index d (direction bit 1 << d): the pixel at frame (step i, line
-// position j) sits at e0 + i * es in an H x W plane whose rows are `pitch`
-// elements apart (pitch = W in global memory, padded in LDS).
+// Direction index d (direction bit 1 << d), frame position (step i, line
+// position j):
+//   pixel offset      e0 + i * es  in an H x W plane whose rows are `pitch`
+//                                  elements apart (pitch = W in global memory,
+//                                  padded in LDS);
+//   line-major offset d0 + i * ds  in a per-direction plane, where every
+//                                  scanned line is contiguous (rows for
+//                                  vertical directions, columns for
+//                                  horizontal ones).
 struct Frame {
     int L;        // scan length
     int P;        // line length
-    int e0;       // offset of (0, j)
-    int es;       // offset change per step
+    int e0, es;   // pixel offset of (0, j), change per step
+    int d0, ds;   // line-major offset of (0, j), change per step
 };
 
 __device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitch)
 {
     Frame f;
     switch (d) {
-    case 0:  f.L = H; f.P = W; f.e0 = j;                           f.es = pitch;  break; // T2B
-    case 1:  f.L = H; f.P = W; f.e0 = (H - 1) * pitch + j;         f.es = -pitch; break; // B2T
-    case 2:  f.L = W; f.P = H; f.e0 = j * pitch;                   f.es = 1;      break; // L2R
-    default: f.L = W; f.P = H; f.e0 = j * pitch + (W - 1);         f.es = -1;     break; // R2L
+    case 0:  f.L = H; f.P = W; f.e0 = j;                   f.es = pitch;
+             f.d0 = j;                   f.ds = W;   break;  // T2B
+    case 1:  f.L = H; f.P = W; f.e0 = (H - 1) * pitch + j; f.es = -pitch;
+             f.d0 = (H - 1) * W + j;     f.ds = -W;  break;  // B2T
+    case 2:  f.L = W; f.P = H; f.e0 = j * pitch;           f.es = 1;
+             f.d0 = j;                   f.ds = H;   break;  // L2R
+    default: f.L = W; f.P = H; f.e0 = j * pitch + (W - 1); f.es = -1;
+             f.d0 = (W - 1) * H + j;     f.ds = -H;  break;  // R2L
     }
     return f;
 }

@@ -54,17 +54,18 @@ __global__ __launch_bounds__(kThreads) void fwd_general_kernel(
         const float *prev = hb + ((i + 2) % 3) * P;
         for (int j = threadIdx.x; j < P; j += blockDim.x) {
             const Frame f = make_frame(d, j, H, W, W);
-            const int e = f.e0 + i * f.es;
-            float v = load_f(lp + e) * load_f(xp + e);
+            const int e = f.e0 + i * f.es;   // pixel (x, y slots)
+            const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+            float v = load_f(lp + q) * load_f(xp + e);
             if (i > 0) {
-                v = fmaf(load_f(wp + HW + e), prev[j], v);
+                v = fmaf(load_f(wp + HW + q), prev[j], v);
                 if (j > 0)
-                    v = fmaf(load_f(wp + e), prev[j - 1], v);
+                    v = fmaf(load_f(wp + q), prev[j - 1], v);
                 if (j + 1 < P)
-                    v = fmaf(load_f(wp + 2 * HW + e), prev[j + 1], v);
+                    v = fmaf(load_f(wp + 2 * HW + q), prev[j + 1], v);
             }
             cur[j] = v;
-            yp[e] = load_f(up + e) * v;
+            yp[e] = load_f(up + q) * v;
         }
         __syncthreads();
     }
@@ -122,14 +123,15 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
                 const Frame f = make_frame(d, j, H, W, W);
                 const int e = f.e0 + i * f.es;
-                float v = load_f(lp + e) * load_f(xp + e);
+                const int q = f.d0 + i * f.ds;
+                float v = load_f(lp + q) * load_f(xp + e);
                 if (i > 0) {
                     const float *prev = hs + (i - 1) * P;
-                    v = fmaf(load_f(wp + HW + e), prev[j], v);
+                    v = fmaf(load_f(wp + HW + q), prev[j], v);
                     if (j > 0)
-                        v = fmaf(load_f(wp + e), prev[j - 1], v);
+                        v = fmaf(load_f(wp + q), prev[j - 1], v);
                     if (j + 1 < P)
-                        v = fmaf(load_f(wp + 2 * HW + e), prev[j + 1], v);
+                        v = fmaf(load_f(wp + 2 * HW + q), prev[j + 1], v);
                 }
                 hs[i * P + j] = v;
             }
@@ -141,28 +143,29 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
             const float *next = ab + ((i + 1) % 3) * P;
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
                 const Frame f = make_frame(d, j, H, W, W);
-                const int e = f.e0 + i * f.es;
+                const int e = f.e0 + i * f.es;   // pixel (x, dy, dx slots)
+                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w, dlam, du, dw)
                 const float dyv = load_f(dyp + e);
-                float a = load_f(up + e) * dyv;
+                float a = load_f(up + q) * dyv;
                 if (i + 1 < L) {
-                    const int step = (i + 1) * f.es;
-                    a = fmaf(load_f(wp + HW + f.e0 + step), next[j], a);
+                    // line i+1 is contiguous: position j' sits at qn + (j' - j)
+                    const int qn = q + f.ds;
+                    a = fmaf(load_f(wp + HW + qn), next[j], a);
                     if (j + 1 < P)   // target j+1 on line i+1 reads j through its tap 0
-                        a = fmaf(load_f(wp + make_frame(d, j + 1, H, W, W).e0 + step), next[j + 1], a);
+                        a = fmaf(load_f(wp + qn + 1), next[j + 1], a);
                     if (j > 0)       // target j-1 on line i+1 reads j through its tap 2
-                        a = fmaf(load_f(wp + 2 * HW + make_frame(d, j - 1, H, W, W).e0 + step),
-                                 next[j - 1], a);
+                        a = fmaf(load_f(wp + 2 * HW + qn - 1), next[j - 1], a);
                 }
                 cur[j] = a;
                 const float hv = hs[i * P + j];
-                store_f(du + pd + e, dyv * hv);
-                store_f(dlam + pd + e, a * load_f(xp + e));
-                dxs[pd + e] = a * load_f(lp + e);
+                store_f(du + pd + q, dyv * hv);
+                store_f(dlam + pd + q, a * load_f(xp + e));
+                dxs[pd + e] = a * load_f(lp + q);
                 for (int k = 0; k < 3; ++k) {
                     const int jj = j + k - 1;
                     const bool valid = i > 0 && jj >= 0 && jj < P;
                     const float t = valid ? a * hs[(i - 1) * P + jj] : 0.f;
-                    float *dst = dwp + k * HW + e;
+                    float *dst = dwp + k * HW + q;
                     *dst = (cl == 0) ? t : *dst + t;
                 }
             }

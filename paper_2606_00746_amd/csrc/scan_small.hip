@@ -68,14 +68,15 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
 #pragma unroll
         for (int i = 0; i < T; ++i) {
             if (i < f.L) {
-                const int e = f.e0 + i * f.es;
-                float inj = load_f(lp + e) * load_f(xp + e);
+                const int e = f.e0 + i * f.es;   // pixel (x)
+                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+                float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
                 if (i > 0) {
-                    float w0 = load_f(wp + e);
-                    float w1 = load_f(wp + HW + e);
-                    float w2 = load_f(wp + 2 * HW + e);
+                    float w0 = load_f(wp + q);
+                    float w1 = load_f(wp + HW + q);
+                    float w2 = load_f(wp + 2 * HW + q);
                     w0 = m0 ? w0 : 0.f;
                     w1 = active ? w1 : 0.f;
                     w2 = m2 ? w2 : 0.f;
@@ -86,7 +87,7 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
                     hn = fmaf(w2, hr, hn);
                 }
                 h = hn;
-                yr[i] = load_f(up + e) * h;
+                yr[i] = load_f(up + q) * h;
             }
         }
     }
@@ -182,14 +183,15 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
 #pragma unroll
         for (int i = 0; i < T; ++i) {
             if (i < L) {
-                const int e = f.e0 + i * f.es;
-                float inj = load_f(lp + e) * load_f(xp + e);
+                const int e = f.e0 + i * f.es;   // pixel (x)
+                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+                float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
                 if (i > 0) {
-                    float w0 = load_f(wp + e);
-                    float w1 = load_f(wp + HW + e);
-                    float w2 = load_f(wp + 2 * HW + e);
+                    float w0 = load_f(wp + q);
+                    float w1 = load_f(wp + HW + q);
+                    float w2 = load_f(wp + 2 * HW + q);
                     w0 = m0 ? w0 : 0.f;
                     w1 = active ? w1 : 0.f;
                     w2 = m2 ? w2 : 0.f;
@@ -210,14 +212,15 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
 #pragma unroll
         for (int i = T - 1; i >= 0; --i) {
             if (i < L) {
-                const int e = f.e0 + i * f.es;
+                const int e = f.e0 + i * f.es;   // pixel (x, dy)
+                const int qd = f.d0 + i * f.ds;  // line-major (lam, u, w, dlam, du)
                 const float dyv = load_f(dyp + e);
-                float a = load_f(up + e) * dyv;
+                float a = load_f(up + qd) * dyv;
                 if (i + 1 < L) {
-                    const int en = e + f.es;
-                    float w0 = load_f(wp + en);
-                    float w1 = load_f(wp + HW + en);
-                    float w2 = load_f(wp + 2 * HW + en);
+                    const int qn = qd + f.ds;
+                    float w0 = load_f(wp + qn);
+                    float w1 = load_f(wp + HW + qn);
+                    float w2 = load_f(wp + 2 * HW + qn);
                     w0 = m0 ? w0 : 0.f;
                     w1 = active ? w1 : 0.f;
                     w2 = m2 ? w2 : 0.f;
@@ -231,10 +234,10 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
                 }
                 a = active ? a : 0.f;
                 const float xv = load_f(xp + e);
-                const float lv = load_f(lp + e);
+                const float lv = load_f(lp + qd);
                 if (active) {
-                    store_f(dup + e, dyv * hist[i]);
-                    store_f(dlp + e, a * xv);
+                    store_f(dup + qd, dyv * hist[i]);
+                    store_f(dlp + qd, a * xv);
                     const int ae = fl.e0 + i * fl.es;
                     Xq[ae] = (d == dfirst) ? a * lv : Xq[ae] + a * lv;
                 }
@@ -262,7 +265,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
                     for (int qq = 0; qq < nvalid; ++qq)
                         sum += src[qq * 3 * T];
                     const Frame ft = make_frame(d, jj, H, W, W);
-                    const int et = k * HW + ft.e0 + i * ft.es;
+                    const int et = k * HW + ft.d0 + i * ft.ds;
                     const int64_t unit = ((int64_t)s * B + b) * G + g;
                     if (nchunk == 1)
                         store_f(dw + unit * 3 * HW + et, sum);

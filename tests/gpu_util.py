@@ -27,8 +27,9 @@ def to_host(t) -> np.ndarray:
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def upload(inputs: dict, dtype: str) -> dict:
-    return {k: to_device(v, dtype) for k, v in inputs.items()}
+def upload(inputs: dict, dtype: str, dirs: int) -> dict:
+    """Device copies of pixel-major inputs, per-direction tensors line-major."""
+    return {k: to_device(v, dtype) for k, v in gi.inputs_line_major(inputs, dirs).items()}
 
 
 def normwise_err(a: np.ndarray, r: np.ndarray) -> float:

@@ -99,3 +99,16 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(_native, "LIB_PATH", str(tmp_path / "libgspn.so"))
     with pytest.raises(RuntimeError, match="missing"):
         _native.load()
+
+
+def test_torch_layout_helpers_match_numpy():
+    import numpy as np
+    import torch
+    import gspn_inputs as gi
+    a = np.random.default_rng(0).standard_normal((4, 2, 4, 5, 6)).astype(np.float32)
+    for dirs in (15, 7, 12, 1):
+        d = bin(dirs).count("1")
+        t = torch.from_numpy(a[:d].copy())
+        lm = g.to_line_major(t, dirs)
+        np.testing.assert_array_equal(lm.numpy(), gi.to_line_major(a[:d], dirs))
+        np.testing.assert_array_equal(g.from_line_major(lm, dirs, 5, 6).numpy(), a[:d])

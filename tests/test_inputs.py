@@ -72,3 +72,21 @@ def test_bf16_helpers_round_trip():
     np.testing.assert_array_equal(gi.round_to_bf16(t), np.array([1.0, 1.0 + 2.0 ** -6], np.float32))
     with pytest.raises(ValueError):
         gi.to_bf16_bits(np.array([1.0 + 2.0 ** -10], dtype=np.float32))
+
+
+def test_line_major_round_trip_and_layout():
+    rng = np.random.default_rng(3)
+    H, W = 3, 5
+    a = rng.standard_normal((4, 2, 2, H, W))
+    lm = gi.to_line_major(a, 15)
+    assert lm.shape == (4, 2, 2, H * W)
+    # vertical planes unchanged, horizontal planes transposed: (r, c) at c*H + r
+    np.testing.assert_array_equal(lm[0, 1, 0], a[0, 1, 0].reshape(-1))
+    for r in range(H):
+        for c in range(W):
+            assert lm[2, 1, 1, c * H + r] == a[2, 1, 1, r, c]
+            assert lm[3, 0, 1, c * H + r] == a[3, 0, 1, r, c]
+    np.testing.assert_array_equal(gi.from_line_major(lm, 15, H, W), a)
+    # subsets keep slot order
+    b = a[:2]
+    np.testing.assert_array_equal(gi.from_line_major(gi.to_line_major(b, 5), 5, H, W), b)

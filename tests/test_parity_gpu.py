@@ -19,15 +19,20 @@ GRAD_KEYS = ("dx", "dw", "dlam", "du")
 
 
 def run_gpu(inputs, wl, backward):
+    """Run the library on pixel-major host inputs; returns pixel-major results."""
     torch = require_gpu()
-    t = upload(inputs, wl.dtype)
+    t = upload(inputs, wl.dtype, wl.dirs)
     y = gspn.scan_fwd(t["x"], t["w"], t["lam"], t["u"], wl.dirs)
     out = {"y": y}
     if backward:
         dx, dw, dlam, du = gspn.scan_bwd(t["x"], t["w"], t["lam"], t["u"], t["dy"], wl.dirs)
         out.update(dx=dx, dw=dw, dlam=dlam, du=du)
     torch.cuda.synchronize()
-    return {k: to_host(v) for k, v in out.items()}
+    res = {k: to_host(v) for k, v in out.items()}
+    for k in ("dw", "dlam", "du"):
+        if k in res:
+            res[k] = gi.from_line_major(res[k], wl.dirs, wl.H, wl.W)
+    return res
 
 
 def check_against_oracle(inputs, got, wl, backward, tag=""):
@@ -77,6 +82,14 @@ EDGE = [
     case("general-70x100", 1, 4, 2, 70, 100),
     case("general-f32-3x130", 1, 3, 1, 3, 130, dtype="f32", gate="normal"),
     case("peaky-48x48", 1, 8, 2, 48, 48, sigma=2.0),
+    # register-streamed path (bf16, 56x56 / 64x64): direction subsets, ragged
+    # channel chunks (idle waves), fewer than three waves per workgroup
+    case("med64-dirs5-cpg20", 1, 40, 2, 64, 64, dirs=5),
+    case("med64-R2L-cpg2", 2, 4, 2, 64, 64, dirs=8),
+    case("med56-dirs6-cpg1", 1, 3, 3, 56, 56, dirs=6),
+    case("med64-all-cpg9", 1, 18, 2, 64, 64),
+    case("med56-T2B-cpg12", 2, 24, 2, 56, 56, dirs=1),
+    case("med64-peaky", 1, 16, 1, 64, 64, sigma=2.0),
 ]
 
 
