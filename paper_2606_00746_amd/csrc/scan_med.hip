@@ -47,7 +47,7 @@ constexpr uint32_t kSelHi = 0x03020C0Cu;   // bf16 in bits [31:16] -> fp32
 constexpr uint32_t kSelZero = 0x0C0C0C0Cu; // -> +0.0f
 constexpr int kYPitch = 68;                // fp32 LDS row pitch (16-byte rows, conflict-free b128)
 constexpr int kDxPitch = 65;               // fp32 LDS row pitch for per-step dx (odd: column walks conflict-free)
-constexpr int kPrefetch = 10;              // steps of per-step loads in flight (backward)
+constexpr int kPrefetch = 8;               // steps of per-step loads in flight (backward)
 
 // Keep the software pipeline as written: nothing is scheduled across a step
 // boundary, so each step's prefetch stays kPrefetch steps ahead of its use
@@ -69,9 +69,17 @@ __device__ __forceinline__ void lds_barrier()
 using rsrc_t = __amdgpu_buffer_rsrc_t;
 constexpr int kRsrcWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data format, no swizzle
 
+// The base address is passed through readfirstlane: every caller's pointer
+// is wave-uniform, and saying so keeps the compiler from wrapping each buffer
+// access in a loop over distinct descriptors.
 __device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
 {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), (short)0, (int)bytes,
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+    void *q = reinterpret_cast<void *>((static_cast<uint64_t>(hi) << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(q, (short)0,
+                                             (int)__builtin_amdgcn_readfirstlane(bytes),
                                              kRsrcWord3);
 }
 __device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
@@ -404,15 +412,15 @@ struct BwdArgs {
     bool first;            // first direction processed: store dx, don't add
 };
 
-// Sum of the step's dw terms over the workgroup's channels, in channel order.
-__device__ __forceinline__ float reduce_slot(const float *slots, int buf, int cw, int nvalid,
-                                             int k, int lane)
+// Per-step dw terms live in LDS as slots[buf][k][q][j] (q = channel slot of
+// the workgroup, 8 slots, absent channels zero): a wave writes one
+// contiguous row per tap and a reducing lane reads its 8 slots, all
+// conflict-free.
+constexpr int kSlots = 8;   // channel slots per (tap, position)
+
+__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int k, int q)
 {
-    const float *src = slots + (buf * cw * 3 + k) * 64 + lane;
-    float sum = 0.f;
-    for (int q = 0; q < nvalid; ++q)
-        sum += src[q * 3 * 64];
-    return sum;
+    return slots + ((buf * 3 + k) * kSlots + q) * 64;
 }
 
 // While the horizontal directions run, a wave's LDS dx plane holds x and dy
@@ -464,15 +472,22 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         for (int i = L - 1; i >= L - kPrefetch && i >= 0; --i)
             ALOAD(i);
         float an = 0.f;
+        // horizontal directions: the staged (x, dy) dword of the next step is
+        // read one step ahead so its LDS latency overlaps the arithmetic
+        auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i))); };
+        uint32_t xd_next = VERT ? 0u : stg_at(L - 1);
 #pragma unroll
         for (int i = L - 1; i >= 0; --i) {
             if (i - kPrefetch >= 0)
                 ALOAD(i - kPrefetch);
             float dyv;
-            if (VERT)
+            if (VERT) {
                 dyv = bf_lo(rd[VERT ? i : 0]);
-            else
-                dyv = bf_hi(lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i))));
+            } else {
+                dyv = bf_hi(xd_next);
+                if (i > 0)
+                    xd_next = stg_at(i - 1);
+            }
             const float inj = widen(ru[i], s.lo1) * dyv;
             float a;
             if (i + 1 == L)
@@ -507,7 +522,47 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #pragma unroll
     for (int i = 0; i < kPrefetch && i < L; ++i)
         BLOAD(i);
+    // Reduction of the dw terms of line i over the workgroup's channels:
+    // wave k (< 3) owns tap k.  Its eight slot reads are issued right after
+    // the barrier and summed one step later, in channel order.  With fewer
+    // than three waves the remaining taps are summed at once by wave 0.
+    float pr[kSlots];
+    auto store_dw = [&](int i, int k, float v) {
+        const uint32_t so = lnoff(i);
+        if (j < P) {
+            if (A.partial)
+                st32f(A.dw, 2u * vo, 2u * (so + k * PL2), v);
+            else
+                st16(A.dw, vo, so + k * PL2, pack1(v));
+        }
+    };
+    auto issue_dw = [&](int i) {
+        if (A.wave < 3) {
+#pragma unroll
+            for (int q = 0; q < kSlots; ++q)
+                pr[q] = slot_ptr(A.slots, i & 1, A.wave, q)[j];
+        }
+        if (A.nwaves < 3 && A.wave == 0) {
+            for (int k = A.nwaves; k < 3; ++k) {
+                float sum = 0.f;
+                for (int q = 0; q < kSlots; ++q)
+                    sum += slot_ptr(A.slots, i & 1, k, q)[j];
+                store_dw(i, k, sum);
+            }
+        }
+    };
+    auto flush_dw = [&](int i) {
+        if (A.wave < 3) {
+            float sum = 0.f;
+#pragma unroll
+            for (int q = 0; q < kSlots; ++q)
+                sum += pr[q];
+            store_dw(i, A.wave, sum);
+        }
+    };
     float h = 0.f;
+    auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i))); };
+    uint32_t xd_next = VERT ? 0u : stg_at(0);
 #pragma unroll
     for (int i = 0; i < L; ++i) {
         if (i + kPrefetch < L)
@@ -517,7 +572,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             xv = bf_lo(rx[VERT ? i : 0]);
             dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
         } else {
-            const uint32_t xd = lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i)));
+            const uint32_t xd = xd_next;
+            if (i + 1 < L)
+                xd_next = stg_at(i + 1);
             xv = bf_lo(xd);
             dyv = bf_hi(xd);
         }
@@ -541,30 +598,32 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             st16(A.du, vo, so, pack1(dyv * h));
             st16(A.dlam, vo, so, pack1(a * xv));
             if (VERT) {
+                // this wave is the only writer of its dx plane: a returnless
+                // LDS add keeps the order and does not wait
                 float *xa = A.Xq + col_of(i) * kDxPitch + jj;
-                *xa = A.first ? a * lv : fmaf(a, lv, *xa);
+                if (A.first)
+                    *xa = a * lv;
+                else
+                    __hip_atomic_fetch_add(xa, a * lv, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_WORKGROUP);
             }
         }
         if (!VERT) {
             const int cc = col_of(i);
             dxr[cc] = dx_first ? a * lv : fmaf(a, lv, dxr[cc]);
         }
-        float *sl = A.slots + ((i & 1) * A.cw + A.wave) * 3 * 64 + j;
-        sl[0] = t0;
-        sl[64] = t1;
-        sl[128] = t2;
+        // finish the reduction of line i-1 (its slot reads were issued after
+        // the previous barrier and overlapped this step's arithmetic)
+        if (i > 0)
+            flush_dw(i - 1);
+        slot_ptr(A.slots, i & 1, 0, A.wave)[j] = t0;
+        slot_ptr(A.slots, i & 1, 1, A.wave)[j] = t1;
+        slot_ptr(A.slots, i & 1, 2, A.wave)[j] = t2;
         lds_barrier();
-        for (int k = A.wave; k < 3; k += A.nwaves) {
-            const float v = reduce_slot(A.slots, i & 1, A.cw, A.nvalid, k, j);
-            if (j < P) {
-                if (A.partial)
-                    st32f(A.dw, 2u * vo, 2u * (so + k * PL2), v);
-                else
-                    st16(A.dw, vo, so + k * PL2, pack1(v));
-            }
-        }
+        issue_dw(i);
         step_fence();
     }
+    flush_dw(L - 1);
 #undef BLOAD
 }
 
@@ -601,6 +660,10 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.dy = make_rsrc(dy + pc, 2 * HW);
     A.Xq = smem + wave * XPLANE;
     A.slots = smem + cw * XPLANE;
+    // slots of channels this workgroup does not have must read as zero
+    for (int t = threadIdx.x; t < 2 * 3 * 64 * kSlots; t += blockDim.x)
+        A.slots[t] = 0.f;
+    lds_barrier();
     A.wave = wave;
     A.nwaves = nwaves;
     A.nvalid = nvalid;
@@ -713,16 +776,20 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     }
 }
 
-template <typename S>
-__global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ dwp,
-                                                     S *__restrict__ dw, int64_t n, int nchunk)
+// dw = sum over chunks of the fp32 partials, in chunk order; 8 outputs per
+// thread with 16-byte accesses (n is a multiple of 8 on this path).
+__global__ __launch_bounds__(256) void dw_sum_kernel(const float4 *__restrict__ dwp,
+                                                     uint4 *__restrict__ dw, int64_t n8, int nchunk)
 {
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
+    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n8;
          e += (int64_t)gridDim.x * blockDim.x) {
-        float sum = 0.f;
-        for (int k = 0; k < nchunk; ++k)
-            sum += dwp[k * n + e];
-        store_f(dw + e, sum);
+        float4 a = dwp[2 * e], b = dwp[2 * e + 1];
+        for (int k = 1; k < nchunk; ++k) {
+            const float4 p = dwp[(k * n8 + e) * 2], q = dwp[(k * n8 + e) * 2 + 1];
+            a = make_float4(a.x + p.x, a.y + p.y, a.z + p.z, a.w + p.w);
+            b = make_float4(b.x + q.x, b.y + q.y, b.z + q.z, b.w + q.w);
+        }
+        dw[e] = make_uint4(pack2(a.x, a.y), pack2(a.z, a.w), pack2(b.x, b.y), pack2(b.z, b.w));
     }
 }
 
@@ -746,15 +813,16 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess)
         return e;
-    const size_t per_ch = (size_t)H * kDxPitch * 4 + 2 * 3 * 64 * 4;
+    const size_t per_ch = (size_t)H * kDxPitch * 4;                 // dx plane
+    const size_t slots = (size_t)2 * 3 * 64 * kSlots * 4;           // per-step dw terms
     const int cpg = p.C / p.G;
-    int cap = (int)((size_t)lds_max / per_ch);
-    cap = cap < 8 ? cap : 8;
+    int cap = lds_max > (int)slots ? (int)(((size_t)lds_max - slots) / per_ch) : 0;
+    cap = cap < kSlots ? cap : kSlots;
     if (cap < 1)
         return hipErrorInvalidConfiguration;
     const int nchunk = (cpg + cap - 1) / cap;
     const int cw = (cpg + nchunk - 1) / nchunk;
-    const size_t lds = (size_t)cw * per_ch;
+    const size_t lds = (size_t)cw * per_ch + slots;
     const int D = __builtin_popcount(p.mask);
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * H * W;
 
@@ -775,10 +843,11 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
                        p.mask, p.B, p.C, p.G, cw, nchunk);
     e = hipGetLastError();
     if (e == hipSuccess && nchunk > 1) {
-        int64_t blocks = (ndw + 255) / 256;
-        blocks = blocks < 8192 ? blocks : 8192;
-        hipLaunchKernelGGL((dw_sum_kernel<bf16_t>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const float *)dwp, (bf16_t *)p.dw, ndw, nchunk);
+        const int64_t n8 = ndw / 8;
+        int64_t blocks = (n8 + 255) / 256;
+        blocks = blocks < 16384 ? blocks : 16384;
+        hipLaunchKernelGGL(dw_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                           (const float4 *)dwp, (uint4 *)p.dw, n8, nchunk);
         e = hipGetLastError();
     }
     if (dwp) {
