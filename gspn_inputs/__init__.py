@@ -166,20 +166,57 @@ def direction_bits(dirs: int) -> list:
     return [bit for bit in DIR_BITS if dirs & bit]
 
 
-def to_line_major(a: np.ndarray, dirs: int) -> np.ndarray:
-    """Pixel-major per-direction tensor [D, ..., H, W] -> line-major [D, ..., H*W].
+LINE_BLOCK = 8   # lines per block of the line-major layout
 
-    Line-major stores every line a direction scans contiguously: planes of
-    vertical directions are unchanged, planes of horizontal directions are
-    transposed ([W][H]).  This is the library's layout for lam, u, w and
-    their gradients.
+
+def block_lines(plane: np.ndarray) -> np.ndarray:
+    """[..., L, P] (line l, position p) -> blocked line-major [..., L*P].
+
+    Lines are grouped in blocks of 8 consecutive lines (the last block holds
+    L mod 8 lines when L is not a multiple of 8); inside a block the values
+    of one position are adjacent, so (l, p) sits at
+    8*P*(l // 8) + n*p + l % 8 with n = min(8, L - 8*(l // 8)).
+    """
+    plane = np.asarray(plane)
+    L, P = plane.shape[-2:]
+    lead = plane.shape[:-2]
+    if L % LINE_BLOCK == 0:
+        blk = plane.reshape(lead + (L // LINE_BLOCK, LINE_BLOCK, P))
+        return np.ascontiguousarray(np.swapaxes(blk, -1, -2)).reshape(lead + (L * P,))
+    parts = [np.swapaxes(plane[..., q:q + LINE_BLOCK, :], -1, -2).reshape(lead + (-1,))
+             for q in range(0, L, LINE_BLOCK)]
+    return np.concatenate(parts, axis=-1)
+
+
+def unblock_lines(flat: np.ndarray, L: int, P: int) -> np.ndarray:
+    """Inverse of :func:`block_lines`: [..., L*P] -> [..., L, P]."""
+    flat = np.asarray(flat)
+    lead = flat.shape[:-1]
+    if L % LINE_BLOCK == 0:
+        blk = flat.reshape(lead + (L // LINE_BLOCK, P, LINE_BLOCK))
+        return np.ascontiguousarray(np.swapaxes(blk, -1, -2)).reshape(lead + (L, P))
+    parts, off = [], 0
+    for q in range(0, L, LINE_BLOCK):
+        n = min(LINE_BLOCK, L - q)
+        parts.append(np.swapaxes(flat[..., off:off + n * P].reshape(lead + (P, n)), -1, -2))
+        off += n * P
+    return np.concatenate(parts, axis=-2)
+
+
+def to_line_major(a: np.ndarray, dirs: int) -> np.ndarray:
+    """Pixel-major per-direction tensor [D, ..., H, W] -> blocked line-major [D, ..., H*W].
+
+    The lines a direction scans are storage rows for vertical directions and
+    storage columns for horizontal ones; each plane is stored as those lines
+    in 8-line blocks (:func:`block_lines`).  This is the library's layout for
+    lam, u, w and their gradients.
     """
     a = np.asarray(a)
     H, W = a.shape[-2:]
     out = np.empty(a.shape[:-2] + (H * W,), dtype=a.dtype)
     for s, bit in enumerate(direction_bits(dirs)):
         plane = a[s] if bit in (T2B, B2T) else np.swapaxes(a[s], -1, -2)
-        out[s] = np.ascontiguousarray(plane).reshape(a.shape[1:-2] + (H * W,))
+        out[s] = block_lines(plane)
     return out
 
 
@@ -189,9 +226,9 @@ def from_line_major(a: np.ndarray, dirs: int, H: int, W: int) -> np.ndarray:
     out = np.empty(a.shape[:-1] + (H, W), dtype=a.dtype)
     for s, bit in enumerate(direction_bits(dirs)):
         if bit in (T2B, B2T):
-            out[s] = a[s].reshape(a.shape[1:-1] + (H, W))
+            out[s] = unblock_lines(a[s], H, W)
         else:
-            out[s] = np.swapaxes(a[s].reshape(a.shape[1:-1] + (W, H)), -1, -2)
+            out[s] = np.swapaxes(unblock_lines(a[s], W, H), -1, -2)
     return out
 
 

@@ -162,19 +162,51 @@ def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
     return dx, dw, dlam, du
 
 
-def to_line_major(t, direction: int):
-    """Pixel-major per-direction tensor [D, ..., H, W] -> line-major [D, ..., H*W].
+LINE_BLOCK = 8   # lines per block of the line-major layout
 
-    Planes of horizontal directions are transposed so that every scanned
-    line is contiguous (a layout a producer can also write directly).
+
+def _block_lines(plane):
+    """[..., L, P] -> [..., L*P]: lines in blocks of 8, positions adjacent inside a block."""
+    import torch
+    L, P = plane.shape[-2:]
+    lead = plane.shape[:-2]
+    if L % LINE_BLOCK == 0:
+        blk = plane.reshape(*lead, L // LINE_BLOCK, LINE_BLOCK, P)
+        return blk.transpose(-1, -2).contiguous().reshape(*lead, L * P)
+    parts = [plane[..., q:q + LINE_BLOCK, :].transpose(-1, -2).reshape(*lead, -1)
+             for q in range(0, L, LINE_BLOCK)]
+    return torch.cat(parts, dim=-1)
+
+
+def _unblock_lines(flat, L, P):
+    import torch
+    lead = flat.shape[:-1]
+    if L % LINE_BLOCK == 0:
+        blk = flat.reshape(*lead, L // LINE_BLOCK, P, LINE_BLOCK)
+        return blk.transpose(-1, -2).contiguous().reshape(*lead, L, P)
+    parts, off = [], 0
+    for q in range(0, L, LINE_BLOCK):
+        n = min(LINE_BLOCK, L - q)
+        parts.append(flat[..., off:off + n * P].reshape(*lead, P, n).transpose(-1, -2))
+        off += n * P
+    return torch.cat(parts, dim=-2)
+
+
+def to_line_major(t, direction: int):
+    """Pixel-major per-direction tensor [D, ..., H, W] -> blocked line-major [D, ..., H*W].
+
+    The lines a direction scans are storage rows (vertical directions) or
+    storage columns (horizontal ones).  Each plane stores its lines in blocks
+    of 8 consecutive lines; inside a block the values of one line position
+    are adjacent: line l, position p sits at 8*P*(l//8) + n*p + l%8 with
+    n = min(8, L - 8*(l//8)).  A producer can also write this layout directly.
     """
     import torch
     bits = [b for b in (T2B, B2T, L2R, R2L) if direction & b]
-    H, W = t.shape[-2:]
     out = []
     for s, b in enumerate(bits):
         p = t[s] if b in (T2B, B2T) else t[s].transpose(-1, -2)
-        out.append(p.contiguous().reshape(*t.shape[1:-2], H * W))
+        out.append(_block_lines(p))
     return torch.stack(out)
 
 
@@ -185,7 +217,7 @@ def from_line_major(t, direction: int, H: int, W: int):
     out = []
     for s, b in enumerate(bits):
         if b in (T2B, B2T):
-            out.append(t[s].reshape(*t.shape[1:-1], H, W))
+            out.append(_unblock_lines(t[s], H, W))
         else:
-            out.append(t[s].reshape(*t.shape[1:-1], W, H).transpose(-1, -2))
+            out.append(_unblock_lines(t[s], W, H).transpose(-1, -2))
     return torch.stack(out).contiguous()

@@ -43,34 +43,50 @@ __device__ __forceinline__ float from_right(float v)
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), ctrl, 0xf, 0xf, true));
 }
 
+// Per-direction planes (lam, u, w and their gradients) are blocked
+// line-major: the lines a direction scans (storage rows for vertical
+// directions, storage columns for horizontal ones) are grouped in blocks of
+// 8 consecutive lines, and inside a block the 8 values of one line position
+// are adjacent.  Offset of (line l, position p) in a plane of L lines of P
+// positions; the last block holds L - 8*(L/8) lines when L is not a multiple
+// of 8.
+constexpr int kLineBlock = 8;
+
+__host__ __device__ __forceinline__ int lm_offset(int l, int p, int L, int P)
+{
+    const int q = l >> 3;
+    const int n = L - 8 * q < 8 ? L - 8 * q : 8;
+    return 8 * P * q + n * p + (l & 7);
+}
+
 // Direction index d (direction bit 1 << d), frame position (step i, line
 // position j):
-//   pixel offset      e0 + i * es  in an H x W plane whose rows are `pitch`
-//                                  elements apart (pitch = W in global memory,
-//                                  padded in LDS);
-//   line-major offset d0 + i * ds  in a per-direction plane, where every
-//                                  scanned line is contiguous (rows for
-//                                  vertical directions, columns for
-//                                  horizontal ones).
+//   pixel offset  e0 + i * es  in an H x W plane whose rows are `pitch`
+//                              elements apart (pitch = W in global memory,
+//                              padded in LDS);
+//   lm(i)                      blocked line-major offset in a per-direction
+//                              plane.
 struct Frame {
     int L;        // scan length
     int P;        // line length
     int e0, es;   // pixel offset of (0, j), change per step
-    int d0, ds;   // line-major offset of (0, j), change per step
+    int j;        // line position
+    bool rev;     // the scan visits storage lines in decreasing order
+    __device__ __forceinline__ int line(int i) const { return rev ? L - 1 - i : i; }
+    __device__ __forceinline__ int lm(int i) const { return lm_offset(line(i), j, L, P); }
+    __device__ __forceinline__ int lm_at(int i, int jj) const { return lm_offset(line(i), jj, L, P); }
 };
 
 __device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitch)
 {
     Frame f;
+    f.j = j;
+    f.rev = d == 1 || d == 3;
     switch (d) {
-    case 0:  f.L = H; f.P = W; f.e0 = j;                   f.es = pitch;
-             f.d0 = j;                   f.ds = W;   break;  // T2B
-    case 1:  f.L = H; f.P = W; f.e0 = (H - 1) * pitch + j; f.es = -pitch;
-             f.d0 = (H - 1) * W + j;     f.ds = -W;  break;  // B2T
-    case 2:  f.L = W; f.P = H; f.e0 = j * pitch;           f.es = 1;
-             f.d0 = j;                   f.ds = H;   break;  // L2R
-    default: f.L = W; f.P = H; f.e0 = j * pitch + (W - 1); f.es = -1;
-             f.d0 = (W - 1) * H + j;     f.ds = -H;  break;  // R2L
+    case 0:  f.L = H; f.P = W; f.e0 = j;                   f.es = pitch; break;  // T2B
+    case 1:  f.L = H; f.P = W; f.e0 = (H - 1) * pitch + j; f.es = -pitch; break; // B2T
+    case 2:  f.L = W; f.P = H; f.e0 = j * pitch;           f.es = 1;     break;  // L2R
+    default: f.L = W; f.P = H; f.e0 = j * pitch + (W - 1); f.es = -1;    break;  // R2L
     }
     return f;
 }

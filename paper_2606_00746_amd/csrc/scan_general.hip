@@ -55,7 +55,7 @@ __global__ __launch_bounds__(kThreads) void fwd_general_kernel(
         for (int j = threadIdx.x; j < P; j += blockDim.x) {
             const Frame f = make_frame(d, j, H, W, W);
             const int e = f.e0 + i * f.es;   // pixel (x, y slots)
-            const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+            const int q = f.lm(i);           // line-major (lam, u, w)
             float v = load_f(lp + q) * load_f(xp + e);
             if (i > 0) {
                 v = fmaf(load_f(wp + HW + q), prev[j], v);
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
                 const Frame f = make_frame(d, j, H, W, W);
                 const int e = f.e0 + i * f.es;
-                const int q = f.d0 + i * f.ds;
+                const int q = f.lm(i);
                 float v = load_f(lp + q) * load_f(xp + e);
                 if (i > 0) {
                     const float *prev = hs + (i - 1) * P;
@@ -144,17 +144,15 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
                 const Frame f = make_frame(d, j, H, W, W);
                 const int e = f.e0 + i * f.es;   // pixel (x, dy, dx slots)
-                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w, dlam, du, dw)
+                const int q = f.lm(i);           // line-major (lam, u, w, dlam, du, dw)
                 const float dyv = load_f(dyp + e);
                 float a = load_f(up + q) * dyv;
                 if (i + 1 < L) {
-                    // line i+1 is contiguous: position j' sits at qn + (j' - j)
-                    const int qn = q + f.ds;
-                    a = fmaf(load_f(wp + HW + qn), next[j], a);
+                    a = fmaf(load_f(wp + HW + f.lm(i + 1)), next[j], a);
                     if (j + 1 < P)   // target j+1 on line i+1 reads j through its tap 0
-                        a = fmaf(load_f(wp + qn + 1), next[j + 1], a);
+                        a = fmaf(load_f(wp + f.lm_at(i + 1, j + 1)), next[j + 1], a);
                     if (j > 0)       // target j-1 on line i+1 reads j through its tap 2
-                        a = fmaf(load_f(wp + 2 * HW + qn - 1), next[j - 1], a);
+                        a = fmaf(load_f(wp + 2 * HW + f.lm_at(i + 1, j - 1)), next[j - 1], a);
                 }
                 cur[j] = a;
                 const float hv = hs[i * P + j];

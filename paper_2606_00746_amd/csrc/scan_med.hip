@@ -1,6 +1,6 @@
-// Line scans for bf16 planes of a compile-time shape (H, W <= 64, multiples
-// of 8), with per-direction tensors in line-major layout (every scanned line
-// contiguous) and x, y, dx, dy pixel-major.
+// Line scans for bf16 planes of a compile-time shape (H = W = 56 or 64), with
+// per-direction tensors in blocked line-major layout (8-line blocks, the 8
+// values of one line position adjacent) and x, y, dx, dy pixel-major.
 //
 // Lane layout: one lane per position of a line (the perpendicular axis), one
 // line per wave, h in a VGPR for the whole scan, DPP for the two neighbours of
@@ -9,32 +9,33 @@
 // grid, so ignored taps may hold any value.
 //
 // Every global access reads or writes whole 128-byte lines: on this GPU the
-// cost of a load is set by the lines it touches, not by its bytes, so a
-// per-lane 16-byte access that straddles 64 different lines runs at a sixth
-// of the bandwidth of a coalesced one.
+// cost of a load is set by the lines it touches, not by its bytes.  With the
+// blocked layout one coalesced 16-byte load gives a lane its position on 8
+// consecutive lines of a tensor, so each per-direction stream costs one load
+// (or store) instruction per 8 steps.
 //
 // Forward (one workgroup = one channel plane, one wave per direction):
 //  * the x plane is loaded once, coalesced, into LDS and read from there by
 //    all four directions (rows for vertical scans, columns for horizontal);
-//  * each wave streams its lam, u and w lines in blocks of 8 lines with
-//    16-byte coalesced loads (two blocks in flight in registers) and turns a
-//    block around through a small per-wave LDS buffer, one bf16 per lane per
-//    line;
+//  * each wave streams its lam, u and w blocks into registers, two blocks
+//    ahead of use;
 //  * u_d * h_d stays in registers; the four directions are summed in
 //    direction-bit order through an fp32 LDS plane and y is stored once.
 //
 // Backward (one workgroup = `cw` channels of one weight group, one wave per
 // channel, directions one after another, waves in lock-step):
-//  * horizontal directions first: each wave loads its x and dy planes
-//    coalesced, turns them around through its own LDS dx plane (still free)
-//    into registers holding its row, then scans;
-//  * vertical directions read x and dy rows directly;
+//  * horizontal directions first: each wave stages its x and dy planes in its
+//    own LDS plane (one dword per pixel) and reads columns from there; their
+//    dx terms collect in registers (this lane's row) and then seed the plane
+//    as an fp32 dx accumulator for the vertical directions, which read x and
+//    dy rows from global memory;
 //  * per direction a reverse sweep computes the adjoint a_i (kept in
-//    registers), then a forward sweep recomputes h_i and forms du, dlam, dx
-//    (an fp32 LDS plane per channel) and the weight-gradient terms
-//    a_i * h_{i-1}[j+k-1], summed over the workgroup's channels through LDS
-//    once per step; when a group spans several workgroups the sums go to
-//    fp32 partials that a second kernel adds in fixed order.
+//    registers), then a forward sweep recomputes h_i and forms du, dlam
+//    (stored once per 8-line block), dx, and the weight-gradient terms
+//    a_i * h_{i-1}[j+k-1], which are summed over the workgroup's channels
+//    through double-buffered LDS slots, one barrier per two steps; when a
+//    group spans several workgroups the sums go to fp32 partials that a
+//    second kernel adds in fixed order.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -46,12 +47,12 @@ constexpr uint32_t kSelLo = 0x01000C0Cu;   // bf16 in bits [15:0]  -> fp32
 constexpr uint32_t kSelHi = 0x03020C0Cu;   // bf16 in bits [31:16] -> fp32
 constexpr uint32_t kSelZero = 0x0C0C0C0Cu; // -> +0.0f
 constexpr int kYPitch = 68;                // fp32 LDS row pitch (16-byte rows, conflict-free b128)
-constexpr int kDxPitch = 65;               // fp32 LDS row pitch for per-step dx (odd: column walks conflict-free)
-constexpr int kPrefetch = 8;               // steps of per-step loads in flight (backward)
+constexpr int kDxPitch = 65;               // fp32 LDS row pitch of the dx plane (odd: column walks conflict-free)
+constexpr int kPrefetch = 8;               // steps of per-step row loads in flight (backward)
 
 // Keep the software pipeline as written: nothing is scheduled across a step
-// boundary, so each step's prefetch stays kPrefetch steps ahead of its use
-// instead of every load of the unrolled scan being hoisted to the top.
+// boundary, so each step's prefetch stays ahead of its use instead of every
+// load of the unrolled scan being hoisted to the top.
 __device__ __forceinline__ void step_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Workgroup barrier that orders LDS only.  __syncthreads() also orders global
@@ -79,8 +80,7 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
     const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
     void *q = reinterpret_cast<void *>((static_cast<uint64_t>(hi) << 32) | lo);
     return __builtin_amdgcn_make_buffer_rsrc(q, (short)0,
-                                             (int)__builtin_amdgcn_readfirstlane(bytes),
-                                             kRsrcWord3);
+                                             (int)__builtin_amdgcn_readfirstlane(bytes), kRsrcWord3);
 }
 __device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
 {
@@ -91,19 +91,50 @@ __device__ __forceinline__ uint4 ld128(rsrc_t r, uint32_t voff, uint32_t soff)
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
-__device__ __forceinline__ void st16(rsrc_t r, uint32_t voff, uint32_t soff, uint16_t v)
+// Stores go through inline assembly, each wide one together with the wait
+// states after it.  A VALU write to a VGPR that a wide store still has to
+// read (its data registers are read after issue, later still when it queues
+// behind another store) corrupts the stored value in some lanes; this
+// compiler inserts no wait states for that on gfx950, and its register
+// allocator can place such a write (a copy) directly after the store, where
+// no scheduling barrier reaches.  One asm block keeps the two together.
+// Store targets use a raw buffer descriptor held in SGPRs as four words.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 make_sdesc(const void *p, uint32_t bytes)
 {
-    __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    u32x4 d;
+    d.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+    d.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32)) & 0xffffu;  // stride 0
+    d.z = __builtin_amdgcn_readfirstlane(bytes);
+    d.w = kRsrcWord3;
+    return d;
 }
-__device__ __forceinline__ void st32f(rsrc_t r, uint32_t voff, uint32_t soff, float v)
+__device__ __forceinline__ void st32(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
 {
-    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, soff, 0);
+    asm volatile("buffer_store_dword %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
+                 : "memory");
 }
-__device__ __forceinline__ void st128(rsrc_t r, uint32_t voff, uint32_t soff, uint4 v)
+__device__ __forceinline__ void st64(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t a,
+                                     uint32_t b)
 {
-    typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-    u4 t = {v.x, v.y, v.z, v.w};
-    __builtin_amdgcn_raw_buffer_store_b128(t, r, voff, soff, 0);
+    const u32x2 t = {a, b};
+    asm volatile("buffer_store_dwordx2 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void st128(const u32x4 &d, uint32_t voff, uint32_t soff, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void gst128(uint4 *p, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 7\n\ts_nop 7" : : "v"(p), "v"(t)
+                 : "memory");
 }
 
 __device__ __forceinline__ float widen(uint32_t v, uint32_t sel)
@@ -115,35 +146,30 @@ __device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 
 
 __device__ __forceinline__ uint32_t pack2(float lo, float hi)
 {
-    typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-    bf2 p;
-    p.x = static_cast<__bf16>(lo);
-    p.y = static_cast<__bf16>(hi);
-    return __builtin_bit_cast(uint32_t, p);
-}
-__device__ __forceinline__ uint16_t pack1(float v)
-{
-    return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
+    // two fp32 -> bf16 (RNE) in one v_cvt_pk_bf16_f32
+    const __bf16 a = static_cast<__bf16>(lo);
+    const __bf16 b = static_cast<__bf16>(hi);
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
+           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
 }
 
-template <int K>
-__device__ __forceinline__ uint32_t comp(const uint4 &v)
+// Component k (0..3) of a 16-byte piece; k is a constant once unrolled.
+__device__ __forceinline__ uint32_t part(const uint4 &v, int k)
 {
-    static_assert(K >= 0 && K < 4, "component");
-    return K == 0 ? v.x : (K == 1 ? v.y : (K == 2 ? v.z : v.w));
+    return k == 0 ? v.x : (k == 1 ? v.y : (k == 2 ? v.z : v.w));
 }
 
-// Element E (0..7) of a 16-byte chunk of 8 bf16, widened with the selector
-// pair (lo, hi) of the lane.
-template <int E>
-__device__ __forceinline__ float elem(const uint4 &v, uint32_t sel_lo, uint32_t sel_hi)
+// Element e (0..7) of a lane's 8-line piece (the lane's position on lines
+// 8q..8q+7 of a block), widened with the selector pair of the lane, or
+// unmasked.
+__device__ __forceinline__ float elem(const uint4 &v, int e, uint32_t sel_lo, uint32_t sel_hi)
 {
-    return widen(comp<E / 2>(v), (E & 1) ? sel_hi : sel_lo);
+    return widen(part(v, e >> 1), (e & 1) ? sel_hi : sel_lo);
 }
-template <int E>
-__device__ __forceinline__ float elem(const uint4 &v)
+__device__ __forceinline__ float elem(const uint4 &v, int e)
 {
-    return (E & 1) ? bf_hi(comp<E / 2>(v)) : bf_lo(comp<E / 2>(v));
+    const uint32_t d = part(v, e >> 1);
+    return (e & 1) ? bf_hi(d) : bf_lo(d);
 }
 
 // Workgroups go to the 8 XCDs round-robin by blockIdx.  Give each XCD a
@@ -206,64 +232,57 @@ __device__ __forceinline__ uint32_t lds_u16(const uint8_t *base, uint32_t byte_o
 {
     return *reinterpret_cast<const uint16_t *>(base + byte_off);
 }
+__device__ __forceinline__ uint32_t lds_u32(const uint8_t *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const uint32_t *>(base + byte_off);
+}
 
 // ---------------------------------------------------------------------------
 // forward
 // ---------------------------------------------------------------------------
 
 // One direction's scan over one channel plane.  D: direction index (0 T2B,
-// 1 B2T, 2 L2R, 3 R2L).  lam, u: line-major channel planes; w: the 3 tap
-// planes; xs: the bf16 x plane in LDS; blk: this wave's block buffer
-// (5 tensors x 8 lines x P bf16).
+// 1 B2T, 2 L2R, 3 R2L).  lam, u: the channel's blocked line-major planes; w:
+// the 3 tap planes; xs: the bf16 x plane in LDS.
 template <int H, int W, int D>
 __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t w,
-                                             const uint8_t *xs, uint8_t *blk, float (&yr)[64])
+                                             const uint8_t *xs, float (&yr)[64])
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;                 // blocks of 8 lines
-    constexpr uint32_t TB = 16 * P;           // bytes of one tensor in one block
+    constexpr uint32_t TB = 16 * P;           // bytes of one block of a plane
     constexpr uint32_t PL = 2 * H * W;        // bytes of one plane
     const Sel s = make_sel(j, P);
     const int jc = j < P ? j : P - 1;
-    const bool ld = j < P;                    // lanes that load a 16-byte piece of a block
-    const uint32_t vo = 16u * (uint32_t)(ld ? j : 0);
-    // block b covers lines [8b', 8b'+8) with b' = b (forward) or NB-1-b (reverse)
-    auto boff = [](int b) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - b : b); };
+    const uint32_t vo = 16u * (uint32_t)jc;   // this lane's piece of a block
+    // frame block fb (steps 8fb..8fb+7) is storage block fb, or NB-1-fb when
+    // the scan runs against the storage order
+    auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
     uint4 rl[NB], ru[NB], r0[NB], r1[NB], r2[NB];
-#define FLOAD(b)                                                     \
+#define FLOAD(fb)                                                    \
     do {                                                             \
-        const uint32_t so_ = boff(b);                                \
-        rl[b] = ld128(lam, vo, so_);                                 \
-        ru[b] = ld128(u, vo, so_);                                   \
-        r0[b] = ld128(w, vo, so_);                                   \
-        r1[b] = ld128(w, vo, so_ + PL);                              \
-        r2[b] = ld128(w, vo, so_ + 2 * PL);                          \
+        const uint32_t so_ = boff(fb);                               \
+        rl[fb] = ld128(lam, vo, so_);                                \
+        ru[fb] = ld128(u, vo, so_);                                  \
+        r0[fb] = ld128(w, vo, so_);                                  \
+        r1[fb] = ld128(w, vo, so_ + PL);                             \
+        r2[fb] = ld128(w, vo, so_ + 2 * PL);                         \
     } while (0)
     FLOAD(0);
     if (NB > 1)
         FLOAD(1);
     float h = 0.f;
-    uint4 *bw = reinterpret_cast<uint4 *>(blk) + j;   // this lane's 16-byte slot
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-        // turn block b around: lane j wrote piece j of each tensor's 8 lines
-        if (ld) {
-            bw[0 * TB / 16] = rl[b];
-            bw[1 * TB / 16] = ru[b];
-            bw[2 * TB / 16] = r0[b];
-            bw[3 * TB / 16] = r1[b];
-            bw[4 * TB / 16] = r2[b];
-        }
-        if (b + 2 < NB)
-            FLOAD(b + 2);
+    for (int fb = 0; fb < NB; ++fb) {
+        if (fb + 2 < NB)
+            FLOAD(fb + 2);
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            const int i = 8 * b + t;
-            const int ln = REV ? 7 - t : t;                     // line within the block
-            const uint32_t lo = 2u * (uint32_t)(ln * P + jc);   // this lane's bf16 in a tensor's block
-            const float lv = widen(lds_u16(blk, lo), s.lo1);
-            const float uv = bf_lo(lds_u16(blk, TB + lo));
+            const int i = 8 * fb + t;
+            const int e = REV ? 7 - t : t;                      // element of the piece
+            const float lv = elem(rl[fb], e, s.lo1, s.hi1);
+            const float uv = elem(ru[fb], e);
             const int row = VERT ? (REV ? H - 1 - i : i) : jc;
             const int col = VERT ? jc : (REV ? W - 1 - i : i);
             const float xv = bf_lo(lds_u16(xs, row * XPlane<W>::kPitchB + 2 * col));
@@ -271,9 +290,8 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
             if (i == 0)
                 h = inj;
             else
-                h = tri_step(h, widen(lds_u16(blk, 2 * TB + lo), s.lo0),
-                             widen(lds_u16(blk, 3 * TB + lo), s.lo1),
-                             widen(lds_u16(blk, 4 * TB + lo), s.lo2), inj);
+                h = tri_step(h, elem(r0[fb], e, s.lo0, s.hi0), elem(r1[fb], e, s.lo1, s.hi1),
+                             elem(r2[fb], e, s.lo2, s.hi2), inj);
             yr[i] = uv * h;
         }
         step_fence();
@@ -282,23 +300,20 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
 }
 
 template <int H, int W>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) void fwd_med_kernel(
+__global__ __launch_bounds__(256) void fwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0, "shape");
     constexpr int HW = H * W;
     constexpr int XB = H * XPlane<W>::kPitchB;              // x plane bytes
-    constexpr int PMAX = H > W ? H : W;
-    constexpr int BLK = 5 * 16 * PMAX;                      // block buffer bytes per wave
     constexpr int YB = H * kYPitch * 4;                     // merge plane bytes
-    static_assert(YB <= 4 * BLK, "merge plane reuses the block buffers");
-    __shared__ float4 lds4[(XB + 4 * BLK + 15) / 16];
-    uint8_t *lds = reinterpret_cast<uint8_t *>(lds4);
-    uint8_t *xs = lds;
-    uint8_t *blks = lds + (XB + 15) / 16 * 16;
-    float4 *Y4 = reinterpret_cast<float4 *>(blks);           // after the scans
-    float *Y = reinterpret_cast<float *>(Y4);
+    constexpr int LB = XB > YB ? XB : YB;
+    // the merge plane replaces the x plane once every scan has finished
+    __shared__ float4 lds4[(LB + 15) / 16];
+    uint8_t *xs = reinterpret_cast<uint8_t *>(lds4);
+    float4 *Y4 = lds4;
+    float *Y = reinterpret_cast<float *>(lds4);
 
     const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
@@ -332,17 +347,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         const rsrc_t rl = make_rsrc(lam + pd, 2 * HW);
         const rsrc_t ru = make_rsrc(u + pd, 2 * HW);
         const rsrc_t rw = make_rsrc(w + pw, 6 * HW);
-        uint8_t *myblk = blks + d * BLK;
         if (d == 0)
-            scan_fwd_dir<H, W, 0>(lane, rl, ru, rw, xs, myblk, yr);
+            scan_fwd_dir<H, W, 0>(lane, rl, ru, rw, xs, yr);
         else if (d == 1)
-            scan_fwd_dir<H, W, 1>(lane, rl, ru, rw, xs, myblk, yr);
+            scan_fwd_dir<H, W, 1>(lane, rl, ru, rw, xs, yr);
         else if (d == 2)
-            scan_fwd_dir<H, W, 2>(lane, rl, ru, rw, xs, myblk, yr);
+            scan_fwd_dir<H, W, 2>(lane, rl, ru, rw, xs, yr);
         else
-            scan_fwd_dir<H, W, 3>(lane, rl, ru, rw, xs, myblk, yr);
+            scan_fwd_dir<H, W, 3>(lane, rl, ru, rw, xs, yr);
     }
-    lds_barrier();   // block buffers become the merge plane
+    lds_barrier();   // the x plane becomes the merge plane
 
     // Sum the directions in bit order through LDS: the first present one
     // stores, the others add, one direction per phase.
@@ -384,7 +398,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
         lds_barrier();
     }
 
-    const rsrc_t yo = make_rsrc(y + pc, 2 * HW);
+    const u32x4 yo = make_sdesc(y + pc, 2 * HW);
     for (int t = threadIdx.x; t < H * (W / 8); t += 256) {
         const int r = t / (W / 8);
         const int cm = t - r * (W / 8);
@@ -399,235 +413,293 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4, 8))) voi
 // backward
 // ---------------------------------------------------------------------------
 
+// Per-step dw terms are summed over the workgroup's channels through LDS
+// slots[buf][st][k][q][j]: two buffers of kBatch steps, 3 taps, kSlots channel
+// slots (slots of absent channels stay zero) and 64 positions.  A wave writes
+// one contiguous row per tap; a reducing lane reads its kSlots slots, all
+// conflict-free.  After the barrier that closes a batch the reducing lanes
+// read it, and they sum and store it while the next batch runs.
+constexpr int kSlots = 8;
+constexpr int kBatch = 2;
+constexpr int kSlotFloats = 2 * kBatch * 3 * kSlots * 64;
+
+__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int st, int k, int q)
+{
+    return slots + (((buf * kBatch + st) * 3 + k) * kSlots + q) * 64;
+}
+
 struct BwdArgs {
     rsrc_t x, dy;          // channel planes (pixel-major)
-    rsrc_t lam, u;         // direction planes (line-major)
+    rsrc_t lam, u;         // direction planes (blocked line-major)
     rsrc_t w;              // the 3 tap planes of (direction, group)
-    rsrc_t dlam, du;       // direction planes
-    rsrc_t dw;             // 3 tap planes: final bf16 dw or fp32 partial
+    u32x4 dlam, du;        // direction planes (store descriptors)
+    u32x4 dw;              // 3 tap planes: final bf16 dw or fp32 partial
     float *Xq;             // this wave's dx plane in LDS, [H][kDxPitch]
-    float *slots;          // [2][cw][3][64] per-step dw terms
-    int wave, nwaves, nvalid, cw;
+    float *slots;          // dw term slots
+    int wave;
     bool partial;          // dw holds fp32 partials
-    bool first;            // first direction processed: store dx, don't add
+    bool first;            // first direction adding into the dx plane: store
 };
 
-// Per-step dw terms live in LDS as slots[buf][k][q][j] (q = channel slot of
-// the workgroup, 8 slots, absent channels zero): a wave writes one
-// contiguous row per tap and a reducing lane reads its 8 slots, all
-// conflict-free.
-constexpr int kSlots = 8;   // channel slots per (tap, position)
-
-__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int k, int q)
-{
-    return slots + ((buf * 3 + k) * kSlots + q) * 64;
-}
-
-// While the horizontal directions run, a wave's LDS dx plane holds x and dy
-// interleaved: one dword per pixel (x in bits [15:0], dy in [31:16]) at row
-// pitch kDxPitch, so one conflict-free read per step returns both.
-__device__ __forceinline__ uint32_t lds_u32(const uint8_t *base, uint32_t byte_off)
-{
-    return *reinterpret_cast<const uint32_t *>(base + byte_off);
-}
-
-// One direction of the backward.  D: direction index.  Horizontal directions
-// read x and dy from the staged planes `stg` (x then dy, bf16, odd pitch) and
-// add their dx terms to dxr (this lane's row); vertical directions read x
-// and dy rows from global memory and add dx into the LDS dx plane.
-template <int H, int W, int D>
+// One direction of the backward.  D: direction index.  U: reduction layout:
+// U = 1 when the workgroup has at least 4 waves (waves 0..3 each reduce 48 of
+// the 192 (tap, position) pairs of a step, one wave per SIMD), U = 3 when it
+// has fewer (wave 0 reduces all of them, one tap per pass).  Horizontal
+// directions read x and dy from the staged plane `stg` and add their dx
+// terms to dxr (this lane's row); vertical directions read x and dy rows from
+// global memory and add dx into the LDS dx plane.
+template <int H, int W, int D, int U>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
-    constexpr uint32_t PL2 = 2 * H * W;                  // bytes of one bf16 plane
-    const Sel s = make_sel(cvalid ? j : 64, P);          // an idle wave computes zeros
+    constexpr int NB = L / 8;
+    constexpr uint32_t TB = 16 * P;                     // bytes of one block of a bf16 plane
+    constexpr uint32_t PL2 = 2 * H * W;                 // bytes of one bf16 plane
+    const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
-    const uint32_t vo = 2u * (uint32_t)jj;               // line-major lane offset (bf16)
-    // line-major byte offset of line(i); pixel offset of a vertical row
-    auto lnoff = [](int i) -> uint32_t { return 2u * (uint32_t)((REV ? L - 1 - i : i) * P); };
-    auto col_of = [](int i) { return REV ? L - 1 - i : i; };   // storage row/col scanned at step i
+    const uint32_t vo = 16u * (uint32_t)jj;             // this lane's piece of a block
+    const uint32_t vr = 2u * (uint32_t)jj;              // this lane's bf16 of a pixel row
+    auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
+    auto line_of = [](int i) { return REV ? L - 1 - i : i; };   // storage line of step i
+    auto rowoff = [&](int i) -> uint32_t { return 2u * (uint32_t)(line_of(i) * W); };
+    auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + line_of(i))); };
 
     // --- reverse sweep: adjoint a_i -------------------------------------
     float ahist[L];
     uint32_t pdy[VERT ? L / 2 : 1];
     {
-        uint32_t ru[L], rd[VERT ? L : 1], r0[L], r1[L], r2[L];
-#define ALOAD(i)                                                     \
+        uint4 ru[NB], q0[NB], q1[NB], q2[NB];
+        uint32_t rd[VERT ? L : 1];
+#define RLOAD(fb)                                                    \
     do {                                                             \
-        const uint32_t so_ = lnoff(i);                               \
-        ru[i] = ld16(A.u, vo, so_);                                  \
-        if (VERT)                                                    \
-            rd[VERT ? (i) : 0] = ld16(A.dy, vo, so_);                \
-        if ((i) + 1 < L) {                                           \
-            const uint32_t sn_ = lnoff((i) + 1);                     \
-            r0[i] = ld16(A.w, vo, sn_);                              \
-            r1[i] = ld16(A.w, vo, sn_ + PL2);                        \
-            r2[i] = ld16(A.w, vo, sn_ + 2 * PL2);                    \
-        }                                                            \
+        const uint32_t so_ = boff(fb);                               \
+        ru[fb] = ld128(A.u, vo, so_);                                \
+        q0[fb] = ld128(A.w, vo, so_);                                \
+        q1[fb] = ld128(A.w, vo, so_ + PL2);                          \
+        q2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
     } while (0)
+        RLOAD(NB - 1);
+        if (NB > 1)
+            RLOAD(NB - 2);
+        if (VERT) {
 #pragma unroll
-        for (int i = L - 1; i >= L - kPrefetch && i >= 0; --i)
-            ALOAD(i);
+            for (int i = L - 1; i >= L - kPrefetch; --i)
+                rd[VERT ? i : 0] = ld16(A.dy, vr, rowoff(i));
+        }
         float an = 0.f;
         // horizontal directions: the staged (x, dy) dword of the next step is
         // read one step ahead so its LDS latency overlaps the arithmetic
-        auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i))); };
         uint32_t xd_next = VERT ? 0u : stg_at(L - 1);
 #pragma unroll
-        for (int i = L - 1; i >= 0; --i) {
-            if (i - kPrefetch >= 0)
-                ALOAD(i - kPrefetch);
-            float dyv;
-            if (VERT) {
-                dyv = bf_lo(rd[VERT ? i : 0]);
-            } else {
-                dyv = bf_hi(xd_next);
-                if (i > 0)
-                    xd_next = stg_at(i - 1);
+        for (int fb = NB - 1; fb >= 0; --fb) {
+            if (fb >= 2)
+                RLOAD(fb - 2);
+#pragma unroll
+            for (int t = 7; t >= 0; --t) {
+                const int i = 8 * fb + t;
+                if (VERT && i - kPrefetch >= 0)
+                    rd[VERT ? i - kPrefetch : 0] = ld16(A.dy, vr, rowoff(i - kPrefetch));
+                float dyv;
+                if (VERT) {
+                    dyv = bf_lo(rd[VERT ? i : 0]);
+                } else {
+                    dyv = bf_hi(xd_next);
+                    if (i > 0)
+                        xd_next = stg_at(i - 1);
+                }
+                const int e = REV ? 7 - t : t;
+                const float inj = elem(ru[fb], e, s.lo1, s.hi1) * dyv;
+                float a;
+                if (i + 1 == L) {
+                    a = inj;
+                } else {
+                    // taps of step i+1 (the next block's first line for t = 7)
+                    const int fn = (i + 1) >> 3, tn = (i + 1) & 7;
+                    const int en = REV ? 7 - tn : tn;
+                    a = tri_step_t(an, elem(q0[fn], en, s.lo0, s.hi0),
+                                   elem(q1[fn], en, s.lo1, s.hi1), elem(q2[fn], en, s.lo2, s.hi2),
+                                   inj);
+                }
+                ahist[i] = a;
+                an = a;
+                if (VERT && (i & 1) == 0)
+                    pdy[VERT ? i >> 1 : 0] =
+                        __builtin_amdgcn_perm(rd[VERT ? i + 1 : 0], rd[VERT ? i : 0], 0x05040100u);
+                step_fence();
             }
-            const float inj = widen(ru[i], s.lo1) * dyv;
-            float a;
-            if (i + 1 == L)
-                a = inj;
-            else
-                a = tri_step_t(an, widen(r0[i], s.lo0), widen(r1[i], s.lo1), widen(r2[i], s.lo2),
-                               inj);
-            ahist[i] = a;
-            an = a;
-            if (VERT && (i & 1) == 0)
-                pdy[VERT ? i >> 1 : 0] =
-                    __builtin_amdgcn_perm(rd[VERT ? i + 1 : 0], rd[VERT ? i : 0], 0x05040100u);
-            step_fence();
         }
-#undef ALOAD
+#undef RLOAD
     }
 
     // --- forward sweep: states, local gradients, dw terms ---------------
-    uint32_t rx[VERT ? L : 1], rl[L], r0[L], r1[L], r2[L];
-#define BLOAD(i)                                                     \
+    uint4 rl[NB], p0[NB], p1[NB], p2[NB];
+    uint32_t rx[VERT ? L : 1];
+#define FLOADB(fb)                                                   \
     do {                                                             \
-        const uint32_t so_ = lnoff(i);                               \
-        if (VERT)                                                    \
-            rx[VERT ? (i) : 0] = ld16(A.x, vo, so_);                 \
-        rl[i] = ld16(A.lam, vo, so_);                                \
-        if ((i) > 0) {                                               \
-            r0[i] = ld16(A.w, vo, so_);                              \
-            r1[i] = ld16(A.w, vo, so_ + PL2);                        \
-            r2[i] = ld16(A.w, vo, so_ + 2 * PL2);                    \
-        }                                                            \
+        const uint32_t so_ = boff(fb);                               \
+        rl[fb] = ld128(A.lam, vo, so_);                              \
+        p0[fb] = ld128(A.w, vo, so_);                                \
+        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
+        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
     } while (0)
+    FLOADB(0);
+    if (NB > 1)
+        FLOADB(1);
+    if (VERT) {
 #pragma unroll
-    for (int i = 0; i < kPrefetch && i < L; ++i)
-        BLOAD(i);
-    // Reduction of the dw terms of line i over the workgroup's channels:
-    // wave k (< 3) owns tap k.  Its eight slot reads are issued right after
-    // the barrier and summed one step later, in channel order.  With fewer
-    // than three waves the remaining taps are summed at once by wave 0.
-    float pr[kSlots];
-    auto store_dw = [&](int i, int k, float v) {
-        const uint32_t so = lnoff(i);
-        if (j < P) {
-            if (A.partial)
-                st32f(A.dw, 2u * vo, 2u * (so + k * PL2), v);
-            else
-                st16(A.dw, vo, so + k * PL2, pack1(v));
-        }
-    };
+        for (int i = 0; i < kPrefetch; ++i)
+            rx[VERT ? i : 0] = ld16(A.x, vr, rowoff(i));
+    }
+
+    // Reduction roles: pair p = (tap k, position jp) with p = k * 64 + jp.
+    const bool reducer = U == 1 ? (A.wave < 4 && j < 48) : A.wave == 0;
+    float pr[U][kBatch][kSlots];
+    auto pair_of = [&](int uu) { return U == 1 ? 48 * A.wave + j : 64 * uu + j; };
+    // issue the slot reads of the batch that ends at step i
     auto issue_dw = [&](int i) {
-        if (A.wave < 3) {
+        if (reducer) {
+            const int buf = (i >> 1) & 1;
 #pragma unroll
-            for (int q = 0; q < kSlots; ++q)
-                pr[q] = slot_ptr(A.slots, i & 1, A.wave, q)[j];
-        }
-        if (A.nwaves < 3 && A.wave == 0) {
-            for (int k = A.nwaves; k < 3; ++k) {
-                float sum = 0.f;
-                for (int q = 0; q < kSlots; ++q)
-                    sum += slot_ptr(A.slots, i & 1, k, q)[j];
-                store_dw(i, k, sum);
+            for (int uu = 0; uu < U; ++uu) {
+                const int p = pair_of(uu);
+#pragma unroll
+                for (int st = 0; st < kBatch; ++st)
+#pragma unroll
+                    for (int q = 0; q < kSlots; ++q)
+                        pr[uu][st][q] = slot_ptr(A.slots, buf, st, p >> 6, q)[p & 63];
             }
         }
     };
+    // sum (in channel-slot order) and store the batch that ends at step i
     auto flush_dw = [&](int i) {
-        if (A.wave < 3) {
-            float sum = 0.f;
+        if (reducer) {
+            const int i0 = i - 1;                             // first step of the batch
+            const int fb = i0 >> 3, t0 = i0 & 7;
+            const uint32_t sb = (uint32_t)(REV ? NB - 1 - fb : fb);
+            // the pair's storage elements: t0, t0+1, or 7-t0-1, 7-t0 reversed
+            const int e0 = REV ? 6 - t0 : t0;
 #pragma unroll
-            for (int q = 0; q < kSlots; ++q)
-                sum += pr[q];
-            store_dw(i, A.wave, sum);
-        }
-    };
-    float h = 0.f;
-    auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + col_of(i))); };
-    uint32_t xd_next = VERT ? 0u : stg_at(0);
+            for (int uu = 0; uu < U; ++uu) {
+                const int p = pair_of(uu);
+                const int k = p >> 6, jp = p & 63;
+                float sum[kBatch];
 #pragma unroll
-    for (int i = 0; i < L; ++i) {
-        if (i + kPrefetch < L)
-            BLOAD(i + kPrefetch);
-        float xv, dyv;
-        if (VERT) {
-            xv = bf_lo(rx[VERT ? i : 0]);
-            dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
-        } else {
-            const uint32_t xd = xd_next;
-            if (i + 1 < L)
-                xd_next = stg_at(i + 1);
-            xv = bf_lo(xd);
-            dyv = bf_hi(xd);
-        }
-        const float lv = widen(rl[i], s.lo1);
-        const float hp = h;
-        if (i == 0)
-            h = lv * xv;
-        else
-            h = tri_step(hp, widen(r0[i], s.lo0), widen(r1[i], s.lo1), widen(r2[i], s.lo2),
-                         lv * xv);
-        const float a = ahist[i];
-        const uint32_t so = lnoff(i);
-        // dw terms of line i (zero on line 0; taps leaving the grid read zeros)
-        float t0 = 0.f, t1 = 0.f, t2 = 0.f;
-        if (i > 0) {
-            t0 = a * from_left<64>(hp);
-            t1 = a * hp;
-            t2 = a * from_right<64>(hp);
-        }
-        if (act) {
-            st16(A.du, vo, so, pack1(dyv * h));
-            st16(A.dlam, vo, so, pack1(a * xv));
-            if (VERT) {
-                // this wave is the only writer of its dx plane: a returnless
-                // LDS add keeps the order and does not wait
-                float *xa = A.Xq + col_of(i) * kDxPitch + jj;
-                if (A.first)
-                    *xa = a * lv;
-                else
-                    __hip_atomic_fetch_add(xa, a * lv, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_WORKGROUP);
+                for (int st = 0; st < kBatch; ++st) {
+                    float v = 0.f;
+#pragma unroll
+                    for (int q = 0; q < kSlots; ++q)
+                        v += pr[uu][st][q];
+                    sum[st] = v;
+                }
+                const float lo = REV ? sum[1] : sum[0];
+                const float hi = REV ? sum[0] : sum[1];
+                if (jp < P) {
+                    const uint32_t el = 8u * (uint32_t)(P * sb + jp) + (uint32_t)e0;
+                    if (A.partial)
+                        st64(A.dw, 4u * el + 2u * PL2 * (uint32_t)k, 0, __float_as_uint(lo),
+                             __float_as_uint(hi));
+                    else
+                        st32(A.dw, 2u * el + PL2 * (uint32_t)k, 0, pack2(lo, hi));
+                }
             }
         }
-        if (!VERT) {
-            const int cc = col_of(i);
-            dxr[cc] = dx_first ? a * lv : fmaf(a, lv, dxr[cc]);
+    };
+
+    float h = 0.f;
+    // this block's du and dlam as bf16 pairs in storage element order; the
+    // value of the first step of a pair waits in du0 / dl0
+    uint32_t dup[4], dlp[4];
+    float du0 = 0.f, dl0 = 0.f;
+    uint32_t xd_next = VERT ? 0u : stg_at(0);
+    float dx_next = 0.f;     // vertical: dx plane value of this step's row, read a step ahead
+    if (VERT && !A.first)
+        dx_next = A.Xq[line_of(0) * kDxPitch + jj];
+#pragma unroll
+    for (int fb = 0; fb < NB; ++fb) {
+        if (fb + 2 < NB)
+            FLOADB(fb + 2);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int i = 8 * fb + t;
+            const int e = REV ? 7 - t : t;
+            if (VERT && i + kPrefetch < L)
+                rx[VERT ? i + kPrefetch : 0] = ld16(A.x, vr, rowoff(i + kPrefetch));
+            float xv, dyv;
+            if (VERT) {
+                xv = bf_lo(rx[VERT ? i : 0]);
+                dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
+            } else {
+                const uint32_t xd = xd_next;
+                if (i + 1 < L)
+                    xd_next = stg_at(i + 1);
+                xv = bf_lo(xd);
+                dyv = bf_hi(xd);
+            }
+            const float lv = elem(rl[fb], e, s.lo1, s.hi1);
+            const float hp = h;
+            if (i == 0)
+                h = lv * xv;
+            else
+                h = tri_step(hp, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
+                             elem(p2[fb], e, s.lo2, s.hi2), lv * xv);
+            const float a = ahist[i];
+            // dw terms of line i (zero on line 0; taps leaving the grid read zeros)
+            float t0 = 0.f, t1 = 0.f, t2 = 0.f;
+            if (i > 0) {
+                t0 = a * from_left<64>(hp);
+                t1 = a * hp;
+                t2 = a * from_right<64>(hp);
+            }
+            const float duv = dyv * h, dlv = a * xv;
+            if ((t & 1) == 0) {
+                du0 = duv;
+                dl0 = dlv;
+            } else {
+                // steps t-1, t hold elements e+1, e (reverse) or e-1, e
+                dup[e >> 1] = REV ? pack2(duv, du0) : pack2(du0, duv);
+                dlp[e >> 1] = REV ? pack2(dlv, dl0) : pack2(dl0, dlv);
+            }
+            if (VERT) {
+                // this wave is the only writer of its dx plane: the row of the
+                // next step is read one step ahead, added to and written back
+                // (an LDS float atomic costs several times more here)
+                float *xa = A.Xq + line_of(i) * kDxPitch + jj;
+                const float prev = dx_next;
+                if (!A.first && i + 1 < L)
+                    dx_next = A.Xq[line_of(i + 1) * kDxPitch + jj];
+                if (act)
+                    *xa = A.first ? a * lv : fmaf(a, lv, prev);
+            } else {
+                const int cc = line_of(i);
+                dxr[cc] = dx_first ? a * lv : fmaf(a, lv, dxr[cc]);
+            }
+            // finish the previous batch (its slot reads were issued after the
+            // last barrier and overlapped a step and a half of arithmetic)
+            if ((i & 1) == 1 && i >= 3)
+                flush_dw(i - 2);
+            const int buf = (i >> 1) & 1;
+            slot_ptr(A.slots, buf, i & 1, 0, A.wave)[j] = t0;
+            slot_ptr(A.slots, buf, i & 1, 1, A.wave)[j] = t1;
+            slot_ptr(A.slots, buf, i & 1, 2, A.wave)[j] = t2;
+            if ((i & 1) == 1) {
+                lds_barrier();
+                issue_dw(i);
+            }
+            if (t == 7 && act) {
+                st128(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                st128(A.dlam, vo, boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+            }
+            step_fence();
         }
-        // finish the reduction of line i-1 (its slot reads were issued after
-        // the previous barrier and overlapped this step's arithmetic)
-        if (i > 0)
-            flush_dw(i - 1);
-        slot_ptr(A.slots, i & 1, 0, A.wave)[j] = t0;
-        slot_ptr(A.slots, i & 1, 1, A.wave)[j] = t1;
-        slot_ptr(A.slots, i & 1, 2, A.wave)[j] = t2;
-        lds_barrier();
-        issue_dw(i);
-        step_fence();
     }
     flush_dw(L - 1);
-#undef BLOAD
+#undef FLOADB
 }
 
-template <int H, int W>
+template <int H, int W, int U>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -641,7 +713,6 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     float *smem = reinterpret_cast<float *>(smem4);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
-    const int nwaves = blockDim.x >> 6;
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
     const int chunk = blk % nchunk;
     const int bg = blk / nchunk;
@@ -661,13 +732,10 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.Xq = smem + wave * XPLANE;
     A.slots = smem + cw * XPLANE;
     // slots of channels this workgroup does not have must read as zero
-    for (int t = threadIdx.x; t < 2 * 3 * 64 * kSlots; t += blockDim.x)
+    for (int t = threadIdx.x; t < kSlotFloats; t += blockDim.x)
         A.slots[t] = 0.f;
     lds_barrier();
     A.wave = wave;
-    A.nwaves = nwaves;
-    A.nvalid = nvalid;
-    A.cw = cw;
     A.partial = nchunk > 1;
 
     // Horizontal directions read x and dy columns: stage both planes in this
@@ -708,13 +776,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         const int64_t unit = ((int64_t)s * B + b) * G + g;
         A.lam = make_rsrc(lam + pd, 2 * HW);
         A.u = make_rsrc(u + pd, 2 * HW);
-        A.dlam = make_rsrc(dlam + pd, 2 * HW);
-        A.du = make_rsrc(du + pd, 2 * HW);
+        A.dlam = make_sdesc(dlam + pd, 2 * HW);
+        A.du = make_sdesc(du + pd, 2 * HW);
         A.w = make_rsrc(w + unit * 3 * HW, 6 * HW);
         if (A.partial)
-            A.dw = make_rsrc(dwp + ((int64_t)chunk * D * B * G + unit) * 3 * HW, 12 * HW);
+            A.dw = make_sdesc(dwp + ((int64_t)chunk * D * B * G + unit) * 3 * HW, 12 * HW);
         else
-            A.dw = make_rsrc(dw + unit * 3 * HW, 6 * HW);
+            A.dw = make_sdesc(dw + unit * 3 * HW, 6 * HW);
     };
 
     // horizontal directions first (x and dy staged), dx in registers
@@ -722,12 +790,12 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, U>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
-        dir_bwd<H, W, 3>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+        dir_bwd<H, W, 3, U>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz) {
@@ -740,7 +808,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
                     A.Xq[lane * kDxPitch + q] = dxr[q];
             }
         } else if (cvalid && lane < H) {
-            const rsrc_t dxo = make_rsrc(dx + pc, 2 * HW);
+            const u32x4 dxo = make_sdesc(dx + pc, 2 * HW);
 #pragma unroll
             for (int q = 0; q < W / 8; ++q)
                 st128(dxo, 2u * (uint32_t)(lane * W), 16u * q,
@@ -753,19 +821,19 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, U>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, U>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
     if (vert && cvalid && lane < H) {
         const float *Xr = A.Xq + lane * kDxPitch;
-        const rsrc_t dxo = make_rsrc(dx + pc, 2 * HW);
+        const u32x4 dxo = make_sdesc(dx + pc, 2 * HW);
         const uint32_t vo = 2u * (uint32_t)(lane * W);
 #pragma unroll
         for (int q = 0; q < W / 8; ++q) {
@@ -789,7 +857,7 @@ __global__ __launch_bounds__(256) void dw_sum_kernel(const float4 *__restrict__ 
             a = make_float4(a.x + p.x, a.y + p.y, a.z + p.z, a.w + p.w);
             b = make_float4(b.x + q.x, b.y + q.y, b.z + q.z, b.w + q.w);
         }
-        dw[e] = make_uint4(pack2(a.x, a.y), pack2(a.z, a.w), pack2(b.x, b.y), pack2(b.z, b.w));
+        gst128(dw + e, make_uint4(pack2(a.x, a.y), pack2(a.z, a.w), pack2(b.x, b.y), pack2(b.z, b.w)));
     }
 }
 
@@ -799,6 +867,22 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     hipLaunchKernelGGL((fwd_med_kernel<H, W>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
                        (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G);
+    return hipGetLastError();
+}
+
+template <int H, int W, int U>
+hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
+                          float *dwp)
+{
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, U>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, U>), dim3((unsigned)(p.B * p.G * nchunk)),
+                       dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
+                       (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
+                       (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
+                       p.mask, p.B, p.C, p.G, cw, nchunk);
     return hipGetLastError();
 }
 
@@ -814,7 +898,7 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     if (e != hipSuccess)
         return e;
     const size_t per_ch = (size_t)H * kDxPitch * 4;                 // dx plane
-    const size_t slots = (size_t)2 * 3 * 64 * kSlots * 4;           // per-step dw terms
+    const size_t slots = (size_t)kSlotFloats * 4;                   // per-step dw terms
     const int cpg = p.C / p.G;
     int cap = lds_max > (int)slots ? (int)(((size_t)lds_max - slots) / per_ch) : 0;
     cap = cap < kSlots ? cap : kSlots;
@@ -826,22 +910,14 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     const int D = __builtin_popcount(p.mask);
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * H * W;
 
-    e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W>,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess)
-        return e;
     float *dwp = nullptr;
     if (nchunk > 1) {
         e = scratch_alloc((void **)&dwp, (size_t)nchunk * ndw * sizeof(float), st);
         if (e != hipSuccess)
             return e;
     }
-    hipLaunchKernelGGL((bwd_med_kernel<H, W>), dim3((unsigned)(p.B * p.G * nchunk)),
-                       dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
-                       (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
-                       (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
-                       p.mask, p.B, p.C, p.G, cw, nchunk);
-    e = hipGetLastError();
+    e = cw >= 4 ? bwd_med_launch<H, W, 1>(p, st, cw, nchunk, lds, dwp)
+                : bwd_med_launch<H, W, 3>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t n8 = ndw / 8;
         int64_t blocks = (n8 + 255) / 256;

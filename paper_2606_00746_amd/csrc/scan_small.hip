@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
         for (int i = 0; i < T; ++i) {
             if (i < f.L) {
                 const int e = f.e0 + i * f.es;   // pixel (x)
-                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+                const int q = f.lm(i);           // line-major (lam, u, w)
                 float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
         for (int i = 0; i < T; ++i) {
             if (i < L) {
                 const int e = f.e0 + i * f.es;   // pixel (x)
-                const int q = f.d0 + i * f.ds;   // line-major (lam, u, w)
+                const int q = f.lm(i);           // line-major (lam, u, w)
                 float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
@@ -213,11 +213,11 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
         for (int i = T - 1; i >= 0; --i) {
             if (i < L) {
                 const int e = f.e0 + i * f.es;   // pixel (x, dy)
-                const int qd = f.d0 + i * f.ds;  // line-major (lam, u, w, dlam, du)
+                const int qd = f.lm(i);          // line-major (lam, u, w, dlam, du)
                 const float dyv = load_f(dyp + e);
                 float a = load_f(up + qd) * dyv;
                 if (i + 1 < L) {
-                    const int qn = qd + f.ds;
+                    const int qn = f.lm(i + 1);
                     float w0 = load_f(wp + qn);
                     float w1 = load_f(wp + HW + qn);
                     float w2 = load_f(wp + 2 * HW + qn);
@@ -265,7 +265,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
                     for (int qq = 0; qq < nvalid; ++qq)
                         sum += src[qq * 3 * T];
                     const Frame ft = make_frame(d, jj, H, W, W);
-                    const int et = k * HW + ft.d0 + i * ft.ds;
+                    const int et = k * HW + ft.lm(i);
                     const int64_t unit = ((int64_t)s * B + b) * G + g;
                     if (nchunk == 1)
                         store_f(dw + unit * 3 * HW + et, sum);

@@ -101,14 +101,15 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
         _native.load()
 
 
-def test_torch_layout_helpers_match_numpy():
+@pytest.mark.parametrize("H,W", [(5, 6), (16, 24), (13, 20)])
+def test_torch_layout_helpers_match_numpy(H, W):
     import numpy as np
     import torch
     import gspn_inputs as gi
-    a = np.random.default_rng(0).standard_normal((4, 2, 4, 5, 6)).astype(np.float32)
+    a = np.random.default_rng(0).standard_normal((4, 2, 4, H, W)).astype(np.float32)
     for dirs in (15, 7, 12, 1):
         d = bin(dirs).count("1")
         t = torch.from_numpy(a[:d].copy())
         lm = g.to_line_major(t, dirs)
         np.testing.assert_array_equal(lm.numpy(), gi.to_line_major(a[:d], dirs))
-        np.testing.assert_array_equal(g.from_line_major(lm, dirs, 5, 6).numpy(), a[:d])
+        np.testing.assert_array_equal(g.from_line_major(lm, dirs, H, W).numpy(), a[:d])

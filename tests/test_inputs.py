@@ -74,18 +74,27 @@ def test_bf16_helpers_round_trip():
         gi.to_bf16_bits(np.array([1.0 + 2.0 ** -10], dtype=np.float32))
 
 
-def test_line_major_round_trip_and_layout():
+def _blocked_offset(l, p, L, P):
+    """Blocked line-major offset written out: 8-line blocks, positions adjacent."""
+    q = l // 8
+    n = min(8, L - 8 * q)
+    return 8 * P * q + n * p + l % 8
+
+
+@pytest.mark.parametrize("H,W", [(3, 5), (11, 19), (16, 8), (24, 17)])
+def test_line_major_round_trip_and_layout(H, W):
     rng = np.random.default_rng(3)
-    H, W = 3, 5
     a = rng.standard_normal((4, 2, 2, H, W))
     lm = gi.to_line_major(a, 15)
     assert lm.shape == (4, 2, 2, H * W)
-    # vertical planes unchanged, horizontal planes transposed: (r, c) at c*H + r
-    np.testing.assert_array_equal(lm[0, 1, 0], a[0, 1, 0].reshape(-1))
     for r in range(H):
         for c in range(W):
-            assert lm[2, 1, 1, c * H + r] == a[2, 1, 1, r, c]
-            assert lm[3, 0, 1, c * H + r] == a[3, 0, 1, r, c]
+            # vertical directions scan rows: line r, position c
+            assert lm[0, 1, 0, _blocked_offset(r, c, H, W)] == a[0, 1, 0, r, c]
+            assert lm[1, 0, 1, _blocked_offset(r, c, H, W)] == a[1, 0, 1, r, c]
+            # horizontal directions scan columns: line c, position r
+            assert lm[2, 1, 1, _blocked_offset(c, r, W, H)] == a[2, 1, 1, r, c]
+            assert lm[3, 0, 1, _blocked_offset(c, r, W, H)] == a[3, 0, 1, r, c]
     np.testing.assert_array_equal(gi.from_line_major(lm, 15, H, W), a)
     # subsets keep slot order
     b = a[:2]
