@@ -48,7 +48,8 @@ constexpr uint32_t kSelHi = 0x03020C0Cu;   // bf16 in bits [31:16] -> fp32
 constexpr uint32_t kSelZero = 0x0C0C0C0Cu; // -> +0.0f
 constexpr int kYPitch = 68;                // fp32 LDS row pitch (16-byte rows, conflict-free b128)
 constexpr int kDxPitch = 65;               // fp32 LDS row pitch of the dx plane (odd: column walks conflict-free)
-constexpr int kPrefetch = 8;               // steps of per-step row loads in flight (backward)
+constexpr int kPrefetch = 16;              // steps of per-step row loads in flight (backward)
+constexpr int kLdsAhead = 3;               // steps of staged (x, dy) LDS reads in flight (backward)
 
 // Keep the software pipeline as written: nothing is scheduled across a step
 // boundary, so each step's prefetch stays ahead of its use instead of every
@@ -91,6 +92,13 @@ __device__ __forceinline__ uint4 ld128(rsrc_t r, uint32_t voff, uint32_t soff)
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
+// Streams read exactly once (lam, u) are loaded non-temporal, so that the L2
+// keeps what several waves or sweeps read again (x, dy and a group's w).
+__device__ __forceinline__ uint4 ld128_nt(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2 /* nt */);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
 // Stores go through inline assembly, each wide one together with the wait
 // states after it.  A VALU write to a VGPR that a wide store still has to
 // read (its data registers are read after issue, later still when it queues
@@ -128,6 +136,15 @@ __device__ __forceinline__ void st128(const u32x4 &d, uint32_t voff, uint32_t so
 {
     const u32x4 t = {v.x, v.y, v.z, v.w};
     asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+// Non-temporal variant for stores whose wave covers whole 128-byte lines
+// (partial-line non-temporal stores are not merged in the L2 and cost more
+// write traffic than they save).
+__device__ __forceinline__ void st128_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen nt\n\ts_nop 7\n\ts_nop 7"
                  : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
 }
 __device__ __forceinline__ void gst128(uint4 *p, uint4 v)
@@ -263,8 +280,8 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
 #define FLOAD(fb)                                                    \
     do {                                                             \
         const uint32_t so_ = boff(fb);                               \
-        rl[fb] = ld128(lam, vo, so_);                                \
-        ru[fb] = ld128(u, vo, so_);                                  \
+        rl[fb] = ld128_nt(lam, vo, so_);                             \
+        ru[fb] = ld128_nt(u, vo, so_);                               \
         r0[fb] = ld128(w, vo, so_);                                  \
         r1[fb] = ld128(w, vo, so_ + PL);                             \
         r2[fb] = ld128(w, vo, so_ + 2 * PL);                         \
@@ -404,7 +421,7 @@ __global__ __launch_bounds__(256) void fwd_med_kernel(
         const int cm = t - r * (W / 8);
         const float4 a0 = Y4[(r * kYPitch + 8 * cm) / 4];
         const float4 a1 = Y4[(r * kYPitch + 8 * cm) / 4 + 1];
-        st128(yo, 16u * t, 0, make_uint4(pack2(a0.x, a0.y), pack2(a0.z, a0.w), pack2(a1.x, a1.y),
+        st128_nt(yo, 16u * t, 0, make_uint4(pack2(a0.x, a0.y), pack2(a0.z, a0.w), pack2(a1.x, a1.y),
                                          pack2(a1.z, a1.w)));
     }
 }
@@ -476,7 +493,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #define RLOAD(fb)                                                    \
     do {                                                             \
         const uint32_t so_ = boff(fb);                               \
-        ru[fb] = ld128(A.u, vo, so_);                                \
+        ru[fb] = ld128_nt(A.u, vo, so_);                             \
         q0[fb] = ld128(A.w, vo, so_);                                \
         q1[fb] = ld128(A.w, vo, so_ + PL2);                          \
         q2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
@@ -490,9 +507,14 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 rd[VERT ? i : 0] = ld16(A.dy, vr, rowoff(i));
         }
         float an = 0.f;
-        // horizontal directions: the staged (x, dy) dword of the next step is
-        // read one step ahead so its LDS latency overlaps the arithmetic
-        uint32_t xd_next = VERT ? 0u : stg_at(L - 1);
+        // horizontal directions: the staged (x, dy) dwords are read kLdsAhead
+        // steps ahead so their LDS latency overlaps the arithmetic
+        uint32_t xq[VERT ? 1 : L];
+        if (!VERT) {
+#pragma unroll
+            for (int i = L - 1; i >= L - kLdsAhead; --i)
+                xq[VERT ? 0 : i] = stg_at(i);
+        }
 #pragma unroll
         for (int fb = NB - 1; fb >= 0; --fb) {
             if (fb >= 2)
@@ -506,9 +528,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 if (VERT) {
                     dyv = bf_lo(rd[VERT ? i : 0]);
                 } else {
-                    dyv = bf_hi(xd_next);
-                    if (i > 0)
-                        xd_next = stg_at(i - 1);
+                    if (i - kLdsAhead >= 0)
+                        xq[VERT ? 0 : i - kLdsAhead] = stg_at(i - kLdsAhead);
+                    dyv = bf_hi(xq[VERT ? 0 : i]);
                 }
                 const int e = REV ? 7 - t : t;
                 const float inj = elem(ru[fb], e, s.lo1, s.hi1) * dyv;
@@ -540,7 +562,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #define FLOADB(fb)                                                   \
     do {                                                             \
         const uint32_t so_ = boff(fb);                               \
-        rl[fb] = ld128(A.lam, vo, so_);                              \
+        rl[fb] = ld128_nt(A.lam, vo, so_);                           \
         p0[fb] = ld128(A.w, vo, so_);                                \
         p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
         p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
@@ -613,7 +635,12 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     // value of the first step of a pair waits in du0 / dl0
     uint32_t dup[4], dlp[4];
     float du0 = 0.f, dl0 = 0.f;
-    uint32_t xd_next = VERT ? 0u : stg_at(0);
+    uint32_t xq[VERT ? 1 : L];
+    if (!VERT) {
+#pragma unroll
+        for (int i = 0; i < kLdsAhead; ++i)
+            xq[VERT ? 0 : i] = stg_at(i);
+    }
     float dx_next = 0.f;     // vertical: dx plane value of this step's row, read a step ahead
     if (VERT && !A.first)
         dx_next = A.Xq[line_of(0) * kDxPitch + jj];
@@ -632,9 +659,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 xv = bf_lo(rx[VERT ? i : 0]);
                 dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
             } else {
-                const uint32_t xd = xd_next;
-                if (i + 1 < L)
-                    xd_next = stg_at(i + 1);
+                if (i + kLdsAhead < L)
+                    xq[VERT ? 0 : i + kLdsAhead] = stg_at(i + kLdsAhead);
+                const uint32_t xd = xq[VERT ? 0 : i];
                 xv = bf_lo(xd);
                 dyv = bf_hi(xd);
             }
@@ -689,8 +716,8 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 issue_dw(i);
             }
             if (t == 7 && act) {
-                st128(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
-                st128(A.dlam, vo, boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                st128_nt(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                st128_nt(A.dlam, vo, boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
             }
             step_fence();
         }
