@@ -287,13 +287,11 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
         r2[fb] = ld128(w, vo, so_ + 2 * PL);                         \
     } while (0)
     FLOAD(0);
-    if (NB > 1)
-        FLOAD(1);
     float h = 0.f;
 #pragma unroll
     for (int fb = 0; fb < NB; ++fb) {
-        if (fb + 2 < NB)
-            FLOAD(fb + 2);
+        if (fb + 1 < NB)
+            FLOAD(fb + 1);
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const int i = 8 * fb + t;
@@ -317,7 +315,7 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
 }
 
 template <int H, int W>
-__global__ __launch_bounds__(256) void fwd_med_kernel(
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G)
 {
