@@ -91,6 +91,31 @@ __device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitc
     return f;
 }
 
+// Division of a non-negative int below 2^31 by a fixed divisor d as a
+// multiply-high and shift (Granlund and Montgomery, "Division by invariant
+// integers using multiplication", 1994): with s = ceil(log2 d) and
+// m = ceil(2^(31+s) / d), n / d = (n * m) >> (31 + s).  Built on the host;
+// on the device a uniform n divides in scalar instructions, where a plain
+// division would be expanded on the vector unit.
+struct Magic {
+    uint32_t m, s;
+};
+
+inline Magic make_magic(uint32_t d)
+{
+    uint32_t l = 0;
+    while ((1ull << l) < d)
+        ++l;
+    const uint64_t num = 1ull << (31 + l);
+    return Magic{static_cast<uint32_t>((num + d - 1) / d), l};
+}
+
+__device__ __forceinline__ int mdiv(int n, Magic q)
+{
+    return static_cast<int>(
+        static_cast<uint32_t>((static_cast<uint64_t>(static_cast<uint32_t>(n)) * q.m) >> (31 + q.s)));
+}
+
 __device__ __forceinline__ int scan_len(int d, int H, int W) { return d < 2 ? H : W; }
 __device__ __forceinline__ int line_len(int d, int H, int W) { return d < 2 ? W : H; }
 

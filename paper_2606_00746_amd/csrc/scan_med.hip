@@ -317,7 +317,8 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
 template <int H, int W>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
-    const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G)
+    const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G,
+    Magic divC, Magic divCpg)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0, "shape");
     constexpr int HW = H * W;
@@ -333,9 +334,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
     const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int b = blk / C;
+    const int b = mdiv(blk, divC);
     const int c = blk - b * C;
-    const int g = c / (C / G);
+    const int g = mdiv(c, divCpg);
     const bool mine = (mask >> d) & 1;
     const int s = __popc(mask & ((1 << d) - 1));
     const int64_t pc = ((int64_t)b * C + c) * HW;
@@ -729,7 +730,8 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
     bf16_t *__restrict__ dw, bf16_t *__restrict__ dlam, bf16_t *__restrict__ du,
-    float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk)
+    float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk, Magic divChunk,
+    Magic divG)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
@@ -739,11 +741,11 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int chunk = blk % nchunk;
-    const int bg = blk / nchunk;
-    const int g = bg % G;
-    const int b = bg / G;
-    const int cpg = C / G;
+    const int bg = mdiv(blk, divChunk);
+    const int chunk = blk - bg * nchunk;
+    const int b = mdiv(bg, divG);
+    const int g = bg - b * G;
+    const int cpg = mdiv(C, divG);
     const int cfirst = chunk * cw;
     const int nvalid = min(cw, cpg - cfirst);
     const bool cvalid = wave < nvalid;
@@ -891,7 +893,8 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
 {
     hipLaunchKernelGGL((fwd_med_kernel<H, W>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
                        (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
-                       (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G);
+                       (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
+                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
     return hipGetLastError();
 }
 
@@ -907,7 +910,8 @@ hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, 
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
-                       p.mask, p.B, p.C, p.G, cw, nchunk);
+                       p.mask, p.B, p.C, p.G, cw, nchunk, make_magic((uint32_t)nchunk),
+                       make_magic((uint32_t)p.G));
     return hipGetLastError();
 }
 
