@@ -132,6 +132,13 @@ __device__ __forceinline__ void st64(const u32x4 &d, uint32_t voff, uint32_t sof
     asm volatile("buffer_store_dwordx2 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
                  : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
 }
+__device__ __forceinline__ void st64_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t a,
+                                        uint32_t b)
+{
+    const u32x2 t = {a, b};
+    asm volatile("buffer_store_dwordx2 %0, %1, %2, %3 offen nt\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
 __device__ __forceinline__ void st128(const u32x4 &d, uint32_t voff, uint32_t soff, uint4 v)
 {
     const u32x4 t = {v.x, v.y, v.z, v.w};
@@ -618,12 +625,16 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 const float lo = REV ? sum[1] : sum[0];
                 const float hi = REV ? sum[0] : sum[1];
                 if (jp < P) {
-                    const uint32_t el = 8u * (uint32_t)(P * sb + jp) + (uint32_t)e0;
-                    if (A.partial)
-                        st64(A.dw, 4u * el + 2u * PL2 * (uint32_t)k, 0, __float_as_uint(lo),
-                             __float_as_uint(hi));
-                    else
+                    if (A.partial) {
+                        // pair-major partials: storage lines (l, l+1), l even, of
+                        // position jp are adjacent, so a wave covers whole lines
+                        const uint32_t pp = (8u * sb + (uint32_t)e0) >> 1;
+                        const uint32_t f = (uint32_t)(k * H * W) + 2u * (pp * P + (uint32_t)jp);
+                        st64_nt(A.dw, 4u * f, 0, __float_as_uint(lo), __float_as_uint(hi));
+                    } else {
+                        const uint32_t el = 8u * (uint32_t)(P * sb + jp) + (uint32_t)e0;
                         st32(A.dw, 2u * el + PL2 * (uint32_t)k, 0, pack2(lo, hi));
+                    }
                 }
             }
         }
@@ -825,25 +836,12 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         dir_bwd<H, W, 3, U>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
-    if (horiz) {
-        // the horizontal dx terms (this lane's row) seed the dx plane the
-        // vertical directions add to, or go out directly
-        if (vert) {
-            if (lane < H) {
+    if (horiz && lane < H) {
+        // the horizontal dx terms (this lane's row) seed the dx plane that the
+        // vertical directions add to
 #pragma unroll
-                for (int q = 0; q < W; ++q)
-                    A.Xq[lane * kDxPitch + q] = dxr[q];
-            }
-        } else if (cvalid && lane < H) {
-            const u32x4 dxo = make_sdesc(dx + pc, 2 * HW);
-#pragma unroll
-            for (int q = 0; q < W / 8; ++q)
-                st128(dxo, 2u * (uint32_t)(lane * W), 16u * q,
-                      make_uint4(pack2(dxr[8 * q], dxr[8 * q + 1]),
-                                 pack2(dxr[8 * q + 2], dxr[8 * q + 3]),
-                                 pack2(dxr[8 * q + 4], dxr[8 * q + 5]),
-                                 pack2(dxr[8 * q + 6], dxr[8 * q + 7])));
-        }
+        for (int q = 0; q < W; ++q)
+            A.Xq[lane * kDxPitch + q] = dxr[q];
     }
     if (mask & 1) {
         setup(0);
@@ -858,33 +856,55 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         lds_barrier();
     }
 
-    if (vert && cvalid && lane < H) {
-        const float *Xr = A.Xq + lane * kDxPitch;
+    // dx out of this wave's plane: lane t takes 8 consecutive columns of a
+    // row, so each store instruction covers whole 128-byte lines (the LDS
+    // reads of a lane hit 64 different banks across the wave)
+    if (cvalid) {
         const u32x4 dxo = make_sdesc(dx + pc, 2 * HW);
-        const uint32_t vo = 2u * (uint32_t)(lane * W);
+        constexpr int NP = HW / 8;
 #pragma unroll
-        for (int q = 0; q < W / 8; ++q) {
-            const float *a = Xr + 8 * q;
-            st128(dxo, vo, 16u * q, make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]),
-                                               pack2(a[4], a[5]), pack2(a[6], a[7])));
+        for (int it = 0; it < (NP + 63) / 64; ++it) {
+            const int t = it * 64 + lane;
+            if (t < NP) {
+                const int r = t / (W / 8), cm = t - r * (W / 8);
+                const float *a = A.Xq + r * kDxPitch + 8 * cm;
+                st128_nt(dxo, 16u * (uint32_t)t, 0,
+                         make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]),
+                                    pack2(a[6], a[7])));
+            }
         }
     }
 }
 
-// dw = sum over chunks of the fp32 partials, in chunk order; 8 outputs per
-// thread with 16-byte accesses (n is a multiple of 8 on this path).
-__global__ __launch_bounds__(256) void dw_sum_kernel(const float4 *__restrict__ dwp,
-                                                     uint4 *__restrict__ dw, int64_t n8, int nchunk)
+// dw (bf16, blocked line-major) = sum over chunks of the fp32 partials, in
+// chunk order.  Partials are pair-major per (chunk, unit, tap): storage lines
+// (2p, 2p+1) of position j at float 2 * (p * S + j).  One thread makes the 8
+// outputs of one (unit, tap, 8-line block, position): four float2 reads per
+// chunk and one 16-byte store, both contiguous across the wave.
+template <int S>
+__global__ __launch_bounds__(256) void dw_sum_kernel(const float2 *__restrict__ dwp,
+                                                     uint4 *__restrict__ dw, int64_t nuk, int nchunk)
 {
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n8;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        float4 a = dwp[2 * e], b = dwp[2 * e + 1];
-        for (int k = 1; k < nchunk; ++k) {
-            const float4 p = dwp[(k * n8 + e) * 2], q = dwp[(k * n8 + e) * 2 + 1];
-            a = make_float4(a.x + p.x, a.y + p.y, a.z + p.z, a.w + p.w);
-            b = make_float4(b.x + q.x, b.y + q.y, b.z + q.z, b.w + q.w);
+    constexpr int NQ = S / 8, HW = S * S;
+    const int64_t n = nuk * NQ * S;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int j = (int)(o % S);
+        const int64_t r = o / S;
+        const int q = (int)(r % NQ);
+        const int64_t uk = r / NQ;                      // unit * 3 + tap
+        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < nchunk; ++c) {
+            const float2 *src = dwp + ((int64_t)c * nuk + uk) * (HW / 2) + (int64_t)(4 * q) * S + j;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const float2 f = src[t * S];
+                v[2 * t] += f.x;
+                v[2 * t + 1] += f.y;
+            }
         }
-        gst128(dw + e, make_uint4(pack2(a.x, a.y), pack2(a.z, a.w), pack2(b.x, b.y), pack2(b.z, b.w)));
+        gst128(dw + (uk * HW + (int64_t)8 * S * q + 8 * j) / 8,
+               make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
     }
 }
 
@@ -948,11 +968,12 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     e = cw >= 4 ? bwd_med_launch<H, W, 1>(p, st, cw, nchunk, lds, dwp)
                 : bwd_med_launch<H, W, 3>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
+        const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
         int64_t blocks = (n8 + 255) / 256;
         blocks = blocks < 16384 ? blocks : 16384;
-        hipLaunchKernelGGL(dw_sum_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const float4 *)dwp, (uint4 *)p.dw, n8, nchunk);
+        hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           (const float2 *)dwp, (uint4 *)p.dw, nuk, nchunk);
         e = hipGetLastError();
     }
     if (dwp) {
