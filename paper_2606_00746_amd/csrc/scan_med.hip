@@ -120,6 +120,11 @@ __device__ __forceinline__ u32x4 make_sdesc(const void *p, uint32_t bytes)
     d.w = kRsrcWord3;
     return d;
 }
+__device__ __forceinline__ void st16(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
+{
+    asm volatile("buffer_store_short %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
+                 : "memory");
+}
 __device__ __forceinline__ void st32(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
 {
     asm volatile("buffer_store_dword %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
@@ -175,6 +180,12 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi)
     const __bf16 b = static_cast<__bf16>(hi);
     return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
            (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+__device__ __forceinline__ uint32_t pack1(float v)
+{
+    const __bf16 a = static_cast<__bf16>(v);
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a));
 }
 
 // Component k (0..3) of a 16-byte piece; k is a constant once unrolled.
@@ -459,15 +470,14 @@ struct BwdArgs {
     u32x4 dw;              // 3 tap planes: final bf16 dw or fp32 partial
     float *Xq;             // this wave's dx plane in LDS, [H][kDxPitch]
     float *slots;          // dw term slots
-    int wave;
+    int wave, cw;          // this wave, waves of the workgroup
     bool partial;          // dw holds fp32 partials
     bool first;            // first direction adding into the dx plane: store
 };
 
-// One direction of the backward.  D: direction index.  U: reduction layout:
-// U = 1 when the workgroup has at least 4 waves (waves 0..3 each reduce 48 of
-// the 192 (tap, position) pairs of a step, one wave per SIMD), U = 3 when it
-// has fewer (wave 0 reduces all of them, one tap per pass).  Horizontal
+// One direction of the backward.  D: direction index.  U: passes of 64 sums
+// each wave makes per batch of the weight-gradient reduction (1 for 6 or more
+// waves, 3 for 2 to 5, 6 for one).  Horizontal
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
@@ -582,58 +592,50 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             rx[VERT ? i : 0] = ld16(A.x, vr, rowoff(i));
     }
 
-    // Reduction roles: pair p = (tap k, position jp) with p = k * 64 + jp.
-    const bool reducer = U == 1 ? (A.wave < 4 && j < 48) : A.wave == 0;
-    float pr[U][kBatch][kSlots];
-    auto pair_of = [&](int uu) { return U == 1 ? 48 * A.wave + j : 64 * uu + j; };
+    // Reduction roles: a batch has kBatch * 192 sums, one per (step st, tap
+    // k, position jp), numbered c = 192 st + 64 k + jp.  They are spread evenly
+    // over the workgroup's waves (48 per wave for 8 waves), so no wave waits
+    // for another at the barrier: wave w owns c = w * per + j + 64 uu.
+    constexpr int kSums = kBatch * 192;
+    const int per = (kSums + A.cw - 1) / A.cw;
+    float pr[U][kSlots];
+    auto owns = [&](int uu) {
+        return j + 64 * uu < per && A.wave * per + j + 64 * uu < kSums;
+    };
     // issue the slot reads of the batch that ends at step i
     auto issue_dw = [&](int i) {
-        if (reducer) {
-            const int buf = (i >> 1) & 1;
+        const int buf = (i >> 1) & 1;
 #pragma unroll
-            for (int uu = 0; uu < U; ++uu) {
-                const int p = pair_of(uu);
+        for (int uu = 0; uu < U; ++uu) {
+            if (owns(uu)) {
+                const int c = A.wave * per + j + 64 * uu;
+                const int st = c >= 192 ? 1 : 0, p = c - 192 * st;
 #pragma unroll
-                for (int st = 0; st < kBatch; ++st)
-#pragma unroll
-                    for (int q = 0; q < kSlots; ++q)
-                        pr[uu][st][q] = slot_ptr(A.slots, buf, st, p >> 6, q)[p & 63];
+                for (int q = 0; q < kSlots; ++q)
+                    pr[uu][q] = slot_ptr(A.slots, buf, st, p >> 6, q)[p & 63];
             }
         }
     };
     // sum (in channel-slot order) and store the batch that ends at step i
     auto flush_dw = [&](int i) {
-        if (reducer) {
-            const int i0 = i - 1;                             // first step of the batch
-            const int fb = i0 >> 3, t0 = i0 & 7;
-            const uint32_t sb = (uint32_t)(REV ? NB - 1 - fb : fb);
-            // the pair's storage elements: t0, t0+1, or 7-t0-1, 7-t0 reversed
-            const int e0 = REV ? 6 - t0 : t0;
 #pragma unroll
-            for (int uu = 0; uu < U; ++uu) {
-                const int p = pair_of(uu);
+        for (int uu = 0; uu < U; ++uu) {
+            if (owns(uu)) {
+                const int c = A.wave * per + j + 64 * uu;
+                const int st = c >= 192 ? 1 : 0, p = c - 192 * st;
                 const int k = p >> 6, jp = p & 63;
-                float sum[kBatch];
+                float v = 0.f;
 #pragma unroll
-                for (int st = 0; st < kBatch; ++st) {
-                    float v = 0.f;
-#pragma unroll
-                    for (int q = 0; q < kSlots; ++q)
-                        v += pr[uu][st][q];
-                    sum[st] = v;
-                }
-                const float lo = REV ? sum[1] : sum[0];
-                const float hi = REV ? sum[0] : sum[1];
+                for (int q = 0; q < kSlots; ++q)
+                    v += pr[uu][q];
+                const int l = line_of(i - 1 + st);            // storage line of the sum
                 if (jp < P) {
                     if (A.partial) {
-                        // pair-major partials: storage lines (l, l+1), l even, of
-                        // position jp are adjacent, so a wave covers whole lines
-                        const uint32_t pp = (8u * sb + (uint32_t)e0) >> 1;
-                        const uint32_t f = (uint32_t)(k * H * W) + 2u * (pp * P + (uint32_t)jp);
-                        st64_nt(A.dw, 4u * f, 0, __float_as_uint(lo), __float_as_uint(hi));
+                        // line-major fp32 partials: one row of a tap plane per line
+                        st32(A.dw, 4u * (uint32_t)(k * H * W + l * P + jp), 0, __float_as_uint(v));
                     } else {
-                        const uint32_t el = 8u * (uint32_t)(P * sb + jp) + (uint32_t)e0;
-                        st32(A.dw, 2u * el + PL2 * (uint32_t)k, 0, pack2(lo, hi));
+                        const uint32_t el = (uint32_t)lm_offset(l, jp, L, P);
+                        st16(A.dw, 2u * el + PL2 * (uint32_t)k, 0, pack1(v));
                     }
                 }
             }
@@ -774,6 +776,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         A.slots[t] = 0.f;
     lds_barrier();
     A.wave = wave;
+    A.cw = cw;
     A.partial = nchunk > 1;
 
     // Horizontal directions read x and dy columns: stage both planes in this
@@ -877,12 +880,12 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
 }
 
 // dw (bf16, blocked line-major) = sum over chunks of the fp32 partials, in
-// chunk order.  Partials are pair-major per (chunk, unit, tap): storage lines
-// (2p, 2p+1) of position j at float 2 * (p * S + j).  One thread makes the 8
-// outputs of one (unit, tap, 8-line block, position): four float2 reads per
-// chunk and one 16-byte store, both contiguous across the wave.
+// chunk order.  Partials are line-major per (chunk, unit, tap): storage line l,
+// position j at float l * S + j.  One thread makes the 8 outputs of one
+// (unit, tap, 8-line block, position): eight reads per chunk and one 16-byte
+// store, both contiguous across the wave.
 template <int S>
-__global__ __launch_bounds__(256) void dw_sum_kernel(const float2 *__restrict__ dwp,
+__global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ dwp,
                                                      uint4 *__restrict__ dw, int64_t nuk, int nchunk)
 {
     constexpr int NQ = S / 8, HW = S * S;
@@ -895,13 +898,10 @@ __global__ __launch_bounds__(256) void dw_sum_kernel(const float2 *__restrict__ 
         const int64_t uk = r / NQ;                      // unit * 3 + tap
         float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
         for (int c = 0; c < nchunk; ++c) {
-            const float2 *src = dwp + ((int64_t)c * nuk + uk) * (HW / 2) + (int64_t)(4 * q) * S + j;
+            const float *src = dwp + ((int64_t)c * nuk + uk) * HW + (int64_t)(8 * q) * S + j;
 #pragma unroll
-            for (int t = 0; t < 4; ++t) {
-                const float2 f = src[t * S];
-                v[2 * t] += f.x;
-                v[2 * t + 1] += f.y;
-            }
+            for (int t = 0; t < 8; ++t)
+                v[t] += src[t * S];
         }
         gst128(dw + (uk * HW + (int64_t)8 * S * q + 8 * j) / 8,
                make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
@@ -965,15 +965,16 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         if (e != hipSuccess)
             return e;
     }
-    e = cw >= 4 ? bwd_med_launch<H, W, 1>(p, st, cw, nchunk, lds, dwp)
-                : bwd_med_launch<H, W, 3>(p, st, cw, nchunk, lds, dwp);
+    e = cw >= 6   ? bwd_med_launch<H, W, 1>(p, st, cw, nchunk, lds, dwp)
+        : cw >= 2 ? bwd_med_launch<H, W, 3>(p, st, cw, nchunk, lds, dwp)
+                  : bwd_med_launch<H, W, 6>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
         int64_t blocks = (n8 + 255) / 256;
         blocks = blocks < 16384 ? blocks : 16384;
         hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const float2 *)dwp, (uint4 *)p.dw, nuk, nchunk);
+                           (const float *)dwp, (uint4 *)p.dw, nuk, nchunk);
         e = hipGetLastError();
     }
     if (dwp) {
