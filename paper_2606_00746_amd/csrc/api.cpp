@@ -106,6 +106,8 @@ extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, cons
         return hip_status(launch_fwd_med(p, s));
     if (H <= kSmallSide && W <= kSmallSide)
         return hip_status(launch_fwd_small(p, s));
+    if (wide_supported(p))
+        return hip_status(launch_fwd_wide(p, s));
     return hip_status(launch_fwd_general(p, s));
 }
 

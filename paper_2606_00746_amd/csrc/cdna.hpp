@@ -1,0 +1,219 @@
+// gfx950 building blocks shared by the libgspn kernels: raw buffer access
+// with uniform descriptors, stores issued with their wait states, bf16
+// widening with per-lane masks, LDS-only barriers and the XCD-aware
+// workgroup order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gspn {
+namespace cdna {
+
+constexpr uint32_t kSelLo = 0x01000C0Cu;   // bf16 in bits [15:0]  -> fp32
+constexpr uint32_t kSelHi = 0x03020C0Cu;   // bf16 in bits [31:16] -> fp32
+constexpr uint32_t kSelZero = 0x0C0C0C0Cu; // -> +0.0f
+
+// Keep the software pipeline as written: nothing is scheduled across a step
+// boundary, so each step's prefetch stays ahead of its use instead of every
+// load of the unrolled scan being hoisted to the top.
+__device__ __forceinline__ void step_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+// Workgroup barrier that orders LDS only.  __syncthreads() also orders global
+// memory, which makes every wave drain its prefetched loads at each barrier.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Raw buffer access: a uniform descriptor per tensor plane (SGPRs), one
+// per-lane byte offset (VGPR) and a uniform per-step offset (SGPR), so no
+// 64-bit per-lane addresses are formed.
+using rsrc_t = __amdgpu_buffer_rsrc_t;
+constexpr int kRsrcWord3 = 0x00020000;   // gfx9 raw buffer: 32-bit data format, no swizzle
+
+// The base address is passed through readfirstlane: every caller's pointer
+// is wave-uniform, and saying so keeps the compiler from wrapping each buffer
+// access in a loop over distinct descriptors.
+__device__ __forceinline__ rsrc_t make_rsrc(const void *p, uint32_t bytes)
+{
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32));
+    void *q = reinterpret_cast<void *>((static_cast<uint64_t>(hi) << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(q, (short)0,
+                                             (int)__builtin_amdgcn_readfirstlane(bytes), kRsrcWord3);
+}
+__device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+__device__ __forceinline__ uint4 ld128(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+// Streams read exactly once (lam, u) are loaded non-temporal, so that the L2
+// keeps what several waves or sweeps read again (x, dy and a group's w).
+__device__ __forceinline__ uint4 ld128_nt(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 2 /* nt */);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+// Stores go through inline assembly, each wide one together with the wait
+// states after it.  A VALU write to a VGPR that a wide store still has to
+// read (its data registers are read after issue, later still when it queues
+// behind another store) corrupts the stored value in some lanes; this
+// compiler inserts no wait states for that on gfx950, and its register
+// allocator can place such a write (a copy) directly after the store, where
+// no scheduling barrier reaches.  One asm block keeps the two together.
+// Store targets use a raw buffer descriptor held in SGPRs as four words.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u32x4 make_sdesc(const void *p, uint32_t bytes)
+{
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    u32x4 d;
+    d.x = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a));
+    d.y = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(a >> 32)) & 0xffffu;  // stride 0
+    d.z = __builtin_amdgcn_readfirstlane(bytes);
+    d.w = kRsrcWord3;
+    return d;
+}
+__device__ __forceinline__ void st16(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
+{
+    asm volatile("buffer_store_short %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
+                 : "memory");
+}
+__device__ __forceinline__ void st32(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
+{
+    asm volatile("buffer_store_dword %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
+                 : "memory");
+}
+// Non-temporal dword store, for waves whose lanes cover whole lines.
+__device__ __forceinline__ void st32_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
+{
+    asm volatile("buffer_store_dword %0, %1, %2, %3 offen nt" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
+                 : "memory");
+}
+__device__ __forceinline__ void st64(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t a,
+                                     uint32_t b)
+{
+    const u32x2 t = {a, b};
+    asm volatile("buffer_store_dwordx2 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void st64_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t a,
+                                        uint32_t b)
+{
+    const u32x2 t = {a, b};
+    asm volatile("buffer_store_dwordx2 %0, %1, %2, %3 offen nt\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void st128(const u32x4 &d, uint32_t voff, uint32_t soff, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+// Non-temporal variant for stores whose wave covers whole 128-byte lines
+// (partial-line non-temporal stores are not merged in the L2 and cost more
+// write traffic than they save).
+__device__ __forceinline__ void st128_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen nt\n\ts_nop 7\n\ts_nop 7"
+                 : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
+}
+__device__ __forceinline__ void gst128(uint4 *p, uint4 v)
+{
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    asm volatile("global_store_dwordx4 %0, %1, off\n\ts_nop 7\n\ts_nop 7" : : "v"(p), "v"(t)
+                 : "memory");
+}
+
+__device__ __forceinline__ float widen(uint32_t v, uint32_t sel)
+{
+    return __uint_as_float(__builtin_amdgcn_perm(0u, v, sel));
+}
+__device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi)
+{
+    // two fp32 -> bf16 (RNE) in one v_cvt_pk_bf16_f32
+    const __bf16 a = static_cast<__bf16>(lo);
+    const __bf16 b = static_cast<__bf16>(hi);
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
+           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+}
+
+__device__ __forceinline__ uint32_t pack1(float v)
+{
+    const __bf16 a = static_cast<__bf16>(v);
+    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a));
+}
+
+// Component k (0..3) of a 16-byte piece; k is a constant once unrolled.
+__device__ __forceinline__ uint32_t part(const uint4 &v, int k)
+{
+    return k == 0 ? v.x : (k == 1 ? v.y : (k == 2 ? v.z : v.w));
+}
+
+// Element e (0..7) of a lane's 8-line piece (the lane's position on lines
+// 8q..8q+7 of a block), widened with the selector pair of the lane, or
+// unmasked.
+__device__ __forceinline__ float elem(const uint4 &v, int e, uint32_t sel_lo, uint32_t sel_hi)
+{
+    return widen(part(v, e >> 1), (e & 1) ? sel_hi : sel_lo);
+}
+__device__ __forceinline__ float elem(const uint4 &v, int e)
+{
+    const uint32_t d = part(v, e >> 1);
+    return (e & 1) ? bf_hi(d) : bf_lo(d);
+}
+
+// Workgroups go to the 8 XCDs round-robin by blockIdx.  Give each XCD a
+// contiguous range of logical ids so that neighbouring channels -- which
+// share a weight group's w -- run under one L2.
+__device__ __forceinline__ int xcd_remap(int bid, int n)
+{
+    constexpr int X = 8;
+    const int q = n / X, r = n % X;
+    const int xcd = bid % X, k = bid / X;
+    return xcd < r ? xcd * (q + 1) + k : r * (q + 1) + (xcd - r) * q + k;
+}
+
+struct Sel {
+    uint32_t lo0, lo1, lo2, hi0, hi1, hi2;   // taps 0/1/2 (1 also gates lam, u)
+};
+
+__device__ __forceinline__ Sel make_sel(int j, int P)
+{
+    const bool act = j < P;
+    const bool v0 = act && j > 0;
+    const bool v2 = act && j + 1 < P;
+    Sel s;
+    s.lo0 = v0 ? kSelLo : kSelZero;
+    s.hi0 = v0 ? kSelHi : kSelZero;
+    s.lo1 = act ? kSelLo : kSelZero;
+    s.hi1 = act ? kSelHi : kSelZero;
+    s.lo2 = v2 ? kSelLo : kSelZero;
+    s.hi2 = v2 ? kSelHi : kSelZero;
+    return s;
+}
+
+__device__ __forceinline__ uint32_t lds_u16(const uint8_t *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const uint16_t *>(base + byte_off);
+}
+__device__ __forceinline__ uint32_t lds_u32(const uint8_t *base, uint32_t byte_off)
+{
+    return *reinterpret_cast<const uint32_t *>(base + byte_off);
+}
+
+}  // namespace cdna
+}  // namespace gspn

@@ -20,6 +20,8 @@ hipError_t launch_bwd_small(const Problem &p, hipStream_t s);
 bool med_supported(const Problem &p);
 hipError_t launch_fwd_med(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_med(const Problem &p, hipStream_t s);
+bool wide_supported(const Problem &p);
+hipError_t launch_fwd_wide(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_general(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_general(const Problem &p, hipStream_t s);
 

@@ -1,0 +1,336 @@
+// Forward line scans for bf16 planes whose lines are longer than a wave
+// (sides up to 256, multiples of 8), with per-direction tensors in the
+// blocked line-major layout.
+//
+// One workgroup per channel plane, one wave per direction (Sec. 3,
+// Eqs. (gspn_recurrence), (gspn_output)):
+//  * the x plane is loaded once, coalesced, into LDS (132 KB at 256 x 256);
+//  * lane l of a wave owns the line positions l + 64 m (m < NPL); the line
+//    state stays in NPL VGPRs for the whole scan; the tridiagonal step takes
+//    neighbours from the adjacent lanes by DPP, and across the boundary
+//    between position groups (lane 0 and lane 63) with readlane;
+//  * lam, u and w come in 8-line blocks of 16-byte coalesced loads, one
+//    block ahead of use.
+// A 256 x 256 fp32 merge plane does not fit in LDS, so each direction writes
+// u_d * h_d to an fp32 plane in its own line-major order (whole lines per
+// store) and a tiled kernel sums the directions in direction-bit order,
+// transposing the horizontal ones through LDS, and stores y once.
+#include "cdna.hpp"
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace gspn {
+
+namespace {
+
+using namespace cdna;
+
+constexpr int kMaxNpl = 4;   // positions per lane: lines of up to 256 positions
+constexpr int kTile = 64;    // tile side of the direction sum
+
+// bf16 x plane in LDS, rows of an odd number of dwords: a row walk (lanes on
+// consecutive columns) and a column walk (lanes on consecutive rows) are both
+// free of bank conflicts.
+__host__ __device__ inline int wide_pitch_dw(int W) { return (W / 2) | 1; }
+
+template <int NPL>
+struct Pieces {
+    uint4 l[NPL], u[NPL], w0[NPL], w1[NPL], w2[NPL];
+};
+
+// One direction of one channel plane.  L, P: scan and line length; the x
+// plane sits in LDS with pitch `pdw` dwords; ys receives u * h as fp32 in the
+// direction's line-major order (line l, position p at l * P + p).
+template <int NPL, bool VERT, bool REV>
+__device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t lam, rsrc_t u,
+                                         rsrc_t w, uint32_t wplane, const uint8_t *xs, u32x4 ys)
+{
+    Sel s[NPL];
+    uint32_t vo[NPL];
+    int jc[NPL];
+    bool valid[NPL];
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) {
+        const int p = lane + 64 * m;
+        valid[m] = p < P;
+        s[m] = make_sel(p, P);
+        jc[m] = p < P ? p : P - 1;
+        vo[m] = 16u * (uint32_t)jc[m];
+    }
+    const bool first_lane = lane == 0, last_lane = lane == 63;
+    const int NB = L / 8;
+    const uint32_t TB = 16u * (uint32_t)P;     // bytes of one block of a bf16 plane
+    auto boff = [&](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
+    auto load = [&](Pieces<NPL> &pc, int fb) {
+        const uint32_t so = boff(fb);
+#pragma unroll
+        for (int m = 0; m < NPL; ++m) {
+            pc.l[m] = ld128_nt(lam, vo[m], so);
+            pc.u[m] = ld128_nt(u, vo[m], so);
+            pc.w0[m] = ld128(w, vo[m], so);
+            pc.w1[m] = ld128(w, vo[m], so + wplane);
+            pc.w2[m] = ld128(w, vo[m], so + 2u * wplane);
+        }
+    };
+    float h[NPL];
+#pragma unroll
+    for (int m = 0; m < NPL; ++m)
+        h[m] = 0.f;
+
+    auto run_block = [&](const Pieces<NPL> &pc, int fb) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int i = 8 * fb + t;
+            const int e = REV ? 7 - t : t;              // element of the 8-line piece
+            const int ln = REV ? L - 1 - i : i;         // storage line of step i
+            // neighbours on the previous line: adjacent lanes by DPP, and the
+            // boundary lanes of neighbouring position groups by readlane
+            float left[NPL], right[NPL];
+#pragma unroll
+            for (int m = 0; m < NPL; ++m) {
+                left[m] = from_left<64>(h[m]);
+                right[m] = from_right<64>(h[m]);
+            }
+#pragma unroll
+            for (int m = 0; m < NPL; ++m) {
+                if (m > 0) {
+                    const float v = __int_as_float(
+                        __builtin_amdgcn_readlane(__float_as_int(h[m - 1]), 63));
+                    left[m] = first_lane ? v : left[m];
+                }
+                if (m + 1 < NPL) {
+                    const float v = __int_as_float(
+                        __builtin_amdgcn_readlane(__float_as_int(h[m + 1]), 0));
+                    right[m] = last_lane ? v : right[m];
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < NPL; ++m) {
+                const int row = VERT ? ln : jc[m];
+                const int col = VERT ? jc[m] : ln;
+                const float xv = bf_lo(lds_u16(xs, 4u * (uint32_t)(row * pdw) + 2u * (uint32_t)col));
+                const float inj = elem(pc.l[m], e, s[m].lo1, s[m].hi1) * xv;
+                float hn = inj;
+                if (i > 0) {
+                    hn = fmaf(elem(pc.w1[m], e, s[m].lo1, s[m].hi1), h[m], hn);
+                    hn = fmaf(elem(pc.w0[m], e, s[m].lo0, s[m].hi0), left[m], hn);
+                    hn = fmaf(elem(pc.w2[m], e, s[m].lo2, s[m].hi2), right[m], hn);
+                }
+                h[m] = hn;
+            }
+#pragma unroll
+            for (int m = 0; m < NPL; ++m) {
+                if (valid[m])
+                    st32_nt(ys, 4u * (uint32_t)(ln * P + lane + 64 * m), 0,
+                            __float_as_uint(elem(pc.u[m], e) * h[m]));
+            }
+        }
+        step_fence();
+    };
+
+    Pieces<NPL> A, B;
+    load(A, 0);
+    for (int fb = 0; fb < NB; fb += 2) {
+        if (fb + 1 < NB)
+            load(B, fb + 1);
+        run_block(A, fb);
+        if (fb + 1 < NB) {
+            if (fb + 2 < NB)
+                load(A, fb + 2);
+            run_block(B, fb + 1);
+        }
+    }
+}
+
+template <int NPL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
+    const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
+    const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H,
+    int W, Magic divC, Magic divCpg, Magic divNq)
+{
+    extern __shared__ uint32_t xs32[];
+    uint8_t *xs = reinterpret_cast<uint8_t *>(xs32);
+    const int pdw = wide_pitch_dw(W);
+    const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+    const int lane = threadIdx.x & 63;
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int b = mdiv(blk, divC);
+    const int c = blk - b * C;
+    const int g = mdiv(c, divCpg);
+    const int64_t HW = (int64_t)H * W;
+    const int64_t pc = ((int64_t)b * C + c) * HW;
+
+    // x plane -> LDS: coalesced 16-byte pieces into padded rows
+    {
+        const rsrc_t xr = make_rsrc(x + pc, (uint32_t)(2 * HW));
+        const int nq = W / 8;
+        const int n = H * nq;
+        for (int t = threadIdx.x; t < n; t += 256) {
+            const uint4 v = ld128(xr, 16u * (uint32_t)t, 0);
+            const int r = mdiv(t, divNq), q = t - r * nq;
+            uint32_t *dst = xs32 + r * pdw + 4 * q;
+            dst[0] = v.x;
+            dst[1] = v.y;
+            dst[2] = v.z;
+            dst[3] = v.w;
+        }
+    }
+    lds_barrier();
+
+    if ((mask >> d) & 1) {
+        const int s = __popc(mask & ((1 << d) - 1));
+        const int64_t pd = (((int64_t)s * B + b) * C + c) * HW;
+        const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
+        const rsrc_t rl = make_rsrc(lam + pd, (uint32_t)(2 * HW));
+        const rsrc_t ru = make_rsrc(u + pd, (uint32_t)(2 * HW));
+        const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
+        const u32x4 yd = make_sdesc(ys + pd, (uint32_t)(4 * HW));
+        const uint32_t wplane = (uint32_t)(2 * HW);
+        if (d == 0)
+            wide_dir<NPL, true, false>(lane, H, W, pdw, rl, ru, rw, wplane, xs, yd);
+        else if (d == 1)
+            wide_dir<NPL, true, true>(lane, H, W, pdw, rl, ru, rw, wplane, xs, yd);
+        else if (d == 2)
+            wide_dir<NPL, false, false>(lane, W, H, pdw, rl, ru, rw, wplane, xs, yd);
+        else
+            wide_dir<NPL, false, true>(lane, W, H, pdw, rl, ru, rw, wplane, xs, yd);
+    }
+}
+
+// y = sum over the directions, in direction-bit order, of the fp32 planes
+// written by fwd_wide_kernel.  One workgroup per 64 x 64 tile of one channel
+// plane; thread t owns row t / 4, columns 16 (t % 4) .. +15 of the tile.
+// Vertical planes are read in place; horizontal ones are stored transposed
+// ([column][row]) and turned around through LDS.
+__global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__ ys,
+                                                       bf16_t *__restrict__ y, int mask, int B,
+                                                       int C, int H, int W, int tiles_w,
+                                                       int tiles_hw, Magic divTilesW,
+                                                       Magic divTilesHW, Magic divC)
+{
+    __shared__ float T[kTile][kTile + 1];
+    const int64_t HW = (int64_t)H * W;
+    const int plane = mdiv((int)blockIdx.x, divTilesHW);              // b * C + c
+    const int local = (int)blockIdx.x - plane * tiles_hw;
+    const int tr = mdiv(local, divTilesW);
+    const int tc = local - tr * tiles_w;
+    const int R0 = tr * kTile, C0 = tc * kTile;
+    const int t = threadIdx.x;
+    const int r = t >> 2, c0 = 16 * (t & 3);
+    const int b = mdiv(plane, divC);
+    const int c = plane - b * C;
+    float acc[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+        acc[k] = 0.f;
+    int s = 0;
+    for (int d = 0; d < 4; ++d) {
+        if (!((mask >> d) & 1))
+            continue;
+        const float *src = ys + (((int64_t)s * B + b) * C + c) * HW;
+        if (d < 2) {
+            const int row = R0 + r;
+            if (row < H) {
+#pragma unroll
+                for (int k = 0; k < 16; ++k) {
+                    const int col = C0 + c0 + k;
+                    if (col < W)
+                        acc[k] += src[(int64_t)row * W + col];
+                }
+            }
+        } else {
+            // transposed plane: line (column) C0 + r, positions (rows) R0 + c0 + k
+            const int col = C0 + r;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                const int row = R0 + c0 + k;
+                T[r][c0 + k] = (col < W && row < H) ? src[(int64_t)col * H + row] : 0.f;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int k = 0; k < 16; ++k)
+                acc[k] += T[c0 + k][r];
+            __syncthreads();
+        }
+        ++s;
+    }
+    const int row = R0 + r;
+    if (row < H) {
+        bf16_t *dst = y + ((int64_t)b * C + c) * HW + (int64_t)row * W;
+#pragma unroll
+        for (int h8 = 0; h8 < 2; ++h8) {
+            const int col = C0 + c0 + 8 * h8;
+            if (col < W) {   // W is a multiple of 8
+                const uint4 v = make_uint4(pack2(acc[8 * h8], acc[8 * h8 + 1]),
+                                           pack2(acc[8 * h8 + 2], acc[8 * h8 + 3]),
+                                           pack2(acc[8 * h8 + 4], acc[8 * h8 + 5]),
+                                           pack2(acc[8 * h8 + 6], acc[8 * h8 + 7]));
+                gst128(reinterpret_cast<uint4 *>(dst + col), v);
+            }
+        }
+    }
+}
+
+template <int NPL>
+hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds)
+{
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL>), dim3((unsigned)(p.B * p.C)), dim3(256), lds, st,
+                       (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
+                       (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
+                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
+                       make_magic((uint32_t)(p.W / 8)));
+    return hipGetLastError();
+}
+
+size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
+
+}  // namespace
+
+bool wide_supported(const Problem &p)
+{
+    if (p.dtype != 1 || p.H % 8 != 0 || p.W % 8 != 0)
+        return false;
+    const int side = p.H > p.W ? p.H : p.W;
+    if (side > 64 * kMaxNpl)
+        return false;
+    int dev = 0, lds_max = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
+            hipSuccess)
+        return false;
+    return wide_lds_bytes(p.H, p.W) <= (size_t)lds_max;
+}
+
+hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
+{
+    const int D = __builtin_popcount(p.mask);
+    const int64_t n = (int64_t)p.B * p.C * p.H * p.W;
+    float *ys = nullptr;
+    hipError_t e = scratch_alloc((void **)&ys, (size_t)D * n * sizeof(float), st);
+    if (e != hipSuccess)
+        return e;
+    const size_t lds = wide_lds_bytes(p.H, p.W);
+    const int side = p.H > p.W ? p.H : p.W;
+    const int npl = (side + 63) / 64;
+    e = npl <= 2 ? fwd_wide_t<2>(p, st, ys, lds)
+        : npl == 3 ? fwd_wide_t<3>(p, st, ys, lds)
+                   : fwd_wide_t<4>(p, st, ys, lds);
+    if (e == hipSuccess) {
+        const int tiles_w = (p.W + kTile - 1) / kTile;
+        const int tiles_h = (p.H + kTile - 1) / kTile;
+        const int64_t nblk = (int64_t)p.B * p.C * tiles_w * tiles_h;
+        hipLaunchKernelGGL(sum_wide_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
+                           (const float *)ys, (bf16_t *)p.y, p.mask, p.B, p.C, p.H, p.W, tiles_w,
+                           tiles_w * tiles_h, make_magic((uint32_t)tiles_w),
+                           make_magic((uint32_t)(tiles_w * tiles_h)), make_magic((uint32_t)p.C));
+        e = hipGetLastError();
+    }
+    hipError_t e2 = scratch_free(ys, st);
+    return e != hipSuccess ? e : e2;
+}
+
+}  // namespace gspn

@@ -90,6 +90,14 @@ EDGE = [
     case("med64-all-cpg9", 1, 18, 2, 64, 64),
     case("med56-T2B-cpg12", 2, 24, 2, 56, 56, dirs=1),
     case("med64-peaky", 1, 16, 1, 64, 64, sigma=2.0),
+    # lines longer than a wave (forward: several positions per lane, fp32
+    # direction planes summed by a tiled kernel): ragged position groups,
+    # unused groups, both orientations, direction subsets, peaky weights
+    case("wide-72x136", 1, 4, 2, 72, 136),
+    case("wide-256x64-fwd", 1, 3, 1, 256, 64, backward=False),
+    case("wide-128x128-dirs9", 1, 6, 3, 128, 128, dirs=9, backward=False),
+    case("wide-200x248-peaky", 1, 2, 1, 200, 248, sigma=2.0, backward=False),
+    case("wide-96x80-R2L", 2, 4, 4, 96, 80, dirs=8),
 ]
 
 
@@ -102,7 +110,8 @@ def test_parity_against_oracle(wl):
 
 @pytest.mark.parametrize("wl", [case("nan-taps-14x14", 2, 8, 2, 14, 14),
                                 case("nan-taps-64x64", 1, 4, 1, 64, 64),
-                                case("nan-taps-general", 1, 2, 1, 3, 80)], ids=lambda w: w.name)
+                                case("nan-taps-general", 1, 2, 1, 3, 80),
+                                case("nan-taps-wide", 1, 2, 1, 72, 136)], ids=lambda w: w.name)
 def test_ignored_taps_may_hold_nan(wl):
     inputs = gi.make_inputs(wl, with_dy=True)
     clean = run_gpu(inputs, wl, True)
