@@ -128,6 +128,12 @@ __device__ __forceinline__ void st128_nt(const u32x4 &d, uint32_t voff, uint32_t
     asm volatile("buffer_store_dwordx4 %0, %1, %2, %3 offen nt\n\ts_nop 7\n\ts_nop 7"
                  : : "v"(t), "v"(voff), "s"(d), "s"(soff) : "memory");
 }
+__device__ __forceinline__ void gst64(uint2 *p, uint32_t a, uint32_t b)
+{
+    const u32x2 t = {a, b};
+    asm volatile("global_store_dwordx2 %0, %1, off\n\ts_nop 7\n\ts_nop 7" : : "v"(p), "v"(t)
+                 : "memory");
+}
 __device__ __forceinline__ void gst128(uint4 *p, uint4 v)
 {
     const u32x4 t = {v.x, v.y, v.z, v.w};

@@ -199,9 +199,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 
 // y = sum over the directions, in direction-bit order, of the fp32 planes
 // written by fwd_wide_kernel.  One workgroup per 64 x 64 tile of one channel
-// plane; thread t owns row t / 4, columns 16 (t % 4) .. +15 of the tile.
-// Vertical planes are read in place; horizontal ones are stored transposed
-// ([column][row]) and turned around through LDS.
+// plane.  Thread (wave v, lane l) owns columns 4 (l % 16) .. +3 of rows
+// 16 k + 4 v + l / 16 (k < 4): each global access of a wave reads 16 bytes
+// per lane, four 256-byte row segments.  Vertical planes are read in place;
+// horizontal ones are stored transposed ([column][row]) and turned around
+// through LDS (pitch 65: the transposed reads are conflict-free).
 __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__ ys,
                                                        bf16_t *__restrict__ y, int mask, int B,
                                                        int C, int H, int W, int tiles_w,
@@ -215,59 +217,66 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
     const int tr = mdiv(local, divTilesW);
     const int tc = local - tr * tiles_w;
     const int R0 = tr * kTile, C0 = tc * kTile;
-    const int t = threadIdx.x;
-    const int r = t >> 2, c0 = 16 * (t & 3);
+    const int v = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int l = threadIdx.x & 63;
     const int b = mdiv(plane, divC);
     const int c = plane - b * C;
-    float acc[16];
+    const int c4 = 4 * (l & 15);                    // first of this lane's 4 columns
+    const int r1 = 4 * v + (l >> 4);                // row within a 16-row band
+    float acc[4][4];
 #pragma unroll
-    for (int k = 0; k < 16; ++k)
-        acc[k] = 0.f;
+    for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            acc[k][e] = 0.f;
     int s = 0;
     for (int d = 0; d < 4; ++d) {
         if (!((mask >> d) & 1))
             continue;
         const float *src = ys + (((int64_t)s * B + b) * C + c) * HW;
         if (d < 2) {
-            const int row = R0 + r;
-            if (row < H) {
 #pragma unroll
-                for (int k = 0; k < 16; ++k) {
-                    const int col = C0 + c0 + k;
-                    if (col < W)
-                        acc[k] += src[(int64_t)row * W + col];
+            for (int k = 0; k < 4; ++k) {
+                const int row = R0 + 16 * k + r1, col = C0 + c4;
+                if (row < H && col < W) {   // W is a multiple of 8: 4 columns in or out
+                    const float4 q = *reinterpret_cast<const float4 *>(src + (int64_t)row * W + col);
+                    acc[k][0] += q.x;
+                    acc[k][1] += q.y;
+                    acc[k][2] += q.z;
+                    acc[k][3] += q.w;
                 }
             }
         } else {
-            // transposed plane: line (column) C0 + r, positions (rows) R0 + c0 + k
-            const int col = C0 + r;
+            // transposed plane: line (column) C0 + 16 k + r1, positions R0 + c4 .. +3
 #pragma unroll
-            for (int k = 0; k < 16; ++k) {
-                const int row = R0 + c0 + k;
-                T[r][c0 + k] = (col < W && row < H) ? src[(int64_t)col * H + row] : 0.f;
+            for (int k = 0; k < 4; ++k) {
+                const int tcol = C0 + 16 * k + r1, trow = R0 + c4;
+                float4 q = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (tcol < W && trow < H)   // H is a multiple of 8
+                    q = *reinterpret_cast<const float4 *>(src + (int64_t)tcol * H + trow);
+                float *t = &T[16 * k + r1][c4];
+                t[0] = q.x;
+                t[1] = q.y;
+                t[2] = q.z;
+                t[3] = q.w;
             }
             __syncthreads();
 #pragma unroll
-            for (int k = 0; k < 16; ++k)
-                acc[k] += T[c0 + k][r];
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[k][e] += T[c4 + e][16 * k + r1];
             __syncthreads();
         }
         ++s;
     }
-    const int row = R0 + r;
-    if (row < H) {
-        bf16_t *dst = y + ((int64_t)b * C + c) * HW + (int64_t)row * W;
+    bf16_t *dst = y + ((int64_t)b * C + c) * HW;
 #pragma unroll
-        for (int h8 = 0; h8 < 2; ++h8) {
-            const int col = C0 + c0 + 8 * h8;
-            if (col < W) {   // W is a multiple of 8
-                const uint4 v = make_uint4(pack2(acc[8 * h8], acc[8 * h8 + 1]),
-                                           pack2(acc[8 * h8 + 2], acc[8 * h8 + 3]),
-                                           pack2(acc[8 * h8 + 4], acc[8 * h8 + 5]),
-                                           pack2(acc[8 * h8 + 6], acc[8 * h8 + 7]));
-                gst128(reinterpret_cast<uint4 *>(dst + col), v);
-            }
-        }
+    for (int k = 0; k < 4; ++k) {
+        const int row = R0 + 16 * k + r1, col = C0 + c4;
+        if (row < H && col < W)
+            gst64(reinterpret_cast<uint2 *>(dst + (int64_t)row * W + col),
+                  pack2(acc[k][0], acc[k][1]), pack2(acc[k][2], acc[k][3]));
     }
 }
 
