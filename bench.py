@@ -177,12 +177,17 @@ def main() -> int:
         f"({step_gbs / HBM_PEAK_GBS:.1%} of peak)")
 
     if bwd_ms > fwd_ms:
-        dom, dom_ms, dom_bytes = "gspn_scan_bwd", bwd_ms, nbytes["bwd"]
+        dom, call, dom_ms, dom_bytes = "gspn_scan_bwd", "bwd", bwd_ms, nbytes["bwd"]
     else:
-        dom, dom_ms, dom_bytes = "gspn_scan_fwd", fwd_ms, nbytes["fwd"]
+        dom, call, dom_ms, dom_bytes = "gspn_scan_fwd", "fwd", fwd_ms, nbytes["fwd"]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    # measured HBM bytes of the same call (FETCH_SIZE + WRITE_SIZE counters, scaled by a
+    # plain copy), kept in profiles/ for the current kernel sources only
+    from paper_2606_00746_amd import profiling
+    traffic = profiling.load_traffic(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.txt"), call)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": traffic,
                 "kernel": dom, "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes}
 
     out = {

@@ -1,0 +1,156 @@
+"""Summaries of rocprofv3 runs, for ``profiles/`` and the benchmark's traffic figure.
+
+Kernel-trace summary (per-kernel call count and durations)::
+
+    python -m paper_2606_00746_amd.profiling trace RESULTS_DB OUT.txt --command "..."
+
+HBM traffic record from two counter runs of ``bench.py --copy-calibration MIB``,
+one collecting ``FETCH_SIZE`` and one ``WRITE_SIZE`` (KiB per dispatch)::
+
+    python -m paper_2606_00746_amd.profiling traffic FETCH_CSV WRITE_CSV OUT.json \\
+        --workload NAME --copy-mib MIB --command "..."
+
+Each counter is scaled by what it reads for the plain copy of known size that
+the same run makes, so the record holds bytes.  The record carries a hash of
+the kernel sources: the benchmark reports the figure only while the sources
+are unchanged.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import json
+import os
+import subprocess
+import sys
+import tempfile
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_ROOT = os.path.dirname(_HERE)
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def source_hash() -> str:
+    """sha256 over the kernel sources, the public header and the build flags."""
+    h = hashlib.sha256()
+    csrc = os.path.join(_HERE, "csrc")
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
+                   if f.endswith((".hip", ".hpp", ".cpp")))
+    files += [os.path.join(_ROOT, "include", "gspn.h"), os.path.join(_HERE, "build.py")]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def short_name(name: str) -> str:
+    for pre in ("void ", "gspn::(anonymous namespace)::"):
+        name = name.replace(pre, "")
+    return name.split("(")[0]
+
+
+def call_of(kernel: str) -> str | None:
+    """Which library call a kernel belongs to ('fwd' or 'bwd'), None for others."""
+    k = short_name(kernel)
+    if k.startswith(("fwd_", "sum_")):
+        return "fwd"
+    if k.startswith(("bwd_", "dw_sum", "dw_reduce", "cast_")):
+        return "bwd"
+    return None
+
+
+def trace_summary(db: str, out: str, command: str) -> str:
+    with tempfile.TemporaryDirectory() as d:
+        subprocess.run(["rocpd2summary", "-i", os.path.abspath(db), "-f", "csv", "-o", "s", "-d", d],
+                       check=True, capture_output=True, cwd=d)
+        rows = list(csv.DictReader(open(os.path.join(d, "s_kernels_summary.csv"))))
+    lines = ["# rocprofv3 kernel-trace summary", f"# command: {command}",
+             "# from: rocpd2summary of the run's results database (durations in ns)", "",
+             f"{'kernel':<58} {'calls':>6} {'avg_ns':>11} {'min_ns':>10} {'max_ns':>10} {'pct':>6}"]
+    for r in rows:
+        lines.append(f"{short_name(r['Name'])[:58]:<58} {r['Calls']:>6} "
+                     f"{float(r['Average (Nsec)']):>11.0f} {float(r['Min (Nsec)']):>10.0f} "
+                     f"{float(r['Max (Nsec)']):>10.0f} {float(r['Percent (Inc)']):>6.1f}")
+    text = "\n".join(lines) + "\n"
+    with open(out, "w") as f:
+        f.write(text)
+    return text
+
+
+def _counter(path: str) -> dict:
+    vals = collections.defaultdict(list)
+    for r in csv.DictReader(open(path)):
+        vals[r["Kernel_Name"]].append(float(r["Counter_Value"]))
+    return vals
+
+
+def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
+                   command: str) -> dict:
+    fetch, write = _counter(fetch_csv), _counter(write_csv)
+    copy = [k for k in fetch if short_name(k) == COPY_KERNEL]
+    if not copy:
+        raise SystemExit(f"no {COPY_KERNEL} dispatch in {fetch_csv}: run bench.py with "
+                         "--copy-calibration")
+    copy_bytes = copy_mib * (1 << 20)
+    f_copy = fetch[copy[0]][0] * 1024.0
+    w_copy = write[copy[0]][0] * 1024.0
+    scale_f, scale_w = copy_bytes / f_copy, copy_bytes / w_copy
+    kernels, calls = {}, collections.defaultdict(float)
+    for k, v in fetch.items():
+        call = call_of(k)
+        if call is None:
+            continue
+        fb = sum(v) / len(v) * 1024.0 * scale_f
+        wb = sum(write[k]) / len(write[k]) * 1024.0 * scale_w
+        kernels[short_name(k)] = {"call": call, "fetch_bytes": round(fb), "write_bytes": round(wb),
+                                  "dispatches": len(v)}
+        calls[call] += fb + wb
+    return {"workload": workload, "source_hash": source_hash(), "command": command,
+            "copy_calibration": {"bytes": copy_bytes, "fetch_kib": f_copy / 1024.0,
+                                 "write_kib": w_copy / 1024.0, "fetch_scale": scale_f,
+                                 "write_scale": scale_w},
+            "kernels": kernels, "bytes_per_call": {k: round(v) for k, v in calls.items()}}
+
+
+def load_traffic(path: str, call: str) -> float | None:
+    """Bytes per call from a traffic record, None if absent or made from other sources."""
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_hash") != source_hash():
+        return None
+    return rec.get("bytes_per_call", {}).get(call)
+
+
+def main(argv=None) -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    t = sub.add_parser("trace")
+    t.add_argument("db")
+    t.add_argument("out")
+    t.add_argument("--command", required=True)
+    c = sub.add_parser("traffic")
+    c.add_argument("fetch_csv")
+    c.add_argument("write_csv")
+    c.add_argument("out")
+    c.add_argument("--workload", required=True)
+    c.add_argument("--copy-mib", type=int, required=True)
+    c.add_argument("--command", required=True)
+    a = ap.parse_args(argv)
+    if a.cmd == "trace":
+        sys.stdout.write(trace_summary(a.db, a.out, a.command))
+    else:
+        rec = traffic_record(a.fetch_csv, a.write_csv, a.workload, a.copy_mib, a.command)
+        with open(a.out, "w") as f:
+            json.dump(rec, f, indent=1)
+            f.write("\n")
+        print(json.dumps(rec, indent=1))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())
