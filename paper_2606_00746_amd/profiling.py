@@ -95,8 +95,12 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
         raise SystemExit(f"no {COPY_KERNEL} dispatch in {fetch_csv}: run bench.py with "
                          "--copy-calibration")
     copy_bytes = copy_mib * (1 << 20)
-    f_copy = fetch[copy[0]][0] * 1024.0
-    w_copy = write[copy[0]][0] * 1024.0
+    # the calibration copy is the copy dispatch that writes the most (small
+    # input uploads may run the same kernel); both runs dispatch in one order
+    wl = write[copy[0]]
+    at = max(range(len(wl)), key=lambda i: wl[i])
+    f_copy = fetch[copy[0]][at] * 1024.0
+    w_copy = wl[at] * 1024.0
     scale_f, scale_w = copy_bytes / f_copy, copy_bytes / w_copy
     kernels, calls = {}, collections.defaultdict(float)
     for k, v in fetch.items():

@@ -1,0 +1,55 @@
+"""The profiling helpers: traffic records scale counters by the copy
+calibration, belong to the kernel sources they were made from, and the
+benchmark ignores them once those sources change."""
+import json
+
+from paper_2606_00746_amd import profiling
+
+HEADER = ('"Correlation_Id","Dispatch_Id","Agent_Id","Queue_Id","Process_Id","Thread_Id",'
+          '"Grid_Size","Kernel_Id","Kernel_Name","Workgroup_Size","LDS_Block_Size",'
+          '"Scratch_Size","VGPR_Count","Accum_VGPR_Count","SGPR_Count","Counter_Name",'
+          '"Counter_Value","Start_Timestamp","End_Timestamp"\n')
+
+
+def _csv(path, counter, rows):
+    with open(path, "w") as f:
+        f.write(HEADER)
+        for i, (kernel, value) in enumerate(rows):
+            f.write(f'{i},{i},"Agent 1",1,1,1,64,1,"{kernel}",256,0,0,8,0,16,"{counter}",{value},0,1\n')
+
+
+def test_traffic_record_scales_by_copy(tmp_path):
+    copy = "__amd_rocclr_copyBuffer(char const*, char*)"
+    fwd = "void gspn::(anonymous namespace)::fwd_med_kernel<64, 64>(int)"
+    bwd = "void gspn::(anonymous namespace)::bwd_med_kernel<64, 64, 1>(int)"
+    dws = "void gspn::(anonymous namespace)::dw_sum_kernel<64>(int)"
+    # a small upload copy first, then the 4 MiB calibration copy: its counter
+    # reads half the bytes for FETCH_SIZE and all of them for WRITE_SIZE
+    _csv(tmp_path / "f.csv", "FETCH_SIZE", [(copy, 1.0), (copy, 2048.0), (fwd, 100.0), (bwd, 300.0),
+                                           (dws, 50.0), (fwd, 100.0)])
+    _csv(tmp_path / "w.csv", "WRITE_SIZE", [(copy, 2.0), (copy, 4096.0), (fwd, 10.0), (bwd, 200.0),
+                                           (dws, 5.0), (fwd, 10.0)])
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd")
+    assert rec["copy_calibration"]["fetch_scale"] == 2.0
+    assert rec["copy_calibration"]["write_scale"] == 1.0
+    assert rec["kernels"]["fwd_med_kernel<64, 64>"]["fetch_bytes"] == 200 * 1024
+    assert rec["bytes_per_call"]["fwd"] == (200 + 10) * 1024
+    assert rec["bytes_per_call"]["bwd"] == (600 + 200 + 100 + 5) * 1024
+    assert rec["source_hash"] == profiling.source_hash()
+
+
+def test_traffic_ignored_for_other_sources(tmp_path):
+    rec = {"source_hash": profiling.source_hash(), "bytes_per_call": {"bwd": 123}}
+    p = tmp_path / "t.txt"
+    p.write_text(json.dumps(rec))
+    assert profiling.load_traffic(str(p), "bwd") == 123
+    rec["source_hash"] = "0" * 64
+    p.write_text(json.dumps(rec))
+    assert profiling.load_traffic(str(p), "bwd") is None
+    assert profiling.load_traffic(str(tmp_path / "missing.txt"), "bwd") is None
+
+
+def test_kernels_map_to_calls():
+    assert profiling.call_of("void gspn::(anonymous namespace)::sum_wide_kernel(float)") == "fwd"
+    assert profiling.call_of("gspn::(anonymous namespace)::dw_reduce_kernel(float)") == "bwd"
+    assert profiling.call_of("__amd_rocclr_copyBuffer") is None
