@@ -28,17 +28,21 @@
  * Layouts.  D = number of directions in the mask; per-direction tensors are
  * stacked in increasing direction-bit order.  Shared tensors are pixel-major:
  *   x, y, dy, dx           [B][C][H][W]          element (r, c) at r*W + c
- * Per-direction tensors are line-major: every line scanned by the direction
- * is contiguous, so the scan reads whole lines (rows for vertical scans,
- * columns for horizontal ones):
+ * Per-direction tensors are blocked line-major: the lines a direction scans
+ * (storage rows for vertical scans, storage columns for horizontal ones) are
+ * grouped in blocks of 8 consecutive lines, and inside a block the 8 values
+ * of one line position are adjacent:
  *   lam, u, dlam, du       [D][B][C][plane]
  *   w, dw                  [D][B][G][3][plane]
- *   plane of a vertical direction (T2B, B2T):    element (r, c) at r*W + c
- *   plane of a horizontal direction (L2R, R2L):  element (r, c) at c*H + r
- * i.e. horizontal-direction planes are stored transposed ([W][H]).  A
- * producer (for instance the 1x1 convolutions that predict lam, u and w)
- * can write this layout directly; it costs nothing compared with the
- * pixel-major one.
+ *   plane of L lines of P positions, line l, position p at
+ *       8*P*(l/8) + n*p + l%8,   n = min(8, L - 8*(l/8))
+ *   vertical direction (T2B, B2T):    line = row r, position = column c,
+ *                                     L = H, P = W
+ *   horizontal direction (L2R, R2L):  line = column c, position = row r,
+ *                                     L = W, P = H
+ * (the last block holds L%8 lines when L is not a multiple of 8; a plane
+ * has exactly H*W elements).  A producer (for instance the 1x1 convolutions
+ * that predict lam, u and w) can write this layout directly.
  *
  * Ownership and threading: all pointers are device pointers owned by the
  * caller; the library keeps none of them after a call returns.  Outputs are
@@ -46,8 +50,9 @@
  * Buffers of one call must not overlap.  Every base pointer must be 16-byte
  * aligned.  Calls are asynchronous on `stream` (a hipStream_t; NULL is the
  * null stream) and never synchronise the device.  gspn_scan_bwd may take
- * stream-ordered scratch memory from the device's default memory pool; it
- * is released on the same stream.  Calls are thread-safe.
+ * stream-ordered scratch memory from the device's default memory pool, and so
+ * may gspn_scan_fwd for planes with a side above 64; it is released on the
+ * same stream.  Calls are thread-safe.
  *
  * Errors: every argument check runs on the host before any HIP call, so an
  * invalid call has no effect on the device.  A failed HIP call returns

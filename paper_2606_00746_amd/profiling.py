@@ -33,12 +33,12 @@ COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
 def source_hash() -> str:
-    """sha256 over the kernel sources, the public header and the build flags."""
+    """sha256 over the kernel sources and the build flags."""
     h = hashlib.sha256()
     csrc = os.path.join(_HERE, "csrc")
     files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
                    if f.endswith((".hip", ".hpp", ".cpp")))
-    files += [os.path.join(_ROOT, "include", "gspn.h"), os.path.join(_HERE, "build.py")]
+    files.append(os.path.join(_HERE, "build.py"))
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
