@@ -104,6 +104,8 @@ extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, cons
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (med_supported(p))
         return hip_status(launch_fwd_med(p, s));
+    if (tiny_supported(p))
+        return hip_status(launch_fwd_tiny(p, s));
     if (H <= kSmallSide && W <= kSmallSide)
         return hip_status(launch_fwd_small(p, s));
     if (wide_supported(p))
@@ -133,6 +135,8 @@ extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, cons
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (med_supported(p))
         return hip_status(launch_bwd_med(p, s));
+    if (tiny_supported(p))
+        return hip_status(launch_bwd_tiny(p, s));
     if (H <= kSmallSide && W <= kSmallSide)
         return hip_status(launch_bwd_small(p, s));
     return hip_status(launch_bwd_general(p, s));

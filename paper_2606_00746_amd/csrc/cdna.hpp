@@ -50,6 +50,10 @@ __device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
 {
     return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
 }
+__device__ __forceinline__ uint32_t ld32(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
 __device__ __forceinline__ uint4 ld128(rsrc_t r, uint32_t voff, uint32_t soff)
 {
     const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);

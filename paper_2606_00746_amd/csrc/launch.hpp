@@ -17,6 +17,9 @@ constexpr int kSmallSide = 64;
 
 hipError_t launch_fwd_small(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_small(const Problem &p, hipStream_t s);
+bool tiny_supported(const Problem &p);
+hipError_t launch_fwd_tiny(const Problem &p, hipStream_t s);
+hipError_t launch_bwd_tiny(const Problem &p, hipStream_t s);
 bool med_supported(const Problem &p);
 hipError_t launch_fwd_med(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_med(const Problem &p, hipStream_t s);

@@ -98,6 +98,14 @@ EDGE = [
     case("wide-128x128-dirs9", 1, 6, 3, 128, 128, dirs=9, backward=False),
     case("wide-200x248-peaky", 1, 2, 1, 200, 248, sigma=2.0, backward=False),
     case("wide-96x80-R2L", 2, 4, 4, 96, 80, dirs=8),
+    # planes of at most 16 x 16 (whole planes staged in LDS, four channels per
+    # wave): idle channel slots, one channel per group, groups split into
+    # chunks (fp32 partials), every size, direction subsets, peaky weights
+    case("tiny-14x14-cpg6-dirs6", 2, 12, 2, 14, 14, dirs=6),
+    case("tiny-8x8-R2L-cpg1", 1, 3, 3, 8, 8, dirs=8),
+    case("tiny-12x12-peaky", 1, 20, 4, 12, 12, sigma=2.0),
+    case("tiny-16x16-cpg72", 1, 144, 2, 16, 16),
+    case("tiny-14x14-T2B-cpg33", 1, 33, 1, 14, 14, dirs=1),
 ]
 
 
