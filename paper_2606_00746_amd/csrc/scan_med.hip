@@ -47,7 +47,7 @@ namespace {
 using namespace cdna;
 
 constexpr int kYPitch = 68;                // fp32 LDS row pitch (16-byte rows, conflict-free b128)
-constexpr int kDxPitch = 65;               // fp32 LDS row pitch of the dx plane (odd: column walks conflict-free)
+constexpr int kPlanePitch = 64;            // dwords per row of a wave's LDS plane (XOR-swizzled)
 constexpr int kPrefetch = 16;              // steps of per-step row loads in flight (backward)
 constexpr int kLdsAhead = 3;               // steps of staged (x, dy) LDS reads in flight (backward)
 
@@ -252,19 +252,27 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 // backward
 // ---------------------------------------------------------------------------
 
-// Per-step dw terms are summed over the workgroup's channels through LDS
-// slots[buf][st][k][q][j]: two buffers of kBatch steps, 3 taps, kSlots channel
-// slots (slots of absent channels stay zero) and 64 positions.  A wave writes
-// one contiguous row per tap; a reducing lane reads its kSlots slots, all
-// conflict-free.  After the barrier that closes a batch the reducing lanes
-// read it, and they sum and store it while the next batch runs.
-constexpr int kSlots = 8;
-constexpr int kBatch = 2;
-constexpr int kSlotFloats = 2 * kBatch * 3 * kSlots * 64;
+// A wave's LDS plane (x and dy staged for the horizontal directions, then the
+// fp32 dx accumulator) has rows of 64 dwords with element (r, c) at
+// r * 64 + (c ^ r): a row walk and a column walk are both free of bank
+// conflicts, at no padding.
+__device__ __forceinline__ int pidx(int r, int c) { return r * kPlanePitch + (c ^ r); }
 
-__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int st, int k, int q)
+// The weight gradient of step i is sum_c a_c,i[j] h_c,i-1[j+k-1] over the
+// workgroup's channels.  Each wave writes its a_i and h_{i-1} to LDS
+// slots[buf][st][v][q][j] (v: a or h; q: channel slot, absent channels stay
+// zero; j: position), two buffers of kBatch steps, one barrier per batch.
+// After the barrier the wave that owns step st of the batch (one per SIMD)
+// reads the 2 x kSlots values of its position, forms the three products with
+// the neighbours' h from adjacent lanes (DPP), sums them in channel order
+// and stores the line while the next batch runs.
+constexpr int kSlots = 8;
+constexpr int kBatch = 4;
+constexpr int kSlotFloats = 2 * kBatch * 2 * kSlots * 64;
+
+__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int st, int v, int q)
 {
-    return slots + (((buf * kBatch + st) * 3 + k) * kSlots + q) * 64;
+    return slots + (((buf * kBatch + st) * 2 + v) * kSlots + q) * 64;
 }
 
 struct BwdArgs {
@@ -273,20 +281,20 @@ struct BwdArgs {
     rsrc_t w;              // the 3 tap planes of (direction, group)
     u32x4 dlam, du;        // direction planes (store descriptors)
     u32x4 dw;              // 3 tap planes: final bf16 dw or fp32 partial
-    float *Xq;             // this wave's dx plane in LDS, [H][kDxPitch]
+    float *Xq;             // this wave's LDS plane (pidx layout)
     float *slots;          // dw term slots
     int wave, cw;          // this wave, waves of the workgroup
     bool partial;          // dw holds fp32 partials
     bool first;            // first direction adding into the dx plane: store
 };
 
-// One direction of the backward.  D: direction index.  U: passes of 64 sums
-// each wave makes per batch of the weight-gradient reduction (1 for 6 or more
-// waves, 3 for 2 to 5, 6 for one).  Horizontal
+// One direction of the backward.  D: direction index.  IMM: the workgroup has
+// fewer waves than steps in a batch, so the reduction is not deferred.
+// Horizontal
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, int U>
+template <int H, int W, int D, bool IMM>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
@@ -303,7 +311,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
     auto line_of = [](int i) { return REV ? L - 1 - i : i; };   // storage line of step i
     auto rowoff = [&](int i) -> uint32_t { return 2u * (uint32_t)(line_of(i) * W); };
-    auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)(jj * kDxPitch + line_of(i))); };
+    auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)pidx(jj, line_of(i))); };
 
     // --- reverse sweep: adjoint a_i -------------------------------------
     float ahist[L];
@@ -397,55 +405,43 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             rx[VERT ? i : 0] = ld16(A.x, vr, rowoff(i));
     }
 
-    // Reduction roles: a batch has kBatch * 192 sums, one per (step st, tap
-    // k, position jp), numbered c = 192 st + 64 k + jp.  They are spread evenly
-    // over the workgroup's waves (48 per wave for 8 waves), so no wave waits
-    // for another at the barrier: wave w owns c = w * per + j + 64 uu.
-    constexpr int kSums = kBatch * 192;
-    const int per = (kSums + A.cw - 1) / A.cw;
-    float pr[U][kSlots];
-    auto owns = [&](int uu) {
-        return j + 64 * uu < per && A.wave * per + j + 64 * uu < kSums;
+    // Reduction roles: step st of a batch belongs to wave st (waves 0..3, one
+    // per SIMD); with fewer than kBatch waves (IMM) each wave takes several
+    // steps and reduces them right after the barrier.
+    float pa[kSlots], ph[kSlots];
+    auto read_step = [&](int buf, int st) {
+#pragma unroll
+        for (int q = 0; q < kSlots; ++q) {
+            pa[q] = slot_ptr(A.slots, buf, st, 0, q)[j];
+            ph[q] = slot_ptr(A.slots, buf, st, 1, q)[j];
+        }
     };
-    // issue the slot reads of the batch that ends at step i
-    auto issue_dw = [&](int i) {
-        const int buf = (i >> 1) & 1;
+    // step i's weight gradient: the three products summed in channel order
+    auto reduce_step = [&](int i) {
+        float d0 = 0.f, d1 = 0.f, d2 = 0.f;
 #pragma unroll
-        for (int uu = 0; uu < U; ++uu) {
-            if (owns(uu)) {
-                const int c = A.wave * per + j + 64 * uu;
-                const int st = c >= 192 ? 1 : 0, p = c - 192 * st;
-#pragma unroll
-                for (int q = 0; q < kSlots; ++q)
-                    pr[uu][q] = slot_ptr(A.slots, buf, st, p >> 6, q)[p & 63];
+        for (int q = 0; q < kSlots; ++q) {
+            d0 = fmaf(pa[q], from_left<64>(ph[q]), d0);
+            d1 = fmaf(pa[q], ph[q], d1);
+            d2 = fmaf(pa[q], from_right<64>(ph[q]), d2);
+        }
+        if (j < P) {
+            const int l = line_of(i);
+            if (A.partial) {
+                // line-major fp32 partials: the wave writes whole lines
+                const uint32_t f = (uint32_t)(l * P + j);
+                st32_nt(A.dw, 4u * f, 0, __float_as_uint(d0));
+                st32_nt(A.dw, 4u * (f + H * W), 0, __float_as_uint(d1));
+                st32_nt(A.dw, 4u * (f + 2 * H * W), 0, __float_as_uint(d2));
+            } else {
+                const uint32_t el = 2u * (uint32_t)lm_offset(l, j, L, P);
+                st16(A.dw, el, 0, pack1(d0));
+                st16(A.dw, el + PL2, 0, pack1(d1));
+                st16(A.dw, el + 2 * PL2, 0, pack1(d2));
             }
         }
     };
-    // sum (in channel-slot order) and store the batch that ends at step i
-    auto flush_dw = [&](int i) {
-#pragma unroll
-        for (int uu = 0; uu < U; ++uu) {
-            if (owns(uu)) {
-                const int c = A.wave * per + j + 64 * uu;
-                const int st = c >= 192 ? 1 : 0, p = c - 192 * st;
-                const int k = p >> 6, jp = p & 63;
-                float v = 0.f;
-#pragma unroll
-                for (int q = 0; q < kSlots; ++q)
-                    v += pr[uu][q];
-                const int l = line_of(i - 1 + st);            // storage line of the sum
-                if (jp < P) {
-                    if (A.partial) {
-                        // line-major fp32 partials: one row of a tap plane per line
-                        st32(A.dw, 4u * (uint32_t)(k * H * W + l * P + jp), 0, __float_as_uint(v));
-                    } else {
-                        const uint32_t el = (uint32_t)lm_offset(l, jp, L, P);
-                        st16(A.dw, 2u * el + PL2 * (uint32_t)k, 0, pack1(v));
-                    }
-                }
-            }
-        }
-    };
+    const bool reducer = A.wave < kBatch;
 
     float h = 0.f;
     // this block's du and dlam as bf16 pairs in storage element order; the
@@ -460,7 +456,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     }
     float dx_next = 0.f;     // vertical: dx plane value of this step's row, read a step ahead
     if (VERT && !A.first)
-        dx_next = A.Xq[line_of(0) * kDxPitch + jj];
+        dx_next = A.Xq[pidx(line_of(0), jj)];
 #pragma unroll
     for (int fb = 0; fb < NB; ++fb) {
         if (fb + 2 < NB)
@@ -490,13 +486,6 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 h = tri_step(hp, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
                              elem(p2[fb], e, s.lo2, s.hi2), lv * xv);
             const float a = ahist[i];
-            // dw terms of line i (zero on line 0; taps leaving the grid read zeros)
-            float t0 = 0.f, t1 = 0.f, t2 = 0.f;
-            if (i > 0) {
-                t0 = a * from_left<64>(hp);
-                t1 = a * hp;
-                t2 = a * from_right<64>(hp);
-            }
             const float duv = dyv * h, dlv = a * xv;
             if ((t & 1) == 0) {
                 du0 = duv;
@@ -510,27 +499,35 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 // this wave is the only writer of its dx plane: the row of the
                 // next step is read one step ahead, added to and written back
                 // (an LDS float atomic costs several times more here)
-                float *xa = A.Xq + line_of(i) * kDxPitch + jj;
+                float *xa = A.Xq + pidx(line_of(i), jj);
                 const float prev = dx_next;
                 if (!A.first && i + 1 < L)
-                    dx_next = A.Xq[line_of(i + 1) * kDxPitch + jj];
+                    dx_next = A.Xq[pidx(line_of(i + 1), jj)];
                 if (act)
                     *xa = A.first ? a * lv : fmaf(a, lv, prev);
             } else {
                 const int cc = line_of(i);
                 dxr[cc] = dx_first ? a * lv : fmaf(a, lv, dxr[cc]);
             }
-            // finish the previous batch (its slot reads were issued after the
-            // last barrier and overlapped a step and a half of arithmetic)
-            if ((i & 1) == 1 && i >= 3)
-                flush_dw(i - 2);
-            const int buf = (i >> 1) & 1;
-            slot_ptr(A.slots, buf, i & 1, 0, A.wave)[j] = t0;
-            slot_ptr(A.slots, buf, i & 1, 1, A.wave)[j] = t1;
-            slot_ptr(A.slots, buf, i & 1, 2, A.wave)[j] = t2;
-            if ((i & 1) == 1) {
+            // finish the previous batch: its slot reads were issued after the
+            // last barrier and overlapped a step of arithmetic
+            if (!IMM && (i & 3) == 1 && i >= 5 && reducer)
+                reduce_step(i - 5 + A.wave);
+            // w_i couples line i-1 to line i: a_i and h_{i-1} go to the slots
+            // (h_{-1} = 0 makes line 0's gradient zero)
+            const int buf = (i >> 2) & 1;
+            slot_ptr(A.slots, buf, i & 3, 0, A.wave)[j] = a;
+            slot_ptr(A.slots, buf, i & 3, 1, A.wave)[j] = hp;
+            if ((i & 3) == 3) {
                 lds_barrier();
-                issue_dw(i);
+                if (IMM) {
+                    for (int st = A.wave; st < kBatch; st += A.cw) {
+                        read_step(buf, st);
+                        reduce_step(i - 3 + st);
+                    }
+                } else if (reducer) {
+                    read_step(buf, A.wave);
+                }
             }
             if (t == 7 && act) {
                 st128_nt(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
@@ -539,11 +536,12 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             step_fence();
         }
     }
-    flush_dw(L - 1);
+    if (!IMM && reducer)
+        reduce_step(L - 4 + A.wave);
 #undef FLOADB
 }
 
-template <int H, int W, int U>
+template <int H, int W, bool IMM>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -553,7 +551,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
-    constexpr int XPLANE = H * kDxPitch;                    // floats per dx plane
+    constexpr int XPLANE = H * kPlanePitch;                 // floats per wave plane
     extern __shared__ float4 smem4[];
     float *smem = reinterpret_cast<float *>(smem4);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
@@ -600,13 +598,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
                 const uint4 vx = ld128(A.x, 16u * p, 0);
                 const uint4 vd = ld128(A.dy, 16u * p, 0);
                 const int pr = p / (W / 8), pq = p - pr * (W / 8);
-                uint32_t *dst = st + pr * kDxPitch + 8 * pq;
                 const uint32_t xs_[4] = {vx.x, vx.y, vx.z, vx.w};
                 const uint32_t ds_[4] = {vd.x, vd.y, vd.z, vd.w};
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    dst[2 * e] = __builtin_amdgcn_perm(ds_[e], xs_[e], 0x05040100u);
-                    dst[2 * e + 1] = __builtin_amdgcn_perm(ds_[e], xs_[e], 0x07060302u);
+                    st[pidx(pr, 8 * pq + 2 * e)] = __builtin_amdgcn_perm(ds_[e], xs_[e], 0x05040100u);
+                    st[pidx(pr, 8 * pq + 2 * e + 1)] =
+                        __builtin_amdgcn_perm(ds_[e], xs_[e], 0x07060302u);
                 }
             }
         }
@@ -636,12 +634,12 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, U>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
-        dir_bwd<H, W, 3, U>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+        dir_bwd<H, W, 3, IMM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
@@ -649,18 +647,18 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         // vertical directions add to
 #pragma unroll
         for (int q = 0; q < W; ++q)
-            A.Xq[lane * kDxPitch + q] = dxr[q];
+            A.Xq[pidx(lane, q)] = dxr[q];
     }
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, U>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, U>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -675,7 +673,10 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
             const int t = it * 64 + lane;
             if (t < NP) {
                 const int r = t / (W / 8), cm = t - r * (W / 8);
-                const float *a = A.Xq + r * kDxPitch + 8 * cm;
+                float a[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    a[e] = A.Xq[pidx(r, 8 * cm + e)];
                 st128_nt(dxo, 16u * (uint32_t)t, 0,
                          make_uint4(pack2(a[0], a[1]), pack2(a[2], a[3]), pack2(a[4], a[5]),
                                     pack2(a[6], a[7])));
@@ -723,15 +724,15 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W, int U>
+template <int H, int W, bool IMM>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, U>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, U>), dim3((unsigned)(p.B * p.G * nchunk)),
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM>), dim3((unsigned)(p.B * p.G * nchunk)),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -751,7 +752,7 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
     if (e != hipSuccess)
         return e;
-    const size_t per_ch = (size_t)H * kDxPitch * 4;                 // dx plane
+    const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
     const size_t slots = (size_t)kSlotFloats * 4;                   // per-step dw terms
     const int cpg = p.C / p.G;
     int cap = lds_max > (int)slots ? (int)(((size_t)lds_max - slots) / per_ch) : 0;
@@ -770,9 +771,8 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         if (e != hipSuccess)
             return e;
     }
-    e = cw >= 6   ? bwd_med_launch<H, W, 1>(p, st, cw, nchunk, lds, dwp)
-        : cw >= 2 ? bwd_med_launch<H, W, 3>(p, st, cw, nchunk, lds, dwp)
-                  : bwd_med_launch<H, W, 6>(p, st, cw, nchunk, lds, dwp);
+    e = cw >= kBatch ? bwd_med_launch<H, W, false>(p, st, cw, nchunk, lds, dwp)
+                     : bwd_med_launch<H, W, true>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
