@@ -8,7 +8,16 @@ of the dominant kernel (algorithmic bytes / average launch time, from HIP
 events on the launch stream) and the CPU oracle timed on a bounded sample of
 the same workload.  Diagnostics go to stderr.
 
-    python bench.py [--steps K] [--warmup W] [--workload IDX|NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload IDX|NAME|all] [--no-cpu-baseline]
+
+Before every step, outside the timed events, reading a 1 GiB buffer evicts
+the L2s and the 256 MB Infinity Cache (writing back what the previous step
+left dirty), so every step reads its inputs from HBM: the small workloads
+would otherwise run from cache.  Step time is then the sum of the
+two calls' event times.  A device-to-device copy that moves the dominant
+call's algorithmic byte count, timed the same way, gives the achievable
+bandwidth; the share of the call's time it does not explain is reported as
+the serialisation share.  `--workload all` prints one line per workload.
 """
 from __future__ import annotations
 
@@ -89,36 +98,26 @@ def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float) -> dict:
                       f"fp64, single thread), {dt:.1f} s"}
 
 
-def main() -> int:
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="3", help="index or name of the workload")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="approximate CPU time of the oracle baseline")
-    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
-                    help="before the timed region, copy MIB MiB device to device once (a plain "
-                         "copy kernel of known traffic, the reference for HBM byte counters)")
-    args = ap.parse_args()
+def timed_copy(nbytes: int, reps: int, flush, torch) -> float:
+    """Mean ms of a device-to-device copy that reads and writes nbytes / 2 each."""
+    n = max(1, nbytes // 8)
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ms = []
+    for _ in range(reps):
+        flush()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms.append(e0.elapsed_time(e1))
+    del src, dst
+    return float(np.mean(ms))
 
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the scan needs no communication, and each GPU "
-              "of a data-parallel job runs this kernel on its own batch shard. Run with --gpus 1.",
-              file=sys.stderr)
-        return 2
 
-    import torch
-    import paper_2606_00746_amd as gspn
-
-    if not torch.cuda.is_available():
-        print("bench.py needs a GPU", file=sys.stderr)
-        return 1
-    gspn.load()
-
-    key = args.workload
-    wl = gi.workload(int(key) if key.isdigit() else key)
+def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     log(f"workload {wl}")
     t0 = time.perf_counter()
     inputs = gi.make_inputs(wl, with_dy=wl.backward)
@@ -132,8 +131,17 @@ def main() -> int:
         grads = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                  torch.empty_like(u))
     stream = torch.cuda.current_stream()
+    scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
+             if args.flush_mib > 0 else None)
+
+    def flush():
+        # read, not write: the caches end up holding clean lines, so the timed
+        # calls do not pay for writing back the flush's own data
+        if scrub is not None:
+            scrub.sum()
 
     def step(ev=None):
+        flush()
         if ev is not None:
             ev[0].record(stream)
         gspn.scan_fwd(x, w, lam, u, wl.dirs, y=y, stream=stream)
@@ -167,9 +175,11 @@ def main() -> int:
 
     fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events])) if wl.backward else 0.0
-    ms_per_step = elapsed * 1e3 / args.steps
+    # with flushing, the step is the two calls (the flush between steps is not
+    # part of it); without, the wall clock over the K steps
+    ms_per_step = fwd_ms + bwd_ms if scrub is not None else elapsed * 1e3 / args.steps
     pixch = wl.pixels_channels
-    value = pixch / (elapsed / args.steps) / 1e9
+    value = pixch / (ms_per_step * 1e-3) / 1e9
     nbytes = algorithmic_bytes(wl)
     step_gbs = (nbytes["fwd"] + nbytes["bwd"]) / (ms_per_step * 1e-3) / 1e9
     log(f"fwd {fwd_ms:.4f} ms  bwd {bwd_ms:.4f} ms  step {ms_per_step:.4f} ms  "
@@ -190,6 +200,17 @@ def main() -> int:
                 "traffic": traffic,
                 "kernel": dom, "avg_ms": round(dom_ms, 5), "algorithmic_bytes": dom_bytes}
 
+    # the achievable-bandwidth ceiling for the same bytes, and how much of the
+    # call's time it leaves unexplained
+    copy_ms = timed_copy(dom_bytes, 10, flush, torch)
+    probe = {"bytes": dom_bytes, "ms": round(copy_ms, 5),
+             "gbs": round(dom_bytes / (copy_ms * 1e-3) / 1e9, 1),
+             "serialisation_share": round(1.0 - copy_ms / dom_ms, 4)}
+    if traffic:
+        # the same with the bytes the call actually moves
+        probe["serialisation_share_measured_bytes"] = round(
+            1.0 - copy_ms * traffic / dom_bytes / dom_ms, 4)
+
     out = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -208,14 +229,58 @@ def main() -> int:
                    "storage": wl.dtype, "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
+        "cache_flush_mib": args.flush_mib,
         "step_hbm_gbs_algorithmic": round(step_gbs, 1),
         "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "roofline": roofline,
+        "copy_probe": probe,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
-    print(json.dumps(out), flush=True)
+    return out
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="3",
+                    help="index or name of the workload, or 'all' (one line each)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="approximate CPU time of the oracle baseline")
+    ap.add_argument("--flush-mib", type=int, default=1024,
+                    help="MiB read before every step, outside the timed events (0: none; "
+                         "the step is then timed by the wall clock over all K steps)")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="before the timed region, copy MIB MiB device to device once (a plain "
+                         "copy kernel of known traffic, the reference for HBM byte counters)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the scan needs no communication, and each GPU "
+              "of a data-parallel job runs this kernel on its own batch shard. Run with --gpus 1.",
+              file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2606_00746_amd as gspn
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    gspn.load()
+
+    key = args.workload
+    if key == "all":
+        wls = list(gi.WORKLOADS)
+    else:
+        wls = [gi.workload(int(key) if key.isdigit() else key)]
+    for wl in wls:
+        print(json.dumps(run_workload(wl, args, torch, gspn)), flush=True)
+        torch.cuda.empty_cache()
     return 0
 
 

@@ -14,6 +14,11 @@ Each counter is scaled by what it reads for the plain copy of known size that
 the same run makes, so the record holds bytes.  The record carries a hash of
 the kernel sources: the benchmark reports the figure only while the sources
 are unchanged.
+
+Where the waves' time goes, from one counter run collecting the SQ_ counters
+in ``WAVE_COUNTERS`` (wave-cycles waiting, issuing, and by instruction kind)::
+
+    python -m paper_2606_00746_amd.profiling waves COUNTERS_CSV OUT.txt --command "..."
 """
 from __future__ import annotations
 
@@ -119,6 +124,47 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
             "kernels": kernels, "bytes_per_call": {k: round(v) for k, v in calls.items()}}
 
 
+WAVE_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+                 "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_VMEM",
+                 "SQ_ACTIVE_INST_LDS")
+
+
+def waves_summary(csv_path: str, out: str, command: str) -> str:
+    """Per kernel, the share of wave-cycles spent waiting and issuing by kind.
+
+    SQ_WAVE_CYCLES counts the cycles of every resident wave; SQ_WAIT_ANY the
+    wave-cycles a wave waited on anything (a dependency on an outstanding
+    memory or LDS access, a barrier); SQ_WAIT_INST_ANY those it waited for an
+    instruction to issue; the SQ_ACTIVE_INST_* those it spent issuing.  All
+    are in the same unit, so their ratios are shares of wave time.
+    """
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(csv_path)):
+        vals[short_name(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    lines = ["# rocprofv3 wave-time summary (SQ counters, mean over dispatches)",
+             f"# command: {command}",
+             "# shares of SQ_WAVE_CYCLES: wait = SQ_WAIT_ANY, issue-wait = SQ_WAIT_INST_ANY, "
+             "busy = SQ_ACTIVE_INST_ANY, valu/vmem/lds = SQ_ACTIVE_INST_*", "",
+             f"{'kernel':<44} {'disp':>4} {'wave_cyc':>12} {'wait':>6} {'iss_wt':>6} "
+             f"{'busy':>6} {'valu':>6} {'vmem':>6} {'lds':>6}"]
+    for k, cv in vals.items():
+        if call_of(k) is None:
+            continue
+        m = {c: sum(v) / len(v) for c, v in cv.items()}
+        wc = m.get("SQ_WAVE_CYCLES", 0.0)
+        if wc <= 0:
+            continue
+        sh = lambda c: m.get(c, 0.0) / wc  # noqa: E731
+        lines.append(f"{k[:44]:<44} {len(cv['SQ_WAVE_CYCLES']):>4} {wc:>12.4g} "
+                     f"{sh('SQ_WAIT_ANY'):>6.3f} {sh('SQ_WAIT_INST_ANY'):>6.3f} "
+                     f"{sh('SQ_ACTIVE_INST_ANY'):>6.3f} {sh('SQ_ACTIVE_INST_VALU'):>6.3f} "
+                     f"{sh('SQ_ACTIVE_INST_VMEM'):>6.3f} {sh('SQ_ACTIVE_INST_LDS'):>6.3f}")
+    text = "\n".join(lines) + "\n"
+    with open(out, "w") as f:
+        f.write(text)
+    return text
+
+
 def load_traffic(path: str, call: str) -> float | None:
     """Bytes per call from a traffic record, None if absent or made from other sources."""
     try:
@@ -144,9 +190,15 @@ def main(argv=None) -> int:
     c.add_argument("--workload", required=True)
     c.add_argument("--copy-mib", type=int, required=True)
     c.add_argument("--command", required=True)
+    v = sub.add_parser("waves")
+    v.add_argument("csv")
+    v.add_argument("out")
+    v.add_argument("--command", required=True)
     a = ap.parse_args(argv)
     if a.cmd == "trace":
         sys.stdout.write(trace_summary(a.db, a.out, a.command))
+    elif a.cmd == "waves":
+        sys.stdout.write(waves_summary(a.csv, a.out, a.command))
     else:
         rec = traffic_record(a.fetch_csv, a.write_csv, a.workload, a.copy_mib, a.command)
         with open(a.out, "w") as f:

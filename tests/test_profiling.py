@@ -53,3 +53,26 @@ def test_kernels_map_to_calls():
     assert profiling.call_of("void gspn::(anonymous namespace)::sum_wide_kernel(float)") == "fwd"
     assert profiling.call_of("gspn::(anonymous namespace)::dw_reduce_kernel(float)") == "bwd"
     assert profiling.call_of("__amd_rocclr_copyBuffer") is None
+
+
+def test_waves_summary_shares(tmp_path):
+    bwd = "void gspn::(anonymous namespace)::bwd_med_kernel<64, 64, 0>(int)"
+    p = tmp_path / "sq.csv"
+    with open(p, "w") as f:
+        f.write(HEADER)
+        i = 0
+        # two dispatches; the shares use the mean of each counter
+        for wave, wait, valu in ((1000.0, 600.0, 200.0), (3000.0, 1400.0, 600.0)):
+            for name, v in (("SQ_WAVE_CYCLES", wave), ("SQ_WAIT_ANY", wait),
+                            ("SQ_ACTIVE_INST_VALU", valu)):
+                f.write(f'{i},{i},"Agent 1",1,1,1,64,1,"{bwd}",256,0,0,8,0,16,"{name}",{v},0,1\n')
+                i += 1
+        f.write(f'{i},{i},"Agent 1",1,1,1,64,1,"__amd_rocclr_copyBuffer",256,0,0,8,0,16,'
+                f'"SQ_WAVE_CYCLES",5,0,1\n')
+    text = profiling.waves_summary(str(p), str(tmp_path / "o.txt"), "cmd")
+    row = [ln for ln in text.splitlines() if ln.startswith("bwd_med_kernel")]
+    assert len(row) == 1 and "copyBuffer" not in text
+    f = row[0].split()
+    # kernel name has spaces: read the numeric columns from the right
+    wait, valu = float(f[-6]), float(f[-3])
+    assert abs(wait - 0.5) < 1e-3 and abs(valu - 0.2) < 1e-3
