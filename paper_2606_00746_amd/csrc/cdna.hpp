@@ -17,6 +17,13 @@ constexpr uint32_t kSelZero = 0x0C0C0C0Cu; // -> +0.0f
 // Keep the software pipeline as written: nothing is scheduled across a step
 // boundary, so each step's prefetch stays ahead of its use instead of every
 // load of the unrolled scan being hoisted to the top.
+// Makes v opaque to the compiler, so values derived from it before this point
+// are not reused after it (they are derived again).
+__device__ __forceinline__ void launder(uint4 &v)
+{
+    asm volatile("" : "+v"(v.x), "+v"(v.y), "+v"(v.z), "+v"(v.w));
+}
+
 __device__ __forceinline__ void step_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 // Workgroup barrier that orders LDS only.  __syncthreads() also orders global
@@ -152,20 +159,40 @@ __device__ __forceinline__ float widen(uint32_t v, uint32_t sel)
 __device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
-__device__ __forceinline__ uint32_t pack2(float lo, float hi)
+// acc + w * v[lane-1] and acc + w * v[lane+1] over the whole wave (the lanes
+// without a neighbour read 0), each one v_fmac_f32 with a DPP wave shift of
+// its first operand: the compiler keeps the shift as a separate v_mov for a
+// fused multiply-add.  The s_nop provides the two wait states a DPP read
+// needs after a VALU write of its source, which the compiler does not track
+// inside inline assembly.
+__device__ __forceinline__ float fmac_left(float acc, float v, float w)
 {
-    // two fp32 -> bf16 (RNE) in one v_cvt_pk_bf16_f32
-    const __bf16 a = static_cast<__bf16>(lo);
-    const __bf16 b = static_cast<__bf16>(hi);
-    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a)) |
-           (static_cast<uint32_t>(__builtin_bit_cast(uint16_t, b)) << 16);
+    asm("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 wave_shr:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+        : "+v"(acc)
+        : "v"(v), "v"(w));
+    return acc;
 }
 
-__device__ __forceinline__ uint32_t pack1(float v)
+__device__ __forceinline__ float fmac_right(float acc, float v, float w)
 {
-    const __bf16 a = static_cast<__bf16>(v);
-    return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, a));
+    asm("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 wave_shl:1 row_mask:0xf bank_mask:0xf bound_ctrl:1"
+        : "+v"(acc)
+        : "v"(v), "v"(w));
+    return acc;
 }
+
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two fp32 -> bf16 (RNE) in one v_cvt_pk_bf16_f32, lo in the low half.
+__device__ __forceinline__ uint32_t pack2(float lo, float hi)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
+}
+
+// One fp32 -> bf16 (RNE) in the low half, for 16-bit stores (the high half
+// holds bf16 zero and is not meant to be read).
+__device__ __forceinline__ uint32_t pack1(float v) { return pack2(v, 0.f); }
 
 // Component k (0..3) of a 16-byte piece; k is a constant once unrolled.
 __device__ __forceinline__ uint32_t part(const uint4 &v, int k)

@@ -60,6 +60,17 @@ __device__ __forceinline__ float tri_step(float h, float w0, float w1, float w2,
     return hn;
 }
 
+// The same in three instructions, the shifts fused into the multiply-adds
+// (same operations in the same order, so the same result).  The backward,
+// whose time goes mostly to issuing instructions, uses this form.
+__device__ __forceinline__ float tri_step_f(float h, float w0, float w1, float w2, float inj)
+{
+    float hn = fmaf(w1, h, inj);
+    hn = fmac_left(hn, h, w0);
+    hn = fmac_right(hn, h, w2);
+    return hn;
+}
+
 // Transposed step: a_i = w1_{i+1}[j] a[j] + (w0_{i+1} a)[j+1] + (w2_{i+1} a)[j-1] + inj.
 __device__ __forceinline__ float tri_step_t(float an, float w0, float w1, float w2, float inj)
 {
@@ -421,9 +432,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         float d0 = 0.f, d1 = 0.f, d2 = 0.f;
 #pragma unroll
         for (int q = 0; q < kSlots; ++q) {
-            d0 = fmaf(pa[q], from_left<64>(ph[q]), d0);
+            d0 = fmac_left(d0, ph[q], pa[q]);
             d1 = fmaf(pa[q], ph[q], d1);
-            d2 = fmaf(pa[q], from_right<64>(ph[q]), d2);
+            d2 = fmac_right(d2, ph[q], pa[q]);
         }
         if (j < P) {
             const int l = line_of(i);
@@ -483,7 +494,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
             if (i == 0)
                 h = lv * xv;
             else
-                h = tri_step(hp, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
+                h = tri_step_f(hp, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
                              elem(p2[fb], e, s.lo2, s.hi2), lv * xv);
             const float a = ahist[i];
             const float duv = dyv * h, dlv = a * xv;
@@ -539,6 +550,261 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     if (!IMM && reducer)
         reduce_step(L - 4 + A.wave);
 #undef FLOADB
+}
+
+// Shape and frame of direction D, shared by both backward variants.
+template <int H, int W, int D>
+struct BwdDir {
+    static constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
+    static constexpr int L = VERT ? H : W, P = VERT ? W : H;
+    static constexpr int NB = L / 8;
+    static constexpr uint32_t TB = 16 * P;              // bytes of one block of a bf16 plane
+    static constexpr uint32_t PL2 = 2 * H * W;          // bytes of one bf16 plane
+    static_assert(L % 8 == 0, "whole blocks");
+
+    __device__ static uint32_t boff(int fb) { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); }
+    __device__ static int line_of(int i) { return REV ? L - 1 - i : i; }   // storage line of step i
+    // the staged (x, dy) dword of step i at position jj
+    __device__ static uint32_t stg_at(const uint8_t *stg, int jj, int i)
+    {
+        const int l = line_of(i);
+        return lds_u32(stg, 4u * (uint32_t)(VERT ? pidx(l, jj) : pidx(jj, l)));
+    }
+};
+
+// The weight-gradient sum of step i from the slot values read for it.
+template <int H, int W, int D>
+__device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const float (&pa)[kSlots],
+                                         const float (&ph)[kSlots])
+{
+    using F = BwdDir<H, W, D>;
+    float d0 = 0.f, d1 = 0.f, d2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+        d0 = fmac_left(d0, ph[q], pa[q]);
+        d1 = fmaf(pa[q], ph[q], d1);
+        d2 = fmac_right(d2, ph[q], pa[q]);
+    }
+    if (j < F::P) {
+        const int l = F::line_of(i);
+        if (A.partial) {
+            // line-major fp32 partials: the wave writes whole lines
+            const uint32_t f = (uint32_t)(l * F::P + j);
+            st32_nt(A.dw, 4u * f, 0, __float_as_uint(d0));
+            st32_nt(A.dw, 4u * (f + H * W), 0, __float_as_uint(d1));
+            st32_nt(A.dw, 4u * (f + 2 * H * W), 0, __float_as_uint(d2));
+        } else {
+            const uint32_t el = 2u * (uint32_t)lm_offset(l, j, F::L, F::P);
+            st16(A.dw, el, 0, pack1(d0));
+            st16(A.dw, el + F::PL2, 0, pack1(d1));
+            st16(A.dw, el + 2 * F::PL2, 0, pack1(d2));
+        }
+    }
+}
+
+__device__ __forceinline__ void read_slots(const BwdArgs &A, int j, int buf, int st,
+                                           float (&pa)[kSlots], float (&ph)[kSlots])
+{
+#pragma unroll
+    for (int q = 0; q < kSlots; ++q) {
+        pa[q] = slot_ptr(A.slots, buf, st, 0, q)[j];
+        ph[q] = slot_ptr(A.slots, buf, st, 1, q)[j];
+    }
+}
+
+// The slot traffic of the n-th step (n = 0, 1, ... in the order a pass takes
+// them; that step is step_of(n)) with its adjoint a and previous state hp.
+// Step st of a batch belongs to wave st (waves 0..3, one per SIMD), which
+// issues the batch's slot reads after the barrier and finishes the sum 1.5
+// steps later; with fewer than kBatch waves (IMM) each wave takes several
+// steps and sums them right after the barrier.
+template <int H, int W, int D, bool IMM, class StepOf>
+__device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float a, float hp,
+                                          float (&pa)[kSlots], float (&ph)[kSlots], StepOf step_of)
+{
+    const bool reducer = A.wave < kBatch;
+    // finish the previous batch: its slot reads were issued after the last
+    // barrier and overlapped a step of arithmetic
+    if (!IMM && (n & 3) == 1 && n >= 5 && reducer)
+        dw_store<H, W, D>(A, j, step_of(n - 5 + A.wave), pa, ph);
+    const int buf = (n >> 2) & 1;
+    slot_ptr(A.slots, buf, n & 3, 0, A.wave)[j] = a;
+    slot_ptr(A.slots, buf, n & 3, 1, A.wave)[j] = hp;
+    if ((n & 3) == 3) {
+        lds_barrier();
+        if (IMM) {
+            for (int st = A.wave; st < kBatch; st += A.cw) {
+                read_slots(A, j, buf, st, pa, ph);
+                dw_store<H, W, D>(A, j, step_of(n - 3 + st), pa, ph);
+            }
+        } else if (reducer) {
+            read_slots(A, j, buf, A.wave, pa, ph);
+        }
+    }
+}
+
+template <int H, int W, int D, bool IMM, class StepOf>
+__device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float (&pa)[kSlots],
+                                            const float (&ph)[kSlots], StepOf step_of)
+{
+    if (!IMM && A.wave < kBatch)
+        dw_store<H, W, D>(A, j, step_of(BwdDir<H, W, D>::L - 4 + A.wave), pa, ph);
+}
+
+// One horizontal direction of the backward without the adjoint history, for
+// when dxa already holds the 64 dx row sums of the other horizontal
+// direction and both would not fit in registers: a forward
+// pass keeps h at the last step of every 8-step block; a reverse pass then
+// takes the blocks last to first, recomputes the block's h from the previous
+// checkpoint and runs the adjoint and every local gradient over the block in
+// reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
+// second read of lam and w (the first one leaves them in L2) and one more h
+// recurrence per step.
+template <int H, int W, int D, bool IMM>
+__device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
+                                           float (&dxa)[64])
+{
+    using F = BwdDir<H, W, D>;
+    constexpr bool REV = F::REV;
+    constexpr int L = F::L, P = F::P, NB = F::NB;
+    constexpr uint32_t PL2 = F::PL2;
+    const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
+    const bool act = cvalid && j < P;
+    const int jj = j < P ? j : P - 1;
+    const uint32_t vo = 16u * (uint32_t)jj;             // this lane's piece of a block
+
+    // --- forward pass: h at the end of every block ------------------------
+    float hck[NB];
+    {
+        uint4 rl[NB], p0[NB], p1[NB], p2[NB];
+#define ALOAD(fb)                                                    \
+    do {                                                             \
+        const uint32_t so_ = F::boff(fb);                            \
+        rl[fb] = ld128(A.lam, vo, so_);                              \
+        p0[fb] = ld128(A.w, vo, so_);                                \
+        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
+        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+    } while (0)
+        ALOAD(0);
+        if (NB > 1)
+            ALOAD(1);
+        uint32_t xq[L];
+#pragma unroll
+        for (int i = 0; i < kLdsAhead; ++i)
+            xq[i] = F::stg_at(stg, jj, i);
+        float h = 0.f;
+#pragma unroll
+        for (int fb = 0; fb < NB; ++fb) {
+            if (fb + 2 < NB)
+                ALOAD(fb + 2);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int i = 8 * fb + t;
+                const int e = REV ? 7 - t : t;
+                if (i + kLdsAhead < L)
+                    xq[i + kLdsAhead] = F::stg_at(stg, jj, i + kLdsAhead);
+                const float inj = elem(rl[fb], e, s.lo1, s.hi1) * bf_lo(xq[i]);
+                h = i == 0 ? inj
+                           : tri_step_f(h, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
+                                      elem(p2[fb], e, s.lo2, s.hi2), inj);
+                if (t == 7)
+                    hck[fb] = h;
+                step_fence();
+            }
+        }
+#undef ALOAD
+    }
+
+    // --- reverse pass by blocks -------------------------------------------
+    float pa[kSlots], ph[kSlots];
+    // the n-th step of this pass is step L-1-n
+    auto step_of = [](int n) { return L - 1 - n; };
+    uint4 rl[NB], ru[NB], p0[NB], p1[NB], p2[NB];
+#define BLOAD(fb)                                                    \
+    do {                                                             \
+        const uint32_t so_ = F::boff(fb);                            \
+        rl[fb] = ld128_nt(A.lam, vo, so_);                           \
+        ru[fb] = ld128_nt(A.u, vo, so_);                             \
+        p0[fb] = ld128(A.w, vo, so_);                                \
+        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
+        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+    } while (0)
+    BLOAD(NB - 1);
+    uint32_t xd[NB][8];        // staged (x, dy) of a block, read a block ahead
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        xd[NB - 1][t] = F::stg_at(stg, jj, 8 * (NB - 1) + t);
+    float an = 0.f, wn0 = 0.f, wn1 = 0.f, wn2 = 0.f;   // a and taps of the step after
+#pragma unroll
+    for (int fb = NB - 1; fb >= 0; --fb) {
+        // one block ahead: a block takes two recurrences per step here
+        if (fb >= 1) {
+            BLOAD(fb - 1);
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                xd[fb - 1][t] = F::stg_at(stg, jj, 8 * (fb - 1) + t);
+        }
+        // h over the block from the previous block's checkpoint
+        const float h0 = fb > 0 ? hck[fb > 0 ? fb - 1 : 0] : 0.f;
+        float hb[8];
+        {
+            float h = h0;
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                const int i = 8 * fb + t;
+                const int e = REV ? 7 - t : t;
+                const float inj = elem(rl[fb], e, s.lo1, s.hi1) * bf_lo(xd[fb][t]);
+                h = i == 0 ? inj
+                           : tri_step_f(h, elem(p0[fb], e, s.lo0, s.hi0), elem(p1[fb], e, s.lo1, s.hi1),
+                                      elem(p2[fb], e, s.lo2, s.hi2), inj);
+                hb[t] = h;
+                step_fence();
+            }
+        }
+        // the adjoint extracts its operands again rather than keeping the
+        // 32 widened values of the recompute alive
+        launder(rl[fb]);
+        launder(p0[fb]);
+        launder(p1[fb]);
+        launder(p2[fb]);
+        // du and dlam of the block as bf16 pairs in storage element order;
+        // the later step of a pair waits in du1 / dl1
+        uint32_t dup[4], dlp[4];
+        float du1 = 0.f, dl1 = 0.f;
+#pragma unroll
+        for (int t = 7; t >= 0; --t) {
+            const int i = 8 * fb + t;
+            const int e = REV ? 7 - t : t;
+            const float xv = bf_lo(xd[fb][t]), dyv = bf_hi(xd[fb][t]);
+            const float inj = elem(ru[fb], e, s.lo1, s.hi1) * dyv;
+            const float a = i + 1 == L ? inj : tri_step_t(an, wn0, wn1, wn2, inj);
+            an = a;
+            wn0 = elem(p0[fb], e, s.lo0, s.hi0);
+            wn1 = elem(p1[fb], e, s.lo1, s.hi1);
+            wn2 = elem(p2[fb], e, s.lo2, s.hi2);
+            const float lv = elem(rl[fb], e, s.lo1, s.hi1);
+            const float hp = t > 0 ? hb[t > 0 ? t - 1 : 0] : h0;     // h_{i-1}
+            const float duv = dyv * hb[t], dlv = a * xv;
+            if (t & 1) {
+                du1 = duv;
+                dl1 = dlv;
+            } else {
+                // steps t, t+1 hold elements e, e+1 (forward) or e, e-1 (reverse)
+                dup[e >> 1] = REV ? pack2(du1, duv) : pack2(duv, du1);
+                dlp[e >> 1] = REV ? pack2(dl1, dlv) : pack2(dlv, dl1);
+            }
+            const int cc = F::line_of(i);
+            dxa[cc] = fmaf(a, lv, dxa[cc]);
+            slot_step<H, W, D, IMM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
+            if (t == 0 && act) {
+                st128_nt(A.du, vo, F::boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                st128_nt(A.dlam, vo, F::boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+            }
+            step_fence();
+        }
+    }
+    slot_finish<H, W, D, IMM>(A, j, pa, ph, step_of);
+#undef BLOAD
 }
 
 template <int H, int W, bool IMM>
@@ -639,7 +905,10 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     }
     if (mask & 8) {
         setup(3);
-        dir_bwd<H, W, 3, IMM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+        if ((mask & 4) && H >= 64)
+            dir_bwd_ck<H, W, 3, IMM>(A, lane, cvalid, stg, dxr);
+        else
+            dir_bwd<H, W, 3, IMM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
