@@ -111,21 +111,32 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
     // the scan runs against the storage order
     auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
     uint4 rl[NB], ru[NB], r0[NB], r1[NB], r2[NB];
-#define FLOAD(fb)                                                    \
+    // lam and u come from HBM once, two blocks ahead; the taps, shared by the
+    // group's channels and mostly served by L2, one block ahead
+#define FLOADLU(fb)                                                  \
     do {                                                             \
         const uint32_t so_ = boff(fb);                               \
         rl[fb] = ld128_nt(lam, vo, so_);                             \
         ru[fb] = ld128_nt(u, vo, so_);                               \
+    } while (0)
+#define FLOADW(fb)                                                   \
+    do {                                                             \
+        const uint32_t so_ = boff(fb);                               \
         r0[fb] = ld128(w, vo, so_);                                  \
         r1[fb] = ld128(w, vo, so_ + PL);                             \
         r2[fb] = ld128(w, vo, so_ + 2 * PL);                         \
     } while (0)
-    FLOAD(0);
+    FLOADLU(0);
+    FLOADW(0);
+    if (NB > 1)
+        FLOADLU(1);
     float h = 0.f;
 #pragma unroll
     for (int fb = 0; fb < NB; ++fb) {
+        if (fb + 2 < NB)
+            FLOADLU(fb + 2);
         if (fb + 1 < NB)
-            FLOAD(fb + 1);
+            FLOADW(fb + 1);
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const int i = 8 * fb + t;
@@ -145,7 +156,8 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
         }
         step_fence();
     }
-#undef FLOAD
+#undef FLOADLU
+#undef FLOADW
 }
 
 template <int H, int W>

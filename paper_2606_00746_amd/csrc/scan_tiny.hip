@@ -10,10 +10,12 @@
 // channels, their lam_d and u_d, the group's three taps) is copied into LDS
 // with the widest coalesced accesses its alignment allows and read from
 // there.
-//  * forward: the directions run one after another; each lane keeps its
-//    channel's u_d * h_d in registers (a column for vertical directions, a row
-//    for horizontal ones); both are added through an fp32 LDS plane and y
-//    leaves with one coalesced copy;
+//  * forward: the directions run one after another; the planes of the next
+//    direction are copied into a second LDS buffer by direct-to-LDS loads
+//    while the current one computes; each lane keeps its channel's u_d * h_d
+//    in registers (a column for vertical directions, a row for horizontal
+//    ones); both are added through an fp32 LDS plane and y leaves with one
+//    coalesced copy;
 //  * backward: a reverse sweep (adjoint, kept in registers) and a forward
 //    sweep (recomputed h) per direction; du and dlam overwrite the staged u
 //    and lam in place and leave with one coalesced copy per plane; the
@@ -67,6 +69,45 @@ __device__ __forceinline__ void stage(uint16_t *dst, const bf16_t *src, int n)
     }
 }
 
+// Starts copying n bf16 elements global -> LDS without passing through
+// registers (global_load_lds: the bytes of each lane land at the wave's LDS
+// address + size * lane), in 16-, 4- or 2-byte pieces as the alignment of
+// both ends and n allow.  The data is in place once every wave has waited
+// for its loads and passed a barrier (lds_wait).  nt: the workgroup's
+// threads, a multiple of 64 (read once by the caller).
+template <int S>
+__device__ __forceinline__ void stage_async_w(uint16_t *dst, const bf16_t *src, int n, int nt)
+{
+    constexpr int E = S / 2;                         // elements per piece
+    for (int t = threadIdx.x; t < n / E; t += nt) {
+        const auto g = (const __attribute__((address_space(1))) void *)(src + E * t);
+        const auto l = (__attribute__((address_space(3))) void *)(dst + E * (t & ~63));
+        if constexpr (S == 16)
+            __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+        else if constexpr (S == 4)
+            __builtin_amdgcn_global_load_lds(g, l, 4, 0, 0);
+        else
+            __builtin_amdgcn_global_load_lds(g, l, 2, 0, 0);
+    }
+}
+
+__device__ __forceinline__ void stage_async(uint16_t *dst, const bf16_t *src, int n, int nt)
+{
+    const uintptr_t a = reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst);
+    if (a % 16 == 0 && n % 8 == 0)
+        stage_async_w<16>(dst, src, n, nt);
+    else if (a % 4 == 0 && n % 2 == 0)
+        stage_async_w<4>(dst, src, n, nt);
+    else
+        stage_async_w<2>(dst, src, n, nt);
+}
+
+__device__ __forceinline__ void lds_wait()
+{
+    __builtin_amdgcn_s_waitcnt(0);     // this wave's loads, direct-to-LDS ones included
+    lds_barrier();
+}
+
 // n bf16 elements, LDS (16-byte aligned) -> global, by all threads.
 __device__ __forceinline__ void unstage(bf16_t *dst, const uint16_t *src, int n)
 {
@@ -95,6 +136,7 @@ struct TinyLds {
     static constexpr int HW = H * W;
     int R;                    // elements of one channel-plane region
     uint16_t *x, *dy, *lam, *u, *wt;
+    uint16_t *lam1, *u1, *wt1;  // forward: a second buffer for the next direction
     float *sl;                // [wave][3][16 steps][16 positions]
     float *mrg;               // fp32 merge plane (aliases lam and u)
     __device__ __forceinline__ TinyLds(uint16_t *base, int cw, bool bwd)
@@ -112,7 +154,22 @@ struct TinyLds {
         p += R;
         wt = p;
         p += round8(3 * HW);
+        lam1 = bwd ? nullptr : p;
+        p += bwd ? 0 : R;
+        u1 = bwd ? nullptr : p;
+        p += bwd ? 0 : R;
+        wt1 = bwd ? nullptr : p;
+        p += bwd ? 0 : round8(3 * HW);
         sl = reinterpret_cast<float *>(p);
+    }
+    // the same regions with the second direction buffer in place of the first
+    __device__ __forceinline__ TinyLds other() const
+    {
+        TinyLds o = *this;
+        o.lam = lam1;
+        o.u = u1;
+        o.wt = wt1;
+        return o;
     }
 };
 
@@ -120,7 +177,8 @@ template <int H, int W>
 size_t tiny_lds_bytes(int cw, bool bwd)
 {
     const int R = round8(cw * H * W);
-    size_t b = 2 * (size_t)((bwd ? 4 : 3) * R + round8(3 * H * W));
+    const int W3 = round8(3 * H * W);
+    size_t b = 2 * (size_t)(bwd ? 4 * R + W3 : 5 * R + 2 * W3);
     if (bwd)
         b += (size_t)((cw + kSlotW - 1) / kSlotW) * 3 * 16 * 16 * 4;
     return b;
@@ -249,7 +307,6 @@ __global__ __launch_bounds__(1024) void fwd_tiny_kernel(
     t.cvalid = t.ch < a.nvalid;
     const int64_t pc = ((int64_t)a.b * C + a.c0) * HW;
 
-    stage(S.x, x + pc, a.nvalid * HW);
     float yv[H], yh[W];
 #pragma unroll
     for (int r = 0; r < H; ++r)
@@ -257,25 +314,39 @@ __global__ __launch_bounds__(1024) void fwd_tiny_kernel(
 #pragma unroll
     for (int c = 0; c < W; ++c)
         yh[c] = 0.f;
-    for (int d = 0; d < 4; ++d) {
-        if (!((mask >> d) & 1))
-            continue;
-        const int s = __popc(mask & ((1 << d) - 1));
-        const int64_t pd = (((int64_t)s * B + a.b) * C + a.c0) * HW;
-        stage(S.lam, lam + pd, a.nvalid * HW);
-        stage(S.u, u + pd, a.nvalid * HW);
-        stage(S.wt, w + (((int64_t)s * B + a.b) * G + a.g) * 3 * HW, 3 * HW);
-        lds_barrier();
+    // The directions run in order; the planes of the next one are copied into
+    // the other LDS buffer while the current one computes.
+    const int nt = blockDim.x;
+    auto issue = [&](int k) {
+        const int64_t pd = (((int64_t)k * B + a.b) * C + a.c0) * HW;
+        const TinyLds<H, W> Sb = (k & 1) ? S.other() : S;
+        stage_async(Sb.lam, lam + pd, a.nvalid * HW, nt);
+        stage_async(Sb.u, u + pd, a.nvalid * HW, nt);
+        stage_async(Sb.wt, w + (((int64_t)k * B + a.b) * G + a.g) * 3 * HW, 3 * HW, nt);
+    };
+    stage_async(S.x, x + pc, a.nvalid * HW, nt);
+    int rem = mask & 15;
+    if (rem)
+        issue(0);
+    for (int k = 0; rem; ++k) {
+        const int d = __builtin_ctz(rem);
+        rem &= rem - 1;
+        // buffer k % 2 is filled, and every wave is done with the other one
+        lds_wait();
+        if (rem)
+            issue(k + 1);
+        const TinyLds<H, W> Sb = (k & 1) ? S.other() : S;
         if (d == 0)
-            fwd_tiny_dir<H, W, 0>(S, t, yv, yh);
+            fwd_tiny_dir<H, W, 0>(Sb, t, yv, yh);
         else if (d == 1)
-            fwd_tiny_dir<H, W, 1>(S, t, yv, yh);
+            fwd_tiny_dir<H, W, 1>(Sb, t, yv, yh);
         else if (d == 2)
-            fwd_tiny_dir<H, W, 2>(S, t, yv, yh);
+            fwd_tiny_dir<H, W, 2>(Sb, t, yv, yh);
         else
-            fwd_tiny_dir<H, W, 3>(S, t, yv, yh);
-        lds_barrier();
+            fwd_tiny_dir<H, W, 3>(Sb, t, yv, yh);
     }
+    // the merge plane aliases the first buffer
+    lds_barrier();
     merge_out<H, W>(S, t, yv, yh, y + pc, a.nvalid);
 }
 
