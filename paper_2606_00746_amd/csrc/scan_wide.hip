@@ -7,8 +7,9 @@
 //  * the x plane is loaded once, coalesced, into LDS (132 KB at 256 x 256);
 //  * lane l of a wave owns the line positions l + 64 m (m < NPL); the line
 //    state stays in NPL VGPRs for the whole scan; the tridiagonal step takes
-//    neighbours from the adjacent lanes by DPP, and across the boundary
-//    between position groups (lane 0 and lane 63) with readlane;
+//    neighbours from the adjacent lanes by DPP wave shifts, and across the
+//    boundary between position groups (lane 0 and lane 63) by DPP wave
+//    rotates;
 //  * lam, u and w come in 8-line blocks of 16-byte coalesced loads, one
 //    block ahead of use.
 // A 256 x 256 fp32 merge plane does not fit in LDS, so each direction writes
@@ -38,13 +39,50 @@ struct Pieces {
     uint4 l[NPL], u[NPL], w0[NPL], w1[NPL], w2[NPL];
 };
 
-// One direction of one channel plane.  L, P: scan and line length; the x
-// plane sits in LDS with pitch `pdw` dwords; ys receives u * h as fp32 in the
-// direction's line-major order (line l, position p at l * P + p).
-template <int NPL, bool VERT, bool REV>
-__device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t lam, rsrc_t u,
-                                         rsrc_t w, uint32_t wplane, const uint8_t *xs, u32x4 ys)
+// The neighbours of h[m] on the line, over all NPL position groups: lanes
+// take lane-1 / lane+1 of their own group by a DPP wave shift; lane 0 and
+// lane 63 take the last / first lane of the adjacent group, which a DPP wave
+// rotate of that group's value brings to them and the shift leaves in place
+// (a shift writes nothing where it has no source).  The line ends read 0.
+template <int NPL>
+__device__ __forceinline__ void neighbours(const float (&h)[NPL], float (&left)[NPL],
+                                           float (&right)[NPL])
 {
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) {
+        const int hv = __float_as_int(h[m]);
+        if (m == 0) {
+            left[m] = from_left<64>(h[m]);
+        } else {
+            const int rot =
+                __builtin_amdgcn_mov_dpp(__float_as_int(h[m - 1]), 0x13C /* wave_ror:1 */, 0xf, 0xf, false);
+            left[m] = __int_as_float(
+                __builtin_amdgcn_update_dpp(rot, hv, 0x138 /* wave_shr:1 */, 0xf, 0xf, false));
+        }
+        if (m + 1 == NPL) {
+            right[m] = from_right<64>(h[m]);
+        } else {
+            const int rot =
+                __builtin_amdgcn_mov_dpp(__float_as_int(h[m + 1]), 0x134 /* wave_rol:1 */, 0xf, 0xf, false);
+            right[m] = __int_as_float(
+                __builtin_amdgcn_update_dpp(rot, hv, 0x130 /* wave_shl:1 */, 0xf, 0xf, false));
+        }
+    }
+}
+
+// One direction of one channel plane.  HC, WC: the plane's sides when they
+// are compile-time constants (0: taken from H, W at run time); L, P: scan and
+// line length; the x plane sits in LDS with pitch (W / 2) | 1 dwords; ys
+// receives u * h as fp32 in the direction's line-major order (line l,
+// position p at l * P + p).
+template <int NPL, bool VERT, bool REV, int HC, int WC>
+__device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, rsrc_t u, rsrc_t w,
+                                         const uint8_t *xs, u32x4 ys)
+{
+    const int H = HC ? HC : H_, W = WC ? WC : W_;
+    const int L = VERT ? H : W, P = VERT ? W : H;
+    const int pdw = wide_pitch_dw(W);
+    const uint32_t wplane = (uint32_t)(2 * H * W);
     Sel s[NPL];
     uint32_t vo[NPL];
     int jc[NPL];
@@ -57,7 +95,6 @@ __device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t
         jc[m] = p < P ? p : P - 1;
         vo[m] = 16u * (uint32_t)jc[m];
     }
-    const bool first_lane = lane == 0, last_lane = lane == 63;
     const int NB = L / 8;
     const uint32_t TB = 16u * (uint32_t)P;     // bytes of one block of a bf16 plane
     auto boff = [&](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
@@ -78,37 +115,25 @@ __device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t
         h[m] = 0.f;
 
     auto run_block = [&](const Pieces<NPL> &pc, int fb) {
+        // this lane's x at the block's lowest storage line: each step adds a
+        // small constant, which the LDS read takes as its offset
+        const int l0 = REV ? L - 8 - 8 * fb : 8 * fb;
+        uint32_t xb[NPL];
+#pragma unroll
+        for (int m = 0; m < NPL; ++m)
+            xb[m] = VERT ? 4u * (uint32_t)(l0 * pdw) + 2u * (uint32_t)jc[m]
+                         : 4u * (uint32_t)(jc[m] * pdw) + 2u * (uint32_t)l0;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             const int i = 8 * fb + t;
             const int e = REV ? 7 - t : t;              // element of the 8-line piece
             const int ln = REV ? L - 1 - i : i;         // storage line of step i
-            // neighbours on the previous line: adjacent lanes by DPP, and the
-            // boundary lanes of neighbouring position groups by readlane
+            const uint32_t dx = VERT ? 4u * (uint32_t)(pdw * e) : 2u * (uint32_t)e;   // ln - l0 = e
             float left[NPL], right[NPL];
+            neighbours<NPL>(h, left, right);
 #pragma unroll
             for (int m = 0; m < NPL; ++m) {
-                left[m] = from_left<64>(h[m]);
-                right[m] = from_right<64>(h[m]);
-            }
-#pragma unroll
-            for (int m = 0; m < NPL; ++m) {
-                if (m > 0) {
-                    const float v = __int_as_float(
-                        __builtin_amdgcn_readlane(__float_as_int(h[m - 1]), 63));
-                    left[m] = first_lane ? v : left[m];
-                }
-                if (m + 1 < NPL) {
-                    const float v = __int_as_float(
-                        __builtin_amdgcn_readlane(__float_as_int(h[m + 1]), 0));
-                    right[m] = last_lane ? v : right[m];
-                }
-            }
-#pragma unroll
-            for (int m = 0; m < NPL; ++m) {
-                const int row = VERT ? ln : jc[m];
-                const int col = VERT ? jc[m] : ln;
-                const float xv = bf_lo(lds_u16(xs, 4u * (uint32_t)(row * pdw) + 2u * (uint32_t)col));
+                const float xv = bf_lo(lds_u16(xs, xb[m] + dx));
                 const float inj = elem(pc.l[m], e, s[m].lo1, s[m].hi1) * xv;
                 float hn = inj;
                 if (i > 0) {
@@ -120,8 +145,9 @@ __device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t
             }
 #pragma unroll
             for (int m = 0; m < NPL; ++m) {
+                // the lane's part in the address register, the line's in soffset
                 if (valid[m])
-                    st32_nt(ys, 4u * (uint32_t)(ln * P + lane + 64 * m), 0,
+                    st32_nt(ys, 4u * (uint32_t)lane, 4u * (uint32_t)(ln * P + 64 * m),
                             __float_as_uint(elem(pc.u[m], e) * h[m]));
             }
         }
@@ -130,6 +156,7 @@ __device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t
 
     Pieces<NPL> A, B;
     load(A, 0);
+#pragma unroll 1
     for (int fb = 0; fb < NB; fb += 2) {
         if (fb + 1 < NB)
             load(B, fb + 1);
@@ -142,12 +169,13 @@ __device__ __forceinline__ void wide_dir(int lane, int L, int P, int pdw, rsrc_t
     }
 }
 
-template <int NPL>
+template <int NPL, int HC, int WC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
-    const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H,
-    int W, Magic divC, Magic divCpg, Magic divNq)
+    const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H_,
+    int W_, Magic divC, Magic divCpg, Magic divNq)
 {
+    const int H = HC ? HC : H_, W = WC ? WC : W_;
     extern __shared__ uint32_t xs32[];
     uint8_t *xs = reinterpret_cast<uint8_t *>(xs32);
     const int pdw = wide_pitch_dw(W);
@@ -167,7 +195,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const int n = H * nq;
         for (int t = threadIdx.x; t < n; t += 256) {
             const uint4 v = ld128(xr, 16u * (uint32_t)t, 0);
-            const int r = mdiv(t, divNq), q = t - r * nq;
+            const int r = WC ? t / (WC / 8) : mdiv(t, divNq), q = t - r * nq;
             uint32_t *dst = xs32 + r * pdw + 4 * q;
             dst[0] = v.x;
             dst[1] = v.y;
@@ -185,15 +213,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const rsrc_t ru = make_rsrc(u + pd, (uint32_t)(2 * HW));
         const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
         const u32x4 yd = make_sdesc(ys + pd, (uint32_t)(4 * HW));
-        const uint32_t wplane = (uint32_t)(2 * HW);
         if (d == 0)
-            wide_dir<NPL, true, false>(lane, H, W, pdw, rl, ru, rw, wplane, xs, yd);
+            wide_dir<NPL, true, false, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
         else if (d == 1)
-            wide_dir<NPL, true, true>(lane, H, W, pdw, rl, ru, rw, wplane, xs, yd);
+            wide_dir<NPL, true, true, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
         else if (d == 2)
-            wide_dir<NPL, false, false>(lane, W, H, pdw, rl, ru, rw, wplane, xs, yd);
+            wide_dir<NPL, false, false, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
         else
-            wide_dir<NPL, false, true>(lane, W, H, pdw, rl, ru, rw, wplane, xs, yd);
+            wide_dir<NPL, false, true, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
     }
 }
 
@@ -280,15 +307,15 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
     }
 }
 
-template <int NPL>
+template <int NPL, int HC, int WC>
 hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_wide_kernel<NPL>), dim3((unsigned)(p.B * p.C)), dim3(256), lds, st,
-                       (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)(p.B * p.C)), dim3(256), lds,
+                       st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
                        make_magic((uint32_t)(p.W / 8)));
@@ -325,9 +352,15 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     const size_t lds = wide_lds_bytes(p.H, p.W);
     const int side = p.H > p.W ? p.H : p.W;
     const int npl = (side + 63) / 64;
-    e = npl <= 2 ? fwd_wide_t<2>(p, st, ys, lds)
-        : npl == 3 ? fwd_wide_t<3>(p, st, ys, lds)
-                   : fwd_wide_t<4>(p, st, ys, lds);
+    // the square planes of 256 and 128 get kernels with their shape built in
+    if (p.H == 256 && p.W == 256)
+        e = fwd_wide_t<4, 256, 256>(p, st, ys, lds);
+    else if (p.H == 128 && p.W == 128)
+        e = fwd_wide_t<2, 128, 128>(p, st, ys, lds);
+    else
+        e = npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds)
+            : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds)
+                       : fwd_wide_t<4, 0, 0>(p, st, ys, lds);
     if (e == hipSuccess) {
         const int tiles_w = (p.W + kTile - 1) / kTile;
         const int tiles_h = (p.H + kTile - 1) / kTile;
