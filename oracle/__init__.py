@@ -5,7 +5,8 @@ tests, the smoke check and the benchmark's CPU-baseline leg use it; the GPU
 library never imports it and shares no code with it.
 
 Follows Sec. 3, Eqs. (gspn_recurrence), (gspn_output) and (row_stochastic_norm)
-and Sec. 4.2, Eq. (2dsp) of the paper; the readings taken where the paper is
+(the scan, and the weights from their logits) and Sec. 4.2, Eq. (2dsp) of the
+paper; the readings taken where the paper is
 silent are listed in ``gspn_oracle.c``.
 """
 from __future__ import annotations
@@ -32,6 +33,10 @@ def _load():
         lib.oracle_scan_fwd.restype = None
         lib.oracle_scan_bwd.argtypes = [P, P, P, P, P, P, P, P, P, I, I, I, I, I, I]
         lib.oracle_scan_bwd.restype = None
+        lib.oracle_norm_w.argtypes = [P, P, I, I, I, I, I]
+        lib.oracle_norm_w.restype = None
+        lib.oracle_norm_w_bwd.argtypes = [P, P, P, I, I, I, I, I]
+        lib.oracle_norm_w_bwd.restype = None
         _lib = lib
     return _lib
 
@@ -84,6 +89,36 @@ def scan_bwd(x, w, lam, u, dy, dirs: int) -> dict:
                             dy.ctypes.data, dx.ctypes.data, dw.ctypes.data, dlam.ctypes.data,
                             du.ctypes.data, dirs, B, C, G, H, W)
     return {"dx": dx, "dw": dw, "dlam": dlam, "du": du}
+
+
+def _check_w(wt, dirs):
+    if not 1 <= dirs <= 15:
+        raise ValueError("direction mask must be in [1, 15]")
+    if wt.ndim != 6 or wt.shape[0] != _ndirs(dirs) or wt.shape[3] != 3:
+        raise ValueError(f"weight shape {wt.shape} is not [D, B, G, 3, H, W]")
+    return wt.shape[1], wt.shape[2], wt.shape[4], wt.shape[5]
+
+
+def normalize_w(wt, dirs: int) -> np.ndarray:
+    """Row-stochastic tridiagonal weights from their logits (Sec. 3,
+    Eq. (row_stochastic_norm)), float64, layout [D, B, G, 3, H, W]."""
+    wt = _f64(wt)
+    B, G, H, W = _check_w(wt, dirs)
+    w = np.empty_like(wt)
+    _load().oracle_norm_w(wt.ctypes.data, w.ctypes.data, dirs, B, G, H, W)
+    return w
+
+
+def normalize_w_bwd(wt, dw, dirs: int) -> np.ndarray:
+    """Gradient with respect to the logits, given the gradient dw of the
+    normalized weights, float64."""
+    wt, dw = _f64(wt), _f64(dw)
+    B, G, H, W = _check_w(wt, dirs)
+    if dw.shape != wt.shape:
+        raise ValueError("dw shape mismatch")
+    dwt = np.empty_like(wt)
+    _load().oracle_norm_w_bwd(wt.ctypes.data, dw.ctypes.data, dwt.ctypes.data, dirs, B, G, H, W)
+    return dwt
 
 
 def slice_group(inputs: dict, b: int, g: int, G: int) -> dict:

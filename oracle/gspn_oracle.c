@@ -25,7 +25,13 @@
  *    scanned line, are ignored;
  *  - the four directional outputs are summed: y = sum_d u_d (.) h_d;
  *  - each direction has its own w_d, lambda_d, u_d; x is shared;
- *  - channel c uses weight group c / (C/G).
+ *  - channel c uses weight group c / (C/G);
+ *  - in the normalization of Eq. (row_stochastic_norm), sigma is the logistic
+ *    sigmoid, N(j) holds the taps whose neighbour lies on the grid (the
+ *    others get weight 0), and the denominator is clamped below at
+ *    NORM_EPS = 1e-30 (the paper's fused normalization clamps but gives no
+ *    constant; this one changes nothing unless every sigmoid of N(j) is
+ *    below 1e-30, i.e. all logits are below about -69).
  *
  * All arithmetic is double precision.  Layouts (row-major):
  *   x, y, dy, dx       [B][C][H][W]
@@ -36,7 +42,10 @@
  */
 #include <stdint.h>
 #include <stdlib.h>
+#include <math.h>
 #include <string.h>
+
+#define NORM_EPS 1e-30
 
 enum { DIR_T2B = 1, DIR_B2T = 2, DIR_L2R = 4, DIR_R2L = 8 };
 
@@ -211,4 +220,92 @@ void oracle_scan_bwd(const double *x, const double *w, const double *lam,
     free(hist);
     free(a_next);
     free(a_cur);
+}
+
+/* Logistic sigmoid. */
+static double sigmoid(double t) { return 1.0 / (1.0 + exp(-t)); }
+
+/* Whether tap k of the weight at storage (r, col) reads a neighbour on the grid. */
+static int tap_on_grid(int d, int k, int r, int col, int H, int W)
+{
+    if (d == DIR_T2B || d == DIR_B2T) {
+        int c2 = col + k - 1;
+        return c2 >= 0 && c2 < W;
+    }
+    int r2 = r + k - 1;
+    return r2 >= 0 && r2 < H;
+}
+
+/*
+ * Sec. 3, Eq. (row_stochastic_norm): the weights from their logits wt,
+ *   w(j, k) = sigma(wt(j, k)) / max(sum_{k' in N(j)} sigma(wt(j, k')), NORM_EPS)
+ * for k in N(j), and 0 for the taps outside the grid.  Layout of wt and w:
+ * [D][B][G][3][H][W].
+ */
+void oracle_norm_w(const double *wt, double *w, int dirmask, int B, int G, int H, int W)
+{
+    int s = 0;
+    for (int d = 1; d <= 8; d <<= 1) {
+        if (!(dirmask & d))
+            continue;
+        for (int b = 0; b < B; ++b)
+            for (int g = 0; g < G; ++g)
+                for (int r = 0; r < H; ++r)
+                    for (int col = 0; col < W; ++col) {
+                        double sg[3], sum = 0.0;
+                        for (int k = 0; k < 3; ++k) {
+                            sg[k] = tap_on_grid(d, k, r, col, H, W)
+                                        ? sigmoid(wt[at_w(s, b, g, k, r, col, B, G, H, W)])
+                                        : 0.0;
+                            sum += sg[k];
+                        }
+                        if (sum < NORM_EPS)
+                            sum = NORM_EPS;
+                        for (int k = 0; k < 3; ++k)
+                            w[at_w(s, b, g, k, r, col, B, G, H, W)] = sg[k] / sum;
+                    }
+        ++s;
+    }
+}
+
+/*
+ * Gradient of a loss with respect to the logits, given dw = dl/dw of the
+ * normalized weights.  With s_k = sigma(wt_k) and S the sum over N(j):
+ *   dl/dwt_m = s_m (1 - s_m) (dw_m - sum_{k in N(j)} w_k dw_k) / S
+ * for m in N(j), and 0 outside it; where the clamp holds S at NORM_EPS the
+ * sum term drops (S no longer depends on the logits).
+ */
+void oracle_norm_w_bwd(const double *wt, const double *dw, double *dwt, int dirmask, int B,
+                       int G, int H, int W)
+{
+    int s = 0;
+    for (int d = 1; d <= 8; d <<= 1) {
+        if (!(dirmask & d))
+            continue;
+        for (int b = 0; b < B; ++b)
+            for (int g = 0; g < G; ++g)
+                for (int r = 0; r < H; ++r)
+                    for (int col = 0; col < W; ++col) {
+                        double sg[3], gw[3], sum = 0.0;
+                        int on[3];
+                        for (int k = 0; k < 3; ++k) {
+                            int64_t o = at_w(s, b, g, k, r, col, B, G, H, W);
+                            on[k] = tap_on_grid(d, k, r, col, H, W);
+                            sg[k] = on[k] ? sigmoid(wt[o]) : 0.0;
+                            gw[k] = dw[o];
+                            sum += sg[k];
+                        }
+                        int clamped = sum < NORM_EPS;
+                        double den = clamped ? NORM_EPS : sum;
+                        double inner = 0.0;
+                        if (!clamped)
+                            for (int k = 0; k < 3; ++k)
+                                if (on[k])
+                                    inner += sg[k] / den * gw[k];
+                        for (int k = 0; k < 3; ++k)
+                            dwt[at_w(s, b, g, k, r, col, B, G, H, W)] =
+                                on[k] ? sg[k] * (1.0 - sg[k]) * (gw[k] - inner) / den : 0.0;
+                    }
+        ++s;
+    }
 }

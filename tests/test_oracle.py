@@ -399,3 +399,98 @@ def test_group_slice_is_self_contained():
     np.testing.assert_array_equal(part["dx"], full_g["dx"][b:b + 1, cs])
     np.testing.assert_array_equal(part["dw"], full_g["dw"][:, b:b + 1, g:g + 1])
     np.testing.assert_array_equal(part["dlam"], full_g["dlam"][:, b:b + 1, cs])
+
+
+# ---------------------------------------------------------------------------
+# weights from logits, Sec. 3, Eq. (row_stochastic_norm)
+# ---------------------------------------------------------------------------
+
+def _logits(rng, dirs, B, G, H, W, scale=1.0):
+    return rng.standard_normal((ndirs(dirs), B, G, 3, H, W)) * scale
+
+
+@pytest.mark.parametrize("d", DIRS)
+def test_norm_equal_logits_closed_form(d):
+    # equal logits: every tap of N(j) gets 1 / |N(j)| (1/3 inside, 1/2 at the
+    # ends of a line), taps off the grid get 0
+    H, W = 4, 5
+    w = oracle.normalize_w(np.full((1, 2, 1, 3, H, W), 0.7), d)
+    m = valid_tap_mask(d, H, W)
+    expect = m / m.sum(axis=0, keepdims=True)
+    assert np.allclose(w[0, 0, 0], expect, rtol=0, atol=1e-15)
+    assert np.allclose(w[0, 1, 0], expect, rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("dirs", [1, 6, 15])
+def test_norm_rows_sum_to_one_and_ratios_are_sigmoid_ratios(dirs):
+    from scipy.special import expit
+    rng = np.random.default_rng(11)
+    H, W = 5, 7
+    wt = _logits(rng, dirs, 2, 3, H, W, scale=2.0)
+    w = oracle.normalize_w(wt, dirs)
+    for s, d in enumerate([d for d in DIRS if dirs & d]):
+        m = valid_tap_mask(d, H, W)
+        ws = w[s]
+        assert np.all(ws[:, :, ~m] == 0.0)
+        assert np.allclose(ws.sum(axis=2), 1.0, rtol=0, atol=1e-14)
+        # w_k / w_1 = sigma(wt_k) / sigma(wt_1) (the centre tap is always on the grid)
+        sg = expit(wt[s])
+        for k in (0, 2):
+            r = np.where(m[k], ws[:, :, k] / ws[:, :, 1], 0.0)
+            e = np.where(m[k], sg[:, :, k] / sg[:, :, 1], 0.0)
+            assert np.allclose(r, e, rtol=1e-13, atol=0)
+
+
+def test_norm_saturated_neighbours_give_one_weight():
+    # two taps with very negative logits: the third carries the whole row
+    H, W = 3, 4
+    wt = np.full((1, 1, 1, 3, H, W), -800.0)
+    wt[0, 0, 0, 1] = 0.3
+    w = oracle.normalize_w(wt, T2B)
+    assert np.allclose(w[0, 0, 0, 1], 1.0, rtol=0, atol=1e-15)
+    assert np.all(np.abs(w[0, 0, 0, 0]) < 1e-300) and np.all(np.abs(w[0, 0, 0, 2]) < 1e-300)
+
+
+def test_norm_clamp_reading():
+    # every sigmoid of N(j) far below 1e-30: the denominator is held at 1e-30,
+    # so the row no longer sums to one (the reading of the unstated clamp)
+    from scipy.special import expit
+    wt = np.full((1, 1, 1, 3, 2, 3), -80.0)
+    w = oracle.normalize_w(wt, T2B)
+    m = valid_tap_mask(T2B, 2, 3)
+    assert np.allclose(w[0, 0, 0][m], expit(-80.0) / 1e-30, rtol=1e-12, atol=0)
+    # just above the clamp the row sums to one again
+    w2 = oracle.normalize_w(np.full((1, 1, 1, 3, 2, 3), -60.0), T2B)
+    assert np.allclose(w2[0, 0, 0].sum(axis=0), 1.0, rtol=0, atol=1e-14)
+
+
+@pytest.mark.parametrize("dirs,scale", [(15, 1.5), (5, 3.0), (2, 1.0)])
+def test_norm_backward_matches_central_differences(dirs, scale):
+    rng = np.random.default_rng(5)
+    H, W = 3, 4
+    wt = _logits(rng, dirs, 1, 2, H, W, scale)
+    dw = rng.standard_normal(wt.shape)
+    g = oracle.normalize_w_bwd(wt, dw, dirs)
+    eps = 1e-6
+    for idx in [tuple(rng.integers(0, n) for n in wt.shape) for _ in range(40)]:
+        wp, wm = wt.copy(), wt.copy()
+        wp[idx] += eps
+        wm[idx] -= eps
+        fd = (np.sum(dw * oracle.normalize_w(wp, dirs)) -
+              np.sum(dw * oracle.normalize_w(wm, dirs))) / (2 * eps)
+        assert abs(fd - g[idx]) < 1e-7 * (1 + abs(fd)), (idx, fd, g[idx])
+
+
+def test_norm_backward_under_the_clamp_matches_central_differences():
+    rng = np.random.default_rng(6)
+    wt = -75.0 + 0.5 * rng.standard_normal((1, 1, 1, 3, 2, 3))
+    dw = rng.standard_normal(wt.shape)
+    g = oracle.normalize_w_bwd(wt, dw, T2B)
+    eps = 1e-4
+    for idx in np.ndindex(*wt.shape):
+        wp, wm = wt.copy(), wt.copy()
+        wp[idx] += eps
+        wm[idx] -= eps
+        fd = (np.sum(dw * oracle.normalize_w(wp, T2B)) -
+              np.sum(dw * oracle.normalize_w(wm, T2B))) / (2 * eps)
+        assert abs(fd - g[idx]) <= 1e-6 * (abs(fd) + abs(g[idx])) + 1e-300, (idx, fd, g[idx])
