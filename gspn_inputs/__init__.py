@@ -25,7 +25,7 @@ ALL_DIRS = 15
 DIR_BITS = (T2B, B2T, L2R, R2L)
 
 # tensor ids of the counter-based streams
-_TID_X, _TID_LOGIT, _TID_LAM, _TID_U, _TID_DY = 0, 1, 2, 3, 4
+_TID_X, _TID_LOGIT, _TID_LAM, _TID_U, _TID_DY, _TID_RAW_LOGIT = 0, 1, 2, 3, 4, 5
 
 
 @dataclass(frozen=True)
@@ -136,6 +136,22 @@ def make_inputs(wl: Workload, with_dy: bool | None = None) -> dict:
         with_dy = wl.backward
     if with_dy:
         out["dy"] = _normal((B, C, H, W), wl.seed, _TID_DY, 0, 0.0, 1.0, 0, bf16)
+    return out
+
+
+def make_logits(wl: Workload) -> np.ndarray:
+    """Raw tap logits [D,B,G,3,H,W] ~ N(0, logit_sigma^2) for the entry points
+    that take the weights as logits (bf16-representable for bf16 workloads).
+    Every tap gets a value, including those the operator ignores."""
+    bf16 = wl.dtype == "bf16"
+    D, B, G, H, W = wl.ndirs, wl.B, wl.G, wl.H, wl.W
+    out = np.empty((D, B, G, 3, H, W), dtype=np.float32)
+    s = 0
+    for bit in DIR_BITS:
+        if wl.dirs & bit:
+            out[s] = _normal((B, G, 3, H, W), wl.seed, _TID_RAW_LOGIT, bit, 0.0, wl.logit_sigma, 0,
+                             bf16)
+            s += 1
     return out
 
 

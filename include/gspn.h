@@ -49,10 +49,10 @@
  * fully overwritten (never accumulated into); inputs are never written.
  * Buffers of one call must not overlap.  Every base pointer must be 16-byte
  * aligned.  Calls are asynchronous on `stream` (a hipStream_t; NULL is the
- * null stream) and never synchronise the device.  gspn_scan_bwd may take
- * stream-ordered scratch memory from the device's default memory pool, and so
- * may gspn_scan_fwd for planes with a side above 64; it is released on the
- * same stream.  Calls are thread-safe.
+ * null stream) and never synchronise the device.  gspn_scan_bwd and the
+ * _norm entry points may take stream-ordered scratch memory from the
+ * device's default memory pool, and so may gspn_scan_fwd for planes with a
+ * side above 64; it is released on the same stream.  Calls are thread-safe.
  *
  * Errors: every argument check runs on the host before any HIP call, so an
  * invalid call has no effect on the device.  A failed HIP call returns
@@ -129,6 +129,31 @@ int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
                   const void *dy, void *dx, void *dw, void *dlam, void *du,
                   int direction, int B, int C, int G, int H, int W, int dtype,
                   void *stream);
+
+/*
+ * The two passes with the weights given by their logits wt, laid out like w:
+ * Sec. 3, Eq. (row_stochastic_norm) forms
+ *   w(j,k) = sigma(wt(j,k)) / max(sum_{k' in N(j)} sigma(wt(j,k')), 1e-30)
+ * with sigma the logistic sigmoid and N(j) the taps whose neighbour lies on
+ * the grid (the others get weight 0; the clamp is a reading, the paper names
+ * no constant).  Taps outside N(j) may hold any value.  The weights are
+ * formed once per group and pixel, in fp32, and stored in the storage type in
+ * stream-ordered scratch memory for the scan.
+ *   w_logits   [D][B][G][3][plane]   in
+ *   dw_logits  [D][B][G][3][plane]   out (backward): dl/dwt, from dl/dw by
+ *       dl/dwt_m = sigma(wt_m)(1 - sigma(wt_m)) (dw_m - sum_k w_k dw_k) / S
+ *     on N(j) (S the clamped sum), 0 elsewhere; dl/dw passes through the
+ *     storage type on the way.
+ * Other arguments, checks and errors as in gspn_scan_fwd / gspn_scan_bwd.
+ */
+int gspn_scan_fwd_norm(const void *x, const void *w_logits, const void *lam,
+                       const void *u, void *y, int direction, int B, int C,
+                       int G, int H, int W, int dtype, void *stream);
+
+int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
+                       const void *u, const void *dy, void *dx, void *dw_logits,
+                       void *dlam, void *du, int direction, int B, int C, int G,
+                       int H, int W, int dtype, void *stream);
 
 /* Static description of a status code (never NULL). */
 const char *gspn_strerror(int status);

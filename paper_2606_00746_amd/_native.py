@@ -20,8 +20,8 @@ OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUP
     0, -1, -2, -3, -4, -5, -6, -7, -8)
 MAX_SIDE = 4096
 
-EXPORTED = ("gspn_scan_fwd", "gspn_scan_bwd", "gspn_strerror", "gspn_last_hip_error",
-            "gspn_version")
+EXPORTED = ("gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
+            "gspn_strerror", "gspn_last_hip_error", "gspn_version")
 
 _lib = None
 
@@ -50,6 +50,11 @@ def load() -> ctypes.CDLL:
         lib.gspn_scan_fwd.restype = i
         lib.gspn_scan_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
         lib.gspn_scan_bwd.restype = i
+        lib.gspn_scan_fwd_norm.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+        lib.gspn_scan_fwd_norm.restype = i
+        lib.gspn_scan_bwd_norm.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i,
+                                           vp]
+        lib.gspn_scan_bwd_norm.restype = i
         lib.gspn_strerror.argtypes = [i]
         lib.gspn_strerror.restype = ctypes.c_char_p
         lib.gspn_last_hip_error.argtypes = []
@@ -72,6 +77,17 @@ def gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, 
                   stream) -> int:
     return load().gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W,
                                 dtype, stream)
+
+
+def gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype, stream) -> int:
+    return load().gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype,
+                                     stream)
+
+
+def gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction, B, C, G, H,
+                       W, dtype, stream) -> int:
+    return load().gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction,
+                                     B, C, G, H, W, dtype, stream)
 
 
 def gspn_strerror(status: int) -> str:
@@ -160,6 +176,34 @@ def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
                            _dtype_code(x), _stream_handle(x, stream))
     _check_raise(status)
     return dx, dw, dlam, du
+
+
+def scan_fwd_norm(x, w_logits, lam, u, direction: int = ALL, y=None, stream=None):
+    """As :func:`scan_fwd`, with the weights given by their logits
+    (Sec. 3, Eq. (row_stochastic_norm))."""
+    import torch
+    B, C, G, H, W = _sizes(x, w_logits, lam, u, direction)
+    if y is None:
+        y = torch.empty_like(x)
+    status = gspn_scan_fwd_norm(*_ptrs(x, w_logits, lam, u, y), direction, B, C, G, H, W,
+                                _dtype_code(x), _stream_handle(x, stream))
+    _check_raise(status)
+    return y
+
+
+def scan_bwd_norm(x, w_logits, lam, u, dy, direction: int = ALL, out=None, stream=None):
+    """Gradients (dx, dw_logits, dlam, du) of <y, dy>, the weights given by
+    their logits."""
+    import torch
+    B, C, G, H, W = _sizes(x, w_logits, lam, u, direction)
+    if out is None:
+        out = (torch.empty_like(x), torch.empty_like(w_logits), torch.empty_like(lam),
+               torch.empty_like(u))
+    dx, dwl, dlam, du = out
+    status = gspn_scan_bwd_norm(*_ptrs(x, w_logits, lam, u, dy, dx, dwl, dlam, du), direction, B,
+                                C, G, H, W, _dtype_code(x), _stream_handle(x, stream))
+    _check_raise(status)
+    return dx, dwl, dlam, du
 
 
 LINE_BLOCK = 8   # lines per block of the line-major layout

@@ -83,6 +83,35 @@ hipError_t scratch_free(void *ptr, hipStream_t s) { return hipFreeAsync(ptr, s);
 
 using namespace gspn;
 
+namespace gspn {
+
+// The kernel family for a problem: the first one that supports its shape.
+hipError_t dispatch_fwd(const Problem &p, hipStream_t s)
+{
+    if (med_supported(p))
+        return launch_fwd_med(p, s);
+    if (tiny_supported(p))
+        return launch_fwd_tiny(p, s);
+    if (p.H <= kSmallSide && p.W <= kSmallSide)
+        return launch_fwd_small(p, s);
+    if (wide_supported(p))
+        return launch_fwd_wide(p, s);
+    return launch_fwd_general(p, s);
+}
+
+hipError_t dispatch_bwd(const Problem &p, hipStream_t s)
+{
+    if (med_supported(p))
+        return launch_bwd_med(p, s);
+    if (tiny_supported(p))
+        return launch_bwd_tiny(p, s);
+    if (p.H <= kSmallSide && p.W <= kSmallSide)
+        return launch_bwd_small(p, s);
+    return launch_bwd_general(p, s);
+}
+
+}  // namespace gspn
+
 extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u, void *y,
                              int direction, int B, int C, int G, int H, int W, int dtype,
                              void *stream)
@@ -101,16 +130,7 @@ extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, cons
         return st;
     Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
               direction, B, C, G, H, W, dtype};
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (med_supported(p))
-        return hip_status(launch_fwd_med(p, s));
-    if (tiny_supported(p))
-        return hip_status(launch_fwd_tiny(p, s));
-    if (H <= kSmallSide && W <= kSmallSide)
-        return hip_status(launch_fwd_small(p, s));
-    if (wide_supported(p))
-        return hip_status(launch_fwd_wide(p, s));
-    return hip_status(launch_fwd_general(p, s));
+    return hip_status(dispatch_fwd(p, static_cast<hipStream_t>(stream)));
 }
 
 extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
@@ -132,14 +152,73 @@ extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, cons
     if (st != GSPN_OK)
         return st;
     Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
+    return hip_status(dispatch_bwd(p, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int gspn_scan_fwd_norm(const void *x, const void *w_logits, const void *lam,
+                                  const void *u, void *y, int direction, int B, int C, int G,
+                                  int H, int W, int dtype, void *stream)
+{
+    int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t n = (int64_t)B * C * H * W;
+    const int64_t nw = D * B * G * 3 * H * W;
+    const Buf bufs[] = {{x, n * es, false},     {w_logits, nw * es, false}, {lam, D * n * es, false},
+                        {u, D * n * es, false}, {y, n * es, true}};
+    st = check_buffers(bufs, 5);
+    if (st != GSPN_OK)
+        return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    if (med_supported(p))
-        return hip_status(launch_bwd_med(p, s));
-    if (tiny_supported(p))
-        return hip_status(launch_bwd_tiny(p, s));
-    if (H <= kSmallSide && W <= kSmallSide)
-        return hip_status(launch_bwd_small(p, s));
-    return hip_status(launch_bwd_general(p, s));
+    void *w = nullptr;
+    hipError_t e = scratch_alloc(&w, (size_t)(nw * es), s);
+    if (e != hipSuccess)
+        return hip_status(e);
+    Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
+              direction, B, C, G, H, W, dtype};
+    e = launch_norm(p, w_logits, nullptr, w, s);
+    if (e == hipSuccess)
+        e = dispatch_fwd(p, s);
+    const hipError_t e2 = scratch_free(w, s);
+    return hip_status(e != hipSuccess ? e : e2);
+}
+
+extern "C" int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
+                                  const void *u, const void *dy, void *dx, void *dw_logits,
+                                  void *dlam, void *du, int direction, int B, int C, int G, int H,
+                                  int W, int dtype, void *stream)
+{
+    int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t n = (int64_t)B * C * H * W;
+    const int64_t nw = D * B * G * 3 * H * W;
+    const Buf bufs[] = {{x, n * es, false},         {w_logits, nw * es, false},
+                        {lam, D * n * es, false},   {u, D * n * es, false},
+                        {dy, n * es, false},        {dx, n * es, true},
+                        {dw_logits, nw * es, true}, {dlam, D * n * es, true},
+                        {du, D * n * es, true}};
+    st = check_buffers(bufs, 9);
+    if (st != GSPN_OK)
+        return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    void *w = nullptr;
+    hipError_t e = scratch_alloc(&w, (size_t)(2 * nw * es), s);   // weights, then their gradient
+    if (e != hipSuccess)
+        return hip_status(e);
+    void *dw = static_cast<char *>(w) + nw * es;
+    Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
+    e = launch_norm(p, w_logits, nullptr, w, s);
+    if (e == hipSuccess)
+        e = dispatch_bwd(p, s);
+    if (e == hipSuccess)
+        e = launch_norm(p, w_logits, dw, dw_logits, s);
+    const hipError_t e2 = scratch_free(w, s);
+    return hip_status(e != hipSuccess ? e : e2);
 }
 
 extern "C" const char *gspn_strerror(int status)

@@ -20,6 +20,10 @@ hipError_t launch_bwd_small(const Problem &p, hipStream_t s);
 bool tiny_supported(const Problem &p);
 hipError_t launch_fwd_tiny(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_tiny(const Problem &p, hipStream_t s);
+// Weights from logits (dw == nullptr) or the logits' gradient from dw, for
+// every direction of p (Sec. 3, Eq. (row_stochastic_norm)); wt, dw, out in
+// p's storage type and weight layout.
+hipError_t launch_norm(const Problem &p, const void *wt, const void *dw, void *out, hipStream_t s);
 bool med_supported(const Problem &p);
 hipError_t launch_fwd_med(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_med(const Problem &p, hipStream_t s);

@@ -1,0 +1,197 @@
+// Tridiagonal weights from their logits, Sec. 3, Eq. (row_stochastic_norm),
+// and the gradient with respect to the logits.
+//
+// For every pixel of a direction's tap planes:
+//   s_k = sigmoid(wt_k) for the taps k whose neighbour lies on the grid
+//         (0 for the others), S = max(s_0 + s_1 + s_2, kNormEps),
+//   w_k = s_k / S,
+//   dwt_m = s_m (1 - s_m) (dw_m - sum_k w_k dw_k) / S   (the sum term drops
+//         where the clamp holds S at kNormEps).
+// A group's weights serve all C/G of its channels, so they are formed once
+// here rather than in every channel's scan.
+//
+// Planes are blocked line-major: one 16-byte piece of a full 8-line block
+// holds the 8 consecutive lines of one line position, which decides the
+// validity of taps 0 and 2; a last, partial block is taken element by
+// element.
+#include "cdna.hpp"
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace gspn {
+
+namespace {
+
+using namespace cdna;
+
+constexpr float kNormEps = 1e-30f;
+
+__device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
+
+__device__ __forceinline__ void load8(const float *p, float (&v)[8])
+{
+    const float4 a = *reinterpret_cast<const float4 *>(p);
+    const float4 b = *reinterpret_cast<const float4 *>(p + 4);
+    v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w, v[4] = b.x, v[5] = b.y, v[6] = b.z, v[7] = b.w;
+}
+__device__ __forceinline__ void load8(const bf16_t *p, float (&v)[8])
+{
+    const uint4 a = *reinterpret_cast<const uint4 *>(p);
+    const uint32_t q[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[2 * e] = __uint_as_float(q[e] << 16);
+        v[2 * e + 1] = __uint_as_float(q[e] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void store8(float *p, const float (&v)[8])
+{
+    *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4 *>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void store8(bf16_t *p, const float (&v)[8])
+{
+    gst128(reinterpret_cast<uint4 *>(p),
+           make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
+}
+
+// Normalized weights of one pixel from its three logits.
+__device__ __forceinline__ void norm3(const float (&t)[3], bool on0, bool on2, float (&w)[3])
+{
+    const float s0 = on0 ? sigmoid(t[0]) : 0.f;
+    const float s1 = sigmoid(t[1]);
+    const float s2 = on2 ? sigmoid(t[2]) : 0.f;
+    const float S = fmaxf((s0 + s1) + s2, kNormEps);
+    w[0] = s0 / S;
+    w[1] = s1 / S;
+    w[2] = s2 / S;
+}
+
+// Gradient with respect to the logits of one pixel.
+__device__ __forceinline__ void norm3_bwd(const float (&t)[3], const float (&g)[3], bool on0,
+                                          bool on2, float (&dt)[3])
+{
+    const float s[3] = {on0 ? sigmoid(t[0]) : 0.f, sigmoid(t[1]), on2 ? sigmoid(t[2]) : 0.f};
+    const float sum = (s[0] + s[1]) + s[2];
+    const bool clamped = sum < kNormEps;
+    const float S = clamped ? kNormEps : sum;
+    const float inner = clamped ? 0.f : ((s[0] / S) * g[0] + (s[1] / S) * g[1]) + (s[2] / S) * g[2];
+    const bool on[3] = {on0, true, on2};
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        dt[k] = on[k] ? s[k] * (1.f - s[k]) * (g[k] - inner) / S : 0.f;
+}
+
+// One direction: np3 tap-plane triples of HW elements, lines of P positions,
+// L lines.  dw == nullptr: write the weights; else the logits' gradient.
+// vec: the planes start on 16-byte boundaries, so full blocks go by pieces.
+template <typename T>
+__global__ __launch_bounds__(256) void norm_kernel(const T *__restrict__ wt, const T *__restrict__ dw,
+                                                   T *__restrict__ out, int64_t nsets, int HW, int L,
+                                                   int P, bool vec)
+{
+    const int nfull = vec ? L / 8 : 0;
+    const int64_t pieces = (int64_t)nfull * P;          // 8-element pieces per plane
+    const int tail = (L - 8 * nfull) * P;               // elements taken one by one
+    const int64_t per = pieces + tail;
+    const int64_t n = nsets * per;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t set = o / per;
+        const int64_t r = o - set * per;
+        const T *src = wt + set * 3 * HW;
+        const T *gsrc = dw ? dw + set * 3 * HW : nullptr;
+        T *dst = out + set * 3 * HW;
+        if (r < pieces) {
+            const int p = (int)(r % P);
+            const int64_t e = 8 * r;                    // 8 lines of position p
+            const bool on0 = p > 0, on2 = p + 1 < P;
+            float t[3][8], v[3][8];
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                load8(src + k * HW + e, t[k]);
+            if (gsrc) {
+                float g[3][8];
+#pragma unroll
+                for (int k = 0; k < 3; ++k)
+                    load8(gsrc + k * HW + e, g[k]);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const float tq[3] = {t[0][q], t[1][q], t[2][q]};
+                    const float gq[3] = {g[0][q], g[1][q], g[2][q]};
+                    float d[3];
+                    norm3_bwd(tq, gq, on0, on2, d);
+                    v[0][q] = d[0], v[1][q] = d[1], v[2][q] = d[2];
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const float tq[3] = {t[0][q], t[1][q], t[2][q]};
+                    float wq[3];
+                    norm3(tq, on0, on2, wq);
+                    v[0][q] = wq[0], v[1][q] = wq[1], v[2][q] = wq[2];
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                store8(dst + k * HW + e, v[k]);
+        } else {
+            // element by element: block q of n lines, position p
+            const int64_t e = 8 * pieces + (r - pieces);
+            const int q = (int)(e / (8 * P));
+            const int rem = (int)(e - (int64_t)q * 8 * P);
+            const int nl = L - 8 * q < 8 ? L - 8 * q : 8;
+            const int p = rem / nl;
+            const bool on0 = p > 0, on2 = p + 1 < P;
+            const float tq[3] = {load_f(src + e), load_f(src + HW + e), load_f(src + 2 * HW + e)};
+            float v[3];
+            if (gsrc) {
+                const float gq[3] = {load_f(gsrc + e), load_f(gsrc + HW + e), load_f(gsrc + 2 * HW + e)};
+                norm3_bwd(tq, gq, on0, on2, v);
+            } else {
+                norm3(tq, on0, on2, v);
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                store_f(dst + k * HW + e, v[k]);
+        }
+    }
+}
+
+template <typename T>
+hipError_t launch_norm_t(const Problem &p, const void *wt, const void *dw, void *out, hipStream_t st)
+{
+    const int64_t HW = (int64_t)p.H * p.W;
+    const int64_t sets = (int64_t)p.B * p.G;            // tap-plane triples per direction
+    int s = 0;
+    for (int d = 0; d < 4; ++d) {
+        if (!((p.mask >> d) & 1))
+            continue;
+        const bool vert = d < 2;
+        const int L = vert ? p.H : p.W, P = vert ? p.W : p.H;
+        const int64_t off = (int64_t)s * sets * 3 * HW;
+        const bool vec = HW % 8 == 0;
+        const int64_t n = sets * (vec ? (int64_t)(L / 8) * P + (int64_t)(L % 8) * P : HW);
+        int64_t blocks = (n + 255) / 256;
+        blocks = blocks < 8192 ? blocks : 8192;
+        hipLaunchKernelGGL((norm_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           static_cast<const T *>(wt) + off,
+                           dw ? static_cast<const T *>(dw) + off : nullptr, static_cast<T *>(out) + off,
+                           sets, (int)HW, L, P, vec);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        ++s;
+    }
+    return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_norm(const Problem &p, const void *wt, const void *dw, void *out, hipStream_t st)
+{
+    return p.dtype == 0 ? launch_norm_t<float>(p, wt, dw, out, st)
+                        : launch_norm_t<bf16_t>(p, wt, dw, out, st);
+}
+
+}  // namespace gspn

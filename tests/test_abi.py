@@ -64,9 +64,26 @@ def bwd(**kw):
                            a["dtype"], a["stream"])
 
 
-@pytest.mark.parametrize("call", [fwd, bwd])
+def fwd_norm(**kw):
+    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), y=P(4), direction=15, B=1, C=4, G=2, H=8, W=8,
+             dtype=g.BF16, stream=None)
+    a.update(kw)
+    return g.gspn_scan_fwd_norm(a["x"], a["w"], a["lam"], a["u"], a["y"], a["direction"], a["B"],
+                                a["C"], a["G"], a["H"], a["W"], a["dtype"], a["stream"])
+
+
+def bwd_norm(**kw):
+    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), dy=P(4), dx=P(5), dw=P(6), dlam=P(7), du=P(8),
+             direction=15, B=1, C=4, G=2, H=8, W=8, dtype=g.BF16, stream=None)
+    a.update(kw)
+    return g.gspn_scan_bwd_norm(a["x"], a["w"], a["lam"], a["u"], a["dy"], a["dx"], a["dw"],
+                                a["dlam"], a["du"], a["direction"], a["B"], a["C"], a["G"],
+                                a["H"], a["W"], a["dtype"], a["stream"])
+
+
+@pytest.mark.parametrize("call", [fwd, bwd, fwd_norm, bwd_norm])
 def test_invalid_arguments(call):
-    ptrs = ["x", "w", "lam", "u", "y"] if call is fwd else \
+    ptrs = ["x", "w", "lam", "u", "y"] if call in (fwd, fwd_norm) else \
         ["x", "w", "lam", "u", "dy", "dx", "dw", "dlam", "du"]
     for name in ptrs:
         assert call(**{name: None}) == _native.ERR_NULL, name
