@@ -9,6 +9,7 @@ events on the launch stream) and the CPU oracle timed on a bounded sample of
 the same workload.  Diagnostics go to stderr.
 
     python bench.py [--steps K] [--warmup W] [--workload IDX|NAME|all] [--no-cpu-baseline]
+                    [--norm]
 
 Before every step, outside the timed events, reading a 1 GiB buffer evicts
 the L2s and the 256 MB Infinity Cache (writing back what the previous step
@@ -64,7 +65,7 @@ def to_device(a, dtype, torch):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
 
 
-def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float) -> dict:
+def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool = False) -> dict:
     """The fp64 oracle, single thread, on (batch, group) units of the workload.
 
     Units run in a fixed order until `min_seconds` have passed or the whole
@@ -80,9 +81,12 @@ def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float) -> dict:
     while True:
         for b, g in order:
             sl = oracle.slice_group(inputs, b, g, wl.G)
-            oracle.scan_fwd(sl["x"], sl["w"], sl["lam"], sl["u"], wl.dirs)
+            w = oracle.normalize_w(sl["w"], wl.dirs) if norm else sl["w"]
+            oracle.scan_fwd(sl["x"], w, sl["lam"], sl["u"], wl.dirs)
             if wl.backward:
-                oracle.scan_bwd(sl["x"], sl["w"], sl["lam"], sl["u"], sl["dy"], wl.dirs)
+                r = oracle.scan_bwd(sl["x"], w, sl["lam"], sl["u"], sl["dy"], wl.dirs)
+                if norm:
+                    oracle.normalize_w_bwd(sl["w"], r["dw"], wl.dirs)
             done += 1
             if passes == 0 and time.perf_counter() - t0 >= min_seconds:
                 break
@@ -121,10 +125,15 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     log(f"workload {wl}")
     t0 = time.perf_counter()
     inputs = gi.make_inputs(wl, with_dy=wl.backward)
+    if args.norm:
+        # the weights as logits: the calls form the row-stochastic weights
+        inputs["w"] = gi.make_logits(wl)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
     dev = {k: to_device(v, wl.dtype, torch)
            for k, v in gi.inputs_line_major(inputs, wl.dirs).items()}
     x, w, lam, u = dev["x"], dev["w"], dev["lam"], dev["u"]
+    fwd_call = gspn.scan_fwd_norm if args.norm else gspn.scan_fwd
+    bwd_call = gspn.scan_bwd_norm if args.norm else gspn.scan_bwd
     y = torch.empty_like(x)
     if wl.backward:
         dy = dev["dy"]
@@ -144,11 +153,11 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         flush()
         if ev is not None:
             ev[0].record(stream)
-        gspn.scan_fwd(x, w, lam, u, wl.dirs, y=y, stream=stream)
+        fwd_call(x, w, lam, u, wl.dirs, y=y, stream=stream)
         if ev is not None:
             ev[1].record(stream)
         if wl.backward:
-            gspn.scan_bwd(x, w, lam, u, dy, wl.dirs, out=grads, stream=stream)
+            bwd_call(x, w, lam, u, dy, wl.dirs, out=grads, stream=stream)
         if ev is not None:
             ev[2].record(stream)
 
@@ -194,7 +203,8 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     # measured HBM bytes of the same call (FETCH_SIZE + WRITE_SIZE counters, scaled by a
     # plain copy), kept in profiles/ for the current kernel sources only
     from paper_2606_00746_amd import profiling
-    traffic = profiling.load_traffic(os.path.join(ROOT, "profiles", f"traffic_{wl.name}.txt"), call)
+    traffic = None if args.norm else profiling.load_traffic(
+        os.path.join(ROOT, "profiles", f"traffic_{wl.name}.txt"), call)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
@@ -226,7 +236,8 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         "data": "synthetic",
         "config": {"workload": wl.name, "B": wl.B, "C": wl.C, "G": wl.G, "H": wl.H, "W": wl.W,
                    "directions": wl.ndirs, "pass": "fwd+bwd" if wl.backward else "fwd",
-                   "storage": wl.dtype, "parallelism": "single GPU"},
+                   "storage": wl.dtype, "weights": "logits" if args.norm else "normalized",
+                   "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
         "cache_flush_mib": args.flush_mib,
@@ -237,7 +248,7 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
-        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm)
     return out
 
 
@@ -249,6 +260,8 @@ def main() -> int:
     ap.add_argument("--workload", default="3",
                     help="index or name of the workload, or 'all' (one line each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--norm", action="store_true",
+                    help="weights given as logits: time gspn_scan_fwd_norm / gspn_scan_bwd_norm")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time of the oracle baseline")
     ap.add_argument("--flush-mib", type=int, default=1024,

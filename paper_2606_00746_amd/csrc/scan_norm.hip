@@ -61,10 +61,10 @@ __device__ __forceinline__ void norm3(const float (&t)[3], bool on0, bool on2, f
     const float s0 = on0 ? sigmoid(t[0]) : 0.f;
     const float s1 = sigmoid(t[1]);
     const float s2 = on2 ? sigmoid(t[2]) : 0.f;
-    const float S = fmaxf((s0 + s1) + s2, kNormEps);
-    w[0] = s0 / S;
-    w[1] = s1 / S;
-    w[2] = s2 / S;
+    const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+    w[0] = s0 * inv;
+    w[1] = s1 * inv;
+    w[2] = s2 * inv;
 }
 
 // Gradient with respect to the logits of one pixel.
@@ -74,31 +74,52 @@ __device__ __forceinline__ void norm3_bwd(const float (&t)[3], const float (&g)[
     const float s[3] = {on0 ? sigmoid(t[0]) : 0.f, sigmoid(t[1]), on2 ? sigmoid(t[2]) : 0.f};
     const float sum = (s[0] + s[1]) + s[2];
     const bool clamped = sum < kNormEps;
-    const float S = clamped ? kNormEps : sum;
-    const float inner = clamped ? 0.f : ((s[0] / S) * g[0] + (s[1] / S) * g[1]) + (s[2] / S) * g[2];
+    const float inv = 1.f / (clamped ? kNormEps : sum);
+    const float inner = clamped ? 0.f : ((s[0] * inv) * g[0] + (s[1] * inv) * g[1]) + (s[2] * inv) * g[2];
     const bool on[3] = {on0, true, on2};
 #pragma unroll
     for (int k = 0; k < 3; ++k)
-        dt[k] = on[k] ? s[k] * (1.f - s[k]) * (g[k] - inner) / S : 0.f;
+        dt[k] = on[k] ? s[k] * (1.f - s[k]) * (g[k] - inner) * inv : 0.f;
 }
 
-// One direction: np3 tap-plane triples of HW elements, lines of P positions,
-// L lines.  dw == nullptr: write the weights; else the logits' gradient.
-// vec: the planes start on 16-byte boundaries, so full blocks go by pieces.
+// Every direction of the mask in one launch: for direction slot s, the B*G
+// tap-plane triples of HW elements, lines of P positions, L lines.
+// dw == nullptr: write the weights; else the logits' gradient.  vec: the
+// planes start on 16-byte boundaries, so full blocks go by 8-element pieces.
 template <typename T>
 __global__ __launch_bounds__(256) void norm_kernel(const T *__restrict__ wt, const T *__restrict__ dw,
-                                                   T *__restrict__ out, int64_t nsets, int HW, int L,
-                                                   int P, bool vec)
+                                                   T *__restrict__ out, int mask, int64_t sets, int H,
+                                                   int W, bool vec)
 {
-    const int nfull = vec ? L / 8 : 0;
-    const int64_t pieces = (int64_t)nfull * P;          // 8-element pieces per plane
-    const int tail = (L - 8 * nfull) * P;               // elements taken one by one
-    const int64_t per = pieces + tail;
-    const int64_t n = nsets * per;
+    const int HW = H * W;
+    // units (pieces, then single elements) per tap-plane triple of each slot
+    int64_t cum[5];
+    int Ls[4], Ps[4];
+    int nd = 0;
+    cum[0] = 0;
+    for (int d = 0; d < 4; ++d) {
+        if (!((mask >> d) & 1))
+            continue;
+        const int L = d < 2 ? H : W, P = d < 2 ? W : H;
+        const int nfull = vec ? L / 8 : 0;
+        Ls[nd] = L;
+        Ps[nd] = P;
+        cum[nd + 1] = cum[nd] + sets * ((int64_t)nfull * P + (int64_t)(L - 8 * nfull) * P);
+        ++nd;
+    }
+    const int64_t n = cum[nd];
     for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
          o += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t set = o / per;
-        const int64_t r = o - set * per;
+        int sl = 0;
+        while (sl + 1 < nd && o >= cum[sl + 1])
+            ++sl;
+        const int L = Ls[sl], P = Ps[sl];
+        const int nfull = vec ? L / 8 : 0;
+        const int64_t pieces = (int64_t)nfull * P;
+        const int64_t per = pieces + (int64_t)(L - 8 * nfull) * P;
+        const int64_t oo = o - cum[sl];
+        const int64_t set = (int64_t)sl * sets + oo / per;
+        const int64_t r = oo % per;
         const T *src = wt + set * 3 * HW;
         const T *gsrc = dw ? dw + set * 3 * HW : nullptr;
         T *dst = out + set * 3 * HW;
@@ -136,7 +157,7 @@ __global__ __launch_bounds__(256) void norm_kernel(const T *__restrict__ wt, con
             for (int k = 0; k < 3; ++k)
                 store8(dst + k * HW + e, v[k]);
         } else {
-            // element by element: block q of n lines, position p
+            // element by element: block q of nl lines, position p
             const int64_t e = 8 * pieces + (r - pieces);
             const int q = (int)(e / (8 * P));
             const int rem = (int)(e - (int64_t)q * 8 * P);
@@ -163,27 +184,15 @@ hipError_t launch_norm_t(const Problem &p, const void *wt, const void *dw, void 
 {
     const int64_t HW = (int64_t)p.H * p.W;
     const int64_t sets = (int64_t)p.B * p.G;            // tap-plane triples per direction
-    int s = 0;
-    for (int d = 0; d < 4; ++d) {
-        if (!((p.mask >> d) & 1))
-            continue;
-        const bool vert = d < 2;
-        const int L = vert ? p.H : p.W, P = vert ? p.W : p.H;
-        const int64_t off = (int64_t)s * sets * 3 * HW;
-        const bool vec = HW % 8 == 0;
-        const int64_t n = sets * (vec ? (int64_t)(L / 8) * P + (int64_t)(L % 8) * P : HW);
-        int64_t blocks = (n + 255) / 256;
-        blocks = blocks < 8192 ? blocks : 8192;
-        hipLaunchKernelGGL((norm_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           static_cast<const T *>(wt) + off,
-                           dw ? static_cast<const T *>(dw) + off : nullptr, static_cast<T *>(out) + off,
-                           sets, (int)HW, L, P, vec);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess)
-            return e;
-        ++s;
-    }
-    return hipSuccess;
+    const bool vec = HW % 8 == 0;
+    const int64_t per = vec ? HW / 8 + 8 : HW;           // units per triple, at most
+    const int64_t n = (int64_t)__builtin_popcount(p.mask) * sets * per;
+    int64_t blocks = (n + 255) / 256;
+    blocks = blocks < 16384 ? blocks : 16384;
+    hipLaunchKernelGGL((norm_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, st,
+                       static_cast<const T *>(wt), static_cast<const T *>(dw), static_cast<T *>(out),
+                       p.mask, sets, p.H, p.W, vec);
+    return hipGetLastError();
 }
 
 }  // namespace
