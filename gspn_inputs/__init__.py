@@ -57,13 +57,17 @@ class Workload:
 
 
 # The five workloads: a tiny fp32 case the oracle checks in full, three ViT /
-# hierarchical-encoder stages and one extreme-resolution inference case.
+# hierarchical-encoder stages and one extreme-resolution inference case; then
+# the 64x64 stage with one weight group per channel (the paper's original,
+# ungrouped recurrence).
 WORKLOADS = [
     Workload("tiny-16x16-c8-f32", 1, 8, 1, 16, 16, "f32", T2B, False, "normal", 1.0, 0),
     Workload("vit-s-14x14-b32-c384", 32, 384, 12, 14, 14, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 1),
     Workload("hier-56x56-b64-c96", 64, 96, 8, 56, 56, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 2),
     Workload("hires-64x64-b8-c768", 8, 768, 24, 64, 64, "bf16", ALL_DIRS, True, "sigmoid", 1.0, 3),
     Workload("xres-256x256-b1-c1024", 1, 1024, 32, 256, 256, "bf16", ALL_DIRS, False, "sigmoid", 2.0, 4),
+    Workload("hires-64x64-b8-c768-g768", 8, 768, 768, 64, 64, "bf16", ALL_DIRS, True, "sigmoid", 1.0,
+             5),
 ]
 
 

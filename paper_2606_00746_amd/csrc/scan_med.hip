@@ -317,7 +317,7 @@ struct BwdArgs {
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM>
+template <int H, int W, int D, bool IMM, bool PC = false>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
@@ -471,6 +471,10 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     // value of the first step of a pair waits in du0 / dl0
     uint32_t dup[4], dlp[4];
     float du0 = 0.f, dl0 = 0.f;
+    // one channel per group (PC): the weight gradient is this wave's own
+    // products, packed per block like du
+    uint32_t dwp[3][4];
+    float dw0[3] = {0.f, 0.f, 0.f};
     uint32_t xq[VERT ? 1 : L];
     if (!VERT) {
 #pragma unroll
@@ -532,34 +536,52 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 const int cc = line_of(i);
                 dxr[cc] = dx_first ? a * lv : fmaf(a, lv, dxr[cc]);
             }
-            // finish the previous batch: its slot reads were issued after the
-            // last barrier and overlapped a step of arithmetic
-            if (!IMM && (i & 3) == 1 && i >= 5 && reducer)
-                reduce_step(i - 5 + A.wave);
-            // w_i couples line i-1 to line i: a_i and h_{i-1} go to the slots
-            // (h_{-1} = 0 makes line 0's gradient zero)
-            const int buf = (i >> 2) & 1;
-            slot_ptr(A.slots, buf, i & 3, 0, A.wave)[j] = a;
-            slot_ptr(A.slots, buf, i & 3, 1, A.wave)[j] = hp;
-            if ((i & 3) == 3) {
-                lds_barrier();
-                if (IMM) {
-                    for (int st = A.wave; st < kBatch; st += A.cw) {
-                        read_step(buf, st);
-                        reduce_step(i - 3 + st);
+            if constexpr (PC) {
+                // w_i couples line i-1 to line i (h_{-1} = 0 zeroes line 0)
+                const float dv[3] = {a * from_left<64>(hp), a * hp, a * from_right<64>(hp)};
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    if ((t & 1) == 0)
+                        dw0[k] = dv[k];
+                    else
+                        dwp[k][e >> 1] = REV ? pack2(dv[k], dw0[k]) : pack2(dw0[k], dv[k]);
+                }
+            } else {
+                // finish the previous batch: its slot reads were issued after
+                // the last barrier and overlapped a step of arithmetic
+                if (!IMM && (i & 3) == 1 && i >= 5 && reducer)
+                    reduce_step(i - 5 + A.wave);
+                // w_i couples line i-1 to line i: a_i and h_{i-1} go to the
+                // slots (h_{-1} = 0 makes line 0's gradient zero)
+                const int buf = (i >> 2) & 1;
+                slot_ptr(A.slots, buf, i & 3, 0, A.wave)[j] = a;
+                slot_ptr(A.slots, buf, i & 3, 1, A.wave)[j] = hp;
+                if ((i & 3) == 3) {
+                    lds_barrier();
+                    if (IMM) {
+                        for (int st = A.wave; st < kBatch; st += A.cw) {
+                            read_step(buf, st);
+                            reduce_step(i - 3 + st);
+                        }
+                    } else if (reducer) {
+                        read_step(buf, A.wave);
                     }
-                } else if (reducer) {
-                    read_step(buf, A.wave);
                 }
             }
             if (t == 7 && act) {
                 st128_nt(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
                 st128_nt(A.dlam, vo, boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                if constexpr (PC) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k)
+                        st128_nt(A.dw, vo, boff(fb) + k * PL2,
+                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]));
+                }
             }
             step_fence();
         }
     }
-    if (!IMM && reducer)
+    if (!PC && !IMM && reducer)
         reduce_step(L - 4 + A.wave);
 #undef FLOADB
 }
@@ -672,7 +694,7 @@ __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float
 // reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
 // second read of lam and w (the first one leaves them in L2) and one more h
 // recurrence per step.
-template <int H, int W, int D, bool IMM>
+template <int H, int W, int D, bool IMM, bool PC = false>
 __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                            float (&dxa)[64])
 {
@@ -783,6 +805,8 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
         // the later step of a pair waits in du1 / dl1
         uint32_t dup[4], dlp[4];
         float du1 = 0.f, dl1 = 0.f;
+        uint32_t dwp[3][4];
+        float dw1[3] = {0.f, 0.f, 0.f};
 #pragma unroll
         for (int t = 7; t >= 0; --t) {
             const int i = 8 * fb + t;
@@ -807,19 +831,40 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
             }
             const int cc = F::line_of(i);
             dxa[cc] = fmaf(a, lv, dxa[cc]);
-            slot_step<H, W, D, IMM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
+            if constexpr (PC) {
+                const float dv[3] = {a * from_left<64>(hp), a * hp, a * from_right<64>(hp)};
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    if (t & 1)
+                        dw1[k] = dv[k];
+                    else
+                        dwp[k][e >> 1] = REV ? pack2(dw1[k], dv[k]) : pack2(dv[k], dw1[k]);
+                }
+            } else {
+                slot_step<H, W, D, IMM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
+            }
             if (t == 0 && act) {
                 st128_nt(A.du, vo, F::boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
                 st128_nt(A.dlam, vo, F::boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                if constexpr (PC) {
+#pragma unroll
+                    for (int k = 0; k < 3; ++k)
+                        st128_nt(A.dw, vo, F::boff(fb) + k * F::PL2,
+                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]));
+                }
             }
             step_fence();
         }
     }
-    slot_finish<H, W, D, IMM>(A, j, pa, ph, step_of);
+    if constexpr (!PC)
+        slot_finish<H, W, D, IMM>(A, j, pa, ph, step_of);
 #undef BLOAD
 }
 
-template <int H, int W, bool IMM>
+// PC: one channel per weight group; a workgroup then takes cw consecutive
+// channels (groups), each wave sums nothing with the others, and nchunk /
+// divChunk count the workgroups per batch.
+template <int H, int W, bool IMM, bool PC>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -835,15 +880,25 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
-    const int bg = mdiv(blk, divChunk);
-    const int chunk = blk - bg * nchunk;
-    const int b = mdiv(bg, divG);
-    const int g = bg - b * G;
-    const int cpg = mdiv(C, divG);
-    const int cfirst = chunk * cw;
-    const int nvalid = min(cw, cpg - cfirst);
-    const bool cvalid = wave < nvalid;
-    const int c = g * cpg + cfirst + (cvalid ? wave : 0);
+    int b, g, c, chunk;
+    bool cvalid;
+    if constexpr (PC) {
+        b = mdiv(blk, divChunk);
+        chunk = blk - b * nchunk;
+        const int c0 = chunk * cw;
+        cvalid = wave < min(cw, C - c0);
+        c = c0 + (cvalid ? wave : 0);
+        g = c;
+    } else {
+        const int bg = mdiv(blk, divChunk);
+        chunk = blk - bg * nchunk;
+        b = mdiv(bg, divG);
+        g = bg - b * G;
+        const int cpg = mdiv(C, divG);
+        const int cfirst = chunk * cw;
+        cvalid = wave < min(cw, cpg - cfirst);
+        c = g * cpg + cfirst + (cvalid ? wave : 0);
+    }
     const int D = __popc(mask);
     const int64_t pc = ((int64_t)b * C + c) * HW;
 
@@ -853,12 +908,14 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.Xq = smem + wave * XPLANE;
     A.slots = smem + cw * XPLANE;
     // slots of channels this workgroup does not have must read as zero
-    for (int t = threadIdx.x; t < kSlotFloats; t += blockDim.x)
-        A.slots[t] = 0.f;
+    if (!PC) {
+        for (int t = threadIdx.x; t < kSlotFloats; t += blockDim.x)
+            A.slots[t] = 0.f;
+    }
     lds_barrier();
     A.wave = wave;
     A.cw = cw;
-    A.partial = nchunk > 1;
+    A.partial = !PC && nchunk > 1;
 
     // Horizontal directions read x and dy columns: stage both planes in this
     // wave's LDS dx plane (still unused), coalesced; their dx terms collect in
@@ -912,15 +969,15 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
         if ((mask & 4) && H >= 64)
-            dir_bwd_ck<H, W, 3, IMM>(A, lane, cvalid, stg, dxr);
+            dir_bwd_ck<H, W, 3, IMM, PC>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
@@ -933,13 +990,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM, PC>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -1005,15 +1062,16 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W, bool IMM>
+template <int H, int W, bool IMM, bool PC = false>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM>), dim3((unsigned)(p.B * p.G * nchunk)),
+    const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -1036,6 +1094,14 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
     const size_t slots = (size_t)kSlotFloats * 4;                   // per-step dw terms
     const int cpg = p.C / p.G;
+    if (cpg == 1) {
+        // one channel per group: workgroups of up to kSlots channels, no slots
+        const int cw = p.C < kSlots ? p.C : kSlots;
+        const int nct = (p.C + cw - 1) / cw;
+        if ((size_t)cw * per_ch > (size_t)lds_max)
+            return hipErrorInvalidConfiguration;
+        return bwd_med_launch<H, W, false, true>(p, st, cw, nct, (size_t)cw * per_ch, nullptr);
+    }
     int cap = lds_max > (int)slots ? (int)(((size_t)lds_max - slots) / per_ch) : 0;
     cap = cap < kSlots ? cap : kSlots;
     if (cap < 1)

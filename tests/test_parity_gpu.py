@@ -106,6 +106,11 @@ EDGE = [
     case("tiny-12x12-peaky", 1, 20, 4, 12, 12, sigma=2.0),
     case("tiny-16x16-cpg72", 1, 144, 2, 16, 16),
     case("tiny-14x14-T2B-cpg33", 1, 33, 1, 14, 14, dirs=1),
+    # one channel per group (per-channel weights): workgroups of up to eight
+    # independent channels, fewer than eight channels, direction subsets
+    case("med64-G=C", 1, 16, 16, 64, 64),
+    case("med64-G=C-3ch-dirs9", 2, 3, 3, 64, 64, dirs=9),
+    case("med56-G=C-dirs6", 2, 12, 12, 56, 56, dirs=6),
 ]
 
 
@@ -144,7 +149,7 @@ def test_deterministic_bitwise():
 
 # full-size workloads: every output computed on the GPU, sampled
 # (batch, group) units checked against the oracle
-@pytest.mark.parametrize("idx", [1, 2, 3, 4])
+@pytest.mark.parametrize("idx", [1, 2, 3, 4, 5])
 def test_full_size_sampled_units(idx):
     wl = gi.workload(idx)
     inputs = gi.make_inputs(wl)
