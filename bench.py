@@ -65,41 +65,63 @@ def to_device(a, dtype, torch):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to("cuda")
 
 
-def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool = False) -> dict:
-    """The fp64 oracle, single thread, on (batch, group) units of the workload.
+def _cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
+def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool = False,
+                 threads: int = 1) -> dict:
+    """The fp64 oracle on (batch, group) units of the workload.
 
     Units run in a fixed order until `min_seconds` have passed or the whole
     workload is done; a workload shorter than that is run again (whole passes
-    only) so the timed region reaches about `min_seconds`.
+    only) so the timed region reaches about `min_seconds`.  With threads > 1
+    the units are spread over that many threads (the oracle's C calls release
+    the interpreter lock, so they run side by side).
     """
+    import concurrent.futures as cf
+
     import oracle
     cpg = wl.C // wl.G
     order = [(b, g) for g in range(wl.G) for b in range(wl.B)]
+
+    def unit(bg):
+        b, g = bg
+        sl = oracle.slice_group(inputs, b, g, wl.G)
+        w = oracle.normalize_w(sl["w"], wl.dirs) if norm else sl["w"]
+        oracle.scan_fwd(sl["x"], w, sl["lam"], sl["u"], wl.dirs)
+        if wl.backward:
+            r = oracle.scan_bwd(sl["x"], w, sl["lam"], sl["u"], sl["dy"], wl.dirs)
+            if norm:
+                oracle.normalize_w_bwd(sl["w"], r["dw"], wl.dirs)
+
     done = 0
     passes = 0
     t0 = time.perf_counter()
-    while True:
-        for b, g in order:
-            sl = oracle.slice_group(inputs, b, g, wl.G)
-            w = oracle.normalize_w(sl["w"], wl.dirs) if norm else sl["w"]
-            oracle.scan_fwd(sl["x"], w, sl["lam"], sl["u"], wl.dirs)
-            if wl.backward:
-                r = oracle.scan_bwd(sl["x"], w, sl["lam"], sl["u"], sl["dy"], wl.dirs)
-                if norm:
-                    oracle.normalize_w_bwd(sl["w"], r["dw"], wl.dirs)
-            done += 1
-            if passes == 0 and time.perf_counter() - t0 >= min_seconds:
+    with cf.ThreadPoolExecutor(max_workers=threads) as ex:
+        while True:
+            for k in range(0, len(order), threads):
+                list(ex.map(unit, order[k:k + threads]))
+                done += len(order[k:k + threads])
+                if passes == 0 and time.perf_counter() - t0 >= min_seconds:
+                    break
+            passes += 1
+            if time.perf_counter() - t0 >= min_seconds:
                 break
-        passes += 1
-        if time.perf_counter() - t0 >= min_seconds:
-            break
     dt = time.perf_counter() - t0
     pixch = done * cpg * wl.H * wl.W
-    return {"value": round(pixch / dt / 1e9, 6), "unit": "Gpix·ch/s", "cores": 1,
+    how = "single thread" if threads == 1 else f"{threads} threads"
+    return {"value": round(pixch / dt / 1e9, 6), "unit": "Gpix·ch/s", "cores": threads,
             "kind": "oracle",
             "sample": f"{done} (batch, group) units of {wl.name} ({wl.B * wl.G} per step; "
                       f"{done * cpg} channel planes, {'fwd+bwd' if wl.backward else 'fwd'}, "
-                      f"fp64, single thread), {dt:.1f} s"}
+                      f"fp64, {how}, {_cpu_model()}), {dt:.1f} s"}
 
 
 def timed_copy(nbytes: int, reps: int, flush, torch) -> float:
@@ -249,6 +271,12 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm)
+        # the same on the host's cores (at most 16, the CPU share of one GPU)
+        nthr = min(16, os.cpu_count() or 1)
+        if nthr > 1:
+            log(f"timing the CPU oracle on {nthr} threads ...")
+            out["cpu_baseline_threads"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm,
+                                                       threads=nthr)
     return out
 
 
