@@ -1,4 +1,5 @@
-// Line scans for bf16 planes of a compile-time shape (H = W = 56 or 64), with
+// Line scans for bf16 square planes of a compile-time side (24 to 64, a
+// multiple of 8), with
 // per-direction tensors in blocked line-major layout (8-line blocks, the 8
 // values of one line position adjacent) and x, y, dx, dy pixel-major.
 //
@@ -1141,21 +1142,32 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
 
 bool med_supported(const Problem &p)
 {
-    return p.dtype == 1 && ((p.H == 64 && p.W == 64) || (p.H == 56 && p.W == 56));
+    // square planes whose side is a multiple of 8 between 24 and 64
+    return p.dtype == 1 && p.H == p.W && p.H % 8 == 0 && p.H >= 24 && p.H <= 64;
 }
 
 hipError_t launch_fwd_med(const Problem &p, hipStream_t st)
 {
-    if (p.H == 64)
-        return fwd_med_t<64, 64>(p, st);
-    return fwd_med_t<56, 56>(p, st);
+    switch (p.H) {
+    case 64: return fwd_med_t<64, 64>(p, st);
+    case 56: return fwd_med_t<56, 56>(p, st);
+    case 48: return fwd_med_t<48, 48>(p, st);
+    case 40: return fwd_med_t<40, 40>(p, st);
+    case 32: return fwd_med_t<32, 32>(p, st);
+    default: return fwd_med_t<24, 24>(p, st);
+    }
 }
 
 hipError_t launch_bwd_med(const Problem &p, hipStream_t st)
 {
-    if (p.H == 64)
-        return bwd_med_t<64, 64>(p, st);
-    return bwd_med_t<56, 56>(p, st);
+    switch (p.H) {
+    case 64: return bwd_med_t<64, 64>(p, st);
+    case 56: return bwd_med_t<56, 56>(p, st);
+    case 48: return bwd_med_t<48, 48>(p, st);
+    case 40: return bwd_med_t<40, 40>(p, st);
+    case 32: return bwd_med_t<32, 32>(p, st);
+    default: return bwd_med_t<24, 24>(p, st);
+    }
 }
 
 }  // namespace gspn

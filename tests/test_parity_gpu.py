@@ -109,6 +109,12 @@ EDGE = [
     # one channel per group (per-channel weights): workgroups of up to eight
     # independent channels, fewer than eight channels, direction subsets
     case("med64-G=C", 1, 16, 16, 64, 64),
+    # the same kernels at the other square sides they are built for
+    case("med48-all-cpg12", 2, 24, 2, 48, 48),
+    case("med40-dirs10-cpg3", 1, 6, 2, 40, 40, dirs=10),
+    case("med32-cpg32", 1, 64, 2, 32, 32),
+    case("med24-G=C-dirs5", 2, 5, 5, 24, 24, dirs=5),
+    case("med32-peaky-R2L", 1, 8, 1, 32, 32, dirs=8, sigma=2.0),
     case("med64-G=C-3ch-dirs9", 2, 3, 3, 64, 64, dirs=9),
     case("med56-G=C-dirs6", 2, 12, 12, 56, 56, dirs=6),
 ]
