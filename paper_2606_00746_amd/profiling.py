@@ -37,14 +37,37 @@ _ROOT = os.path.dirname(_HERE)
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
-def source_hash() -> str:
-    """sha256 over the kernel sources and the build flags."""
-    h = hashlib.sha256()
+# the source file of each kernel family, by a part of the kernel's name
+_FAMILY_SOURCES = (("_med_", "scan_med.hip"), ("dw_sum", "scan_med.hip"),
+                   ("_wide_", "scan_wide.hip"), ("_tiny_", "scan_tiny.hip"),
+                   ("_small_", "scan_small.hip"), ("_general_", "scan_general.hip"),
+                   ("norm", "scan_norm.hip"))
+# shared by every family: device helpers, launch declarations, the dispatch
+# and the build flags
+_COMMON_SOURCES = ("cdna.hpp", "device.hpp", "launch.hpp", "api.cpp")
+
+
+def source_files(kernels=None) -> list:
+    """The sources that decide what the named kernels do (all of them if None
+    or if a name belongs to no known family)."""
     csrc = os.path.join(_HERE, "csrc")
-    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
-                   if f.endswith((".hip", ".hpp", ".cpp")))
-    files.append(os.path.join(_HERE, "build.py"))
-    for f in files:
+    every = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".hpp", ".cpp")))
+    names = set(_COMMON_SOURCES)
+    for k in kernels or ():
+        hit = [f for part, f in _FAMILY_SOURCES if part in k]
+        if not hit:
+            return [os.path.join(csrc, f) for f in every] + [os.path.join(_HERE, "build.py")]
+        names.update(hit)
+    if not kernels:
+        names = set(every)
+    return [os.path.join(csrc, f) for f in sorted(names)] + [os.path.join(_HERE, "build.py")]
+
+
+def source_hash(kernels=None) -> str:
+    """sha256 over the sources of the named kernels (all sources if None) and
+    the build flags."""
+    h = hashlib.sha256()
+    for f in source_files(kernels):
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:
             h.update(fh.read())
@@ -117,7 +140,9 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
         kernels[short_name(k)] = {"call": call, "fetch_bytes": round(fb), "write_bytes": round(wb),
                                   "dispatches": len(v)}
         calls[call] += fb + wb
-    return {"workload": workload, "source_hash": source_hash(), "command": command,
+    return {"workload": workload, "source_hash": source_hash(sorted(kernels)),
+            "source_files": [os.path.basename(f) for f in source_files(sorted(kernels))],
+            "command": command,
             "copy_calibration": {"bytes": copy_bytes, "fetch_kib": f_copy / 1024.0,
                                  "write_kib": w_copy / 1024.0, "fetch_scale": scale_f,
                                  "write_scale": scale_w},
@@ -171,7 +196,7 @@ def load_traffic(path: str, call: str) -> float | None:
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if rec.get("source_hash") != source_hash():
+    if rec.get("source_hash") != source_hash(sorted(rec.get("kernels", {}))):
         return None
     return rec.get("bytes_per_call", {}).get(call)
 

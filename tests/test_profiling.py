@@ -35,11 +35,16 @@ def test_traffic_record_scales_by_copy(tmp_path):
     assert rec["kernels"]["fwd_med_kernel<64, 64>"]["fetch_bytes"] == 200 * 1024
     assert rec["bytes_per_call"]["fwd"] == (200 + 10) * 1024
     assert rec["bytes_per_call"]["bwd"] == (600 + 200 + 100 + 5) * 1024
-    assert rec["source_hash"] == profiling.source_hash()
+    assert rec["source_hash"] == profiling.source_hash(sorted(rec["kernels"]))
+    # the record depends on its kernels' family and the shared sources only
+    assert "scan_med.hip" in rec["source_files"] and "api.cpp" in rec["source_files"]
+    assert "scan_wide.hip" not in rec["source_files"]
 
 
 def test_traffic_ignored_for_other_sources(tmp_path):
-    rec = {"source_hash": profiling.source_hash(), "bytes_per_call": {"bwd": 123}}
+    kern = {"bwd_med_kernel<64, 64, false, false>": {}}
+    rec = {"source_hash": profiling.source_hash(sorted(kern)), "kernels": kern,
+           "bytes_per_call": {"bwd": 123}}
     p = tmp_path / "t.txt"
     p.write_text(json.dumps(rec))
     assert profiling.load_traffic(str(p), "bwd") == 123
