@@ -26,6 +26,7 @@ DIR_BITS = (T2B, B2T, L2R, R2L)
 
 # tensor ids of the counter-based streams
 _TID_X, _TID_LOGIT, _TID_LAM, _TID_U, _TID_DY, _TID_RAW_LOGIT = 0, 1, 2, 3, 4, 5
+_TID_LATENT = 6   # slots: 0 x, 1 P_down, 2 L_u, 3 L_lambda, 4 L_w, 5 P_up
 
 
 @dataclass(frozen=True)
@@ -258,3 +259,55 @@ PER_DIRECTION = ("lam", "u", "w", "dlam", "du", "dw")
 def inputs_line_major(inputs: dict, dirs: int) -> dict:
     """Copy of a pixel-major input dict with the per-direction tensors line-major."""
     return {k: (to_line_major(v, dirs) if k in PER_DIRECTION else v) for k, v in inputs.items()}
+
+
+@dataclass(frozen=True)
+class LatentWorkload:
+    """A latent-space propagation sublayer (C-GSPN, Sec. 5): feature map
+    [B, C, H, W] projected to Cc latent channels, scanned, projected back."""
+    name: str
+    B: int
+    C: int
+    Cc: int
+    H: int
+    W: int
+    dirs: int
+    seed: int
+
+    @property
+    def ndirs(self) -> int:
+        return bin(self.dirs & 15).count("1")
+
+    def with_(self, **kw) -> "LatentWorkload":
+        return replace(self, **kw)
+
+
+# Token grids of a ViT with 14-pixel patches at 518 and 1022 pixels, width
+# 1152 compressed to 64 latent channels, batch 32.
+LATENT_WORKLOADS = (
+    LatentWorkload("cgspn-37x37-b32-c1152-cc64", 32, 1152, 64, 37, 37, ALL_DIRS, 21),
+    LatentWorkload("cgspn-73x73-b32-c1152-cc64", 32, 1152, 64, 73, 73, ALL_DIRS, 22),
+)
+
+
+def latent_workload(name_or_index) -> LatentWorkload:
+    if isinstance(name_or_index, int):
+        return LATENT_WORKLOADS[name_or_index]
+    for w in LATENT_WORKLOADS:
+        if w.name == name_or_index:
+            return w
+    raise KeyError(name_or_index)
+
+
+def make_latent_inputs(lw: LatentWorkload) -> dict:
+    """bf16-representable float32 inputs of the sublayer: x ~ N(0, 1); every
+    projection ~ N(0, 1/fan_in) (P_down: 1/C, the others 1/Cc), so that the
+    latent map, u, lambda and the tap logits are of unit scale."""
+    B, C, Cc, H, W, D = lw.B, lw.C, lw.Cc, lw.H, lw.W, lw.ndirs
+    g = lambda shape, slot, sig: _normal(shape, lw.seed, _TID_LATENT, slot, 0.0, sig, 0, True)
+    return {"x": g((B, C, H, W), 0, 1.0),
+            "p_down": g((Cc, C), 1, C ** -0.5),
+            "l_u": g((D, Cc, Cc), 2, Cc ** -0.5),
+            "l_lam": g((D, Cc, Cc), 3, Cc ** -0.5),
+            "l_w": g((D, Cc, 3, Cc), 4, Cc ** -0.5),
+            "p_up": g((C, Cc), 5, Cc ** -0.5)}

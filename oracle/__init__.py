@@ -140,3 +140,63 @@ def slice_group(inputs: dict, b: int, g: int, G: int) -> dict:
     if "dy" in inputs:
         out["dy"] = inputs["dy"][b:b + 1, cs]
     return out
+
+
+# ---------------------------------------------------------------------------
+# Latent-space propagation sublayer (Sec. 5, Eqs. (latent_down),
+# (latent_params), (latent_recurrence), (latent_up)).
+#
+# Readings: the per-pixel projections are linear maps without bias and u,
+# lambda take no activation (the paper names neither); every direction of the
+# mask has its own L_u, L_lambda, L_w; w is normalized from its logits as in
+# Eq. (row_stochastic_norm); the scan runs with one weight group per latent
+# channel.  With ``storage="bf16"`` the stage results that a bf16
+# implementation keeps in memory (x_c, u, lambda, w, y_c) are rounded to
+# bf16 between the stages and the logits are not; the arithmetic itself is
+# float64 throughout.
+# ---------------------------------------------------------------------------
+
+def round_bf16(a) -> np.ndarray:
+    """Nearest bfloat16 value (8 significant bits, ties to even), as float64."""
+    a = _f64(a)
+    m, e = np.frexp(a)                       # a = m * 2**e, 0.5 <= |m| < 1
+    return np.ldexp(np.round(np.ldexp(m, 8)), e - 8)
+
+
+def project(a, x) -> np.ndarray:
+    """Per-pixel projection (1x1 convolution) y[b] = a @ x[b]: a [M, K],
+    x [B, K, H, W] -> [B, M, H, W], float64."""
+    a, x = _f64(a), _f64(x)
+    B, K, H, W = x.shape
+    if a.ndim != 2 or a.shape[1] != K:
+        raise ValueError("a must be [M, K] with K = x.shape[1]")
+    return np.matmul(a, x.reshape(B, K, H * W)).reshape(B, a.shape[0], H, W)
+
+
+def latent_params(xc, l_u, l_lam, l_w, dirs: int, storage: str = "f64") -> dict:
+    """u, lambda [D, B, Cc, H, W] and normalized w [D, B, Cc, 3, H, W] from the
+    latent map xc [B, Cc, H, W] (Eq. (latent_params), then
+    Eq. (row_stochastic_norm) on the tap logits)."""
+    xc = _f64(xc)
+    D = _ndirs(dirs)
+    B, Cc, H, W = xc.shape
+    l_u, l_lam, l_w = _f64(l_u), _f64(l_lam), _f64(l_w)
+    if l_u.shape != (D, Cc, Cc) or l_lam.shape != (D, Cc, Cc) or l_w.shape != (D, Cc, 3, Cc):
+        raise ValueError("l_u, l_lam must be [D, Cc, Cc] and l_w [D, Cc, 3, Cc]")
+    u = np.stack([project(l_u[s], xc) for s in range(D)])
+    lam = np.stack([project(l_lam[s], xc) for s in range(D)])
+    wt = np.stack([project(l_w[s].reshape(3 * Cc, Cc), xc).reshape(B, Cc, 3, H, W)
+                   for s in range(D)])
+    w = normalize_w(wt, dirs)
+    if storage == "bf16":
+        u, lam, w = round_bf16(u), round_bf16(lam), round_bf16(w)
+    return {"u": u, "lam": lam, "w": w, "wt": wt}
+
+
+def latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, dirs: int, storage: str = "f64") -> np.ndarray:
+    """The sublayer y = P_up(Prop_2D(P_down x)), float64 [B, C, H, W]."""
+    rnd = round_bf16 if storage == "bf16" else (lambda a: a)
+    xc = rnd(project(p_down, x))
+    prm = latent_params(xc, l_u, l_lam, l_w, dirs, storage)
+    yc = rnd(scan_fwd(xc, prm["w"], prm["lam"], prm["u"], dirs))
+    return project(p_up, yc)
