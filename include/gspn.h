@@ -155,6 +155,53 @@ int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
                        void *dlam, void *du, int direction, int B, int C, int G,
                        int H, int W, int dtype, void *stream);
 
+/*
+ * Latent-space propagation sublayer of C-GSPN (Sec. 5, Eqs. (latent_down),
+ * (latent_params), (latent_recurrence), (latent_up)): the feature map is
+ * projected per pixel from C to Cc channels, the propagation parameters are
+ * predicted per pixel from the latent map, the four-direction scan runs on
+ * the Cc latent channels with one weight group per channel (G = Cc), and the
+ * result is projected back to C channels:
+ *   x_c   = P_down x                        [B][Cc][H][W]
+ *   u_d   = L_u,d x_c,  lam_d = L_lam,d x_c  (per direction d of the mask)
+ *   wt_d  = L_w,d x_c   (three tap logits per latent channel and pixel)
+ *   w_d   = row-stochastic weights from wt_d (as in gspn_scan_fwd_norm)
+ *   y_c   = scan(x_c, w, lam, u)             (gspn_scan_fwd, G = Cc)
+ *   y     = P_up y_c                         [B][C][H][W]
+ * The paper fixes neither biases nor activations on u and lambda: the
+ * projections here are linear without bias.  Storage is bf16 only
+ * (dtype GSPN_BF16; GSPN_F32 is GSPN_ERR_UNSUPPORTED); products accumulate in
+ * fp32 on the matrix cores.  x_c, u, lam, w and y_c are stored in bf16
+ * between the stages (stream-ordered scratch memory, released on the same
+ * stream); the logits wt are normalized in registers and never stored.
+ * Weight layouts (row-major, output channel first):
+ *   p_down [Cc][C]      l_u, l_lam [D][Cc][Cc]      l_w [D][Cc][3][Cc]
+ *   p_up   [C][Cc]      (row (c, k) of l_w gives the logit of tap k of
+ *                        latent channel c)
+ * C and Cc must be multiples of 8 (GSPN_ERR_UNSUPPORTED otherwise).  Other
+ * arguments, checks and errors as in gspn_scan_fwd.
+ */
+int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
+                    const void *l_lam, const void *l_w, const void *p_up, void *y,
+                    int direction, int B, int C, int Cc, int H, int W, int dtype,
+                    void *stream);
+/*
+ * The two kinds of stage of gspn_latent_fwd, for callers that keep the
+ * latent tensors themselves.
+ * gspn_project: the per-pixel projection (1x1 convolution) of Eqs.
+ * (latent_down) and (latent_up), y[b] = a x[b]:
+ *   a [M][K], x [B][K][H][W], y [B][M][H][W]; K a multiple of 8; bf16.
+ * gspn_latent_params: Eq. (latent_params) with the weights normalized as in
+ * Eq. (row_stochastic_norm), written in the scan's layouts (G = Cc):
+ *   xc [B][Cc][H][W] in; u, lam [D][B][Cc][plane], w [D][B][Cc][3][plane] out;
+ *   Cc a multiple of 8; bf16.
+ */
+int gspn_project(const void *a, const void *x, void *y, int B, int M, int K,
+                 int H, int W, int dtype, void *stream);
+int gspn_latent_params(const void *xc, const void *l_u, const void *l_lam,
+                       const void *l_w, void *u, void *lam, void *w,
+                       int direction, int B, int Cc, int H, int W, int dtype,
+                       void *stream);
 /* Static description of a status code (never NULL). */
 const char *gspn_strerror(int status);
 

@@ -6,11 +6,14 @@ scan directions, forward and backward, as hand-written HIP kernels for gfx950
 behind a C ABI (``include/gspn.h``).  This package is the ctypes binding.
 """
 from ._native import (ALL, B2T, BF16, F32, L2R, LIB_PATH, R2L, T2B, GspnError, gspn_last_hip_error,
-                      gspn_scan_bwd, gspn_scan_bwd_norm, gspn_scan_fwd, gspn_scan_fwd_norm,
-                      gspn_strerror, gspn_version, load, scan_bwd, scan_bwd_norm, scan_fwd,
-                      scan_fwd_norm, to_line_major, from_line_major)
+                      gspn_latent_fwd, gspn_latent_params, gspn_project, gspn_scan_bwd,
+                      gspn_scan_bwd_norm, gspn_scan_fwd, gspn_scan_fwd_norm, gspn_strerror,
+                      gspn_version, latent_fwd, latent_params, load, project, scan_bwd,
+                      scan_bwd_norm, scan_fwd, scan_fwd_norm, to_line_major, from_line_major)
 
 __all__ = ["ALL", "B2T", "BF16", "F32", "L2R", "LIB_PATH", "R2L", "T2B", "GspnError",
-           "gspn_last_hip_error", "gspn_scan_bwd", "gspn_scan_bwd_norm", "gspn_scan_fwd",
-           "gspn_scan_fwd_norm", "gspn_strerror", "gspn_version", "load", "scan_bwd",
-           "scan_bwd_norm", "scan_fwd", "scan_fwd_norm", "to_line_major", "from_line_major"]
+           "gspn_last_hip_error", "gspn_latent_fwd", "gspn_latent_params", "gspn_project",
+           "gspn_scan_bwd", "gspn_scan_bwd_norm", "gspn_scan_fwd", "gspn_scan_fwd_norm",
+           "gspn_strerror", "gspn_version", "latent_fwd", "latent_params", "load", "project",
+           "scan_bwd", "scan_bwd_norm", "scan_fwd", "scan_fwd_norm", "to_line_major",
+           "from_line_major"]

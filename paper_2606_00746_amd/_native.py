@@ -21,6 +21,7 @@ OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUP
 MAX_SIDE = 4096
 
 EXPORTED = ("gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
+            "gspn_project", "gspn_latent_params", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
 
 _lib = None
@@ -55,6 +56,12 @@ def load() -> ctypes.CDLL:
         lib.gspn_scan_bwd_norm.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i,
                                            vp]
         lib.gspn_scan_bwd_norm.restype = i
+        lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
+        lib.gspn_project.restype = i
+        lib.gspn_latent_params.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp]
+        lib.gspn_latent_params.restype = i
+        lib.gspn_latent_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
+        lib.gspn_latent_fwd.restype = i
         lib.gspn_strerror.argtypes = [i]
         lib.gspn_strerror.restype = ctypes.c_char_p
         lib.gspn_last_hip_error.argtypes = []
@@ -88,6 +95,22 @@ def gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, directi
                        W, dtype, stream) -> int:
     return load().gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction,
                                      B, C, G, H, W, dtype, stream)
+
+
+def gspn_project(a, x, y, B, M, K, H, W, dtype, stream) -> int:
+    return load().gspn_project(a, x, y, B, M, K, H, W, dtype, stream)
+
+
+def gspn_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W, dtype,
+                       stream) -> int:
+    return load().gspn_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W,
+                                     dtype, stream)
+
+
+def gspn_latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H, W, dtype,
+                    stream) -> int:
+    return load().gspn_latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H,
+                                  W, dtype, stream)
 
 
 def gspn_strerror(status: int) -> str:
@@ -204,6 +227,66 @@ def scan_bwd_norm(x, w_logits, lam, u, dy, direction: int = ALL, out=None, strea
                                 C, G, H, W, _dtype_code(x), _stream_handle(x, stream))
     _check_raise(status)
     return dx, dwl, dlam, du
+
+
+def project(a, x, y=None, stream=None):
+    """1x1 convolution y[b] = a @ x[b]: a [M, K], x [B, K, H, W] -> y [B, M, H, W] (bf16)."""
+    import torch
+    if a.dim() != 2 or x.dim() != 4 or a.shape[1] != x.shape[1]:
+        raise ValueError("a must be [M, K] and x [B, K, H, W]")
+    M, K = a.shape
+    B, _, H, W = x.shape
+    if y is None:
+        y = torch.empty((B, M, H, W), dtype=x.dtype, device=x.device)
+    status = gspn_project(*_ptrs(a, x, y), B, M, K, H, W, _dtype_code(x),
+                          _stream_handle(x, stream))
+    _check_raise(status)
+    return y
+
+
+def _latent_weights(l_u, l_lam, l_w, direction):
+    D = bin(direction & 15).count("1")
+    Cc = l_u.shape[-1]
+    if (tuple(l_u.shape) != (D, Cc, Cc) or tuple(l_lam.shape) != (D, Cc, Cc)
+            or tuple(l_w.shape) != (D, Cc, 3, Cc)):
+        raise ValueError("l_u, l_lam must be [D, Cc, Cc] and l_w [D, Cc, 3, Cc]")
+    return D, Cc
+
+
+def latent_params(xc, l_u, l_lam, l_w, direction: int = ALL, out=None, stream=None):
+    """u, lam and normalized w of every direction from the latent map xc [B, Cc, H, W]
+    (Sec. 5, Eq. (latent_params); Sec. 3, Eq. (row_stochastic_norm)), in the
+    scan's blocked line-major layout: u, lam [D, B, Cc, H*W], w [D, B, Cc, 3, H*W]."""
+    import torch
+    D, Cc = _latent_weights(l_u, l_lam, l_w, direction)
+    B, _, H, W = xc.shape
+    if out is None:
+        kw = dict(dtype=xc.dtype, device=xc.device)
+        out = (torch.empty((D, B, Cc, H * W), **kw), torch.empty((D, B, Cc, H * W), **kw),
+               torch.empty((D, B, Cc, 3, H * W), **kw))
+    u, lam, w = out
+    status = gspn_latent_params(*_ptrs(xc, l_u, l_lam, l_w, u, lam, w), direction, B, Cc, H, W,
+                                _dtype_code(xc), _stream_handle(xc, stream))
+    _check_raise(status)
+    return u, lam, w
+
+
+def latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, direction: int = ALL, y=None, stream=None):
+    """The latent-space propagation sublayer (Sec. 5): y = P_up(Prop_2D(P_down x))
+    with the propagation parameters predicted from the latent map.
+    x [B, C, H, W], p_down [Cc, C], l_u, l_lam [D, Cc, Cc], l_w [D, Cc, 3, Cc],
+    p_up [C, Cc] -> y [B, C, H, W] (bf16)."""
+    import torch
+    D, Cc = _latent_weights(l_u, l_lam, l_w, direction)
+    B, C, H, W = x.shape
+    if tuple(p_down.shape) != (Cc, C) or tuple(p_up.shape) != (C, Cc):
+        raise ValueError("p_down must be [Cc, C] and p_up [C, Cc]")
+    if y is None:
+        y = torch.empty_like(x)
+    status = gspn_latent_fwd(*_ptrs(x, p_down, l_u, l_lam, l_w, p_up, y), direction, B, C, Cc, H,
+                             W, _dtype_code(x), _stream_handle(x, stream))
+    _check_raise(status)
+    return y
 
 
 LINE_BLOCK = 8   # lines per block of the line-major layout

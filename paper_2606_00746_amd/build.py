@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgspn.so")
 SOURCES = ["api.cpp", "scan_tiny.hip", "scan_small.hip", "scan_med.hip", "scan_wide.hip",
-           "scan_norm.hip", "scan_general.hip"]
+           "scan_norm.hip", "scan_general.hip", "latent.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -221,6 +221,127 @@ extern "C" int gspn_scan_bwd_norm(const void *x, const void *w_logits, const voi
     return hip_status(e != hipSuccess ? e : e2);
 }
 
+namespace gspn {
+namespace {
+
+// Sizes of a 1x1 convolution out[b] = A x[b] with A M x K and x[b] K x HW.
+int check_project(int B, int M, int K, int H, int W, int dtype)
+{
+    if (dtype != GSPN_F32 && dtype != GSPN_BF16)
+        return GSPN_ERR_DTYPE;
+    if (B < 1 || M < 1 || K < 1 || H < 1 || W < 1)
+        return GSPN_ERR_DIM;
+    if (dtype != GSPN_BF16 || K % 8 != 0 || H > GSPN_MAX_SIDE || W > GSPN_MAX_SIDE)
+        return GSPN_ERR_UNSUPPORTED;
+    const int64_t HW = (int64_t)H * W;
+    if ((int64_t)B * M > GSPN_MAX_ELEMS / HW || (int64_t)B * K > GSPN_MAX_ELEMS / HW)
+        return GSPN_ERR_UNSUPPORTED;
+    // one workgroup per 64 output rows x 128 pixels of one image
+    if ((int64_t)B * ((HW + 127) / 128) * ((M + 63) / 64) > 0x7fffffff)
+        return GSPN_ERR_UNSUPPORTED;
+    return GSPN_OK;
+}
+
+// Sizes of the latent parameter product: Cc latent channels, 6 D Cc rows.
+int check_latent(int direction, int B, int Cc, int H, int W, int dtype)
+{
+    int st = check_common(direction, B, Cc, Cc, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    if (Cc % 8 != 0)
+        return GSPN_ERR_UNSUPPORTED;
+    return check_project(B, 6 * __builtin_popcount(direction) * Cc, Cc, H, W, dtype);
+}
+
+constexpr int64_t round8(int64_t n) { return (n + 7) / 8 * 8; }
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_project(const void *a, const void *x, void *y, int B, int M, int K, int H,
+                            int W, int dtype, void *stream)
+{
+    int st = check_project(B, M, K, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t HW = (int64_t)H * W;
+    const Buf bufs[] = {{a, (int64_t)M * K * 2, false},
+                        {x, (int64_t)B * K * HW * 2, false},
+                        {y, (int64_t)B * M * HW * 2, true}};
+    st = check_buffers(bufs, 3);
+    if (st != GSPN_OK)
+        return st;
+    return hip_status(launch_project(a, x, y, B, M, K, H, W, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int gspn_latent_params(const void *xc, const void *l_u, const void *l_lam,
+                                  const void *l_w, void *u, void *lam, void *w, int direction,
+                                  int B, int Cc, int H, int W, int dtype, void *stream)
+{
+    int st = check_latent(direction, B, Cc, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t n = (int64_t)B * Cc * H * W;
+    const int64_t cc2 = (int64_t)Cc * Cc;
+    const Buf bufs[] = {{xc, n * 2, false},          {l_u, D * cc2 * 2, false},
+                        {l_lam, D * cc2 * 2, false}, {l_w, 3 * D * cc2 * 2, false},
+                        {u, D * n * 2, true},        {lam, D * n * 2, true},
+                        {w, 3 * D * n * 2, true}};
+    st = check_buffers(bufs, 7);
+    if (st != GSPN_OK)
+        return st;
+    return hip_status(launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
+                               const void *l_lam, const void *l_w, const void *p_up, void *y,
+                               int direction, int B, int C, int Cc, int H, int W, int dtype,
+                               void *stream)
+{
+    int st = check_latent(direction, B, Cc, H, W, dtype);
+    if (st == GSPN_OK)
+        st = check_project(B, C, Cc, H, W, dtype);
+    if (st == GSPN_OK)
+        st = check_project(B, Cc, C, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const int64_t D = __builtin_popcount(direction);
+    const int64_t HW = (int64_t)H * W;
+    const int64_t n = (int64_t)B * C * HW, nc = (int64_t)B * Cc * HW;
+    const int64_t cc2 = (int64_t)Cc * Cc;
+    const Buf bufs[] = {{x, n * 2, false},           {p_down, (int64_t)Cc * C * 2, false},
+                        {l_u, D * cc2 * 2, false},   {l_lam, D * cc2 * 2, false},
+                        {l_w, 3 * D * cc2 * 2, false}, {p_up, (int64_t)C * Cc * 2, false},
+                        {y, n * 2, true}};
+    st = check_buffers(bufs, 7);
+    if (st != GSPN_OK)
+        return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // latent x_c, u, lambda, w and y_c in one scratch block, 16-byte aligned parts
+    const int64_t o_u = round8(nc), o_l = o_u + round8(D * nc), o_w = o_l + round8(D * nc);
+    const int64_t o_y = o_w + round8(3 * D * nc), total = o_y + round8(nc);
+    void *scr = nullptr;
+    hipError_t e = scratch_alloc(&scr, (size_t)(total * 2), s);
+    if (e != hipSuccess)
+        return hip_status(e);
+    uint16_t *base = static_cast<uint16_t *>(scr);
+    uint16_t *xc = base, *u = base + o_u, *lam = base + o_l, *w = base + o_w, *yc = base + o_y;
+    e = launch_project(p_down, x, xc, B, Cc, C, H, W, s);
+    if (e == hipSuccess)
+        e = launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W, s);
+    if (e == hipSuccess) {
+        Problem p{xc, w, lam, u, nullptr, yc, nullptr, nullptr, nullptr, nullptr,
+                  direction, B, Cc, Cc, H, W, GSPN_BF16};
+        e = dispatch_fwd(p, s);
+    }
+    if (e == hipSuccess)
+        e = launch_project(p_up, yc, y, B, C, Cc, H, W, s);
+    const hipError_t e2 = scratch_free(scr, s);
+    return hip_status(e != hipSuccess ? e : e2);
+}
+
 extern "C" const char *gspn_strerror(int status)
 {
     switch (status) {

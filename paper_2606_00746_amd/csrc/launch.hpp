@@ -32,6 +32,16 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_general(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_general(const Problem &p, hipStream_t s);
 
+// 1x1 convolutions of the latent sublayer (bf16, fp32 accumulation):
+// y[b] = a x[b] with a [M][K], x [B][K][H*W], y [B][M][H*W]; and the
+// parameter product that writes u, lambda and normalized w of every
+// direction in the scan's blocked layout from x_c [B][Cc][H*W].
+hipError_t launch_project(const void *a, const void *x, void *y, int B, int M, int K, int H, int W,
+                          hipStream_t s);
+hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, const void *lw,
+                                void *u, void *lam, void *w, int mask, int B, int Cc, int H, int W,
+                                hipStream_t s);
+
 // Stream-ordered scratch from the device's default pool.
 hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s);
 hipError_t scratch_free(void *ptr, hipStream_t s);

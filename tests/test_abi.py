@@ -130,3 +130,54 @@ def test_torch_layout_helpers_match_numpy(H, W):
         lm = g.to_line_major(t, dirs)
         np.testing.assert_array_equal(lm.numpy(), gi.to_line_major(a[:d], dirs))
         np.testing.assert_array_equal(g.from_line_major(lm, dirs, H, W).numpy(), a[:d])
+
+
+def project(**kw):
+    a = dict(a=P(0), x=P(1), y=P(2), B=1, M=64, K=64, H=8, W=8, dtype=g.BF16, stream=None)
+    a.update(kw)
+    return g.gspn_project(a["a"], a["x"], a["y"], a["B"], a["M"], a["K"], a["H"], a["W"],
+                          a["dtype"], a["stream"])
+
+
+def latent_params(**kw):
+    a = dict(xc=P(0), l_u=P(1), l_lam=P(2), l_w=P(3), u=P(4), lam=P(5), w=P(6), direction=15,
+             B=1, Cc=16, H=8, W=8, dtype=g.BF16, stream=None)
+    a.update(kw)
+    return g.gspn_latent_params(a["xc"], a["l_u"], a["l_lam"], a["l_w"], a["u"], a["lam"],
+                                a["w"], a["direction"], a["B"], a["Cc"], a["H"], a["W"],
+                                a["dtype"], a["stream"])
+
+
+def latent_fwd(**kw):
+    a = dict(x=P(0), p_down=P(1), l_u=P(2), l_lam=P(3), l_w=P(4), p_up=P(5), y=P(6),
+             direction=15, B=1, C=32, Cc=16, H=8, W=8, dtype=g.BF16, stream=None)
+    a.update(kw)
+    return g.gspn_latent_fwd(a["x"], a["p_down"], a["l_u"], a["l_lam"], a["l_w"], a["p_up"],
+                             a["y"], a["direction"], a["B"], a["C"], a["Cc"], a["H"], a["W"],
+                             a["dtype"], a["stream"])
+
+
+@pytest.mark.parametrize("call,ptrs,dims", [
+    (project, ["a", "x", "y"], ["B", "M", "K", "H", "W"]),
+    (latent_params, ["xc", "l_u", "l_lam", "l_w", "u", "lam", "w"], ["B", "Cc", "H", "W"]),
+    (latent_fwd, ["x", "p_down", "l_u", "l_lam", "l_w", "p_up", "y"], ["B", "C", "Cc", "H", "W"]),
+])
+def test_latent_invalid_arguments(call, ptrs, dims):
+    for name in ptrs:
+        assert call(**{name: None}) == _native.ERR_NULL, name
+        assert call(**{name: P(ptrs.index(name), 8)}) == _native.ERR_ALIGN, name
+    for dim in dims:
+        assert call(**{dim: 0}) == _native.ERR_DIM, dim
+    assert call(dtype=7) == _native.ERR_DTYPE
+    assert call(dtype=g.F32) == _native.ERR_UNSUPPORTED     # bf16 only
+    assert call(H=4097) == _native.ERR_UNSUPPORTED
+    if call is not project:
+        for bad in (0, 16):
+            assert call(direction=bad) == _native.ERR_DIRECTION
+        assert call(Cc=12) == _native.ERR_UNSUPPORTED       # latent channels: multiple of 8
+    else:
+        assert call(K=12) == _native.ERR_UNSUPPORTED        # K: multiple of 8
+    if call is latent_fwd:
+        assert call(C=36) == _native.ERR_UNSUPPORTED
+    # an output over an input
+    assert call(**{ptrs[-1]: P(0)}) == _native.ERR_ALIAS
