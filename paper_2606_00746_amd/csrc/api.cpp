@@ -236,6 +236,9 @@ int check_project(int B, int M, int K, int H, int W, int dtype)
     const int64_t HW = (int64_t)H * W;
     if ((int64_t)B * M > GSPN_MAX_ELEMS / HW || (int64_t)B * K > GSPN_MAX_ELEMS / HW)
         return GSPN_ERR_UNSUPPORTED;
+    // one image's input and output maps are addressed with 32-bit byte offsets
+    if ((int64_t)M * HW * 2 >= ((int64_t)1 << 31) || (int64_t)K * HW * 2 >= ((int64_t)1 << 31))
+        return GSPN_ERR_UNSUPPORTED;
     // one workgroup per 64 output rows x 128 pixels of one image
     if ((int64_t)B * ((HW + 127) / 128) * ((M + 63) / 64) > 0x7fffffff)
         return GSPN_ERR_UNSUPPORTED;

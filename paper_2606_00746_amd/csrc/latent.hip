@@ -4,23 +4,26 @@
 // weight matrix and x[b] a K x HW channel-major feature map, both bf16;
 // products accumulate in fp32 and the result is rounded to bf16 once.
 //
-// Workgroup: 4 waves and an output tile of 64 rows x 128 pixels.  Wave v
-// owns pixels 32v .. 32v+31 of the tile and both 32-row halves, as two
-// v_mfma_f32_32x32x16_bf16 accumulators (16 fp32 registers each).  K runs
-// in stages of 64: a stage's 64 x 128 block of x and 64 x 64 block of A go to
-// LDS, and each wave then takes 4 steps of 16 along K.  Operand layout of the
-// instruction: lane l holds row (or column) l % 32 and the 8 consecutive
-// K-values from 8 (l / 32); the result's register r of lane l is row
-// 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
+// Operand layout of v_mfma_f32_32x32x16_bf16: lane l holds row (or column)
+// l % 32 and the 8 consecutive K-values from 8 (l / 32); the result's
+// register r of lane l is row 8 (r / 4) + 4 (l / 32) + r % 4, column l % 32.
 //
-// The x block is kept as [k][pixel]; a B fragment takes 8 rows of one pixel
-// column.  Lanes 32..63 read the 8 rows after those of lanes 0..31, which
-// with a 256-byte row pitch would fall in the same LDS banks; rows whose
-// bit 3 is set therefore keep their two 64-byte halves swapped.
+// A workgroup (4 waves) owns a tile of 128 pixels of one image; its block of
+// x (64 K-rows x 128 pixels) is staged in LDS as [k][pixel].  A B fragment
+// takes 8 rows of one pixel column; lanes 32..63 read the 8 rows after those
+// of lanes 0..31, which with a 256-byte row pitch would fall in the same LDS
+// banks, so rows whose bit 3 is set keep their two 64-byte halves swapped.
+// Two kernels:
+//  * proj_rows_kernel, K <= 64 (P_up, the parameter product): x is staged
+//    once, every wave keeps the B fragments of all 128 pixels in registers
+//    and the waves take the 32-row tiles of A in turn, 4 accumulators each;
+//  * proj_stage_kernel, K > 64 (P_down): a workgroup owns 64 rows x 128
+//    pixels, wave v pixels 32v .. 32v+31 of both 32-row halves; K runs in
+//    stages of 64 staged in LDS, the next stage's loads in flight while the
+//    current one is multiplied.
 //
 // Tiles and outputs:
-//  * plain product (P_down, P_up): 128 consecutive pixels; the tile goes
-//    through LDS once more so that every store writes 128 contiguous bytes;
+//  * plain product (P_down, P_up): 128 consecutive pixels;
 //  * the parameter product (L_u, L_lambda, L_w of all directions stacked):
 //    8 image rows x 16 columns, so that the stores of one tile fill whole
 //    8-line runs of the scan's blocked line-major planes.  Its rows are
@@ -109,8 +112,233 @@ __device__ __forceinline__ int plane_offset(int d, int row, int col, int H, int 
     return d < 2 ? lm_offset(row, col, H, W) : lm_offset(col, row, W, H);
 }
 
+// Stores of the parameter product for result rows m .. m+3 (m a multiple of
+// 4) at pixel (row, col) of image b.
+__device__ __forceinline__ void store_params(const ProjArgs &A, int b, int m, int row, int col,
+                                             float v0, float v1, float v2, float v3)
+{
+    const int64_t HW = A.HW;
+    if (m < 2 * A.DCc) {
+        // four channels c .. c+3 of one direction: u, or lambda
+        const bool is_u = m < A.DCc;
+        const int q = is_u ? m : m - A.DCc;
+        const int s = mdiv(q, A.div_cc), c = q - s * A.Cc;
+        bf16_t *dst = (is_u ? A.u : A.lam) + ((int64_t)s * A.B + b) * A.Cc * HW +
+                      (int64_t)c * HW + plane_offset(A.dirs[s], row, col, A.H, A.W);
+        dst[0] = bf16_bits(v0);
+        dst[HW] = bf16_bits(v1);
+        dst[2 * HW] = bf16_bits(v2);
+        dst[3 * HW] = bf16_bits(v3);
+    } else if (m < A.M) {
+        // the three tap logits of channel c, direction slot s
+        const int dc = (m - 2 * A.DCc) >> 2;
+        const int s = mdiv(dc, A.div_cc), c = dc - s * A.Cc;
+        const int d = A.dirs[s];
+        const int p = d < 2 ? col : row, P = d < 2 ? A.W : A.H;
+        const float s0 = p > 0 ? sigmoid(v0) : 0.f;
+        const float s1 = sigmoid(v1);
+        const float s2 = p < P - 1 ? sigmoid(v2) : 0.f;
+        const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+        bf16_t *dst = A.w + (((int64_t)s * A.B + b) * A.Cc + c) * 3 * HW +
+                      plane_offset(d, row, col, A.H, A.W);
+        dst[0] = bf16_bits(s0 * inv);
+        dst[HW] = bf16_bits(s1 * inv);
+        dst[2 * HW] = bf16_bits(s2 * inv);
+    }
+}
+
+// The 64 x 128 block of x from K-row kc on: rows kc + 2 i + (t / 128), this
+// thread's pixel column; 0 past K and off the image.
+__device__ __forceinline__ void load_x_block(rsrc_t xr, int K, int HW, int kc, int ks0, int spix,
+                                             uint32_t (&xv)[kKS / 2])
+{
+#pragma unroll
+    for (int i = 0; i < kKS / 2; ++i) {
+        const int k = kc + 2 * i + ks0;
+        xv[i] = (spix >= 0 && k < K) ? ld16(xr, 2u * (uint32_t)(k * HW + spix), 0) : 0u;
+    }
+}
+
+__device__ __forceinline__ void store_x_block(uint16_t *xs, int js, int ks0,
+                                              const uint32_t (&xv)[kKS / 2])
+{
+#pragma unroll
+    for (int i = 0; i < kKS / 2; ++i) {
+        const int kr = 2 * i + ks0;
+        xs[kr * kNT + (js ^ ((kr & 8) << 2))] = (uint16_t)xv[i];
+    }
+}
+
+// B fragment of K-step s (16 rows from 16 s) for tile pixel column jc.
+__device__ __forceinline__ bf16x8_t b_fragment(const uint16_t *xs, int s, int h, int jc)
+{
+    bf16x8_t bf;
+    const uint16_t *xr = xs + (16 * s + 8 * h) * kNT + (jc ^ (h << 5));
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        bf[i] = __builtin_bit_cast(__bf16, xr[i * kNT]);
+    return bf;
+}
+
 template <Mode MODE>
-__global__ __launch_bounds__(256) void proj_kernel(ProjArgs A)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void proj_rows_kernel(
+    ProjArgs A)
+{
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kKS * kNT];
+
+    const int t = threadIdx.x;
+    const int v = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int l = t & 63, h = l >> 5, l32 = l & 31;
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int b = mdiv(blk, A.div_n);
+    const int nt = blk - b * A.ntiles;
+
+    {
+        const int js = t & (kNT - 1), ks0 = t >> 7;
+        int r_, c_;
+        const int spix = tile_pixel<MODE>(A, nt, js, r_, c_);
+        const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HW, (uint32_t)(2 * A.K * A.HW));
+        uint32_t xv[kKS / 2];
+        load_x_block(xr, A.K, A.HW, 0, ks0, spix, xv);
+        store_x_block(xs, js, ks0, xv);
+    }
+    __syncthreads();
+
+    const int nsteps = (A.K + 15) >> 4;   // K-steps of 16 holding data
+    const int RT = (A.M + 31) >> 5;
+    // parameter product with Cc a multiple of 32: the 32 rows of a row tile
+    // are 32 channels of u or lambda, or 8 channels x 4 taps of w, of one
+    // direction slot, so a row's plane offset is a scalar.  The waves then
+    // take the row tiles of vertical directions in a first pass and those of
+    // horizontal ones in a second, each with the tile's pixels ordered along
+    // the pass's blocked layout (8 lines of one position, resp. 8 positions
+    // of one line, adjacent), so that the 32 lanes of a store write 64
+    // contiguous bytes.
+    const bool fast = MODE == Mode::Params && A.Cc % 32 == 0;
+    int rb = 0, cb = 0;
+    if (MODE == Mode::Params) {
+        rb = mdiv(nt, A.div_tw);
+        cb = nt - rb * A.tiles_w;
+    }
+    u32x4 yd = {};
+    if (MODE == Mode::Plain)
+        yd = make_sdesc(A.y + (int64_t)b * A.M * A.HW, (uint32_t)(2 * A.M * A.HW));
+#pragma unroll 1
+    for (int pass = 0; pass < (fast ? 2 : 1); ++pass) {
+    // this pass's pixel of lane column 32 ct + l32 and its B fragments
+    bf16x8_t bfr[4][kKS / 16];
+    int prow[4], pcol[4], ppix[4];
+    uint32_t po[4];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+        const int jp = 32 * ct + l32;
+        int js = jp;                      // the pixel's column in the staged block
+        if (fast) {
+            const int rl = pass == 0 ? (jp & 7) : ((jp >> 3) & 7);
+            const int cl = pass == 0 ? (jp >> 3) : 8 * (jp >> 6) + (jp & 7);
+            js = rl * 16 + cl;
+        }
+#pragma unroll
+        for (int s = 0; s < kKS / 16; ++s)
+            if (s < nsteps)
+                bfr[ct][s] = b_fragment(xs, s, h, js);
+        ppix[ct] = tile_pixel<MODE>(A, nt, js, prow[ct], pcol[ct]);
+        po[ct] = 0;
+        if (fast && ppix[ct] >= 0)
+            po[ct] = 2u * (uint32_t)(pass == 0 ? lm_offset(prow[ct], pcol[ct], A.H, A.W)
+                                                : lm_offset(pcol[ct], prow[ct], A.W, A.H));
+    }
+#pragma unroll 1
+    for (int rt = v; rt < RT; rt += 4) {
+        bool is_w = false, vert = true;
+        u32x4 dd = {};
+        if (fast) {
+            const int m0 = 32 * rt;
+            is_w = m0 >= 2 * A.DCc;
+            const int q0 = is_w ? (m0 - 2 * A.DCc) >> 2 : (m0 < A.DCc ? m0 : m0 - A.DCc);
+            const int sl = mdiv(q0, A.div_cc), c0 = q0 - sl * A.Cc;
+            vert = A.dirs[sl] < 2;
+            if (vert != (pass == 0))
+                continue;
+            const int64_t HW = A.HW;
+            const bf16_t *base =
+                is_w ? A.w + (((int64_t)sl * A.B + b) * A.Cc + c0) * 3 * HW
+                     : (m0 < A.DCc ? A.u : A.lam) + (((int64_t)sl * A.B + b) * A.Cc + c0) * HW;
+            dd = make_sdesc(base, (uint32_t)(2 * (is_w ? 24 : 32) * HW));
+        }
+        bf16x8_t af[kKS / 16];
+        const bf16_t *src = a_row<MODE>(A, 32 * rt + l32);
+#pragma unroll
+        for (int s = 0; s < kKS / 16; ++s) {
+            const int k = 16 * s + 8 * h;
+            if (s < nsteps)
+                af[s] = (src != nullptr && k < A.K) ? *reinterpret_cast<const bf16x8_t *>(src + k)
+                                                    : bf16x8_t{};
+        }
+        f32x16_t acc[4];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[ct][r] = 0.f;
+#pragma unroll
+        for (int s = 0; s < kKS / 16; ++s)
+            if (s < nsteps)
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct)
+                    acc[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[ct][s], acc[ct],
+                                                                      0, 0, 0);
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) {
+            if (ppix[ct] < 0)
+                continue;
+            if (MODE == Mode::Plain) {
+                // the lane's part of the offset in a register, the row's in soffset
+                const uint32_t vo = 2u * (uint32_t)(ppix[ct] + 4 * h * A.HW);
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int m = 32 * rt + 8 * (r >> 2) + (r & 3);
+                    if (m + 4 * h < A.M)
+                        st16(yd, vo, 2u * (uint32_t)(m * A.HW), bf16_bits(acc[ct][r]));
+                }
+            } else if (!fast) {
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    store_params(A, b, 32 * rt + 8 * g + 4 * h, prow[ct], pcol[ct],
+                                 acc[ct][4 * g], acc[ct][4 * g + 1], acc[ct][4 * g + 2],
+                                 acc[ct][4 * g + 3]);
+            } else {
+                // row 8 g + 4 h + e of the tile: plane 8 g + e (scalar) plus
+                // 4 h (u, lambda) or channel 2 g + h, tap e: plane 6 g + e plus 3 h (w)
+                const uint32_t vo = po[ct] + 2u * (uint32_t)((is_w ? 3 : 4) * h * A.HW);
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    float o[4] = {acc[ct][4 * g], acc[ct][4 * g + 1], acc[ct][4 * g + 2],
+                                  acc[ct][4 * g + 3]};
+                    if (is_w) {
+                        const int p = vert ? pcol[ct] : prow[ct], P = vert ? A.W : A.H;
+                        const float s0 = p > 0 ? sigmoid(o[0]) : 0.f;
+                        const float s1 = sigmoid(o[1]);
+                        const float s2 = p < P - 1 ? sigmoid(o[2]) : 0.f;
+                        const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+                        o[0] = s0 * inv, o[1] = s1 * inv, o[2] = s2 * inv;
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if (is_w && e == 3)
+                            continue;
+                        const int plane = is_w ? 6 * g + e : 8 * g + e;
+                        st16(dd, vo, 2u * (uint32_t)(plane * A.HW), bf16_bits(o[e]));
+                    }
+                }
+            }
+        }
+    }
+    }
+}
+
+template <Mode MODE>
+__global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
 {
     __shared__ __attribute__((aligned(16))) uint16_t xs[kKS * kNT];
     __shared__ __attribute__((aligned(16))) uint16_t as[kMT * kAP];
@@ -126,11 +354,25 @@ __global__ __launch_bounds__(256) void proj_kernel(ProjArgs A)
     const int nt = rest - b * A.ntiles;
     const int m0 = mt * kMT;
 
-    // this thread's staging pixel (the same in every stage)
+    // this thread's staging pixel and A pieces (the same in every stage)
     const int js = t & (kNT - 1), ks0 = t >> 7;
     int srow, scol;
     const int spix = tile_pixel<MODE>(A, nt, js, srow, scol);
-    const bf16_t *xb = A.x + (int64_t)b * A.K * A.HW;
+    const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HW, (uint32_t)(2 * A.K * A.HW));
+    const bf16_t *asrc[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        asrc[i] = a_row<MODE>(A, m0 + ((t + 256 * i) >> 3));
+
+    auto load_a = [&](int kc, uint4 (&av)[2]) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int kq = kc + 8 * ((t + 256 * i) & 7);
+            av[i] = (asrc[i] != nullptr && kq < A.K)
+                        ? *reinterpret_cast<const uint4 *>(asrc[i] + kq)
+                        : make_uint4(0, 0, 0, 0);
+        }
+    };
 
     f32x16_t acc[2];
 #pragma unroll
@@ -139,42 +381,26 @@ __global__ __launch_bounds__(256) void proj_kernel(ProjArgs A)
         for (int r = 0; r < 16; ++r)
             acc[rt][r] = 0.f;
 
+    uint32_t xv[kKS / 2];
+    uint4 av[2];
+    load_x_block(xr, A.K, A.HW, 0, ks0, spix, xv);
+    load_a(0, av);
     for (int kc = 0; kc < A.K; kc += kKS) {
         __syncthreads();   // the previous stage's fragments are read
-        // x block: rows kc + 2 i + ks0, this thread's pixel column
-        uint16_t xv[kKS / 2];
-#pragma unroll
-        for (int i = 0; i < kKS / 2; ++i) {
-            const int k = kc + 2 * i + ks0;
-            xv[i] = (spix >= 0 && k < A.K) ? xb[(int64_t)k * A.HW + spix] : (uint16_t)0;
-        }
-        // A block: 64 rows x 8 pieces of 8 K-values
-        uint4 av[2];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int p = t + 256 * i, r = p >> 3, kq = kc + 8 * (p & 7);
-            const bf16_t *src = a_row<MODE>(A, m0 + r);
-            av[i] = (src != nullptr && kq < A.K) ? *reinterpret_cast<const uint4 *>(src + kq)
-                                                  : make_uint4(0, 0, 0, 0);
-        }
-#pragma unroll
-        for (int i = 0; i < kKS / 2; ++i) {
-            const int kr = 2 * i + ks0;
-            xs[kr * kNT + (js ^ ((kr & 8) << 2))] = xv[i];
-        }
+        store_x_block(xs, js, ks0, xv);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int p = t + 256 * i;
             *reinterpret_cast<uint4 *>(&as[(p >> 3) * kAP + 8 * (p & 7)]) = av[i];
         }
         __syncthreads();
+        if (kc + kKS < A.K) {   // the next stage's loads overlap this stage's products
+            load_x_block(xr, A.K, A.HW, kc + kKS, ks0, spix, xv);
+            load_a(kc + kKS, av);
+        }
 #pragma unroll
         for (int s = 0; s < kKS / 16; ++s) {
-            bf16x8_t bf;
-            const uint16_t *xr = xs + (16 * s + 8 * h) * kNT + ((32 * v + l32) ^ (h << 5));
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                bf[i] = __builtin_bit_cast(__bf16, xr[i * kNT]);
+            const bf16x8_t bf = b_fragment(xs, s, h, 32 * v + l32);
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 const bf16x8_t af =
@@ -207,57 +433,28 @@ __global__ __launch_bounds__(256) void proj_kernel(ProjArgs A)
         int row, col;
         if (tile_pixel<MODE>(A, nt, jc, row, col) < 0)
             return;
-        const int64_t HW = A.HW;
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int m = m0 + 32 * rt + 8 * g + 4 * h;   // a multiple of 4
-                const float v0 = acc[rt][4 * g], v1 = acc[rt][4 * g + 1];
-                const float v2 = acc[rt][4 * g + 2], v3 = acc[rt][4 * g + 3];
-                if (m < 2 * A.DCc) {
-                    // four channels c .. c+3 of one direction: u, or lambda
-                    const bool is_u = m < A.DCc;
-                    const int q = is_u ? m : m - A.DCc;
-                    const int s = mdiv(q, A.div_cc), c = q - s * A.Cc;
-                    const int d = A.dirs[s];
-                    bf16_t *dst = (is_u ? A.u : A.lam) + ((int64_t)s * A.B + b) * A.Cc * HW +
-                                  (int64_t)c * HW + plane_offset(d, row, col, A.H, A.W);
-                    dst[0] = bf16_bits(v0);
-                    dst[HW] = bf16_bits(v1);
-                    dst[2 * HW] = bf16_bits(v2);
-                    dst[3 * HW] = bf16_bits(v3);
-                } else if (m < A.M) {
-                    // the three tap logits of channel c, direction slot s
-                    const int dc = (m - 2 * A.DCc) >> 2;
-                    const int s = mdiv(dc, A.div_cc), c = dc - s * A.Cc;
-                    const int d = A.dirs[s];
-                    const int p = d < 2 ? col : row, P = d < 2 ? A.W : A.H;
-                    const float s0 = p > 0 ? sigmoid(v0) : 0.f;
-                    const float s1 = sigmoid(v1);
-                    const float s2 = p < P - 1 ? sigmoid(v2) : 0.f;
-                    const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
-                    bf16_t *dst = A.w + (((int64_t)s * A.B + b) * A.Cc + c) * 3 * HW +
-                                  plane_offset(d, row, col, A.H, A.W);
-                    dst[0] = bf16_bits(s0 * inv);
-                    dst[HW] = bf16_bits(s1 * inv);
-                    dst[2 * HW] = bf16_bits(s2 * inv);
-                }
-            }
-        }
+            for (int g = 0; g < 4; ++g)
+                store_params(A, b, m0 + 32 * rt + 8 * g + 4 * h, row, col, acc[rt][4 * g],
+                             acc[rt][4 * g + 1], acc[rt][4 * g + 2], acc[rt][4 * g + 3]);
     }
 }
 
 template <Mode MODE>
 hipError_t launch_proj(ProjArgs &A, hipStream_t st)
 {
-    A.mtiles = (A.M + kMT - 1) / kMT;
-    A.div_m = make_magic((uint32_t)A.mtiles);
     A.div_n = make_magic((uint32_t)A.ntiles);
-    const int64_t nblk = (int64_t)A.B * A.ntiles * A.mtiles;
-    if (nblk > 0x7fffffff)
-        return hipErrorInvalidValue;
-    hipLaunchKernelGGL(proj_kernel<MODE>, dim3((unsigned)nblk), dim3(256), 0, st, A);
+    if (A.K <= kKS) {
+        const int64_t nblk = (int64_t)A.B * A.ntiles;
+        hipLaunchKernelGGL(proj_rows_kernel<MODE>, dim3((unsigned)nblk), dim3(256), 0, st, A);
+    } else {
+        A.mtiles = (A.M + kMT - 1) / kMT;
+        A.div_m = make_magic((uint32_t)A.mtiles);
+        const int64_t nblk = (int64_t)A.B * A.ntiles * A.mtiles;
+        hipLaunchKernelGGL(proj_stage_kernel<MODE>, dim3((unsigned)nblk), dim3(256), 0, st, A);
+    }
     return hipGetLastError();
 }
 

@@ -65,6 +65,8 @@ LATENT_CASES = [
     _lw("odd-9x8-dirs10", 2, 24, 24, 9, 8, dirs=10),
     _lw("tall-70x9-dirs3", 1, 32, 8, 70, 9, dirs=3),
     _lw("paper-width-20x20", 1, 1152, 64, 20, 20),
+    # more than 64 latent channels: the parameter product takes K in stages
+    _lw("cc128-9x10-dirs5", 1, 128, 128, 9, 10, dirs=5),
 ]
 
 
