@@ -9,7 +9,7 @@ events on the launch stream) and the CPU oracle timed on a bounded sample of
 the same workload.  Diagnostics go to stderr.
 
     python bench.py [--steps K] [--warmup W] [--workload IDX|NAME|all] [--no-cpu-baseline]
-                    [--norm]
+                    [--norm] [--latent IDX|NAME|all]
 
 Before every step, outside the timed events, reading a 1 GiB buffer evicts
 the L2s and the 256 MB Infinity Cache (writing back what the previous step
@@ -19,6 +19,11 @@ two calls' event times.  A device-to-device copy that moves the dominant
 call's algorithmic byte count, timed the same way, gives the achievable
 bandwidth; the share of the call's time it does not explain is reported as
 the serialisation share.  `--workload all` prints one line per workload.
+
+`--latent` times the latent-space sublayer of C-GSPN instead (gspn_latent_fwd:
+P_down, the parameter product, the scan over the latent channels, P_up), one
+step being one forward call; each stage is also timed on its own, and the
+roofline is that of the slowest stage.
 """
 from __future__ import annotations
 
@@ -280,6 +285,133 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     return out
 
 
+LATENT_METRIC = ("C-GSPN latent sublayer fwd Gpix·ch/s (input pixel-channels) at 1 MI355X; "
+                 "achieved HBM GB/s vs peak")
+
+
+def latent_stage_bytes(lw: gi.LatentWorkload) -> dict:
+    """Compulsory HBM bytes of the sublayer's stages (bf16): every input read
+    once, every output written once."""
+    HW, D = lw.H * lw.W, lw.ndirs
+    x, xc = lw.B * lw.C * HW * 2, lw.B * lw.Cc * HW * 2
+    scan = algorithmic_bytes(gi.Workload("latent-scan", lw.B, lw.Cc, lw.Cc, lw.H, lw.W, "bf16",
+                                         lw.dirs, False, "sigmoid", 1.0, 0))["fwd"]
+    return {"down": x + xc + lw.Cc * lw.C * 2,
+            "params": xc + 5 * D * xc + 5 * D * lw.Cc * lw.Cc * 2,
+            "scan": scan,
+            "up": xc + x + lw.C * lw.Cc * 2}
+
+
+def latent_cpu_baseline(lw: gi.LatentWorkload, inp: dict, min_seconds: float) -> dict:
+    """The fp64 oracle on single images of the workload, until about
+    `min_seconds` have passed."""
+    import oracle
+    done = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < min_seconds and done < 4 * lw.B:
+        b = done % lw.B
+        oracle.latent_fwd(inp["x"][b:b + 1], inp["p_down"], inp["l_u"], inp["l_lam"],
+                          inp["l_w"], inp["p_up"], lw.dirs, storage="bf16")
+        done += 1
+    dt = time.perf_counter() - t0
+    return {"value": round(done * lw.C * lw.H * lw.W / dt / 1e9, 6), "unit": "Gpix·ch/s",
+            "cores": 1, "kind": "oracle",
+            "sample": f"{done} images of {lw.name} ({lw.B} per step; fp64 with bf16 storage "
+                      f"points, numpy matmuls + C scan, single thread, {_cpu_model()}), "
+                      f"{dt:.1f} s"}
+
+
+def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
+    log(f"latent workload {lw}")
+    inp = gi.make_latent_inputs(lw)
+    dev = {k: to_device(v, "bf16", torch) for k, v in inp.items()}
+    stream = torch.cuda.current_stream()
+    scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
+             if args.flush_mib > 0 else None)
+    D, HW = lw.ndirs, lw.H * lw.W
+    kw = dict(dtype=torch.bfloat16, device="cuda")
+    y = torch.empty_like(dev["x"])
+    xc = torch.empty((lw.B, lw.Cc, lw.H, lw.W), **kw)
+    yc = torch.empty_like(xc)
+    prm = (torch.empty((D, lw.B, lw.Cc, HW), **kw), torch.empty((D, lw.B, lw.Cc, HW), **kw),
+           torch.empty((D, lw.B, lw.Cc, 3, HW), **kw))
+
+    def flush():
+        if scrub is not None:
+            scrub.sum()
+
+    calls = {
+        "sublayer": lambda: gspn.latent_fwd(dev["x"], dev["p_down"], dev["l_u"], dev["l_lam"],
+                                            dev["l_w"], dev["p_up"], lw.dirs, y=y,
+                                            stream=stream),
+        "down": lambda: gspn.project(dev["p_down"], dev["x"], y=xc, stream=stream),
+        "params": lambda: gspn.latent_params(xc, dev["l_u"], dev["l_lam"], dev["l_w"], lw.dirs,
+                                             out=prm, stream=stream),
+        "scan": lambda: gspn.scan_fwd(xc, prm[2], prm[1], prm[0], lw.dirs, y=yc,
+                                      stream=stream),
+        "up": lambda: gspn.project(dev["p_up"], yc, y=y, stream=stream),
+    }
+
+    def timed(fn, reps):
+        ms = []
+        for _ in range(reps):
+            flush()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return float(np.mean(ms))
+
+    for fn in calls.values():
+        for _ in range(max(1, args.warmup)):
+            fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ms_step = timed(calls["sublayer"], args.steps)
+    log(f"sublayer {ms_step:.4f} ms over {args.steps} steps ({time.perf_counter() - t0:.1f} s)")
+    stage_ms = {k: timed(fn, args.steps) for k, fn in calls.items() if k != "sublayer"}
+    nbytes = latent_stage_bytes(lw)
+    stages = {k: {"ms": round(v, 5), "algorithmic_bytes": nbytes[k],
+                  "hbm_frac": round(nbytes[k] / (v * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+              for k, v in stage_ms.items()}
+    log("stages: " + ", ".join(f"{k} {v['ms']:.4f} ms ({v['hbm_frac']:.1%})"
+                               for k, v in stages.items()))
+    dom = max(stage_ms, key=stage_ms.get)
+    achieved = nbytes[dom] / (stage_ms[dom] * 1e-3) / 1e9
+    total = sum(nbytes.values())
+    out = {
+        "metric": LATENT_METRIC,
+        "value": round(lw.B * lw.C * HW / (ms_step * 1e-3) / 1e9, 3),
+        "unit": "Gpix·ch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": lw.name, "B": lw.B, "C": lw.C, "Cc": lw.Cc, "H": lw.H,
+                   "W": lw.W, "directions": D, "pass": "fwd", "storage": "bf16",
+                   "parallelism": "single GPU"},
+        "cache_flush_mib": args.flush_mib,
+        "step_hbm_gbs_algorithmic": round(total / (ms_step * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(total / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "stages": stages,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": dom, "avg_ms": round(stage_ms[dom], 5),
+                     "algorithmic_bytes": nbytes[dom]},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle ...")
+        out["cpu_baseline"] = latent_cpu_baseline(lw, inp, args.cpu_seconds)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -290,6 +422,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--norm", action="store_true",
                     help="weights given as logits: time gspn_scan_fwd_norm / gspn_scan_bwd_norm")
+    ap.add_argument("--latent", default=None,
+                    help="time the latent sublayer instead: index or name of the latent "
+                         "workload, or 'all'")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="approximate CPU time of the oracle baseline")
     ap.add_argument("--flush-mib", type=int, default=1024,
@@ -313,6 +448,15 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
     gspn.load()
+
+    if args.latent is not None:
+        key = args.latent
+        lws = (list(gi.LATENT_WORKLOADS) if key == "all"
+               else [gi.latent_workload(int(key) if key.isdigit() else key)])
+        for lw in lws:
+            print(json.dumps(run_latent(lw, args, torch, gspn)), flush=True)
+            torch.cuda.empty_cache()
+        return 0
 
     key = args.workload
     if key == "all":

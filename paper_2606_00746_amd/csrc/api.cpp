@@ -308,11 +308,14 @@ extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_
         st = check_project(B, C, Cc, H, W, dtype);
     if (st == GSPN_OK)
         st = check_project(B, Cc, C, H, W, dtype);
+    // the latent grid may be padded by up to 7 lines each way
+    if (st == GSPN_OK && H + 7 <= GSPN_MAX_SIDE && W + 7 <= GSPN_MAX_SIDE)
+        st = check_latent(direction, B, Cc, H + 7, W + 7, dtype);
     if (st != GSPN_OK)
         return st;
     const int64_t D = __builtin_popcount(direction);
     const int64_t HW = (int64_t)H * W;
-    const int64_t n = (int64_t)B * C * HW, nc = (int64_t)B * Cc * HW;
+    const int64_t n = (int64_t)B * C * HW;
     const int64_t cc2 = (int64_t)Cc * Cc;
     const Buf bufs[] = {{x, n * 2, false},           {p_down, (int64_t)Cc * C * 2, false},
                         {l_u, D * cc2 * 2, false},   {l_lam, D * cc2 * 2, false},
@@ -322,25 +325,39 @@ extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_
     if (st != GSPN_OK)
         return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    // The latent tensors belong to this call, so the scan may run on a grid
+    // padded at the bottom and right to whole 8-line blocks, where the
+    // register-streamed and wide kernels apply.  Padded pixels hold x_c = 0,
+    // hence u = lambda = 0; the taps of real pixels that point into the
+    // padding are normalized as off the grid (weight exactly 0); and a scan
+    // that starts in the padding carries h = 0 up to the first real line,
+    // which then starts from h = lambda x as on the unpadded grid.  Real
+    // pixels therefore see the same recurrence; P_up reads only them.
+    const auto up8 = [](int v) { return (v + 7) / 8 * 8; };
+    const bool pad = (H % 8 != 0 || W % 8 != 0) && (H > 16 || W > 16) && up8(H) <= 256 &&
+                     up8(W) <= 256;
+    const int Hp = pad ? up8(H) : H, Wp = pad ? up8(W) : W;
+    const int64_t ncp = (int64_t)B * Cc * Hp * Wp;
     // latent x_c, u, lambda, w and y_c in one scratch block, 16-byte aligned parts
-    const int64_t o_u = round8(nc), o_l = o_u + round8(D * nc), o_w = o_l + round8(D * nc);
-    const int64_t o_y = o_w + round8(3 * D * nc), total = o_y + round8(nc);
+    const int64_t o_u = round8(ncp), o_l = o_u + round8(D * ncp), o_w = o_l + round8(D * ncp);
+    const int64_t o_y = o_w + round8(3 * D * ncp), total = o_y + round8(ncp);
     void *scr = nullptr;
     hipError_t e = scratch_alloc(&scr, (size_t)(total * 2), s);
     if (e != hipSuccess)
         return hip_status(e);
     uint16_t *base = static_cast<uint16_t *>(scr);
     uint16_t *xc = base, *u = base + o_u, *lam = base + o_l, *w = base + o_w, *yc = base + o_y;
-    e = launch_project(p_down, x, xc, B, Cc, C, H, W, s);
+    e = launch_project(p_down, x, xc, B, Cc, C, Hp, Wp, s, H, W);
     if (e == hipSuccess)
-        e = launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W, s);
+        e = launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, Hp, Wp, s, H,
+                                 W);
     if (e == hipSuccess) {
         Problem p{xc, w, lam, u, nullptr, yc, nullptr, nullptr, nullptr, nullptr,
-                  direction, B, Cc, Cc, H, W, GSPN_BF16};
+                  direction, B, Cc, Cc, Hp, Wp, GSPN_BF16};
         e = dispatch_fwd(p, s);
     }
     if (e == hipSuccess)
-        e = launch_project(p_up, yc, y, B, C, Cc, H, W, s);
+        e = launch_project(p_up, yc, y, B, C, Cc, H, W, s, Hp, Wp);
     const hipError_t e2 = scratch_free(scr, s);
     return hip_status(e != hipSuccess ? e : e2);
 }

@@ -58,11 +58,15 @@ struct ProjArgs {
     const bf16_t *x;                 // [B][K][HW]
     bf16_t *y;                       // plain: [B][M][HW]
     bf16_t *u, *lam, *w;             // params: [D][B][Cc][plane], [D][B][Cc][plane], [D][B][Cc][3][plane]
-    int B, M, K, H, W, HW;
+    int B, M, K, H, W, HW;           // output grid (params: the planes' grid)
+    int HWi;                         // pixels of one input channel
+    int Hi, Wi;                      // plain with remap: the input grid
+    int Hv, Wv;                      // params: the grid whose edges decide which taps exist
+    bool remap;                      // plain: input and output grids differ
     int ntiles, mtiles, tiles_w;     // pixel tiles, row tiles, params: tiles across a row
     int Cc, DCc;                     // params: latent channels, D * Cc
     int dirs[4];                     // params: direction index of each stacked slot
-    Magic div_m, div_n, div_cc, div_tw;
+    Magic div_m, div_n, div_cc, div_tw, div_w;
 };
 
 __device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
@@ -72,20 +76,35 @@ __device__ __forceinline__ uint16_t bf16_bits(float v)
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
 }
 
-// Pixel of tile position j (0 .. 127): image row and column, or -1 if off
-// the image.
+// Pixel of tile position j (0 .. 127) in the output grid, or -1 if off it;
+// `ipix` is the same pixel in the input map (-1: not there, reads as 0).
+// Plain products may map between grids of different sizes that share their
+// top-left corner (a grid padded at the bottom and right and the unpadded
+// one); `row`, `col` are the output pixel's coordinates for the parameter
+// product.
 template <Mode MODE>
-__device__ __forceinline__ int tile_pixel(const ProjArgs &A, int nt, int j, int &row, int &col)
+__device__ __forceinline__ int tile_pixel(const ProjArgs &A, int nt, int j, int &row, int &col,
+                                          int &ipix)
 {
     if (MODE == Mode::Plain) {
         const int n = nt * kNT + j;
         row = col = 0;
-        return n < A.HW ? n : -1;
+        if (n >= A.HW) {
+            ipix = -1;
+            return -1;
+        }
+        ipix = n;
+        if (A.remap) {
+            const int r = mdiv(n, A.div_w), c = n - r * A.W;
+            ipix = (r < A.Hi && c < A.Wi) ? r * A.Wi + c : -1;
+        }
+        return n;
     } else {
         const int rb = mdiv(nt, A.div_tw), cb = nt - rb * A.tiles_w;
         row = 8 * rb + (j >> 4);
         col = 16 * cb + (j & 15);
-        return (row < A.H && col < A.W) ? row * A.W + col : -1;
+        ipix = (row < A.H && col < A.W) ? row * A.W + col : -1;
+        return ipix;
     }
 }
 
@@ -134,7 +153,7 @@ __device__ __forceinline__ void store_params(const ProjArgs &A, int b, int m, in
         const int dc = (m - 2 * A.DCc) >> 2;
         const int s = mdiv(dc, A.div_cc), c = dc - s * A.Cc;
         const int d = A.dirs[s];
-        const int p = d < 2 ? col : row, P = d < 2 ? A.W : A.H;
+        const int p = d < 2 ? col : row, P = d < 2 ? A.Wv : A.Hv;
         const float s0 = p > 0 ? sigmoid(v0) : 0.f;
         const float s1 = sigmoid(v1);
         const float s2 = p < P - 1 ? sigmoid(v2) : 0.f;
@@ -195,11 +214,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 
     {
         const int js = t & (kNT - 1), ks0 = t >> 7;
-        int r_, c_;
-        const int spix = tile_pixel<MODE>(A, nt, js, r_, c_);
-        const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HW, (uint32_t)(2 * A.K * A.HW));
+        int r_, c_, spix;
+        tile_pixel<MODE>(A, nt, js, r_, c_, spix);
+        const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HWi, (uint32_t)(2 * A.K * A.HWi));
         uint32_t xv[kKS / 2];
-        load_x_block(xr, A.K, A.HW, 0, ks0, spix, xv);
+        load_x_block(xr, A.K, A.HWi, 0, ks0, spix, xv);
         store_x_block(xs, js, ks0, xv);
     }
     __syncthreads();
@@ -242,7 +261,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         for (int s = 0; s < kKS / 16; ++s)
             if (s < nsteps)
                 bfr[ct][s] = b_fragment(xs, s, h, js);
-        ppix[ct] = tile_pixel<MODE>(A, nt, js, prow[ct], pcol[ct]);
+        int ip_;
+        ppix[ct] = tile_pixel<MODE>(A, nt, js, prow[ct], pcol[ct], ip_);
         po[ct] = 0;
         if (fast && ppix[ct] >= 0)
             po[ct] = 2u * (uint32_t)(pass == 0 ? lm_offset(prow[ct], pcol[ct], A.H, A.W)
@@ -316,7 +336,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                     float o[4] = {acc[ct][4 * g], acc[ct][4 * g + 1], acc[ct][4 * g + 2],
                                   acc[ct][4 * g + 3]};
                     if (is_w) {
-                        const int p = vert ? pcol[ct] : prow[ct], P = vert ? A.W : A.H;
+                        const int p = vert ? pcol[ct] : prow[ct], P = vert ? A.Wv : A.Hv;
                         const float s0 = p > 0 ? sigmoid(o[0]) : 0.f;
                         const float s1 = sigmoid(o[1]);
                         const float s2 = p < P - 1 ? sigmoid(o[2]) : 0.f;
@@ -356,9 +376,9 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
 
     // this thread's staging pixel and A pieces (the same in every stage)
     const int js = t & (kNT - 1), ks0 = t >> 7;
-    int srow, scol;
-    const int spix = tile_pixel<MODE>(A, nt, js, srow, scol);
-    const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HW, (uint32_t)(2 * A.K * A.HW));
+    int srow, scol, spix;
+    const int sopix = tile_pixel<MODE>(A, nt, js, srow, scol, spix);
+    const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HWi, (uint32_t)(2 * A.K * A.HWi));
     const bf16_t *asrc[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -383,7 +403,7 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
 
     uint32_t xv[kKS / 2];
     uint4 av[2];
-    load_x_block(xr, A.K, A.HW, 0, ks0, spix, xv);
+    load_x_block(xr, A.K, A.HWi, 0, ks0, spix, xv);
     load_a(0, av);
     for (int kc = 0; kc < A.K; kc += kKS) {
         __syncthreads();   // the previous stage's fragments are read
@@ -395,7 +415,7 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
         }
         __syncthreads();
         if (kc + kKS < A.K) {   // the next stage's loads overlap this stage's products
-            load_x_block(xr, A.K, A.HW, kc + kKS, ks0, spix, xv);
+            load_x_block(xr, A.K, A.HWi, kc + kKS, ks0, spix, xv);
             load_a(kc + kKS, av);
         }
 #pragma unroll
@@ -420,8 +440,8 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
             for (int r = 0; r < 16; ++r)
                 os[(32 * rt + 8 * (r >> 2) + 4 * h + (r & 3)) * kNT + jc] = bf16_bits(acc[rt][r]);
         __syncthreads();
-        if (spix >= 0) {
-            bf16_t *yb = A.y + (int64_t)b * A.M * A.HW + spix;
+        if (sopix >= 0) {
+            bf16_t *yb = A.y + (int64_t)b * A.M * A.HW + sopix;
 #pragma unroll 4
             for (int i = 0; i < kMT / 2; ++i) {
                 const int r = 2 * i + ks0;
@@ -430,8 +450,8 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
             }
         }
     } else {
-        int row, col;
-        if (tile_pixel<MODE>(A, nt, jc, row, col) < 0)
+        int row, col, ip_;
+        if (tile_pixel<MODE>(A, nt, jc, row, col, ip_) < 0)
             return;
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
@@ -461,20 +481,23 @@ hipError_t launch_proj(ProjArgs &A, hipStream_t st)
 }  // namespace
 
 hipError_t launch_project(const void *a, const void *x, void *y, int B, int M, int K, int H, int W,
-                          hipStream_t st)
+                          hipStream_t st, int Hi, int Wi)
 {
     ProjArgs A{};
     A.a = static_cast<const bf16_t *>(a);
     A.x = static_cast<const bf16_t *>(x);
     A.y = static_cast<bf16_t *>(y);
     A.B = B, A.M = M, A.K = K, A.H = H, A.W = W, A.HW = H * W;
+    A.Hi = Hi > 0 ? Hi : H, A.Wi = Wi > 0 ? Wi : W, A.HWi = A.Hi * A.Wi;
+    A.remap = A.Hi != H || A.Wi != W;
+    A.div_w = make_magic((uint32_t)W);
     A.ntiles = (A.HW + kNT - 1) / kNT;
     return launch_proj<Mode::Plain>(A, st);
 }
 
 hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, const void *lw,
                                 void *u, void *lam, void *w, int mask, int B, int Cc, int H, int W,
-                                hipStream_t st)
+                                hipStream_t st, int Hv, int Wv)
 {
     ProjArgs A{};
     A.lu = static_cast<const bf16_t *>(lu);
@@ -488,7 +511,8 @@ hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, 
     for (int d = 0; d < 4; ++d)
         if ((mask >> d) & 1)
             A.dirs[D++] = d;
-    A.B = B, A.K = Cc, A.H = H, A.W = W, A.HW = H * W;
+    A.B = B, A.K = Cc, A.H = H, A.W = W, A.HW = H * W, A.HWi = A.HW;
+    A.Hv = Hv > 0 ? Hv : H, A.Wv = Wv > 0 ? Wv : W;
     A.Cc = Cc, A.DCc = D * Cc, A.M = 6 * D * Cc;
     A.tiles_w = (W + 15) / 16;
     A.ntiles = ((H + 7) / 8) * A.tiles_w;

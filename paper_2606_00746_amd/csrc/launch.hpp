@@ -36,11 +36,15 @@ hipError_t launch_bwd_general(const Problem &p, hipStream_t s);
 // y[b] = a x[b] with a [M][K], x [B][K][H*W], y [B][M][H*W]; and the
 // parameter product that writes u, lambda and normalized w of every
 // direction in the scan's blocked layout from x_c [B][Cc][H*W].
+// launch_project may read x on a different grid Hi x Wi sharing the top-left
+// corner (pixels outside it read as 0); launch_latent_params may write planes
+// of a grid padded beyond the image Hv x Wv, whose edges decide the taps
+// (0: the same grid).
 hipError_t launch_project(const void *a, const void *x, void *y, int B, int M, int K, int H, int W,
-                          hipStream_t s);
+                          hipStream_t s, int Hi = 0, int Wi = 0);
 hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, const void *lw,
                                 void *u, void *lam, void *w, int mask, int B, int Cc, int H, int W,
-                                hipStream_t s);
+                                hipStream_t s, int Hv = 0, int Wv = 0);
 
 // Stream-ordered scratch from the device's default pool.
 hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s);

@@ -77,6 +77,8 @@ def source_hash(kernels=None) -> str:
 def short_name(name: str) -> str:
     for pre in ("void ", "gspn::(anonymous namespace)::"):
         name = name.replace(pre, "")
+    # enum template arguments print as "(gspn::(anonymous namespace)::Mode)1"
+    name = name.replace("(Mode)0", "Plain").replace("(Mode)1", "Params")
     return name.split("(")[0]
 
 

@@ -89,7 +89,15 @@ def test_latent_params_match_oracle(lw):
     assert np.all(got_w[ref["w"] == 0.0] == 0.0), f"{lw.name} off-grid taps not 0"
 
 
-FWD_CASES = LATENT_CASES + [_lw("r2l-only-14x30", 3, 16, 16, 14, 30, dirs=8)]
+# sides that are not multiples of 8 run the latent scan on a grid padded to
+# whole 8-line blocks: scans that start in the padding (B2T, R2L), wide
+# padded grids, square and oblong ones
+FWD_CASES = LATENT_CASES + [
+    _lw("r2l-only-14x30", 3, 16, 16, 14, 30, dirs=8),
+    _lw("b2t-r2l-37x45", 1, 32, 32, 37, 45, dirs=10),
+    _lw("pad-to-wide-73x73", 1, 64, 64, 73, 73),
+    _lw("pad-to-64-57x61-dirs6", 2, 32, 32, 57, 61, dirs=6),
+]
 
 
 @pytest.mark.parametrize("lw", FWD_CASES, ids=lambda w: w.name)
