@@ -22,8 +22,9 @@ the serialisation share.  `--workload all` prints one line per workload.
 
 `--latent` times the latent-space sublayer of C-GSPN instead (gspn_latent_fwd:
 P_down, the parameter product, the scan over the latent channels, P_up), one
-step being one forward call; each stage is also timed on its own, and the
-roofline is that of the slowest stage.
+step being one forward call; each stage is also timed on its own through the
+public entry points (the parameter product and the scan on the sublayer's
+latent grid), and the roofline is that of the slowest stage.
 """
 from __future__ import annotations
 
@@ -289,9 +290,20 @@ LATENT_METRIC = ("C-GSPN latent sublayer fwd Gpix·ch/s (input pixel-channels) a
                  "achieved HBM GB/s vs peak")
 
 
+def latent_grid(lw: gi.LatentWorkload) -> tuple:
+    """The grid of the sublayer's latent tensors: gspn_latent_fwd pads sides
+    that are not multiples of 8 up to whole 8-line blocks (above 16 pixels,
+    up to 256)."""
+    up8 = lambda v: (v + 7) // 8 * 8
+    pad = ((lw.H % 8 or lw.W % 8) and max(lw.H, lw.W) > 16 and up8(lw.H) <= 256
+           and up8(lw.W) <= 256)
+    return (up8(lw.H), up8(lw.W)) if pad else (lw.H, lw.W)
+
+
 def latent_stage_bytes(lw: gi.LatentWorkload) -> dict:
     """Compulsory HBM bytes of the sublayer's stages (bf16): every input read
-    once, every output written once."""
+    once, every output written once, on the image's own grid (a padded
+    latent grid's extra pixels count as overhead, not as work)."""
     HW, D = lw.H * lw.W, lw.ndirs
     x, xc = lw.B * lw.C * HW * 2, lw.B * lw.Cc * HW * 2
     scan = algorithmic_bytes(gi.Workload("latent-scan", lw.B, lw.Cc, lw.Cc, lw.H, lw.W, "bf16",
@@ -329,12 +341,18 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
     scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
              if args.flush_mib > 0 else None)
     D, HW = lw.ndirs, lw.H * lw.W
+    Hp, Wp = latent_grid(lw)
     kw = dict(dtype=torch.bfloat16, device="cuda")
     y = torch.empty_like(dev["x"])
     xc = torch.empty((lw.B, lw.Cc, lw.H, lw.W), **kw)
     yc = torch.empty_like(xc)
-    prm = (torch.empty((D, lw.B, lw.Cc, HW), **kw), torch.empty((D, lw.B, lw.Cc, HW), **kw),
-           torch.empty((D, lw.B, lw.Cc, 3, HW), **kw))
+    # the parameter product and the scan on the latent grid, as the sublayer
+    # runs them (its padding holds x_c = 0)
+    xcp = torch.zeros((lw.B, lw.Cc, Hp, Wp), **kw)
+    ycp = torch.empty_like(xcp)
+    prm = (torch.empty((D, lw.B, lw.Cc, Hp * Wp), **kw),
+           torch.empty((D, lw.B, lw.Cc, Hp * Wp), **kw),
+           torch.empty((D, lw.B, lw.Cc, 3, Hp * Wp), **kw))
 
     def flush():
         if scrub is not None:
@@ -345,9 +363,9 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
                                             dev["l_w"], dev["p_up"], lw.dirs, y=y,
                                             stream=stream),
         "down": lambda: gspn.project(dev["p_down"], dev["x"], y=xc, stream=stream),
-        "params": lambda: gspn.latent_params(xc, dev["l_u"], dev["l_lam"], dev["l_w"], lw.dirs,
+        "params": lambda: gspn.latent_params(xcp, dev["l_u"], dev["l_lam"], dev["l_w"], lw.dirs,
                                              out=prm, stream=stream),
-        "scan": lambda: gspn.scan_fwd(xc, prm[2], prm[1], prm[0], lw.dirs, y=yc,
+        "scan": lambda: gspn.scan_fwd(xcp, prm[2], prm[1], prm[0], lw.dirs, y=ycp,
                                       stream=stream),
         "up": lambda: gspn.project(dev["p_up"], yc, y=y, stream=stream),
     }
@@ -364,9 +382,11 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
             ms.append(e0.elapsed_time(e1))
         return float(np.mean(ms))
 
-    for fn in calls.values():
+    for k, fn in calls.items():
         for _ in range(max(1, args.warmup)):
             fn()
+        if k == "down":
+            xcp[:, :, :lw.H, :lw.W] = xc
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ms_step = timed(calls["sublayer"], args.steps)
@@ -395,7 +415,8 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": lw.name, "B": lw.B, "C": lw.C, "Cc": lw.Cc, "H": lw.H,
-                   "W": lw.W, "directions": D, "pass": "fwd", "storage": "bf16",
+                   "W": lw.W, "latent_grid": [Hp, Wp], "directions": D, "pass": "fwd",
+                   "storage": "bf16",
                    "parallelism": "single GPU"},
         "cache_flush_mib": args.flush_mib,
         "step_hbm_gbs_algorithmic": round(total / (ms_step * 1e-3) / 1e9, 1),

@@ -52,7 +52,9 @@
  * null stream) and never synchronise the device.  gspn_scan_bwd and the
  * _norm entry points may take stream-ordered scratch memory from the
  * device's default memory pool, and so may gspn_scan_fwd for planes with a
- * side above 64; it is released on the same stream.  Calls are thread-safe.
+ * side above 64, and gspn_latent_fwd; it is released on the same stream.
+ * The library sets that pool to keep released memory for reuse rather than
+ * return it to the device.  Calls are thread-safe.
  *
  * Errors: every argument check runs on the host before any HIP call, so an
  * invalid call has no effect on the device.  A failed HIP call returns

@@ -4,6 +4,8 @@
 
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/gspn.h"
 #include "launch.hpp"
 
@@ -74,6 +76,20 @@ int hip_status(hipError_t e)
 
 hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s)
 {
+    // Keep freed scratch in the device's default pool instead of returning it
+    // to the device at the next synchronization, so that repeated calls do not
+    // map their scratch afresh each time (once per device and process).
+    static std::once_flag once[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+        std::call_once(once[dev], [dev] {
+            hipMemPool_t pool;
+            if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+                uint64_t keep = UINT64_MAX;
+                (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+            }
+        });
+    }
     return hipMallocAsync(ptr, bytes, s);
 }
 
