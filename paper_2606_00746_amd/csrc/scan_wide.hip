@@ -16,6 +16,8 @@
 // u_d * h_d to an fp32 plane in its own line-major order (whole lines per
 // store) and a tiled kernel sums the directions in direction-bit order,
 // transposing the horizontal ones through LDS, and stores y once.
+#include <algorithm>
+
 #include "cdna.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -70,14 +72,25 @@ __device__ __forceinline__ void neighbours(const float (&h)[NPL], float (&left)[
     }
 }
 
-// One direction of one channel plane.  HC, WC: the plane's sides when they
-// are compile-time constants (0: taken from H, W at run time); L, P: scan and
-// line length; the x plane sits in LDS with pitch (W / 2) | 1 dwords; ys
-// receives u * h as fp32 in the direction's line-major order (line l,
-// position p at l * P + p).
-template <int NPL, bool VERT, bool REV, int HC, int WC>
+// What a pass over a range of line blocks does (Sec. 3 recurrence; the chunk
+// split follows the block lower-triangular form of Eq. (global)):
+//   kStore  the recurrence, u * h written to the direction's fp32 plane;
+//   kEnd    the recurrence, nothing written: the caller keeps the end state;
+//   kHomog  the recurrence without the injection lam * x (only w is read):
+//           it carries a state across the blocks, h -> Phi h.
+enum PassMode { kStore, kEnd, kHomog };
+
+// One direction of one channel plane over the scan's line blocks fb0 .. fb1-1
+// (blocks of 8 lines in scan order), starting from state h (0 before the
+// first line) and leaving the state after the last one in h.  HC, WC: the
+// plane's sides when they are compile-time constants (0: taken from H, W at
+// run time); L, P: scan and line length; the x plane sits in LDS with pitch
+// (W / 2) | 1 dwords; ys receives u * h as fp32 in the direction's
+// line-major order (line l, position p at l * P + p).
+template <int NPL, bool VERT, bool REV, int HC, int WC, int MODE>
 __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, rsrc_t u, rsrc_t w,
-                                         const uint8_t *xs, u32x4 ys)
+                                         const uint8_t *xs, u32x4 ys, int fb0, int fb1,
+                                         float (&h)[NPL])
 {
     const int H = HC ? HC : H_, W = WC ? WC : W_;
     const int L = VERT ? H : W, P = VERT ? W : H;
@@ -102,17 +115,15 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
         const uint32_t so = boff(fb);
 #pragma unroll
         for (int m = 0; m < NPL; ++m) {
-            pc.l[m] = ld128_nt(lam, vo[m], so);
-            pc.u[m] = ld128_nt(u, vo[m], so);
+            if (MODE != kHomog)
+                pc.l[m] = ld128_nt(lam, vo[m], so);
+            if (MODE == kStore)
+                pc.u[m] = ld128_nt(u, vo[m], so);
             pc.w0[m] = ld128(w, vo[m], so);
             pc.w1[m] = ld128(w, vo[m], so + wplane);
             pc.w2[m] = ld128(w, vo[m], so + 2u * wplane);
         }
     };
-    float h[NPL];
-#pragma unroll
-    for (int m = 0; m < NPL; ++m)
-        h[m] = 0.f;
 
     auto run_block = [&](const Pieces<NPL> &pc, int fb) {
         // this lane's x at the block's lowest storage line: each step adds a
@@ -133,9 +144,11 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
             neighbours<NPL>(h, left, right);
 #pragma unroll
             for (int m = 0; m < NPL; ++m) {
-                const float xv = bf_lo(lds_u16(xs, xb[m] + dx));
-                const float inj = elem(pc.l[m], e, s[m].lo1, s[m].hi1) * xv;
-                float hn = inj;
+                float hn = 0.f;
+                if (MODE != kHomog) {
+                    const float xv = bf_lo(lds_u16(xs, xb[m] + dx));
+                    hn = elem(pc.l[m], e, s[m].lo1, s[m].hi1) * xv;
+                }
                 if (i > 0) {
                     hn = fmaf(elem(pc.w1[m], e, s[m].lo1, s[m].hi1), h[m], hn);
                     hn = fmaf(elem(pc.w0[m], e, s[m].lo0, s[m].hi0), left[m], hn);
@@ -143,29 +156,68 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
                 }
                 h[m] = hn;
             }
+            if (MODE == kStore) {
 #pragma unroll
-            for (int m = 0; m < NPL; ++m) {
-                // the lane's part in the address register, the line's in soffset
-                if (valid[m])
-                    st32_nt(ys, 4u * (uint32_t)lane, 4u * (uint32_t)(ln * P + 64 * m),
-                            __float_as_uint(elem(pc.u[m], e) * h[m]));
+                for (int m = 0; m < NPL; ++m) {
+                    // the lane's part in the address register, the line's in soffset
+                    if (valid[m])
+                        st32_nt(ys, 4u * (uint32_t)lane, 4u * (uint32_t)(ln * P + 64 * m),
+                                __float_as_uint(elem(pc.u[m], e) * h[m]));
+                }
             }
         }
         step_fence();
     };
 
     Pieces<NPL> A, B;
-    load(A, 0);
+    load(A, fb0);
 #pragma unroll 1
-    for (int fb = 0; fb < NB; fb += 2) {
-        if (fb + 1 < NB)
+    for (int fb = fb0; fb < fb1; fb += 2) {
+        if (fb + 1 < fb1)
             load(B, fb + 1);
         run_block(A, fb);
-        if (fb + 1 < NB) {
-            if (fb + 2 < NB)
+        if (fb + 1 < fb1) {
+            if (fb + 2 < fb1)
                 load(A, fb + 2);
             run_block(B, fb + 1);
         }
+    }
+}
+
+// Direction d's pass over blocks fb0 .. fb1-1 (direction-uniform dispatch).
+template <int NPL, int HC, int WC, int MODE>
+__device__ __forceinline__ void wide_pass(int d, int lane, int H, int W, rsrc_t rl, rsrc_t ru,
+                                          rsrc_t rw, const uint8_t *xs, u32x4 yd, int fb0,
+                                          int fb1, float (&h)[NPL])
+{
+    if (d == 0)
+        wide_dir<NPL, true, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+    else if (d == 1)
+        wide_dir<NPL, true, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+    else if (d == 2)
+        wide_dir<NPL, false, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+    else
+        wide_dir<NPL, false, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+}
+
+// x plane of channel plane pc -> LDS: coalesced 16-byte pieces into padded rows.
+template <int WC>
+__device__ __forceinline__ void stage_x_plane(const bf16_t *x, int64_t pc, int H, int W,
+                                              Magic divNq, uint32_t *xs32)
+{
+    const int64_t HW = (int64_t)H * W;
+    const int pdw = wide_pitch_dw(W);
+    const rsrc_t xr = make_rsrc(x + pc, (uint32_t)(2 * HW));
+    const int nq = W / 8;
+    const int n = H * nq;
+    for (int t = threadIdx.x; t < n; t += 256) {
+        const uint4 v = ld128(xr, 16u * (uint32_t)t, 0);
+        const int r = WC ? t / (WC / 8) : mdiv(t, divNq), q = t - r * nq;
+        uint32_t *dst = xs32 + r * pdw + 4 * q;
+        dst[0] = v.x;
+        dst[1] = v.y;
+        dst[2] = v.z;
+        dst[3] = v.w;
     }
 }
 
@@ -178,7 +230,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int H = HC ? HC : H_, W = WC ? WC : W_;
     extern __shared__ uint32_t xs32[];
     uint8_t *xs = reinterpret_cast<uint8_t *>(xs32);
-    const int pdw = wide_pitch_dw(W);
     const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
     const int blk = xcd_remap(blockIdx.x, gridDim.x);
@@ -188,21 +239,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int64_t HW = (int64_t)H * W;
     const int64_t pc = ((int64_t)b * C + c) * HW;
 
-    // x plane -> LDS: coalesced 16-byte pieces into padded rows
-    {
-        const rsrc_t xr = make_rsrc(x + pc, (uint32_t)(2 * HW));
-        const int nq = W / 8;
-        const int n = H * nq;
-        for (int t = threadIdx.x; t < n; t += 256) {
-            const uint4 v = ld128(xr, 16u * (uint32_t)t, 0);
-            const int r = WC ? t / (WC / 8) : mdiv(t, divNq), q = t - r * nq;
-            uint32_t *dst = xs32 + r * pdw + 4 * q;
-            dst[0] = v.x;
-            dst[1] = v.y;
-            dst[2] = v.z;
-            dst[3] = v.w;
-        }
-    }
+    stage_x_plane<WC>(x, pc, H, W, divNq, xs32);
     lds_barrier();
 
     if ((mask >> d) & 1) {
@@ -213,14 +250,129 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         const rsrc_t ru = make_rsrc(u + pd, (uint32_t)(2 * HW));
         const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
         const u32x4 yd = make_sdesc(ys + pd, (uint32_t)(4 * HW));
-        if (d == 0)
-            wide_dir<NPL, true, false, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
-        else if (d == 1)
-            wide_dir<NPL, true, true, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
-        else if (d == 2)
-            wide_dir<NPL, false, false, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
-        else
-            wide_dir<NPL, false, true, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
+        float h[NPL];
+#pragma unroll
+        for (int m = 0; m < NPL; ++m)
+            h[m] = 0.f;
+        const int NB = (d < 2 ? H : W) / 8;
+        wide_pass<NPL, HC, WC, kStore>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
+    }
+}
+
+// Scan-axis chunks (NEXT to the single-pass kernel when few channel planes
+// leave most CUs idle): every direction's scan is cut into K chunks of whole
+// line blocks.  By the block lower-triangular form of Eq. (global) the state
+// after chunk k from carry c is Phi_k c + e_k, with e_k the chunk's end state
+// from a zero carry and Phi_k the chunk's product of tridiagonal steps.
+//  1. fwd_wide_chunk_kernel<kEnd>: every (plane, chunk) -- e_k, stored;
+//  2. wide_carry_kernel: per plane, c_1 = e_0, c_{k+1} = Phi_k c_k + e_k, the
+//     Phi_k c_k by the recurrence without injection (w only);
+//  3. fwd_wide_chunk_kernel<kStore>: every (plane, chunk) from its carry,
+//     u * h to the fp32 direction planes; then sum_wide_kernel as usual.
+// States are fp32 [plane][direction slot][chunk][max(H, W)], the first P
+// (the direction's line length) of each slot used.
+template <int NPL, int HC, int WC, int MODE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_chunk_kernel(
+    const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
+    const bf16_t *__restrict__ u, float *__restrict__ ys, float *__restrict__ st, int mask, int B,
+    int C, int G, int H_, int W_, int K, Magic divC, Magic divCpg, Magic divNq, Magic divK)
+{
+    const int H = HC ? HC : H_, W = WC ? WC : W_;
+    extern __shared__ uint32_t xs32[];
+    uint8_t *xs = reinterpret_cast<uint8_t *>(xs32);
+    const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+    const int lane = threadIdx.x & 63;
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int plane = mdiv(blk, divK);                                 // b * C + c
+    const int k = blk - plane * K;                                     // chunk, in scan order
+    const int b = mdiv(plane, divC);
+    const int c = plane - b * C;
+    const int g = mdiv(c, divCpg);
+    const int64_t HW = (int64_t)H * W;
+    const int64_t pc = ((int64_t)b * C + c) * HW;
+    const int D = __popc(mask);
+    const int P = d < 2 ? W : H, NBc = (d < 2 ? H : W) / 8 / K;
+
+    stage_x_plane<WC>(x, pc, H, W, divNq, xs32);
+    lds_barrier();
+
+    if ((mask >> d) & 1) {
+        const int s = __popc(mask & ((1 << d) - 1));
+        const int64_t pd = (((int64_t)s * B + b) * C + c) * HW;
+        const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
+        const rsrc_t rl = make_rsrc(lam + pd, (uint32_t)(2 * HW));
+        const rsrc_t ru = make_rsrc(u + pd, (uint32_t)(2 * HW));
+        const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
+        const u32x4 yd = make_sdesc(ys + pd, (uint32_t)(4 * HW));
+        // this direction's states: chunk k's slot (every slot max(H, W) long)
+        float *sk = st + (((int64_t)plane * D + s) * K + k) * (H > W ? H : W);
+        float h[NPL];
+#pragma unroll
+        for (int m = 0; m < NPL; ++m) {
+            const int p = lane + 64 * m;
+            h[m] = (MODE == kStore && k > 0 && p < P) ? sk[p] : 0.f;
+        }
+        wide_pass<NPL, HC, WC, MODE>(d, lane, H, W, rl, ru, rw, xs, yd, k * NBc, (k + 1) * NBc,
+                                     h);
+        if (MODE == kEnd) {
+#pragma unroll
+            for (int m = 0; m < NPL; ++m) {
+                const int p = lane + 64 * m;
+                if (p < P)
+                    sk[p] = h[m];
+            }
+        }
+    }
+}
+
+// The carries: for each plane and direction, c_{k+1} = Phi_k c_k + e_k,
+// written over e_{k+1}'s slot neighbour: the state array holds e_k after
+// the first pass and c_k (k >= 1; slot 0 unused) after this one.
+template <int NPL, int HC, int WC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void wide_carry_kernel(
+    const bf16_t *__restrict__ w, float *__restrict__ st, int mask, int B, int C, int G, int H_,
+    int W_, int K, Magic divC, Magic divCpg)
+{
+    const int H = HC ? HC : H_, W = WC ? WC : W_;
+    const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int plane = xcd_remap(blockIdx.x, gridDim.x);
+    const int b = mdiv(plane, divC);
+    const int c = plane - b * C;
+    const int g = mdiv(c, divCpg);
+    const int64_t HW = (int64_t)H * W;
+    const int D = __popc(mask);
+    if (!((mask >> d) & 1))
+        return;
+    const int s = __popc(mask & ((1 << d) - 1));
+    const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
+    const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
+    const int P = d < 2 ? W : H, NBc = (d < 2 ? H : W) / 8 / K;
+    const int PM = H > W ? H : W;   // every slot is max(H, W) long
+    float *sp = st + ((int64_t)plane * D + s) * K * PM;
+    float h[NPL], e[NPL];
+    // c_1 = e_0
+#pragma unroll
+    for (int m = 0; m < NPL; ++m) {
+        const int p = lane + 64 * m;
+        h[m] = p < P ? sp[p] : 0.f;
+    }
+    for (int k = 1; k < K; ++k) {
+        // e_k is read before c_k takes its slot
+#pragma unroll
+        for (int m = 0; m < NPL; ++m) {
+            const int p = lane + 64 * m;
+            e[m] = p < P ? sp[(int64_t)k * PM + p] : 0.f;
+            if (p < P)
+                sp[(int64_t)k * PM + p] = h[m];
+        }
+        if (k + 1 < K) {
+            wide_pass<NPL, HC, WC, kHomog>(d, lane, H, W, rw, rw, rw, nullptr, u32x4{}, k * NBc,
+                                           (k + 1) * NBc, h);
+#pragma unroll
+            for (int m = 0; m < NPL; ++m)
+                h[m] += e[m];
+        }
     }
 }
 
@@ -322,7 +474,63 @@ hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds)
     return hipGetLastError();
 }
 
+// The three launches of the chunked forward (see fwd_wide_chunk_kernel).
+template <int NPL, int HC, int WC>
+hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float *states,
+                              size_t lds, int K)
+{
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e == hipSuccess)
+        e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kStore>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    const Magic divC = make_magic((uint32_t)p.C), divCpg = make_magic((uint32_t)(p.C / p.G));
+    const Magic divNq = make_magic((uint32_t)(p.W / 8)), divK = make_magic((uint32_t)K);
+    const unsigned planes = (unsigned)(p.B * p.C);
+    const bf16_t *x = (const bf16_t *)p.x, *w = (const bf16_t *)p.w;
+    const bf16_t *lam = (const bf16_t *)p.lam, *u = (const bf16_t *)p.u;
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>), dim3(planes * K), dim3(256),
+                       lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
+                       divCpg, divNq, divK);
+    hipLaunchKernelGGL((wide_carry_kernel<NPL, HC, WC>), dim3(planes), dim3(256), 0, st, w,
+                       states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC, divCpg);
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kStore>), dim3(planes * K), dim3(256),
+                       lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
+                       divCpg, divNq, divK);
+    return hipGetLastError();
+}
+
 size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
+
+// Chunks per scan for the chunked forward, or 1 for the single pass.  The
+// chunked forward does more than twice the single pass's work (both passes
+// over every line, and the carries), and its carry chain still takes every
+// line block of a scan in turn, each step bound by issue latency at one wave
+// per SIMD (about 380 cycles for the w-only step against about 890 for the
+// full one at 256 positions).  It is chosen only where it measured faster:
+// scans of at least 256 lines in both orientations, and at least 8 chunks,
+// the count doubling while B*C*K workgroups still fit the device at once and
+// every chunk keeps at least 2 line blocks.
+int wide_chunks(const Problem &p, size_t lds)
+{
+    int dev = 0, ncu = 0, lds_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess)
+        return 1;
+    const int64_t per_cu = std::max<int64_t>(1, (int64_t)lds_cu / (int64_t)std::max<size_t>(lds, 1));
+    const int64_t fit = (int64_t)ncu * std::min<int64_t>(per_cu, 8);
+    const int64_t planes = (int64_t)p.B * p.C;
+    const int nbh = p.H / 8, nbw = p.W / 8;
+    int K = 1;
+    while (K < 16 && planes * 2 * K <= fit && nbh % (2 * K) == 0 && nbw % (2 * K) == 0 &&
+           nbh / (2 * K) >= 2 && nbw / (2 * K) >= 2)
+        K *= 2;
+    return (K >= 8 && nbh >= 32 && nbw >= 32) ? K : 1;
+}
 
 }  // namespace
 
@@ -345,15 +553,28 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
 {
     const int D = __builtin_popcount(p.mask);
     const int64_t n = (int64_t)p.B * p.C * p.H * p.W;
+    const size_t lds = wide_lds_bytes(p.H, p.W);
+    const int K = wide_chunks(p, lds);
+    // fp32 direction planes, then (chunked) the chunk states
+    const int64_t nst = K > 1 ? (int64_t)p.B * p.C * D * K * std::max(p.H, p.W) : 0;
     float *ys = nullptr;
-    hipError_t e = scratch_alloc((void **)&ys, (size_t)D * n * sizeof(float), st);
+    hipError_t e = scratch_alloc((void **)&ys, (size_t)(D * n + nst) * sizeof(float), st);
     if (e != hipSuccess)
         return e;
-    const size_t lds = wide_lds_bytes(p.H, p.W);
+    float *states = ys + D * n;
     const int side = p.H > p.W ? p.H : p.W;
     const int npl = (side + 63) / 64;
     // the square planes of 256 and 128 get kernels with their shape built in
-    if (p.H == 256 && p.W == 256)
+    if (K > 1) {
+        if (p.H == 256 && p.W == 256)
+            e = fwd_wide_chunked_t<4, 256, 256>(p, st, ys, states, lds, K);
+        else if (p.H == 128 && p.W == 128)
+            e = fwd_wide_chunked_t<2, 128, 128>(p, st, ys, states, lds, K);
+        else
+            e = npl <= 2 ? fwd_wide_chunked_t<2, 0, 0>(p, st, ys, states, lds, K)
+                : npl == 3 ? fwd_wide_chunked_t<3, 0, 0>(p, st, ys, states, lds, K)
+                           : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
+    } else if (p.H == 256 && p.W == 256)
         e = fwd_wide_t<4, 256, 256>(p, st, ys, lds);
     else if (p.H == 128 && p.W == 128)
         e = fwd_wide_t<2, 128, 128>(p, st, ys, lds);

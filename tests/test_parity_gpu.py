@@ -98,6 +98,14 @@ EDGE = [
     case("wide-128x128-dirs9", 1, 6, 3, 128, 128, dirs=9, backward=False),
     case("wide-200x248-peaky", 1, 2, 1, 200, 248, sigma=2.0, backward=False),
     case("wide-96x80-R2L", 2, 4, 4, 96, 80, dirs=8),
+    case("wide-128x192-dirs6", 1, 4, 4, 128, 192, dirs=6, backward=False),
+    case("wide-256x128-dirs9-peaky", 1, 2, 1, 256, 128, dirs=9, sigma=2.0, backward=False),
+    # few channel planes of 256 x 256: the forward cuts every scan into
+    # chunks of whole line blocks, end states from zero, carries through w,
+    # then the chunks again from their carries (16, 16 and 8 chunks)
+    case("chunk-256x256-c8", 1, 8, 2, 256, 256, backward=False),
+    case("chunk-256x256-dirs6-peaky", 1, 4, 4, 256, 256, dirs=6, sigma=2.0, backward=False),
+    case("chunk8-256x256-c20-R2L", 1, 20, 4, 256, 256, dirs=8, backward=False),
     # planes of at most 16 x 16 (whole planes staged in LDS, four channels per
     # wave): idle channel slots, one channel per group, groups split into
     # chunks (fp32 partials), every size, direction subsets, peaky weights
