@@ -71,6 +71,17 @@ struct ProjArgs {
 
 __device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
 
+// 2- and 4-byte buffer stores the compiler sees, so that it keeps the stored
+// register intact until the store has read it.
+__device__ __forceinline__ void bst16(rsrc_t r, uint32_t voff, uint32_t soff, uint16_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
+}
+__device__ __forceinline__ void bst32(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t v)
+{
+    __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
+}
+
 __device__ __forceinline__ uint16_t bf16_bits(float v)
 {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
@@ -239,9 +250,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
         rb = mdiv(nt, A.div_tw);
         cb = nt - rb * A.tiles_w;
     }
-    u32x4 yd = {};
+    rsrc_t yd = make_rsrc(A.y, 0);
     if (MODE == Mode::Plain)
-        yd = make_sdesc(A.y + (int64_t)b * A.M * A.HW, (uint32_t)(2 * A.M * A.HW));
+        yd = make_rsrc(A.y + (int64_t)b * A.M * A.HW, (uint32_t)(2 * A.M * A.HW));
 #pragma unroll 1
     for (int pass = 0; pass < (fast ? 2 : 1); ++pass) {
     // this pass's pixel of lane column 32 ct + l32 and its B fragments
@@ -271,7 +282,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 #pragma unroll 1
     for (int rt = v; rt < RT; rt += 4) {
         bool is_w = false, vert = true;
-        u32x4 dd = {};
+        rsrc_t dd = make_rsrc(A.u, 0);
         if (fast) {
             const int m0 = 32 * rt;
             is_w = m0 >= 2 * A.DCc;
@@ -284,7 +295,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             const bf16_t *base =
                 is_w ? A.w + (((int64_t)sl * A.B + b) * A.Cc + c0) * 3 * HW
                      : (m0 < A.DCc ? A.u : A.lam) + (((int64_t)sl * A.B + b) * A.Cc + c0) * HW;
-            dd = make_sdesc(base, (uint32_t)(2 * (is_w ? 24 : 32) * HW));
+            dd = make_rsrc(base, (uint32_t)(2 * (is_w ? 24 : 32) * HW));
         }
         bf16x8_t af[kKS / 16];
         const bf16_t *src = a_row<MODE>(A, 32 * rt + l32);
@@ -295,6 +306,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                 af[s] = (src != nullptr && k < A.K) ? *reinterpret_cast<const bf16x8_t *>(src + k)
                                                     : bf16x8_t{};
         }
+
         f32x16_t acc[4];
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct)
@@ -319,7 +331,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                 for (int r = 0; r < 16; ++r) {
                     const int m = 32 * rt + 8 * (r >> 2) + (r & 3);
                     if (m + 4 * h < A.M)
-                        st16(yd, vo, 2u * (uint32_t)(m * A.HW), bf16_bits(acc[ct][r]));
+                        bst16(yd, vo, 2u * (uint32_t)(m * A.HW), bf16_bits(acc[ct][r]));
                 }
             } else if (!fast) {
 #pragma unroll
@@ -348,7 +360,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                         if (is_w && e == 3)
                             continue;
                         const int plane = is_w ? 6 * g + e : 8 * g + e;
-                        st16(dd, vo, 2u * (uint32_t)(plane * A.HW), bf16_bits(o[e]));
+                        bst16(dd, vo, 2u * (uint32_t)(plane * A.HW), bf16_bits(o[e]));
                     }
                 }
             }
