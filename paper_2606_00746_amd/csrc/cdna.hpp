@@ -94,21 +94,27 @@ __device__ __forceinline__ u32x4 make_sdesc(const void *p, uint32_t bytes)
     d.w = kRsrcWord3;
     return d;
 }
+// 2- and 4-byte stores go through the compiler's buffer-store builtins, so that
+// it keeps the stored register intact until the store has read it (an asm
+// store of 2 bytes lost its data to the next VALU write of that register) and
+// counts the stores in its memory-counter waits.
+__device__ __forceinline__ rsrc_t as_rsrc(const u32x4 &d)
+{
+    void *p = reinterpret_cast<void *>((static_cast<uint64_t>(d.y & 0xffffu) << 32) | d.x);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)d.z, (int)d.w);
+}
 __device__ __forceinline__ void st16(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
 {
-    asm volatile("buffer_store_short %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
-                 : "memory");
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)v, as_rsrc(d), voff, soff, 0);
 }
 __device__ __forceinline__ void st32(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
 {
-    asm volatile("buffer_store_dword %0, %1, %2, %3 offen" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
-                 : "memory");
+    __builtin_amdgcn_raw_buffer_store_b32(v, as_rsrc(d), voff, soff, 0);
 }
 // Non-temporal dword store, for waves whose lanes cover whole lines.
 __device__ __forceinline__ void st32_nt(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t v)
 {
-    asm volatile("buffer_store_dword %0, %1, %2, %3 offen nt" : : "v"(v), "v"(voff), "s"(d), "s"(soff)
-                 : "memory");
+    __builtin_amdgcn_raw_buffer_store_b32(v, as_rsrc(d), voff, soff, 2 /* nt */);
 }
 __device__ __forceinline__ void st64(const u32x4 &d, uint32_t voff, uint32_t soff, uint32_t a,
                                      uint32_t b)
