@@ -81,6 +81,11 @@ EDGE = [
     case("general-65x3", 1, 2, 1, 65, 3),
     case("general-70x100", 1, 4, 2, 70, 100),
     case("general-f32-3x130", 1, 3, 1, 3, 130, dtype="f32", gate="normal"),
+    # the largest side the library takes (4096): a single row, 4096-step
+    # scans of narrow planes
+    case("maxside-row-1x4096", 1, 2, 1, 1, 4096),
+    case("maxside-f32-4096x2", 1, 2, 2, 4096, 2, dtype="f32", gate="normal"),
+    case("maxside-4096x8-dirs9", 1, 1, 1, 4096, 8, dirs=9),
     case("peaky-48x48", 1, 8, 2, 48, 48, sigma=2.0),
     # register-streamed path (bf16, 56x56 / 64x64): direction subsets, ragged
     # channel chunks (idle waves), fewer than three waves per workgroup
