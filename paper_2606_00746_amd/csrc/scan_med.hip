@@ -284,7 +284,7 @@ __device__ __forceinline__ int pidx(int r, int c) { return r * kPlanePitch + (c 
 
 // The weight gradient of step i is sum_c a_c,i[j] h_c,i-1[j+k-1] over the
 // workgroup's channels.  Each wave writes its a_i and h_{i-1} to LDS
-// slots[buf][st][v][q][j] (v: a or h; q: channel slot, absent channels stay
+// slots[buf][st][q][j][v] (v: a or h; q: channel slot, absent channels stay
 // zero; j: position), two buffers of kBatch steps, one barrier per batch.
 // After the barrier the wave that owns step st of the batch (one per SIMD)
 // reads the 2 x kSlots values of its position, forms the three products with
@@ -294,9 +294,12 @@ constexpr int kSlots = 8;
 constexpr int kBatch = 4;
 constexpr int kSlotFloats = 2 * kBatch * 2 * kSlots * 64;
 
-__device__ __forceinline__ float *slot_ptr(float *slots, int buf, int st, int v, int q)
+// a and h of (buffer, step, channel slot q, position j) are adjacent, so a
+// wave writes both with one 8-byte LDS store and a reducer reads them with one
+// 8-byte load.
+__device__ __forceinline__ float2 *slot_pair(float *slots, int buf, int st, int q)
 {
-    return slots + (((buf * kBatch + st) * 2 + v) * kSlots + q) * 64;
+    return reinterpret_cast<float2 *>(slots + ((buf * kBatch + st) * kSlots + q) * 128);
 }
 
 struct BwdArgs {
@@ -436,8 +439,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     auto read_step = [&](int buf, int st) {
 #pragma unroll
         for (int q = 0; q < kSlots; ++q) {
-            pa[q] = slot_ptr(A.slots, buf, st, 0, q)[j];
-            ph[q] = slot_ptr(A.slots, buf, st, 1, q)[j];
+            const float2 v2 = slot_pair(A.slots, buf, st, q)[j];
+            pa[q] = v2.x;
+            ph[q] = v2.y;
         }
     };
     // step i's weight gradient: the three products summed in channel order
@@ -555,8 +559,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 // w_i couples line i-1 to line i: a_i and h_{i-1} go to the
                 // slots (h_{-1} = 0 makes line 0's gradient zero)
                 const int buf = (i >> 2) & 1;
-                slot_ptr(A.slots, buf, i & 3, 0, A.wave)[j] = a;
-                slot_ptr(A.slots, buf, i & 3, 1, A.wave)[j] = hp;
+                slot_pair(A.slots, buf, i & 3, A.wave)[j] = make_float2(a, hp);
                 if ((i & 3) == 3) {
                     lds_barrier();
                     if (IMM) {
@@ -642,8 +645,9 @@ __device__ __forceinline__ void read_slots(const BwdArgs &A, int j, int buf, int
 {
 #pragma unroll
     for (int q = 0; q < kSlots; ++q) {
-        pa[q] = slot_ptr(A.slots, buf, st, 0, q)[j];
-        ph[q] = slot_ptr(A.slots, buf, st, 1, q)[j];
+        const float2 v2 = slot_pair(A.slots, buf, st, q)[j];
+        pa[q] = v2.x;
+        ph[q] = v2.y;
     }
 }
 
@@ -663,8 +667,7 @@ __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float 
     if (!IMM && (n & 3) == 1 && n >= 5 && reducer)
         dw_store<H, W, D>(A, j, step_of(n - 5 + A.wave), pa, ph);
     const int buf = (n >> 2) & 1;
-    slot_ptr(A.slots, buf, n & 3, 0, A.wave)[j] = a;
-    slot_ptr(A.slots, buf, n & 3, 1, A.wave)[j] = hp;
+    slot_pair(A.slots, buf, n & 3, A.wave)[j] = make_float2(a, hp);
     if ((n & 3) == 3) {
         lds_barrier();
         if (IMM) {
