@@ -15,8 +15,17 @@
 // A 256 x 256 fp32 merge plane does not fit in LDS, so each direction writes
 // u_d * h_d to an fp32 plane in its own line-major order (whole lines per
 // store) and a tiled kernel sums the directions in direction-bit order,
-// transposing the horizontal ones through LDS, and stores y once.
+// transposing the horizontal ones through LDS, and stores y once.  With many
+// planes the scan goes in rounds of what fits the device at once, and each
+// round's sum runs on a side stream beside the next round's scan.
+//
+// With few channel planes the same direction pass runs on chunks of the scan
+// (fwd_wide_chunk_kernel, wide_carry_kernel): end states from zero, carries
+// through w alone, then every chunk again from its carry; wide_chunks picks
+// the chunk count from the shape.
 #include <algorithm>
+#include <mutex>
+#include <vector>
 
 #include "cdna.hpp"
 #include "device.hpp"
@@ -225,14 +234,14 @@ template <int NPL, int HC, int WC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H_,
-    int W_, Magic divC, Magic divCpg, Magic divNq)
+    int W_, Magic divC, Magic divCpg, Magic divNq, int plane0)
 {
     const int H = HC ? HC : H_, W = WC ? WC : W_;
     extern __shared__ uint32_t xs32[];
     uint8_t *xs = reinterpret_cast<uint8_t *>(xs32);
     const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
-    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int blk = plane0 + xcd_remap(blockIdx.x, gridDim.x);
     const int b = mdiv(blk, divC);
     const int c = blk - b * C;
     const int g = mdiv(c, divCpg);
@@ -259,8 +268,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     }
 }
 
-// Scan-axis chunks (NEXT to the single-pass kernel when few channel planes
-// leave most CUs idle): every direction's scan is cut into K chunks of whole
+// Scan-axis chunks, for when few channel planes leave most CUs idle under the
+// single-pass kernel: every direction's scan is cut into K chunks of whole
 // line blocks.  By the block lower-triangular form of Eq. (global) the state
 // after chunk k from carry c is Phi_k c + e_k, with e_k the chunk's end state
 // from a zero carry and Phi_k the chunk's product of tridiagonal steps.
@@ -387,12 +396,13 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
                                                        bf16_t *__restrict__ y, int mask, int B,
                                                        int C, int H, int W, int tiles_w,
                                                        int tiles_hw, Magic divTilesW,
-                                                       Magic divTilesHW, Magic divC)
+                                                       Magic divTilesHW, Magic divC, int plane0)
 {
     __shared__ float T[kTile][kTile + 1];
     const int64_t HW = (int64_t)H * W;
-    const int plane = mdiv((int)blockIdx.x, divTilesHW);              // b * C + c
-    const int local = (int)blockIdx.x - plane * tiles_hw;
+    const int pl = mdiv((int)blockIdx.x, divTilesHW);
+    const int local = (int)blockIdx.x - pl * tiles_hw;
+    const int plane = plane0 + pl;                                     // b * C + c
     const int tr = mdiv(local, divTilesW);
     const int tc = local - tr * tiles_w;
     const int R0 = tr * kTile, C0 = tc * kTile;
@@ -460,17 +470,18 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
 }
 
 template <int NPL, int HC, int WC>
-hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds)
+hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, int plane0,
+                      int nplanes)
 {
     hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)(p.B * p.C)), dim3(256), lds,
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)nplanes), dim3(256), lds,
                        st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
-                       make_magic((uint32_t)(p.W / 8)));
+                       make_magic((uint32_t)(p.W / 8)), plane0);
     return hipGetLastError();
 }
 
@@ -500,6 +511,36 @@ hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float
                        lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
                        divCpg, divNq, divK);
     return hipGetLastError();
+}
+
+// The direction sum of planes plane0 .. plane0 + nplanes - 1.
+hipError_t launch_sum_wide(const Problem &p, const float *ys, hipStream_t st, int plane0,
+                           int nplanes)
+{
+    const int tiles_w = (p.W + kTile - 1) / kTile;
+    const int tiles_h = (p.H + kTile - 1) / kTile;
+    const int64_t nblk = (int64_t)nplanes * tiles_w * tiles_h;
+    hipLaunchKernelGGL(sum_wide_kernel, dim3((unsigned)nblk), dim3(256), 0, st, ys,
+                       (bf16_t *)p.y, p.mask, p.B, p.C, p.H, p.W, tiles_w, tiles_w * tiles_h,
+                       make_magic((uint32_t)tiles_w), make_magic((uint32_t)(tiles_w * tiles_h)),
+                       make_magic((uint32_t)p.C), plane0);
+    return hipGetLastError();
+}
+
+// A non-blocking stream of default priority per device, created once, for
+// work that overlaps the caller's stream within one call.
+hipError_t side_stream(int dev, hipStream_t *out)
+{
+    static std::once_flag once[64];
+    static hipStream_t streams[64];
+    static hipError_t status[64];
+    if (dev < 0 || dev >= 64)
+        return hipErrorInvalidDevice;
+    std::call_once(once[dev], [dev] {
+        status[dev] = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
+    });
+    *out = streams[dev];
+    return status[dev];
 }
 
 size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
@@ -574,24 +615,69 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
             e = npl <= 2 ? fwd_wide_chunked_t<2, 0, 0>(p, st, ys, states, lds, K)
                 : npl == 3 ? fwd_wide_chunked_t<3, 0, 0>(p, st, ys, states, lds, K)
                            : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
-    } else if (p.H == 256 && p.W == 256)
-        e = fwd_wide_t<4, 256, 256>(p, st, ys, lds);
-    else if (p.H == 128 && p.W == 128)
-        e = fwd_wide_t<2, 128, 128>(p, st, ys, lds);
-    else
-        e = npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds)
-            : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds)
-                       : fwd_wide_t<4, 0, 0>(p, st, ys, lds);
-    if (e == hipSuccess) {
-        const int tiles_w = (p.W + kTile - 1) / kTile;
-        const int tiles_h = (p.H + kTile - 1) / kTile;
-        const int64_t nblk = (int64_t)p.B * p.C * tiles_w * tiles_h;
-        hipLaunchKernelGGL(sum_wide_kernel, dim3((unsigned)nblk), dim3(256), 0, st,
-                           (const float *)ys, (bf16_t *)p.y, p.mask, p.B, p.C, p.H, p.W, tiles_w,
-                           tiles_w * tiles_h, make_magic((uint32_t)tiles_w),
-                           make_magic((uint32_t)(tiles_w * tiles_h)), make_magic((uint32_t)p.C));
-        e = hipGetLastError();
+    } else {
+        // Single pass.  With more planes than fit the device at once, the
+        // planes go in rounds, and each round's direction sum runs on a side
+        // stream while the next round scans: the scan leaves HBM bandwidth
+        // unused, and a sum workgroup fits beside a scan workgroup on a CU.
+        // (with two rounds the extra launches cost more than the overlap gains)
+        const int planes = p.B * p.C;
+        int ncu = 0, dev = 0, lds_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  dev) != hipSuccess)
+            ncu = 0;
+        const int round = ncu * std::max(1, lds_cu / (int)std::max<size_t>(lds, 1));
+        hipStream_t side = nullptr;
+        const bool overlap = ncu > 0 && planes >= 4 * round && side_stream(dev, &side) == hipSuccess;
+        const int step = overlap ? round : planes;
+        std::vector<hipEvent_t> evs;
+        for (int p0 = 0; p0 < planes && e == hipSuccess; p0 += step) {
+            const int np = std::min(step, planes - p0);
+            if (p.H == 256 && p.W == 256)
+                e = fwd_wide_t<4, 256, 256>(p, st, ys, lds, p0, np);
+            else if (p.H == 128 && p.W == 128)
+                e = fwd_wide_t<2, 128, 128>(p, st, ys, lds, p0, np);
+            else
+                e = npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds, p0, np)
+                    : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds, p0, np)
+                               : fwd_wide_t<4, 0, 0>(p, st, ys, lds, p0, np);
+            hipStream_t ss = st;
+            if (e == hipSuccess && overlap) {
+                hipEvent_t ev;
+                e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+                if (e == hipSuccess) {
+                    evs.push_back(ev);
+                    e = hipEventRecord(ev, st);
+                }
+                if (e == hipSuccess)
+                    e = hipStreamWaitEvent(side, ev, 0);
+                ss = side;
+            }
+            if (e == hipSuccess)
+                e = launch_sum_wide(p, ys, ss, p0, np);
+        }
+        if (overlap) {
+            // the caller's stream waits for the last sum
+            hipEvent_t done;
+            hipError_t e3 = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+            if (e3 == hipSuccess) {
+                e3 = hipEventRecord(done, side);
+                if (e3 == hipSuccess)
+                    e3 = hipStreamWaitEvent(st, done, 0);
+                evs.push_back(done);
+            }
+            if (e == hipSuccess)
+                e = e3;
+            for (hipEvent_t ev : evs)
+                (void)hipEventDestroy(ev);   // released once complete
+        }
+        hipError_t e2 = scratch_free(ys, st);
+        return e != hipSuccess ? e : e2;
     }
+    if (e == hipSuccess)
+        e = launch_sum_wide(p, ys, st, 0, p.B * p.C);
     hipError_t e2 = scratch_free(ys, st);
     return e != hipSuccess ? e : e2;
 }

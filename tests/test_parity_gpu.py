@@ -175,6 +175,9 @@ def test_full_size_sampled_units(idx):
     got = run_gpu(inputs, wl, wl.backward)
     rng = np.random.default_rng(idx)
     units = {(0, 0), (wl.B - 1, wl.G - 1), (int(rng.integers(wl.B)), int(rng.integers(wl.G)))}
+    # groups spread over the planes: kernels that take the planes in rounds
+    # (the 256 x 256 forward) get a unit checked in every round
+    units |= {(0, g) for g in range(0, wl.G, max(1, wl.G // 4))}
     cpg = wl.C // wl.G
     for b, g in sorted(units):
         sl = oracle.slice_group(inputs, b, g, wl.G)
