@@ -31,6 +31,8 @@
 //    logits of w and one zero row: a lane's 4 consecutive result rows are
 //    the three logits of one pixel, normalized in registers (Sec. 3,
 //    Eq. (row_stochastic_norm)) before they are stored.
+#include <algorithm>
+
 #include "cdna.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -49,6 +51,16 @@ constexpr int kNT = 128;    // pixels of a workgroup
 constexpr int kKS = 64;     // K of one LDS stage
 constexpr int kAP = 72;     // pitch of the A block in LDS, in bf16 (16-byte aligned rows)
 constexpr float kNormEps = 1e-30f;
+// Plain products with K > 64 stage each K-row of a tile as whole 16-byte
+// pieces: the tile's 128 pixels start at byte delta (0 .. 14) of the row's
+// first piece, since a row of a map with an odd pixel count is only 2-byte
+// aligned.  17 pieces a row; each 8-row octet sits 64 bytes after the end
+// of the one before, so that a fragment's two 8-row halves fall in
+// different LDS banks.
+constexpr int kPieces = 2 * kNT / 16 + 1;
+constexpr int kRawRow = 16 * kPieces;                // bytes of a staged row
+constexpr int kRawBytes = kKS * kRawRow + 64 * (kKS / 8 - 1);
+constexpr int kRawLoads = (kKS * kPieces + 255) / 256;   // pieces per thread and stage
 
 enum class Mode { Plain, Params };
 
@@ -66,7 +78,7 @@ struct ProjArgs {
     int ntiles, mtiles, tiles_w;     // pixel tiles, row tiles, params: tiles across a row
     int Cc, DCc;                     // params: latent channels, D * Cc
     int dirs[4];                     // params: direction index of each stacked slot
-    Magic div_m, div_n, div_cc, div_tw, div_w;
+    Magic div_m, div_n, div_cc, div_tw, div_w, div_wi;
 };
 
 __device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
@@ -197,6 +209,23 @@ __device__ __forceinline__ void store_x_block(uint16_t *xs, int js, int ks0,
         const int kr = 2 * i + ks0;
         xs[kr * kNT + (js ^ ((kr & 8) << 2))] = (uint16_t)xv[i];
     }
+}
+
+// B fragment of K-step s (16 rows from 16 s) for tile pixel column jc from
+// rows staged as 16-byte pieces: row r's pixels start at byte
+// (dbase + r * dstep) mod 16 of its first piece.
+__device__ __forceinline__ bf16x8_t b_fragment_raw(const uint16_t *xs, int s, int h, int jc,
+                                                   uint32_t dbase, uint32_t dstep)
+{
+    bf16x8_t bf;
+    const uint8_t *xr = reinterpret_cast<const uint8_t *>(xs) + (16 * s + 8 * h) * kRawRow +
+                        64 * (2 * s + h) + 2 * jc;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const uint32_t d = (dbase + (uint32_t)(16 * s + 8 * h + i) * dstep) & 15u;
+        bf[i] = *reinterpret_cast<const __bf16 *>(xr + i * kRawRow + d);
+    }
+    return bf;
 }
 
 // B fragment of K-step s (16 rows from 16 s) for tile pixel column jc.
@@ -372,7 +401,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
 template <Mode MODE>
 __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
 {
-    __shared__ __attribute__((aligned(16))) uint16_t xs[kKS * kNT];
+    // plain products: tiles of 128 consecutive input pixels, K-rows staged
+    // as whole 16-byte pieces (the parameter product keeps 2-byte loads)
+    constexpr bool RAW = MODE == Mode::Plain;
+    __shared__ __attribute__((aligned(16))) uint16_t xs[RAW ? kRawBytes / 2 : kKS * kNT];
     __shared__ __attribute__((aligned(16))) uint16_t as[kMT * kAP];
 
     const int t = threadIdx.x;
@@ -389,8 +421,27 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
     // this thread's staging pixel and A pieces (the same in every stage)
     const int js = t & (kNT - 1), ks0 = t >> 7;
     int srow, scol, spix;
-    const int sopix = tile_pixel<MODE>(A, nt, js, srow, scol, spix);
-    const rsrc_t xr = make_rsrc(A.x + (int64_t)b * A.K * A.HWi, (uint32_t)(2 * A.K * A.HWi));
+    int sopix;
+    if constexpr (RAW) {
+        // input pixel n of the tile -> output pixel (grids share their
+        // top-left corner; -1: not on the output grid)
+        const int n = nt * kNT + js;
+        sopix = n < A.HWi ? n : -1;
+        if (A.remap && sopix >= 0) {
+            const int r = mdiv(n, A.div_wi), c = n - r * A.Wi;
+            sopix = (r < A.H && c < A.W) ? r * A.W + c : -1;
+        }
+        spix = 0;
+    } else {
+        sopix = tile_pixel<MODE>(A, nt, js, srow, scol, spix);
+    }
+    const bf16_t *ximg = A.x + (int64_t)b * A.K * A.HWi;
+    // RAW: the image's pieces counted from its base rounded down to 16 bytes
+    const uint32_t d0 = RAW ? (uint32_t)(reinterpret_cast<uintptr_t>(ximg) & 15u) : 0u;
+    const rsrc_t xr = make_rsrc(reinterpret_cast<const uint8_t *>(ximg) - d0,
+                                (d0 + (uint32_t)(2 * A.K * A.HWi) + 15u) & ~15u);
+    const uint32_t p0b = d0 + 2u * (uint32_t)(nt * kNT);          // byte of the tile's pixel 0, row 0
+    const uint32_t rowb = 2u * (uint32_t)A.HWi;                     // bytes per K-row
     const bf16_t *asrc[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -405,6 +456,31 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
                         : make_uint4(0, 0, 0, 0);
         }
     };
+    // RAW: piece q = t + 256 i of a stage is piece q % 17 of K-row q / 17;
+    // a piece holds only bytes of its own 16-byte block, which lies in one
+    // page with the row byte it was taken for, so no read leaves the map's
+    // pages (pieces past the image read as 0, past the tile they are unused)
+    auto load_raw = [&](int kc, uint4 (&rv)[kRawLoads]) {
+#pragma unroll
+        for (int i = 0; i < kRawLoads; ++i) {
+            const int q = t + 256 * i;
+            const int kr = q / kPieces, pc = q - kr * kPieces;
+            const int k = kc + kr;
+            rv[i] = (q < kKS * kPieces && k < A.K)
+                        ? ld128(xr, ((p0b + (uint32_t)k * rowb) & ~15u) + 16u * (uint32_t)pc, 0)
+                        : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto store_raw = [&](const uint4 (&rv)[kRawLoads]) {
+#pragma unroll
+        for (int i = 0; i < kRawLoads; ++i) {
+            const int q = t + 256 * i;
+            const int kr = q / kPieces, pc = q - kr * kPieces;
+            if (q < kKS * kPieces)
+                *reinterpret_cast<uint4 *>(reinterpret_cast<uint8_t *>(xs) + kr * kRawRow +
+                                           64 * (kr >> 3) + 16 * pc) = rv[i];
+        }
+    };
 
     f32x16_t acc[2];
 #pragma unroll
@@ -413,13 +489,21 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
         for (int r = 0; r < 16; ++r)
             acc[rt][r] = 0.f;
 
-    uint32_t xv[kKS / 2];
+    uint32_t xv[RAW ? 1 : kKS / 2];
+    uint4 rv[RAW ? kRawLoads : 1];
     uint4 av[2];
-    load_x_block(xr, A.K, A.HWi, 0, ks0, spix, xv);
+    if constexpr (RAW)
+        load_raw(0, rv);
+    else
+        load_x_block(xr, A.K, A.HWi, 0, ks0, spix, xv);
     load_a(0, av);
+    const uint32_t dstep = rowb & 15u;
     for (int kc = 0; kc < A.K; kc += kKS) {
         __syncthreads();   // the previous stage's fragments are read
-        store_x_block(xs, js, ks0, xv);
+        if constexpr (RAW)
+            store_raw(rv);
+        else
+            store_x_block(xs, js, ks0, xv);
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
             const int p = t + 256 * i;
@@ -427,12 +511,17 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
         }
         __syncthreads();
         if (kc + kKS < A.K) {   // the next stage's loads overlap this stage's products
-            load_x_block(xr, A.K, A.HWi, kc + kKS, ks0, spix, xv);
+            if constexpr (RAW)
+                load_raw(kc + kKS, rv);
+            else
+                load_x_block(xr, A.K, A.HWi, kc + kKS, ks0, spix, xv);
             load_a(kc + kKS, av);
         }
+        const uint32_t dbase = (p0b + (uint32_t)kc * rowb) & 15u;
 #pragma unroll
         for (int s = 0; s < kKS / 16; ++s) {
-            const bf16x8_t bf = b_fragment(xs, s, h, 32 * v + l32);
+            const bf16x8_t bf = RAW ? b_fragment_raw(xs, s, h, 32 * v + l32, dbase, dstep)
+                                    : b_fragment(xs, s, h, 32 * v + l32);
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 const bf16x8_t af =
@@ -474,14 +563,52 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
     }
 }
 
+// Output pixels (r, c) with r >= Hi or c >= Wi of every plane of an H x W
+// output grid: 0.
+__global__ __launch_bounds__(256) void zero_margin_kernel(bf16_t *y, int planes, int H, int W,
+                                                          int Hi, int Wi)
+{
+    const int hi = min(H, Hi), wi = min(W, Wi);
+    const int per = H * W - hi * wi;          // margin pixels of a plane
+    const int side = hi * (W - wi);           // right of the rows that have input
+    const int64_t n = (int64_t)planes * per;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t pl = o / per;
+        int q = (int)(o - pl * per), r, c;
+        if (q < side) {
+            r = q / (W - wi);
+            c = wi + (q - r * (W - wi));
+        } else {
+            q -= side;
+            r = hi + q / W;
+            c = q - (r - hi) * W;
+        }
+        y[pl * H * W + (int64_t)r * W + c] = 0;
+    }
+}
+
 template <Mode MODE>
 hipError_t launch_proj(ProjArgs &A, hipStream_t st)
 {
-    A.div_n = make_magic((uint32_t)A.ntiles);
     if (A.K <= kKS) {
+        A.div_n = make_magic((uint32_t)A.ntiles);
         const int64_t nblk = (int64_t)A.B * A.ntiles;
         hipLaunchKernelGGL(proj_rows_kernel<MODE>, dim3((unsigned)nblk), dim3(256), 0, st, A);
     } else {
+        if (MODE == Mode::Plain) {
+            // the stage kernel tiles the input pixels; output pixels with no
+            // input pixel (the margin of a larger output grid) are zeroed
+            A.ntiles = (A.HWi + kNT - 1) / kNT;
+            if (A.H > A.Hi || A.W > A.Wi) {
+                const int64_t per = (int64_t)A.H * A.W - (int64_t)std::min(A.H, A.Hi) * std::min(A.W, A.Wi);
+                const int64_t n = (int64_t)A.B * A.M * per;
+                const int64_t nb = std::min<int64_t>((n + 255) / 256, 4096);
+                hipLaunchKernelGGL(zero_margin_kernel, dim3((unsigned)nb), dim3(256), 0, st, A.y,
+                                   A.B * A.M, A.H, A.W, A.Hi, A.Wi);
+            }
+        }
+        A.div_n = make_magic((uint32_t)A.ntiles);
         A.mtiles = (A.M + kMT - 1) / kMT;
         A.div_m = make_magic((uint32_t)A.mtiles);
         const int64_t nblk = (int64_t)A.B * A.ntiles * A.mtiles;
@@ -503,6 +630,7 @@ hipError_t launch_project(const void *a, const void *x, void *y, int B, int M, i
     A.Hi = Hi > 0 ? Hi : H, A.Wi = Wi > 0 ? Wi : W, A.HWi = A.Hi * A.Wi;
     A.remap = A.Hi != H || A.Wi != W;
     A.div_w = make_magic((uint32_t)W);
+    A.div_wi = make_magic((uint32_t)A.Wi);
     A.ntiles = (A.HW + kNT - 1) / kNT;
     return launch_proj<Mode::Plain>(A, st);
 }

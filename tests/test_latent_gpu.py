@@ -44,6 +44,10 @@ PROJECT_CASES = [
     (1, 1152, 64, 12, 12),
     (3, 128, 136, 16, 8),
     (1, 64, 1152, 37, 37),
+    # K > 64, not a multiple of 64, with K-rows at every 2-byte offset from
+    # 16-byte alignment (H * W odd): the stage kernel's 16-byte pieces
+    (3, 40, 104, 7, 9),
+    (2, 17, 200, 5, 5),
 ]
 
 
