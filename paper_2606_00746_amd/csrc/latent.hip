@@ -83,15 +83,11 @@ struct ProjArgs {
 
 __device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
 
-// 2- and 4-byte buffer stores the compiler sees, so that it keeps the stored
+// 2-byte buffer store the compiler sees, so that it keeps the stored
 // register intact until the store has read it.
 __device__ __forceinline__ void bst16(rsrc_t r, uint32_t voff, uint32_t soff, uint16_t v)
 {
     __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
-}
-__device__ __forceinline__ void bst32(rsrc_t r, uint32_t voff, uint32_t soff, uint32_t v)
-{
-    __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
 }
 
 __device__ __forceinline__ uint16_t bf16_bits(float v)
@@ -274,11 +270,6 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
     // of one line, adjacent), so that the 32 lanes of a store write 64
     // contiguous bytes.
     const bool fast = MODE == Mode::Params && A.Cc % 32 == 0;
-    int rb = 0, cb = 0;
-    if (MODE == Mode::Params) {
-        rb = mdiv(nt, A.div_tw);
-        cb = nt - rb * A.tiles_w;
-    }
     rsrc_t yd = make_rsrc(A.y, 0);
     if (MODE == Mode::Plain)
         yd = make_rsrc(A.y + (int64_t)b * A.M * A.HW, (uint32_t)(2 * A.M * A.HW));

@@ -929,7 +929,6 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     // wave's LDS dx plane (still unused), coalesced; their dx terms collect in
     // registers (this lane's row) and move into the dx plane afterwards.
     const bool horiz = (mask & 12) != 0;
-    const bool vert = (mask & 3) != 0;
     const uint8_t *stg = reinterpret_cast<const uint8_t *>(A.Xq);
     if (horiz) {
         uint32_t *st = reinterpret_cast<uint32_t *>(A.Xq);
