@@ -5,10 +5,12 @@ Kernel-trace summary (per-kernel call count and durations)::
     python -m paper_2606_00746_amd.profiling trace RESULTS_DB OUT.txt --command "..."
 
 HBM traffic record from two counter runs of ``bench.py --copy-calibration MIB``,
-one collecting ``FETCH_SIZE`` and one ``WRITE_SIZE`` (KiB per dispatch)::
+one collecting ``FETCH_SIZE`` and one ``WRITE_SIZE`` (KiB per dispatch), each
+making CALLS calls of the forward and of the backward (``--warmup 1 --steps 2``:
+3)::
 
     python -m paper_2606_00746_amd.profiling traffic FETCH_CSV WRITE_CSV OUT.json \\
-        --workload NAME --copy-mib MIB --command "..."
+        --workload NAME --copy-mib MIB --calls CALLS --command "..."
 
 Each counter is scaled by what it reads for the plain copy of known size that
 the same run makes, so the record holds bytes.  The record carries a hash of
@@ -118,7 +120,10 @@ def _counter(path: str) -> dict:
 
 
 def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
-                   command: str) -> dict:
+                   command: str, calls: int = 3) -> dict:
+    """Bytes per call of the library: every dispatch of its kernels counted,
+    divided by the number of calls the run made (a call may dispatch a kernel
+    several times, e.g. one scan per round of planes)."""
     fetch, write = _counter(fetch_csv), _counter(write_csv)
     copy = [k for k in fetch if short_name(k) == COPY_KERNEL]
     if not copy:
@@ -132,7 +137,7 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
     f_copy = fetch[copy[0]][at] * 1024.0
     w_copy = wl[at] * 1024.0
     scale_f, scale_w = copy_bytes / f_copy, copy_bytes / w_copy
-    kernels, calls = {}, collections.defaultdict(float)
+    kernels, per_call = {}, collections.defaultdict(float)
     for k, v in fetch.items():
         call = call_of(k)
         if call is None:
@@ -140,15 +145,16 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
         fb = sum(v) / len(v) * 1024.0 * scale_f
         wb = sum(write[k]) / len(write[k]) * 1024.0 * scale_w
         kernels[short_name(k)] = {"call": call, "fetch_bytes": round(fb), "write_bytes": round(wb),
-                                  "dispatches": len(v)}
-        calls[call] += fb + wb
+                                  "dispatches": len(v), "dispatches_per_call": len(v) / calls}
+        per_call[call] += (fb + wb) * len(v) / calls
     return {"workload": workload, "source_hash": source_hash(sorted(kernels)),
             "source_files": [os.path.basename(f) for f in source_files(sorted(kernels))],
             "command": command,
             "copy_calibration": {"bytes": copy_bytes, "fetch_kib": f_copy / 1024.0,
                                  "write_kib": w_copy / 1024.0, "fetch_scale": scale_f,
                                  "write_scale": scale_w},
-            "kernels": kernels, "bytes_per_call": {k: round(v) for k, v in calls.items()}}
+            "calls": calls, "kernels": kernels,
+            "bytes_per_call": {k: round(v) for k, v in per_call.items()}}
 
 
 WAVE_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
@@ -216,6 +222,8 @@ def main(argv=None) -> int:
     c.add_argument("out")
     c.add_argument("--workload", required=True)
     c.add_argument("--copy-mib", type=int, required=True)
+    c.add_argument("--calls", type=int, default=3,
+                   help="calls of each kind in the counter runs (warmup + steps)")
     c.add_argument("--command", required=True)
     v = sub.add_parser("waves")
     v.add_argument("csv")
@@ -227,7 +235,7 @@ def main(argv=None) -> int:
     elif a.cmd == "waves":
         sys.stdout.write(waves_summary(a.csv, a.out, a.command))
     else:
-        rec = traffic_record(a.fetch_csv, a.write_csv, a.workload, a.copy_mib, a.command)
+        rec = traffic_record(a.fetch_csv, a.write_csv, a.workload, a.copy_mib, a.command, a.calls)
         with open(a.out, "w") as f:
             json.dump(rec, f, indent=1)
             f.write("\n")

@@ -25,11 +25,13 @@ def test_traffic_record_scales_by_copy(tmp_path):
     dws = "void gspn::(anonymous namespace)::dw_sum_kernel<64>(int)"
     # a small upload copy first, then the 4 MiB calibration copy: its counter
     # reads half the bytes for FETCH_SIZE and all of them for WRITE_SIZE
+    # two calls of each kind
     _csv(tmp_path / "f.csv", "FETCH_SIZE", [(copy, 1.0), (copy, 2048.0), (fwd, 100.0), (bwd, 300.0),
-                                           (dws, 50.0), (fwd, 100.0)])
+                                           (dws, 50.0), (fwd, 100.0), (bwd, 300.0), (dws, 50.0)])
     _csv(tmp_path / "w.csv", "WRITE_SIZE", [(copy, 2.0), (copy, 4096.0), (fwd, 10.0), (bwd, 200.0),
-                                           (dws, 5.0), (fwd, 10.0)])
-    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd")
+                                           (dws, 5.0), (fwd, 10.0), (bwd, 200.0), (dws, 5.0)])
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd",
+                                   calls=2)
     assert rec["copy_calibration"]["fetch_scale"] == 2.0
     assert rec["copy_calibration"]["write_scale"] == 1.0
     assert rec["kernels"]["fwd_med_kernel<64, 64>"]["fetch_bytes"] == 200 * 1024
@@ -39,6 +41,22 @@ def test_traffic_record_scales_by_copy(tmp_path):
     # the record depends on its kernels' family and the shared sources only
     assert "scan_med.hip" in rec["source_files"] and "api.cpp" in rec["source_files"]
     assert "scan_wide.hip" not in rec["source_files"]
+
+
+def test_traffic_counts_every_dispatch_of_a_call(tmp_path):
+    # a call that runs its scan and its direction sum in 4 rounds: 3 calls,
+    # 12 dispatches of each kernel
+    copy = "__amd_rocclr_copyBuffer(char const*, char*)"
+    scan = "void gspn::(anonymous namespace)::fwd_wide_kernel<4, 256, 256>(int)"
+    summ = "void gspn::(anonymous namespace)::sum_wide_kernel(float)"
+    rows_f = [(copy, 512.0)] + [(scan, 100.0), (summ, 40.0)] * 12
+    rows_w = [(copy, 1024.0)] + [(scan, 80.0), (summ, 8.0)] * 12
+    _csv(tmp_path / "f.csv", "FETCH_SIZE", rows_f)
+    _csv(tmp_path / "w.csv", "WRITE_SIZE", rows_w)
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 1, "cmd",
+                                   calls=3)
+    assert rec["kernels"]["sum_wide_kernel"]["dispatches_per_call"] == 4
+    assert rec["bytes_per_call"]["fwd"] == 4 * (200 + 80 + 80 + 8) * 1024
 
 
 def test_traffic_ignored_for_other_sources(tmp_path):
