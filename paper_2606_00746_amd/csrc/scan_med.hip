@@ -287,19 +287,23 @@ __device__ __forceinline__ int pidx(int r, int c) { return r * kPlanePitch + (c 
 // slots[buf][st][q][j][v] (v: a or h; q: channel slot, absent channels stay
 // zero; j: position), two buffers of kBatch steps, one barrier per batch.
 // After the barrier the wave that owns step st of the batch (one per SIMD)
-// reads the 2 x kSlots values of its position, forms the three products with
+// reads the 2 x NS values of its position, forms the three products with
 // the neighbours' h from adjacent lanes (DPP), sums them in channel order
 // and stores the line while the next batch runs.
-constexpr int kSlots = 8;
+// NS channel slots per step: 8, or 4 where two 4-channel workgroups per CU
+// keep more waves busy than one of up to 8 channels (the slot area shrinks
+// with NS).
+constexpr int kSlots = 8;                  // the most channels of a workgroup
 constexpr int kBatch = 4;
-constexpr int kSlotFloats = 2 * kBatch * 2 * kSlots * 64;
+constexpr int slot_floats(int ns) { return 2 * kBatch * 2 * ns * 64; }
 
 // a and h of (buffer, step, channel slot q, position j) are adjacent, so a
 // wave writes both with one 8-byte LDS store and a reducer reads them with one
 // 8-byte load.
+template <int NS>
 __device__ __forceinline__ float2 *slot_pair(float *slots, int buf, int st, int q)
 {
-    return reinterpret_cast<float2 *>(slots + ((buf * kBatch + st) * kSlots + q) * 128);
+    return reinterpret_cast<float2 *>(slots + ((buf * kBatch + st) * NS + q) * 128);
 }
 
 struct BwdArgs {
@@ -321,7 +325,7 @@ struct BwdArgs {
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM, bool PC = false>
+template <int H, int W, int D, bool IMM, bool PC, int NS>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
@@ -435,11 +439,11 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     // Reduction roles: step st of a batch belongs to wave st (waves 0..3, one
     // per SIMD); with fewer than kBatch waves (IMM) each wave takes several
     // steps and reduces them right after the barrier.
-    float pa[kSlots], ph[kSlots];
+    float pa[NS], ph[NS];
     auto read_step = [&](int buf, int st) {
 #pragma unroll
-        for (int q = 0; q < kSlots; ++q) {
-            const float2 v2 = slot_pair(A.slots, buf, st, q)[j];
+        for (int q = 0; q < NS; ++q) {
+            const float2 v2 = slot_pair<NS>(A.slots, buf, st, q)[j];
             pa[q] = v2.x;
             ph[q] = v2.y;
         }
@@ -448,7 +452,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     auto reduce_step = [&](int i) {
         float d0 = 0.f, d1 = 0.f, d2 = 0.f;
 #pragma unroll
-        for (int q = 0; q < kSlots; ++q) {
+        for (int q = 0; q < NS; ++q) {
             d0 = fmac_left(d0, ph[q], pa[q]);
             d1 = fmaf(pa[q], ph[q], d1);
             d2 = fmac_right(d2, ph[q], pa[q]);
@@ -562,7 +566,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 // w_i couples line i-1 to line i: a_i and h_{i-1} go to the
                 // slots (h_{-1} = 0 makes line 0's gradient zero)
                 const int buf = (i >> 2) & 1;
-                slot_pair(A.slots, buf, i & 3, A.wave)[j] = make_float2(a, hp);
+                slot_pair<NS>(A.slots, buf, i & 3, A.wave)[j] = make_float2(a, hp);
                 if ((i & 3) == 3) {
                     lds_barrier();
                     if (IMM) {
@@ -614,14 +618,14 @@ struct BwdDir {
 };
 
 // The weight-gradient sum of step i from the slot values read for it.
-template <int H, int W, int D>
-__device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const float (&pa)[kSlots],
-                                         const float (&ph)[kSlots])
+template <int H, int W, int D, int NS>
+__device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const float (&pa)[NS],
+                                         const float (&ph)[NS])
 {
     using F = BwdDir<H, W, D>;
     float d0 = 0.f, d1 = 0.f, d2 = 0.f;
 #pragma unroll
-    for (int q = 0; q < kSlots; ++q) {
+    for (int q = 0; q < NS; ++q) {
         d0 = fmac_left(d0, ph[q], pa[q]);
         d1 = fmaf(pa[q], ph[q], d1);
         d2 = fmac_right(d2, ph[q], pa[q]);
@@ -644,12 +648,13 @@ __device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const f
     }
 }
 
+template <int NS>
 __device__ __forceinline__ void read_slots(const BwdArgs &A, int j, int buf, int st,
-                                           float (&pa)[kSlots], float (&ph)[kSlots])
+                                           float (&pa)[NS], float (&ph)[NS])
 {
 #pragma unroll
-    for (int q = 0; q < kSlots; ++q) {
-        const float2 v2 = slot_pair(A.slots, buf, st, q)[j];
+    for (int q = 0; q < NS; ++q) {
+        const float2 v2 = slot_pair<NS>(A.slots, buf, st, q)[j];
         pa[q] = v2.x;
         ph[q] = v2.y;
     }
@@ -661,36 +666,36 @@ __device__ __forceinline__ void read_slots(const BwdArgs &A, int j, int buf, int
 // issues the batch's slot reads after the barrier and finishes the sum 1.5
 // steps later; with fewer than kBatch waves (IMM) each wave takes several
 // steps and sums them right after the barrier.
-template <int H, int W, int D, bool IMM, class StepOf>
+template <int H, int W, int D, bool IMM, int NS, class StepOf>
 __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float a, float hp,
-                                          float (&pa)[kSlots], float (&ph)[kSlots], StepOf step_of)
+                                          float (&pa)[NS], float (&ph)[NS], StepOf step_of)
 {
     const bool reducer = A.wave < kBatch;
     // finish the previous batch: its slot reads were issued after the last
     // barrier and overlapped a step of arithmetic
     if (!IMM && (n & 3) == 1 && n >= 5 && reducer)
-        dw_store<H, W, D>(A, j, step_of(n - 5 + A.wave), pa, ph);
+        dw_store<H, W, D, NS>(A, j, step_of(n - 5 + A.wave), pa, ph);
     const int buf = (n >> 2) & 1;
-    slot_pair(A.slots, buf, n & 3, A.wave)[j] = make_float2(a, hp);
+    slot_pair<NS>(A.slots, buf, n & 3, A.wave)[j] = make_float2(a, hp);
     if ((n & 3) == 3) {
         lds_barrier();
         if (IMM) {
             for (int st = A.wave; st < kBatch; st += A.cw) {
-                read_slots(A, j, buf, st, pa, ph);
-                dw_store<H, W, D>(A, j, step_of(n - 3 + st), pa, ph);
+                read_slots<NS>(A, j, buf, st, pa, ph);
+                dw_store<H, W, D, NS>(A, j, step_of(n - 3 + st), pa, ph);
             }
         } else if (reducer) {
-            read_slots(A, j, buf, A.wave, pa, ph);
+            read_slots<NS>(A, j, buf, A.wave, pa, ph);
         }
     }
 }
 
-template <int H, int W, int D, bool IMM, class StepOf>
-__device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float (&pa)[kSlots],
-                                            const float (&ph)[kSlots], StepOf step_of)
+template <int H, int W, int D, bool IMM, int NS, class StepOf>
+__device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float (&pa)[NS],
+                                            const float (&ph)[NS], StepOf step_of)
 {
     if (!IMM && A.wave < kBatch)
-        dw_store<H, W, D>(A, j, step_of(BwdDir<H, W, D>::L - 4 + A.wave), pa, ph);
+        dw_store<H, W, D, NS>(A, j, step_of(BwdDir<H, W, D>::L - 4 + A.wave), pa, ph);
 }
 
 // One horizontal direction of the backward without the adjoint history, for
@@ -702,7 +707,7 @@ __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float
 // reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
 // second read of lam and w (the first one leaves them in L2) and one more h
 // recurrence per step.
-template <int H, int W, int D, bool IMM, bool PC = false>
+template <int H, int W, int D, bool IMM, bool PC, int NS>
 __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                            float (&dxa)[64])
 {
@@ -758,7 +763,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
     }
 
     // --- reverse pass by blocks -------------------------------------------
-    float pa[kSlots], ph[kSlots];
+    float pa[NS], ph[NS];
     // the n-th step of this pass is step L-1-n
     auto step_of = [](int n) { return L - 1 - n; };
     uint4 rl[NB], ru[NB], p0[NB], p1[NB], p2[NB];
@@ -849,7 +854,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
                         dwp[k][e >> 1] = REV ? pack2(dw1[k], dv[k]) : pack2(dv[k], dw1[k]);
                 }
             } else {
-                slot_step<H, W, D, IMM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
+                slot_step<H, W, D, IMM, NS>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
             }
             if (t == 0 && act) {
                 st128_nt(A.du, vo, F::boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
@@ -865,14 +870,14 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
         }
     }
     if constexpr (!PC)
-        slot_finish<H, W, D, IMM>(A, j, pa, ph, step_of);
+        slot_finish<H, W, D, IMM, NS>(A, j, pa, ph, step_of);
 #undef BLOAD
 }
 
 // PC: one channel per weight group; a workgroup then takes cw consecutive
 // channels (groups), each wave sums nothing with the others, and nchunk /
 // divChunk count the workgroups per batch.
-template <int H, int W, bool IMM, bool PC>
+template <int H, int W, bool IMM, bool PC, int NS>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -917,7 +922,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.slots = smem + cw * XPLANE;
     // slots of channels this workgroup does not have must read as zero
     if (!PC) {
-        for (int t = threadIdx.x; t < kSlotFloats; t += blockDim.x)
+        for (int t = threadIdx.x; t < slot_floats(NS); t += blockDim.x)
             A.slots[t] = 0.f;
     }
     lds_barrier();
@@ -976,15 +981,15 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM, PC>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC, NS>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
         if ((mask & 4) && H >= 64)
-            dir_bwd_ck<H, W, 3, IMM, PC>(A, lane, cvalid, stg, dxr);
+            dir_bwd_ck<H, W, 3, IMM, PC, NS>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM, PC>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC, NS>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
@@ -997,13 +1002,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC, NS>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM, PC>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM, PC, NS>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -1069,16 +1074,16 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W, bool IMM, bool PC = false>
+template <int H, int W, bool IMM, bool PC, int NS>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
     const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC>), dim3(grid),
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -1099,7 +1104,6 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     if (e != hipSuccess)
         return e;
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
-    const size_t slots = (size_t)kSlotFloats * 4;                   // per-step dw terms
     const int cpg = p.C / p.G;
     if (cpg == 1) {
         // one channel per group: workgroups of up to kSlots channels, no slots
@@ -1107,15 +1111,53 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         const int nct = (p.C + cw - 1) / cw;
         if ((size_t)cw * per_ch > (size_t)lds_max)
             return hipErrorInvalidConfiguration;
-        return bwd_med_launch<H, W, false, true>(p, st, cw, nct, (size_t)cw * per_ch, nullptr);
+        return bwd_med_launch<H, W, false, true, kSlots>(p, st, cw, nct, (size_t)cw * per_ch,
+                                                         nullptr);
     }
-    int cap = lds_max > (int)slots ? (int)(((size_t)lds_max - slots) / per_ch) : 0;
-    cap = cap < kSlots ? cap : kSlots;
-    if (cap < 1)
+    // A group's channels in nchunk workgroups of cw channels, NS slots per
+    // step.  NS = 4 (at most 4 channels, a smaller slot area) is taken where
+    // it puts more waves on a CU than NS = 8 for at most one more chunk, e.g.
+    // 56 x 56 with 12 channels per group: two 4-wave workgroups per CU (8
+    // waves, 2 per SIMD) instead of one of 6 waves.
+    struct Plan {
+        int nchunk = 0, cw = 0;
+        size_t lds = 0;
+    };
+    auto plan = [&](int ns) {
+        Plan q;
+        const size_t sl = (size_t)slot_floats(ns) * 4;
+        int cap = lds_max > (int)sl ? (int)(((size_t)lds_max - sl) / per_ch) : 0;
+        cap = cap < ns ? cap : ns;
+        if (cap >= 1) {
+            q.nchunk = (cpg + cap - 1) / cap;
+            q.cw = (cpg + q.nchunk - 1) / q.nchunk;
+            q.lds = (size_t)q.cw * per_ch + sl;
+        }
+        return q;
+    };
+    const Plan p8 = plan(kSlots), p4 = plan(4);
+    if (p8.nchunk < 1)
         return hipErrorInvalidConfiguration;
-    const int nchunk = (cpg + cap - 1) / cap;
-    const int cw = (cpg + nchunk - 1) / nchunk;
-    const size_t lds = (size_t)cw * per_ch + slots;
+    bool use4 = false;
+    if (p4.nchunk >= 1 && p4.cw == 4 && p4.nchunk <= p8.nchunk + 1) {
+        int lds_cu = 0;
+        if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
+                                  dev) != hipSuccess || lds_cu < lds_max)
+            lds_cu = lds_max;
+        hipFuncAttributes fa;
+        if (hipFuncGetAttributes(&fa, (const void *)bwd_med_kernel<H, W, false, false, 4>) ==
+                hipSuccess && fa.numRegs > 0) {
+            const int per_simd = 512 / ((fa.numRegs + 7) / 8 * 8);   // waves a SIMD holds
+            auto waves = [&](const Plan &q) {
+                const int by_lds = (int)((size_t)lds_cu / q.lds) * q.cw;
+                return by_lds < 4 * per_simd ? by_lds : 4 * per_simd;
+            };
+            use4 = waves(p4) > waves(p8);
+        }
+    }
+    const Plan &pl = use4 ? p4 : p8;
+    const int nchunk = pl.nchunk, cw = pl.cw;
+    const size_t lds = pl.lds;
     const int D = __builtin_popcount(p.mask);
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * H * W;
 
@@ -1125,8 +1167,11 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         if (e != hipSuccess)
             return e;
     }
-    e = cw >= kBatch ? bwd_med_launch<H, W, false>(p, st, cw, nchunk, lds, dwp)
-                     : bwd_med_launch<H, W, true>(p, st, cw, nchunk, lds, dwp);
+    if (use4)
+        e = bwd_med_launch<H, W, false, false, 4>(p, st, cw, nchunk, lds, dwp);
+    else
+        e = cw >= kBatch ? bwd_med_launch<H, W, false, false, kSlots>(p, st, cw, nchunk, lds, dwp)
+                         : bwd_med_launch<H, W, true, false, kSlots>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
