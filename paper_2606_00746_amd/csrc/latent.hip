@@ -555,27 +555,24 @@ __global__ __launch_bounds__(256) void proj_stage_kernel(ProjArgs A)
 }
 
 // Output pixels (r, c) with r >= Hi or c >= Wi of every plane of an H x W
-// output grid: 0.
-__global__ __launch_bounds__(256) void zero_margin_kernel(bf16_t *y, int planes, int H, int W,
-                                                          int Hi, int Wi)
+// output grid: 0.  blockIdx.x is the plane; the blocks along y stride over
+// its margin pixels.
+__global__ __launch_bounds__(256) void zero_margin_kernel(bf16_t *y, int H, int W, int Hi, int Wi)
 {
     const int hi = min(H, Hi), wi = min(W, Wi);
     const int per = H * W - hi * wi;          // margin pixels of a plane
     const int side = hi * (W - wi);           // right of the rows that have input
-    const int64_t n = (int64_t)planes * per;
-    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
-         o += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t pl = o / per;
-        int q = (int)(o - pl * per), r, c;
+    bf16_t *plane = y + (int64_t)blockIdx.x * H * W;
+    for (int q = blockIdx.y * blockDim.x + threadIdx.x; q < per; q += gridDim.y * blockDim.x) {
+        int r, c;
         if (q < side) {
             r = q / (W - wi);
             c = wi + (q - r * (W - wi));
         } else {
-            q -= side;
-            r = hi + q / W;
-            c = q - (r - hi) * W;
+            r = hi + (q - side) / W;
+            c = (q - side) - (r - hi) * W;
         }
-        y[pl * H * W + (int64_t)r * W + c] = 0;
+        plane[r * W + c] = 0;
     }
 }
 
@@ -592,11 +589,10 @@ hipError_t launch_proj(ProjArgs &A, hipStream_t st)
             // input pixel (the margin of a larger output grid) are zeroed
             A.ntiles = (A.HWi + kNT - 1) / kNT;
             if (A.H > A.Hi || A.W > A.Wi) {
-                const int64_t per = (int64_t)A.H * A.W - (int64_t)std::min(A.H, A.Hi) * std::min(A.W, A.Wi);
-                const int64_t n = (int64_t)A.B * A.M * per;
-                const int64_t nb = std::min<int64_t>((n + 255) / 256, 4096);
-                hipLaunchKernelGGL(zero_margin_kernel, dim3((unsigned)nb), dim3(256), 0, st, A.y,
-                                   A.B * A.M, A.H, A.W, A.Hi, A.Wi);
+                const int per = A.H * A.W - std::min(A.H, A.Hi) * std::min(A.W, A.Wi);
+                hipLaunchKernelGGL(zero_margin_kernel,
+                                   dim3((unsigned)(A.B * A.M), (unsigned)std::min((per + 255) / 256, 256)),
+                                   dim3(256), 0, st, A.y, A.H, A.W, A.Hi, A.Wi);
             }
         }
         A.div_n = make_magic((uint32_t)A.ntiles);
