@@ -130,6 +130,11 @@ EDGE = [
     case("med32-peaky-R2L", 1, 8, 1, 32, 32, dirs=8, sigma=2.0),
     case("med64-G=C-3ch-dirs9", 2, 3, 3, 64, 64, dirs=9),
     case("med56-G=C-dirs6", 2, 12, 12, 56, 56, dirs=6),
+    # shapes whose backward takes 4 slots per step (two 4-channel workgroups
+    # per CU): 3 chunks of 4, one chunk of 4 (no partials), a direction subset
+    case("med48-ns4-cpg12", 1, 24, 2, 48, 48),
+    case("med64-ns4-cpg4", 2, 16, 4, 64, 64),
+    case("med40-ns4-cpg12-dirs6", 1, 12, 1, 40, 40, dirs=6),
 ]
 
 
