@@ -2,14 +2,17 @@
 """Benchmark of the 4-direction GSPN line scan (forward + backward) on one MI355X.
 
 One step = gspn_scan_fwd + gspn_scan_bwd over one batch of the workload, with
-every input already resident in HBM.  Prints ONE JSON line on stdout:
+every input already resident in HBM, every tensor pixel-major as the C ABI's
+plain entry points take them; the same step through the _blocked entry
+points (per-direction tensors in their scan order) is timed beside it and
+reported under "blocked".  Prints ONE JSON line on stdout:
 throughput in G pixel-channels per second (B*C*H*W per step), the roofline
 of the dominant kernel (algorithmic bytes / average launch time, from HIP
 events on the launch stream) and the CPU oracle timed on a bounded sample of
 the same workload.  Diagnostics go to stderr.
 
     python bench.py [--steps K] [--warmup W] [--workload IDX|NAME|all] [--no-cpu-baseline]
-                    [--norm] [--latent IDX|NAME|all]
+                    [--layout pixel|blocked] [--no-blocked] [--norm] [--latent IDX|NAME|all]
 
 Before every step, outside the timed events, reading a 1 GiB buffer evicts
 the L2s and the 256 MB Infinity Cache (writing back what the previous step
@@ -82,52 +85,74 @@ def _cpu_model() -> str:
 
 
 def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool = False,
-                 threads: int = 1) -> dict:
+                 threads: int = 1, runs: int = 3) -> dict:
     """The fp64 oracle on (batch, group) units of the workload.
 
-    Units run in a fixed order until `min_seconds` have passed or the whole
-    workload is done; a workload shorter than that is run again (whole passes
-    only) so the timed region reaches about `min_seconds`.  With threads > 1
-    the units are spread over that many threads (the oracle's C calls release
-    the interpreter lock, so they run side by side).
+    `runs` runs, each over the same sample of units: all their forward passes
+    (spread over `threads` threads; the oracle's C calls release the
+    interpreter lock, so they run side by side), then all their backward
+    passes, each phase timed on its own.  The sample is sized so that the runs
+    take about `min_seconds` in all.  Reported: the median over the runs of
+    the throughput (B*C*H*W of the sample over forward + backward time) and
+    the medians of the two phases.
     """
     import concurrent.futures as cf
 
     import oracle
     cpg = wl.C // wl.G
     order = [(b, g) for g in range(wl.G) for b in range(wl.B)]
+    slices = {}
 
-    def unit(bg):
-        b, g = bg
-        sl = oracle.slice_group(inputs, b, g, wl.G)
-        w = oracle.normalize_w(sl["w"], wl.dirs) if norm else sl["w"]
-        oracle.scan_fwd(sl["x"], w, sl["lam"], sl["u"], wl.dirs)
-        if wl.backward:
-            r = oracle.scan_bwd(sl["x"], w, sl["lam"], sl["u"], sl["dy"], wl.dirs)
-            if norm:
-                oracle.normalize_w_bwd(sl["w"], r["dw"], wl.dirs)
+    def sl(bg):
+        if bg not in slices:
+            b, g = bg
+            s_ = oracle.slice_group(inputs, b, g, wl.G)
+            s_["wn"] = oracle.normalize_w(s_["w"], wl.dirs) if norm else s_["w"]
+            slices[bg] = s_
+        return slices[bg]
 
-    done = 0
-    passes = 0
-    t0 = time.perf_counter()
+    def fwd(bg):
+        s_ = sl(bg)
+        oracle.scan_fwd(s_["x"], s_["wn"], s_["lam"], s_["u"], wl.dirs)
+
+    def bwd(bg):
+        s_ = sl(bg)
+        r = oracle.scan_bwd(s_["x"], s_["wn"], s_["lam"], s_["u"], s_["dy"], wl.dirs)
+        if norm:
+            oracle.normalize_w_bwd(s_["w"], r["dw"], wl.dirs)
+
+    def phase(ex, fn, units):
+        t0 = time.perf_counter()
+        list(ex.map(fn, units))
+        return time.perf_counter() - t0
+
     with cf.ThreadPoolExecutor(max_workers=threads) as ex:
-        while True:
-            for k in range(0, len(order), threads):
-                list(ex.map(unit, order[k:k + threads]))
-                done += len(order[k:k + threads])
-                if passes == 0 and time.perf_counter() - t0 >= min_seconds:
-                    break
-            passes += 1
-            if time.perf_counter() - t0 >= min_seconds:
-                break
-    dt = time.perf_counter() - t0
-    pixch = done * cpg * wl.H * wl.W
+        # size the sample: one unit per thread, timed once, sets the count
+        probe = order[:threads]
+        for bg in probe:
+            sl(bg)
+        t1 = phase(ex, fwd, probe) + (phase(ex, bwd, probe) if wl.backward else 0.0)
+        per_round = max(t1, 1e-6)
+        rounds = max(1, int(min_seconds / runs / per_round))
+        units = [order[k % len(order)] for k in range(rounds * threads)]
+        for bg in units:
+            sl(bg)
+        tf, tb = [], []
+        for _ in range(runs):
+            tf.append(phase(ex, fwd, units))
+            tb.append(phase(ex, bwd, units) if wl.backward else 0.0)
+    pixch = len(units) * cpg * wl.H * wl.W
+    rates = sorted(pixch / (f + b) / 1e9 for f, b in zip(tf, tb))
     how = "single thread" if threads == 1 else f"{threads} threads"
-    return {"value": round(pixch / dt / 1e9, 6), "unit": "Gpix·ch/s", "cores": threads,
+    med = lambda v: float(sorted(v)[len(v) // 2])     # noqa: E731
+    return {"value": round(rates[len(rates) // 2], 6), "unit": "Gpix·ch/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{done} (batch, group) units of {wl.name} ({wl.B * wl.G} per step; "
-                      f"{done * cpg} channel planes, {'fwd+bwd' if wl.backward else 'fwd'}, "
-                      f"fp64, {how}, {_cpu_model()}), {dt:.1f} s"}
+            "fwd_s": round(med(tf), 4), "bwd_s": round(med(tb), 4), "runs": runs,
+            "host_nproc": os.cpu_count(),
+            "sample": f"{len(units)} (batch, group) units of {wl.name} ({wl.B * wl.G} per step; "
+                      f"{len(units) * cpg} channel planes), fwd then bwd, each timed, median of "
+                      f"{runs} runs, fp64, {how} of {os.cpu_count()} host CPUs ({_cpu_model()}), "
+                      f"{sum(tf) + sum(tb):.1f} s"}
 
 
 def timed_copy(nbytes: int, reps: int, flush, torch) -> float:
@@ -157,9 +182,23 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         # the weights as logits: the calls form the row-stochastic weights
         inputs["w"] = gi.make_logits(wl)
     log(f"inputs generated in {time.perf_counter() - t0:.1f} s")
-    dev = {k: to_device(v, wl.dtype, torch)
-           for k, v in gi.inputs_line_major(inputs, wl.dirs).items()}
+    stream = torch.cuda.current_stream()
+    scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
+             if args.flush_mib > 0 else None)
+    main = time_step(wl, inputs, args, torch, gspn, args.layout, scrub, stream)
+    other = None
+    if not args.norm and not args.no_blocked:
+        other = time_step(wl, inputs, args, torch, gspn,
+                          gspn.BLOCKED if args.layout == gspn.PIXEL else gspn.PIXEL, scrub, stream)
+    return summarize(wl, inputs, args, torch, main, other, scrub)
+
+
+def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream) -> dict:
+    """Event times of K steps with the per-direction tensors in `layout`."""
+    host = gi.inputs_line_major(inputs, wl.dirs) if layout == gspn.BLOCKED else inputs
+    dev = {k: to_device(v, wl.dtype, torch) for k, v in host.items()}
     x, w, lam, u = dev["x"], dev["w"], dev["lam"], dev["u"]
+    kw = {} if args.norm else {"layout": layout}
     fwd_call = gspn.scan_fwd_norm if args.norm else gspn.scan_fwd
     bwd_call = gspn.scan_bwd_norm if args.norm else gspn.scan_bwd
     y = torch.empty_like(x)
@@ -167,9 +206,13 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         dy = dev["dy"]
         grads = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                  torch.empty_like(u))
-    stream = torch.cuda.current_stream()
-    scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
-             if args.flush_mib > 0 else None)
+    # the calls' workspace, taken once (a caller that keeps it allocates nothing per call)
+    ops = ((gspn.OP_FWD_NORM, gspn.OP_BWD_NORM) if args.norm else
+           (gspn.OP_FWD, gspn.OP_BWD) if layout == gspn.PIXEL else
+           (gspn.OP_FWD_BLOCKED, gspn.OP_BWD_BLOCKED))
+    nws = max(gspn.workspace_size(op, x, w, wl.dirs) for op in ops)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
+    log(f"layout {layout}: workspace {nws} bytes")
 
     def flush():
         # read, not write: the caches end up holding clean lines, so the timed
@@ -181,11 +224,11 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         flush()
         if ev is not None:
             ev[0].record(stream)
-        fwd_call(x, w, lam, u, wl.dirs, y=y, stream=stream)
+        fwd_call(x, w, lam, u, wl.dirs, y=y, stream=stream, workspace=ws, **kw)
         if ev is not None:
             ev[1].record(stream)
         if wl.backward:
-            bwd_call(x, w, lam, u, dy, wl.dirs, out=grads, stream=stream)
+            bwd_call(x, w, lam, u, dy, wl.dirs, out=grads, stream=stream, workspace=ws, **kw)
         if ev is not None:
             ev[2].record(stream)
 
@@ -212,9 +255,26 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
 
     fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in events]))
     bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in events])) if wl.backward else 0.0
+    fwd_med = float(np.median([e[0].elapsed_time(e[1]) for e in events]))
+    bwd_med = (float(np.median([e[1].elapsed_time(e[2]) for e in events]))
+               if wl.backward else 0.0)
     # with flushing, the step is the two calls (the flush between steps is not
     # part of it); without, the wall clock over the K steps
     ms_per_step = fwd_ms + bwd_ms if scrub is not None else elapsed * 1e3 / args.steps
+    del dev, x, w, lam, u, y, ws
+    if wl.backward:
+        del dy, grads
+    return {"layout": layout, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms, "fwd_median_ms": fwd_med,
+            "bwd_median_ms": bwd_med, "ms_per_step": ms_per_step}
+
+
+def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
+    fwd_ms, bwd_ms, ms_per_step = main["fwd_ms"], main["bwd_ms"], main["ms_per_step"]
+
+    def flush():
+        if scrub is not None:
+            scrub.sum()
+
     pixch = wl.pixels_channels
     value = pixch / (ms_per_step * 1e-3) / 1e9
     nbytes = algorithmic_bytes(wl)
@@ -232,7 +292,7 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     # plain copy), kept in profiles/ for the current kernel sources only
     from paper_2606_00746_amd import profiling
     traffic = None if args.norm else profiling.load_traffic(
-        os.path.join(ROOT, "profiles", f"traffic_{wl.name}.txt"), call)
+        os.path.join(ROOT, "profiles", f"traffic_{wl.name}-{args.layout}.txt"), call)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
@@ -265,24 +325,38 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
         "config": {"workload": wl.name, "B": wl.B, "C": wl.C, "G": wl.G, "H": wl.H, "W": wl.W,
                    "directions": wl.ndirs, "pass": "fwd+bwd" if wl.backward else "fwd",
                    "storage": wl.dtype, "weights": "logits" if args.norm else "normalized",
+                   "layout": ("pixel-major [D][B][C][H][W] / [D][B][G][3][H][W]"
+                              if args.layout == "pixel" else "blocked line-major"),
                    "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
+        "fwd_median_ms": round(main["fwd_median_ms"], 5),
+        "bwd_median_ms": round(main["bwd_median_ms"], 5),
         "cache_flush_mib": args.flush_mib,
         "step_hbm_gbs_algorithmic": round(step_gbs, 1),
         "step_hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "roofline": roofline,
         "copy_probe": probe,
     }
+    if other is not None:
+        o_ms = other["ms_per_step"]
+        out[other["layout"]] = {
+            "value": round(pixch / (o_ms * 1e-3) / 1e9, 3), "ms_per_step": round(o_ms, 5),
+            "fwd_ms": round(other["fwd_ms"], 5), "bwd_ms": round(other["bwd_ms"], 5),
+            "step_hbm_frac": round((nbytes["fwd"] + nbytes["bwd"]) / (o_ms * 1e-3) / 1e9
+                                   / HBM_PEAK_GBS, 4)}
+        log(f"{other['layout']} layout: fwd {other['fwd_ms']:.4f} ms  bwd {other['bwd_ms']:.4f} ms"
+            f"  step {o_ms:.4f} ms")
     if not args.no_cpu_baseline:
-        log("timing the CPU oracle ...")
-        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm)
-        # the same on the host's cores (at most 16, the CPU share of one GPU)
-        nthr = min(16, os.cpu_count() or 1)
-        if nthr > 1:
-            log(f"timing the CPU oracle on {nthr} threads ...")
-            out["cpu_baseline_threads"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm,
-                                                       threads=nthr)
+        # the oracle on all of the host's cores (the reported baseline), and
+        # on one thread beside it
+        nthr = os.cpu_count() or 1
+        log(f"timing the CPU oracle on {nthr} threads ...")
+        out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm,
+                                           threads=nthr)
+        log("timing the CPU oracle on one thread ...")
+        out["cpu_baseline_single_thread"] = cpu_baseline(wl, inputs, args.cpu_seconds / 2,
+                                                         args.norm)
     return out
 
 
@@ -366,7 +440,7 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
         "params": lambda: gspn.latent_params(xcp, dev["l_u"], dev["l_lam"], dev["l_w"], lw.dirs,
                                              out=prm, stream=stream),
         "scan": lambda: gspn.scan_fwd(xcp, prm[2], prm[1], prm[0], lw.dirs, y=ycp,
-                                      stream=stream),
+                                      stream=stream, layout=gspn.BLOCKED),
         "up": lambda: gspn.project(dev["p_up"], yc, y=y, stream=stream),
     }
 
@@ -441,6 +515,10 @@ def main() -> int:
     ap.add_argument("--workload", default="3",
                     help="index or name of the workload, or 'all' (one line each)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layout", default="pixel", choices=("pixel", "blocked"),
+                    help="layout of the per-direction tensors of the reported step")
+    ap.add_argument("--no-blocked", action="store_true",
+                    help="do not time the other layout beside the reported one")
     ap.add_argument("--norm", action="store_true",
                     help="weights given as logits: time gspn_scan_fwd_norm / gspn_scan_bwd_norm")
     ap.add_argument("--latent", default=None,

@@ -26,12 +26,16 @@
  * type (round to nearest even) once, when stored.
  *
  * Layouts.  D = number of directions in the mask; per-direction tensors are
- * stacked in increasing direction-bit order.  Shared tensors are pixel-major:
+ * stacked in increasing direction-bit order.  The entry points without a
+ * suffix take every tensor pixel-major (row-major images):
  *   x, y, dy, dx           [B][C][H][W]          element (r, c) at r*W + c
- * Per-direction tensors are blocked line-major: the lines a direction scans
- * (storage rows for vertical scans, storage columns for horizontal ones) are
- * grouped in blocks of 8 consecutive lines, and inside a block the 8 values
- * of one line position are adjacent:
+ *   lam, u, dlam, du       [D][B][C][H][W]
+ *   w, dw                  [D][B][G][3][H][W]    tap k of pixel (r, c)
+ * The _blocked entry points take the per-direction tensors in the order in
+ * which their direction scans them ("blocked line-major"): the lines a
+ * direction scans (storage rows for vertical scans, storage columns for
+ * horizontal ones) are grouped in blocks of 8 consecutive lines, and inside a
+ * block the 8 values of one line position are adjacent:
  *   lam, u, dlam, du       [D][B][C][plane]
  *   w, dw                  [D][B][G][3][plane]
  *   plane of L lines of P positions, line l, position p at
@@ -41,20 +45,31 @@
  *   horizontal direction (L2R, R2L):  line = column c, position = row r,
  *                                     L = W, P = H
  * (the last block holds L%8 lines when L is not a multiple of 8; a plane
- * has exactly H*W elements).  A producer (for instance the 1x1 convolutions
- * that predict lam, u and w) can write this layout directly.
+ * has exactly H*W elements).  A producer of lam, u and w (for instance the
+ * 1x1 convolutions that predict them) can write this layout directly; the
+ * kernels then read every stream with whole-line accesses.  x, y, dy and dx
+ * are pixel-major in both.
  *
  * Ownership and threading: all pointers are device pointers owned by the
- * caller; the library keeps none of them after a call returns.  Outputs are
- * fully overwritten (never accumulated into); inputs are never written.
- * Buffers of one call must not overlap.  Every base pointer must be 16-byte
- * aligned.  Calls are asynchronous on `stream` (a hipStream_t; NULL is the
- * null stream) and never synchronise the device.  gspn_scan_bwd and the
- * _norm entry points may take stream-ordered scratch memory from the
- * device's default memory pool, and so may gspn_scan_fwd for planes with a
- * side above 64, and gspn_latent_fwd; it is released on the same stream.
- * The library sets that pool to keep released memory for reuse rather than
- * return it to the device.  Calls are thread-safe.
+ * caller; the library keeps none of them after a call returns, allocates no
+ * memory and holds no state between calls.  Outputs are fully overwritten
+ * (never accumulated into); inputs are never written.  Buffers of one call
+ * must not overlap.  Every base pointer must be 16-byte aligned.  Calls are
+ * asynchronous on `stream` (a hipStream_t; NULL is the null stream), launch
+ * only on that stream and never synchronise the device.  Calls are
+ * thread-safe.
+ *
+ * Workspace: some shapes need device memory beyond their inputs and outputs
+ * (partial sums of a weight group split over several workgroups, per-direction
+ * fp32 planes of long lines, the normalized weights of the _norm entry points,
+ * the latent tensors of gspn_latent_fwd).  The caller provides it:
+ * gspn_workspace_size (gspn_latent_workspace_size) gives the bytes a call
+ * takes for its sizes; the call takes `workspace` (16-byte aligned, not
+ * overlapping any other buffer of the call; may be NULL when the size is 0)
+ * and its size `workspace_bytes`, and returns GSPN_ERR_WORKSPACE when it is
+ * smaller than needed.  The workspace's contents on entry do not matter and
+ * are undefined after the call; calls that share a workspace must not run
+ * concurrently.
  *
  * Errors: every argument check runs on the host before any HIP call, so an
  * invalid call has no effect on the device.  A failed HIP call returns
@@ -90,27 +105,47 @@ extern "C" {
 #define GSPN_ERR_ALIAS (-6)       /* two buffers of the call overlap            */
 #define GSPN_ERR_UNSUPPORTED (-7) /* H or W > GSPN_MAX_SIDE, or too many elements */
 #define GSPN_ERR_HIP (-8)         /* a HIP runtime call or launch failed        */
+#define GSPN_ERR_WORKSPACE (-9)   /* workspace missing or smaller than needed   */
+
+/* Operations, for gspn_workspace_size. */
+#define GSPN_OP_FWD 0
+#define GSPN_OP_BWD 1
+#define GSPN_OP_FWD_NORM 2
+#define GSPN_OP_BWD_NORM 3
+#define GSPN_OP_FWD_BLOCKED 4
+#define GSPN_OP_BWD_BLOCKED 5
 
 /* Largest supported H and W, and largest B*C*H*W and B*G*H*W*3*D. */
 #define GSPN_MAX_SIDE 4096
 #define GSPN_MAX_ELEMS (((int64_t)1) << 40)
 
 /*
+ * Bytes of workspace that operation `op` (GSPN_OP_*) takes for these sizes,
+ * in *bytes (0 for most shapes).  The same argument checks as the call; the
+ * plan of a call is the same for every call with these sizes on one device.
+ * Needs the current device (GSPN_ERR_HIP without one).
+ */
+int gspn_workspace_size(int op, int direction, int B, int C, int G, int H, int W, int dtype,
+                        int64_t *bytes);
+
+/*
  * Forward pass (Sec. 3, Eqs. (gspn_recurrence) and (gspn_output)).
  *   x    [B][C][H][W]        input feature map
- *   w    [D][B][G][3][plane] neighbour weights (normalised, e.g. row-stochastic)
- *   lam  [D][B][C][plane]    input scaling lambda_d
- *   u    [D][B][C][plane]    output gate u_d
+ *   w    [D][B][G][3][H][W]  neighbour weights (normalised, e.g. row-stochastic)
+ *   lam  [D][B][C][H][W]     input scaling lambda_d
+ *   u    [D][B][C][H][W]     output gate u_d
  *   y    [B][C][H][W]        out: sum over directions of u_d * h_d
  *   direction  bitmask of GSPN_T2B | GSPN_B2T | GSPN_L2R | GSPN_R2L
  *   G          weight groups; channel c uses group c / (C/G); C % G == 0
+ *              (G = 1 is Eq. (2dsp) of Sec. 4.2, G = C Eq. (gspn_recurrence))
  *   dtype      GSPN_F32 or GSPN_BF16 (all tensors)
+ *   workspace, workspace_bytes   see "Workspace" above
  *   stream     hipStream_t to launch on
  * Returns GSPN_OK or a negative status.
  */
 int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u,
                   void *y, int direction, int B, int C, int G, int H, int W,
-                  int dtype, void *stream);
+                  int dtype, void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * Backward pass: gradients of a loss l(y) given dy = dl/dy.  The backward of
@@ -122,27 +157,41 @@ int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u,
  * h is recomputed on the GPU; nothing is saved by the forward pass.
  *   dy   [B][C][H][W]        in: gradient of the merged output y
  *   dx   [B][C][H][W]        out
- *   dw   [D][B][G][3][plane] out
- *   dlam [D][B][C][plane]    out
- *   du   [D][B][C][plane]    out
+ *   dw   [D][B][G][3][H][W]  out
+ *   dlam [D][B][C][H][W]     out
+ *   du   [D][B][C][H][W]     out
  * Other arguments as in gspn_scan_fwd.
  */
 int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
                   const void *dy, void *dx, void *dw, void *dlam, void *du,
                   int direction, int B, int C, int G, int H, int W, int dtype,
-                  void *stream);
+                  void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
- * The two passes with the weights given by their logits wt, laid out like w:
- * Sec. 3, Eq. (row_stochastic_norm) forms
+ * gspn_scan_fwd and gspn_scan_bwd with lam, u, w, dlam, du and dw in the
+ * blocked line-major layout (see "Layouts" above), for producers that write
+ * the per-direction tensors in their scan order.  Same operation, arguments,
+ * checks and errors.
+ */
+int gspn_scan_fwd_blocked(const void *x, const void *w, const void *lam, const void *u,
+                          void *y, int direction, int B, int C, int G, int H, int W,
+                          int dtype, void *workspace, int64_t workspace_bytes, void *stream);
+int gspn_scan_bwd_blocked(const void *x, const void *w, const void *lam, const void *u,
+                          const void *dy, void *dx, void *dw, void *dlam, void *du,
+                          int direction, int B, int C, int G, int H, int W, int dtype,
+                          void *workspace, int64_t workspace_bytes, void *stream);
+
+/*
+ * The two passes with the weights given by their logits wt, laid out like w
+ * (pixel-major): Sec. 3, Eq. (row_stochastic_norm) forms
  *   w(j,k) = sigma(wt(j,k)) / max(sum_{k' in N(j)} sigma(wt(j,k')), 1e-30)
  * with sigma the logistic sigmoid and N(j) the taps whose neighbour lies on
  * the grid (the others get weight 0; the clamp is a reading, the paper names
  * no constant).  Taps outside N(j) may hold any value.  The weights are
  * formed once per group and pixel, in fp32, and stored in the storage type in
- * stream-ordered scratch memory for the scan.
- *   w_logits   [D][B][G][3][plane]   in
- *   dw_logits  [D][B][G][3][plane]   out (backward): dl/dwt, from dl/dw by
+ * the workspace for the scan.
+ *   w_logits   [D][B][G][3][H][W]   in
+ *   dw_logits  [D][B][G][3][H][W]   out (backward): dl/dwt, from dl/dw by
  *       dl/dwt_m = sigma(wt_m)(1 - sigma(wt_m)) (dw_m - sum_k w_k dw_k) / S
  *     on N(j) (S the clamped sum), 0 elsewhere; dl/dw passes through the
  *     storage type on the way.
@@ -150,12 +199,14 @@ int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
  */
 int gspn_scan_fwd_norm(const void *x, const void *w_logits, const void *lam,
                        const void *u, void *y, int direction, int B, int C,
-                       int G, int H, int W, int dtype, void *stream);
+                       int G, int H, int W, int dtype, void *workspace,
+                       int64_t workspace_bytes, void *stream);
 
 int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
                        const void *u, const void *dy, void *dx, void *dw_logits,
                        void *dlam, void *du, int direction, int B, int C, int G,
-                       int H, int W, int dtype, void *stream);
+                       int H, int W, int dtype, void *workspace,
+                       int64_t workspace_bytes, void *stream);
 
 /*
  * Latent-space propagation sublayer of C-GSPN (Sec. 5, Eqs. (latent_down),
@@ -174,8 +225,8 @@ int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
  * projections here are linear without bias.  Storage is bf16 only
  * (dtype GSPN_BF16; GSPN_F32 is GSPN_ERR_UNSUPPORTED); products accumulate in
  * fp32 on the matrix cores.  x_c, u, lam, w and y_c are stored in bf16
- * between the stages (stream-ordered scratch memory, released on the same
- * stream); the logits wt are normalized in registers and never stored.
+ * between the stages, in the workspace (gspn_latent_workspace_size gives its
+ * size); the logits wt are normalized in registers and never stored.
  * Weight layouts (row-major, output channel first):
  *   p_down [Cc][C]      l_u, l_lam [D][Cc][Cc]      l_w [D][Cc][3][Cc]
  *   p_up   [C][Cc]      (row (c, k) of l_w gives the logit of tap k of
@@ -183,10 +234,12 @@ int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
  * C and Cc must be multiples of 8 (GSPN_ERR_UNSUPPORTED otherwise).  Other
  * arguments, checks and errors as in gspn_scan_fwd.
  */
+int gspn_latent_workspace_size(int direction, int B, int C, int Cc, int H, int W,
+                               int dtype, int64_t *bytes);
 int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
                     const void *l_lam, const void *l_w, const void *p_up, void *y,
                     int direction, int B, int C, int Cc, int H, int W, int dtype,
-                    void *stream);
+                    void *workspace, int64_t workspace_bytes, void *stream);
 /*
  * The two kinds of stage of gspn_latent_fwd, for callers that keep the
  * latent tensors themselves.
@@ -194,7 +247,8 @@ int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
  * (latent_down) and (latent_up), y[b] = a x[b]:
  *   a [M][K], x [B][K][H][W], y [B][M][H][W]; K a multiple of 8; bf16.
  * gspn_latent_params: Eq. (latent_params) with the weights normalized as in
- * Eq. (row_stochastic_norm), written in the scan's layouts (G = Cc):
+ * Eq. (row_stochastic_norm), written in the blocked line-major layout of
+ * gspn_scan_fwd_blocked (G = Cc):
  *   xc [B][Cc][H][W] in; u, lam [D][B][Cc][plane], w [D][B][Cc][3][plane] out;
  *   Cc a multiple of 8; bf16.
  */

@@ -5,15 +5,20 @@ h_i = w_i h_{i-1} + lambda_i * x_i with output y = sum_d u_d * h_d over four
 scan directions, forward and backward, as hand-written HIP kernels for gfx950
 behind a C ABI (``include/gspn.h``).  This package is the ctypes binding.
 """
-from ._native import (ALL, B2T, BF16, F32, L2R, LIB_PATH, R2L, T2B, GspnError, gspn_last_hip_error,
-                      gspn_latent_fwd, gspn_latent_params, gspn_project, gspn_scan_bwd,
-                      gspn_scan_bwd_norm, gspn_scan_fwd, gspn_scan_fwd_norm, gspn_strerror,
-                      gspn_version, latent_fwd, latent_params, load, project, scan_bwd,
-                      scan_bwd_norm, scan_fwd, scan_fwd_norm, to_line_major, from_line_major)
+from ._native import (ALL, B2T, BF16, BLOCKED, F32, L2R, LIB_PATH, OP_BWD, OP_BWD_BLOCKED,
+                      OP_BWD_NORM, OP_FWD, OP_FWD_BLOCKED, OP_FWD_NORM, PIXEL, R2L, T2B,
+                      GspnError, gspn_last_hip_error, gspn_latent_fwd, gspn_latent_params,
+                      gspn_latent_workspace_size, gspn_project, gspn_scan_bwd,
+                      gspn_scan_bwd_blocked, gspn_scan_bwd_norm, gspn_scan_fwd,
+                      gspn_scan_fwd_blocked, gspn_scan_fwd_norm, gspn_strerror, gspn_version,
+                      gspn_workspace_size, latent_fwd, latent_params, load, project, scan_bwd,
+                      scan_bwd_norm, scan_fwd, scan_fwd_norm, workspace_size)
 
-__all__ = ["ALL", "B2T", "BF16", "F32", "L2R", "LIB_PATH", "R2L", "T2B", "GspnError",
-           "gspn_last_hip_error", "gspn_latent_fwd", "gspn_latent_params", "gspn_project",
-           "gspn_scan_bwd", "gspn_scan_bwd_norm", "gspn_scan_fwd", "gspn_scan_fwd_norm",
-           "gspn_strerror", "gspn_version", "latent_fwd", "latent_params", "load", "project",
-           "scan_bwd", "scan_bwd_norm", "scan_fwd", "scan_fwd_norm", "to_line_major",
-           "from_line_major"]
+__all__ = ["ALL", "B2T", "BF16", "BLOCKED", "F32", "L2R", "LIB_PATH", "OP_BWD", "OP_BWD_BLOCKED",
+           "OP_BWD_NORM", "OP_FWD", "OP_FWD_BLOCKED", "OP_FWD_NORM", "PIXEL", "R2L", "T2B",
+           "GspnError", "gspn_last_hip_error", "gspn_latent_fwd", "gspn_latent_params",
+           "gspn_latent_workspace_size", "gspn_project", "gspn_scan_bwd", "gspn_scan_bwd_blocked",
+           "gspn_scan_bwd_norm", "gspn_scan_fwd", "gspn_scan_fwd_blocked", "gspn_scan_fwd_norm",
+           "gspn_strerror", "gspn_version", "gspn_workspace_size", "latent_fwd", "latent_params",
+           "load", "project", "scan_bwd", "scan_bwd_norm", "scan_fwd", "scan_fwd_norm",
+           "workspace_size"]

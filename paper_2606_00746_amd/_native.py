@@ -1,10 +1,12 @@
 """ctypes binding of libgspn (argument marshalling only).
 
 The raw functions keep the C names and signatures of ``include/gspn.h``.
-``scan_fwd`` / ``scan_bwd`` take torch tensors, derive the sizes from their
-shapes, and raise :class:`GspnError` on a non-zero status.  Every step of the
-scan runs in the library's HIP kernels; there is no other code path, and
-loading fails loudly when the library is missing.
+The torch front end (``scan_fwd``, ``scan_bwd``, ...) takes device tensors,
+checks their sizes, dtypes and devices, derives the sizes from the shapes,
+asks the library how much workspace the call needs and hands it a torch
+buffer of that size, and raises :class:`GspnError` on a non-zero status.
+Every step of the scan runs in the library's HIP kernels; there is no other
+code path, and loading fails loudly when the library is missing.
 """
 from __future__ import annotations
 
@@ -16,12 +18,17 @@ LIB_PATH = os.path.join(_HERE, "libgspn.so")
 
 T2B, B2T, L2R, R2L, ALL = 1, 2, 4, 8, 15
 F32, BF16 = 0, 1
-OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUPPORTED, ERR_HIP = (
-    0, -1, -2, -3, -4, -5, -6, -7, -8)
+(OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUPPORTED, ERR_HIP,
+ ERR_WORKSPACE) = (0, -1, -2, -3, -4, -5, -6, -7, -8, -9)
+OP_FWD, OP_BWD, OP_FWD_NORM, OP_BWD_NORM, OP_FWD_BLOCKED, OP_BWD_BLOCKED = range(6)
 MAX_SIDE = 4096
 
-EXPORTED = ("gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
-            "gspn_project", "gspn_latent_params", "gspn_latent_fwd",
+# layouts of the per-direction tensors
+PIXEL, BLOCKED = "pixel", "blocked"
+
+EXPORTED = ("gspn_workspace_size", "gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_blocked",
+            "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm", "gspn_project",
+            "gspn_latent_params", "gspn_latent_workspace_size", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
 
 _lib = None
@@ -46,28 +53,25 @@ def load() -> ctypes.CDLL:
                 f"{LIB_PATH} is missing: build it with `python -m paper_2606_00746_amd.build` "
                 "(there is no fallback implementation)")
         lib = ctypes.CDLL(LIB_PATH)
-        vp, i = ctypes.c_void_p, ctypes.c_int
-        lib.gspn_scan_fwd.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
-        lib.gspn_scan_fwd.restype = i
-        lib.gspn_scan_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
-        lib.gspn_scan_bwd.restype = i
-        lib.gspn_scan_fwd_norm.argtypes = [vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
-        lib.gspn_scan_fwd_norm.restype = i
-        lib.gspn_scan_bwd_norm.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i,
-                                           vp]
-        lib.gspn_scan_bwd_norm.restype = i
+        vp, i, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+        pi64 = ctypes.POINTER(ctypes.c_int64)
+        scan8 = [i] * 7                     # direction, B, C, G, H, W, dtype
+        ws = [vp, i64, vp]                  # workspace, workspace_bytes, stream
+        lib.gspn_workspace_size.argtypes = [i] + scan8 + [pi64]
+        for name in ("gspn_scan_fwd", "gspn_scan_fwd_blocked", "gspn_scan_fwd_norm"):
+            getattr(lib, name).argtypes = [vp] * 5 + scan8 + ws
+        for name in ("gspn_scan_bwd", "gspn_scan_bwd_blocked", "gspn_scan_bwd_norm"):
+            getattr(lib, name).argtypes = [vp] * 9 + scan8 + ws
         lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
-        lib.gspn_project.restype = i
-        lib.gspn_latent_params.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, vp]
-        lib.gspn_latent_params.restype = i
-        lib.gspn_latent_fwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, i, i, i, i, i, i, i, vp]
-        lib.gspn_latent_fwd.restype = i
+        lib.gspn_latent_params.argtypes = [vp] * 7 + [i] * 6 + [vp]
+        lib.gspn_latent_workspace_size.argtypes = [i] * 7 + [pi64]
+        lib.gspn_latent_fwd.argtypes = [vp] * 7 + [i] * 7 + ws
+        for name in EXPORTED:
+            getattr(lib, name).restype = i
         lib.gspn_strerror.argtypes = [i]
         lib.gspn_strerror.restype = ctypes.c_char_p
         lib.gspn_last_hip_error.argtypes = []
-        lib.gspn_last_hip_error.restype = i
         lib.gspn_version.argtypes = []
-        lib.gspn_version.restype = i
         _lib = lib
     return _lib
 
@@ -76,25 +80,46 @@ def load() -> ctypes.CDLL:
 # raw C entry points (pointers as ints, sizes as ints)
 # ---------------------------------------------------------------------------
 
-def gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, stream) -> int:
-    return load().gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, stream)
+def gspn_workspace_size(op, direction, B, C, G, H, W, dtype):
+    """(status, bytes) of gspn_workspace_size."""
+    n = ctypes.c_int64(0)
+    st = load().gspn_workspace_size(op, direction, B, C, G, H, W, dtype, ctypes.byref(n))
+    return st, n.value
 
 
-def gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
-                  stream) -> int:
+def gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, ws, ws_bytes, stream) -> int:
+    return load().gspn_scan_fwd(x, w, lam, u, y, direction, B, C, G, H, W, dtype, ws, ws_bytes,
+                                stream)
+
+
+def gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype, ws,
+                  ws_bytes, stream) -> int:
     return load().gspn_scan_bwd(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W,
-                                dtype, stream)
+                                dtype, ws, ws_bytes, stream)
 
 
-def gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype, stream) -> int:
-    return load().gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype,
-                                     stream)
+def gspn_scan_fwd_blocked(x, w, lam, u, y, direction, B, C, G, H, W, dtype, ws, ws_bytes,
+                          stream) -> int:
+    return load().gspn_scan_fwd_blocked(x, w, lam, u, y, direction, B, C, G, H, W, dtype, ws,
+                                        ws_bytes, stream)
+
+
+def gspn_scan_bwd_blocked(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype, ws,
+                          ws_bytes, stream) -> int:
+    return load().gspn_scan_bwd_blocked(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H,
+                                        W, dtype, ws, ws_bytes, stream)
+
+
+def gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype, ws, ws_bytes,
+                       stream) -> int:
+    return load().gspn_scan_fwd_norm(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype, ws,
+                                     ws_bytes, stream)
 
 
 def gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction, B, C, G, H,
-                       W, dtype, stream) -> int:
+                       W, dtype, ws, ws_bytes, stream) -> int:
     return load().gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction,
-                                     B, C, G, H, W, dtype, stream)
+                                     B, C, G, H, W, dtype, ws, ws_bytes, stream)
 
 
 def gspn_project(a, x, y, B, M, K, H, W, dtype, stream) -> int:
@@ -107,10 +132,17 @@ def gspn_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, H, W, d
                                      dtype, stream)
 
 
-def gspn_latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H, W, dtype,
-                    stream) -> int:
+def gspn_latent_workspace_size(direction, B, C, Cc, H, W, dtype):
+    """(status, bytes) of gspn_latent_workspace_size."""
+    n = ctypes.c_int64(0)
+    st = load().gspn_latent_workspace_size(direction, B, C, Cc, H, W, dtype, ctypes.byref(n))
+    return st, n.value
+
+
+def gspn_latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H, W, dtype, ws,
+                    ws_bytes, stream) -> int:
     return load().gspn_latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H,
-                                  W, dtype, stream)
+                                  W, dtype, ws, ws_bytes, stream)
 
 
 def gspn_strerror(status: int) -> str:
@@ -150,83 +182,148 @@ def _check_raise(status):
         raise GspnError(status, gspn_last_hip_error() if status == ERR_HIP else 0)
 
 
-def _sizes(x, w, lam, u, direction):
-    """(B, C, G, H, W) from x [B,C,H,W] and w [D,B,G,3,...] (line-major planes)."""
-    if x.dim() != 4 or w.dim() < 3:
-        raise ValueError("x must be [B,C,H,W] and w [D,B,G,3,plane]")
-    B, C, H, W = x.shape
-    G = w.shape[2]
-    D = bin(direction & 15).count("1")
-    if w.numel() != D * B * G * 3 * H * W:
-        raise ValueError("w must hold D*B*G*3*H*W elements")
-    if lam.numel() != D * B * C * H * W or u.numel() != D * B * C * H * W:
-        raise ValueError("lam and u must hold D*B*C*H*W elements")
-    return B, C, G, H, W
+def _ndirs(direction: int) -> int:
+    return bin(direction & 15).count("1")
 
 
-def _ptrs(*ts):
-    for t in ts:
+def _check_tensors(ref, named):
+    """Every tensor of `named` ({name: (tensor, numel)}) must sit on ref's GPU,
+    share its dtype, be contiguous and hold exactly numel elements."""
+    if not ref.is_contiguous():
+        raise ValueError("x must be contiguous")
+    for name, (t, numel) in named.items():
+        if t.numel() != numel:
+            raise ValueError(f"{name} must hold {numel} elements, not {t.numel()}")
+        if t.dtype != ref.dtype:
+            raise ValueError(f"{name} must have dtype {ref.dtype}, not {t.dtype}")
         if not t.is_contiguous():
-            raise ValueError("all tensors must be contiguous")
-    return [t.data_ptr() for t in ts]
+            raise ValueError(f"{name} must be contiguous")
+    if not ref.is_cuda:
+        raise ValueError("tensors must be on a GPU")
+    for name, (t, _) in named.items():
+        if not t.is_cuda or t.device != ref.device:
+            raise ValueError(f"{name} must be on {ref.device}")
 
 
-def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None):
+def _sizes(x, w, direction):
+    """(B, C, G, H, W) from x [B,C,H,W] and w [D,B,G,3,...]."""
+    if x.dim() != 4 or w.dim() < 3:
+        raise ValueError("x must be [B,C,H,W] and w [D,B,G,3,...]")
+    B, C, H, W = x.shape
+    return B, C, w.shape[2], H, W
+
+
+def workspace_size(op, x, w, direction) -> int:
+    """Bytes of workspace operation `op` (OP_*) takes for these tensors."""
+    B, C, G, H, W = _sizes(x, w, direction)
+    st, n = gspn_workspace_size(op, direction, B, C, G, H, W, _dtype_code(x))
+    _check_raise(st)
+    return n
+
+
+def _workspace(op, direction, B, C, G, H, W, dtype, device, given=None):
+    """The device buffer operation `op` works in: `given` (a uint8 tensor on
+    the same device) when it is large enough, else a new one (None if the
+    call needs none)."""
+    import torch
+    st, n = gspn_workspace_size(op, direction, B, C, G, H, W, dtype)
+    _check_raise(st)
+    if n == 0:
+        return None, 0
+    if given is not None:
+        if given.device != device or given.dtype != torch.uint8 or not given.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 tensor on the inputs' device")
+        if given.numel() >= n:
+            return given, given.numel()
+    return torch.empty(n, dtype=torch.uint8, device=device), n
+
+
+def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=None):
+    B, C, G, H, W = _sizes(x, w, direction)
+    D = _ndirs(direction)
+    n, nd, nw = B * C * H * W, D * B * C * H * W, D * B * G * 3 * H * W
+    named = {"w": (w, nw), "lam": (lam, nd), "u": (u, nd)}
+    bwd = dy is not None
+    if bwd:
+        dx, dw, dlam, du = outs
+        named.update(dy=(dy, n), dx=(dx, n), dw=(dw, nw), dlam=(dlam, nd), du=(du, nd))
+    else:
+        named.update(y=(outs[0], n))
+    _check_tensors(x, named)
+    dt = _dtype_code(x)
+    ws, nbytes = _workspace(op, direction, B, C, G, H, W, dt, x.device, workspace)
+    ptrs = [t.data_ptr() for t in (x, w, lam, u)]
+    if bwd:
+        ptrs += [t.data_ptr() for t in (dy, dx, dw, dlam, du)]
+    else:
+        ptrs.append(outs[0].data_ptr())
+    fn = {OP_FWD: gspn_scan_fwd, OP_BWD: gspn_scan_bwd, OP_FWD_BLOCKED: gspn_scan_fwd_blocked,
+          OP_BWD_BLOCKED: gspn_scan_bwd_blocked, OP_FWD_NORM: gspn_scan_fwd_norm,
+          OP_BWD_NORM: gspn_scan_bwd_norm}[op]
+    status = fn(*ptrs, direction, B, C, G, H, W, dt, ws.data_ptr() if ws is not None else None,
+                nbytes, _stream_handle(x, stream))
+    _check_raise(status)
+
+
+def _check_layout(layout):
+    if layout not in (PIXEL, BLOCKED):
+        raise ValueError(f"layout must be {PIXEL!r} or {BLOCKED!r}")
+
+
+def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None, layout: str = PIXEL,
+             workspace=None):
     """y = sum_d u_d * h_d for device tensors (see include/gspn.h).
 
-    x is pixel-major [B,C,H,W]; lam, u and w are line-major per direction
-    (horizontal-direction planes transposed), e.g. from :func:`to_line_major`.
-    """
+    x [B,C,H,W]; lam, u [D,B,C,H,W] and w [D,B,G,3,H,W] pixel-major, or, with
+    layout="blocked", in the blocked line-major layout of the _blocked entry
+    points (each plane H*W elements long).  `workspace`: an optional uint8
+    device tensor the call may use (a new one is taken when it is missing or
+    too small)."""
     import torch
-    B, C, G, H, W = _sizes(x, w, lam, u, direction)
+    _check_layout(layout)
     if y is None:
         y = torch.empty_like(x)
-    status = gspn_scan_fwd(*_ptrs(x, w, lam, u, y), direction, B, C, G, H, W, _dtype_code(x),
-                           _stream_handle(x, stream))
-    _check_raise(status)
+    _scan(OP_FWD if layout == PIXEL else OP_FWD_BLOCKED, x, w, lam, u, direction, (y,),
+          stream=stream, workspace=workspace)
     return y
 
 
-def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None):
-    """Gradients (dx, dw, dlam, du) of <y, dy> for device tensors."""
+def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None, layout: str = PIXEL,
+             workspace=None):
+    """Gradients (dx, dw, dlam, du) of <y, dy> for device tensors, in the
+    layout of the inputs."""
     import torch
-    B, C, G, H, W = _sizes(x, w, lam, u, direction)
+    _check_layout(layout)
     if out is None:
         out = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                torch.empty_like(u))
-    dx, dw, dlam, du = out
-    status = gspn_scan_bwd(*_ptrs(x, w, lam, u, dy, dx, dw, dlam, du), direction, B, C, G, H, W,
-                           _dtype_code(x), _stream_handle(x, stream))
-    _check_raise(status)
-    return dx, dw, dlam, du
+    _scan(OP_BWD if layout == PIXEL else OP_BWD_BLOCKED, x, w, lam, u, direction, out, dy=dy,
+          stream=stream, workspace=workspace)
+    return out
 
 
-def scan_fwd_norm(x, w_logits, lam, u, direction: int = ALL, y=None, stream=None):
+def scan_fwd_norm(x, w_logits, lam, u, direction: int = ALL, y=None, stream=None,
+                  workspace=None):
     """As :func:`scan_fwd`, with the weights given by their logits
-    (Sec. 3, Eq. (row_stochastic_norm))."""
+    (Sec. 3, Eq. (row_stochastic_norm)); pixel-major."""
     import torch
-    B, C, G, H, W = _sizes(x, w_logits, lam, u, direction)
     if y is None:
         y = torch.empty_like(x)
-    status = gspn_scan_fwd_norm(*_ptrs(x, w_logits, lam, u, y), direction, B, C, G, H, W,
-                                _dtype_code(x), _stream_handle(x, stream))
-    _check_raise(status)
+    _scan(OP_FWD_NORM, x, w_logits, lam, u, direction, (y,), stream=stream, workspace=workspace)
     return y
 
 
-def scan_bwd_norm(x, w_logits, lam, u, dy, direction: int = ALL, out=None, stream=None):
+def scan_bwd_norm(x, w_logits, lam, u, dy, direction: int = ALL, out=None, stream=None,
+                  workspace=None):
     """Gradients (dx, dw_logits, dlam, du) of <y, dy>, the weights given by
-    their logits."""
+    their logits; pixel-major."""
     import torch
-    B, C, G, H, W = _sizes(x, w_logits, lam, u, direction)
     if out is None:
         out = (torch.empty_like(x), torch.empty_like(w_logits), torch.empty_like(lam),
                torch.empty_like(u))
-    dx, dwl, dlam, du = out
-    status = gspn_scan_bwd_norm(*_ptrs(x, w_logits, lam, u, dy, dx, dwl, dlam, du), direction, B,
-                                C, G, H, W, _dtype_code(x), _stream_handle(x, stream))
-    _check_raise(status)
-    return dx, dwl, dlam, du
+    _scan(OP_BWD_NORM, x, w_logits, lam, u, direction, out, dy=dy, stream=stream,
+          workspace=workspace)
+    return out
 
 
 def project(a, x, y=None, stream=None):
@@ -238,14 +335,15 @@ def project(a, x, y=None, stream=None):
     B, _, H, W = x.shape
     if y is None:
         y = torch.empty((B, M, H, W), dtype=x.dtype, device=x.device)
-    status = gspn_project(*_ptrs(a, x, y), B, M, K, H, W, _dtype_code(x),
+    _check_tensors(x, {"a": (a, M * K), "y": (y, B * M * H * W)})
+    status = gspn_project(a.data_ptr(), x.data_ptr(), y.data_ptr(), B, M, K, H, W, _dtype_code(x),
                           _stream_handle(x, stream))
     _check_raise(status)
     return y
 
 
 def _latent_weights(l_u, l_lam, l_w, direction):
-    D = bin(direction & 15).count("1")
+    D = _ndirs(direction)
     Cc = l_u.shape[-1]
     if (tuple(l_u.shape) != (D, Cc, Cc) or tuple(l_lam.shape) != (D, Cc, Cc)
             or tuple(l_w.shape) != (D, Cc, 3, Cc)):
@@ -265,8 +363,12 @@ def latent_params(xc, l_u, l_lam, l_w, direction: int = ALL, out=None, stream=No
         out = (torch.empty((D, B, Cc, H * W), **kw), torch.empty((D, B, Cc, H * W), **kw),
                torch.empty((D, B, Cc, 3, H * W), **kw))
     u, lam, w = out
-    status = gspn_latent_params(*_ptrs(xc, l_u, l_lam, l_w, u, lam, w), direction, B, Cc, H, W,
-                                _dtype_code(xc), _stream_handle(xc, stream))
+    n = B * Cc * H * W
+    _check_tensors(xc, {"l_u": (l_u, D * Cc * Cc), "l_lam": (l_lam, D * Cc * Cc),
+                        "l_w": (l_w, 3 * D * Cc * Cc), "u": (u, D * n), "lam": (lam, D * n),
+                        "w": (w, 3 * D * n)})
+    status = gspn_latent_params(*[t.data_ptr() for t in (xc, l_u, l_lam, l_w, u, lam, w)],
+                                direction, B, Cc, H, W, _dtype_code(xc), _stream_handle(xc, stream))
     _check_raise(status)
     return u, lam, w
 
@@ -283,68 +385,16 @@ def latent_fwd(x, p_down, l_u, l_lam, l_w, p_up, direction: int = ALL, y=None, s
         raise ValueError("p_down must be [Cc, C] and p_up [C, Cc]")
     if y is None:
         y = torch.empty_like(x)
-    status = gspn_latent_fwd(*_ptrs(x, p_down, l_u, l_lam, l_w, p_up, y), direction, B, C, Cc, H,
-                             W, _dtype_code(x), _stream_handle(x, stream))
+    _check_tensors(x, {"p_down": (p_down, Cc * C), "l_u": (l_u, D * Cc * Cc),
+                       "l_lam": (l_lam, D * Cc * Cc), "l_w": (l_w, 3 * D * Cc * Cc),
+                       "p_up": (p_up, C * Cc), "y": (y, B * C * H * W)})
+    dt = _dtype_code(x)
+    st, nbytes = gspn_latent_workspace_size(direction, B, C, Cc, H, W, dt)
+    _check_raise(st)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device=x.device) if nbytes else None
+    status = gspn_latent_fwd(*[t.data_ptr() for t in (x, p_down, l_u, l_lam, l_w, p_up, y)],
+                             direction, B, C, Cc, H, W, dt,
+                             ws.data_ptr() if ws is not None else None, nbytes,
+                             _stream_handle(x, stream))
     _check_raise(status)
     return y
-
-
-LINE_BLOCK = 8   # lines per block of the line-major layout
-
-
-def _block_lines(plane):
-    """[..., L, P] -> [..., L*P]: lines in blocks of 8, positions adjacent inside a block."""
-    import torch
-    L, P = plane.shape[-2:]
-    lead = plane.shape[:-2]
-    if L % LINE_BLOCK == 0:
-        blk = plane.reshape(*lead, L // LINE_BLOCK, LINE_BLOCK, P)
-        return blk.transpose(-1, -2).contiguous().reshape(*lead, L * P)
-    parts = [plane[..., q:q + LINE_BLOCK, :].transpose(-1, -2).reshape(*lead, -1)
-             for q in range(0, L, LINE_BLOCK)]
-    return torch.cat(parts, dim=-1)
-
-
-def _unblock_lines(flat, L, P):
-    import torch
-    lead = flat.shape[:-1]
-    if L % LINE_BLOCK == 0:
-        blk = flat.reshape(*lead, L // LINE_BLOCK, P, LINE_BLOCK)
-        return blk.transpose(-1, -2).contiguous().reshape(*lead, L, P)
-    parts, off = [], 0
-    for q in range(0, L, LINE_BLOCK):
-        n = min(LINE_BLOCK, L - q)
-        parts.append(flat[..., off:off + n * P].reshape(*lead, P, n).transpose(-1, -2))
-        off += n * P
-    return torch.cat(parts, dim=-2)
-
-
-def to_line_major(t, direction: int):
-    """Pixel-major per-direction tensor [D, ..., H, W] -> blocked line-major [D, ..., H*W].
-
-    The lines a direction scans are storage rows (vertical directions) or
-    storage columns (horizontal ones).  Each plane stores its lines in blocks
-    of 8 consecutive lines; inside a block the values of one line position
-    are adjacent: line l, position p sits at 8*P*(l//8) + n*p + l%8 with
-    n = min(8, L - 8*(l//8)).  A producer can also write this layout directly.
-    """
-    import torch
-    bits = [b for b in (T2B, B2T, L2R, R2L) if direction & b]
-    out = []
-    for s, b in enumerate(bits):
-        p = t[s] if b in (T2B, B2T) else t[s].transpose(-1, -2)
-        out.append(_block_lines(p))
-    return torch.stack(out)
-
-
-def from_line_major(t, direction: int, H: int, W: int):
-    """Inverse of :func:`to_line_major`."""
-    import torch
-    bits = [b for b in (T2B, B2T, L2R, R2L) if direction & b]
-    out = []
-    for s, b in enumerate(bits):
-        if b in (T2B, B2T):
-            out.append(_unblock_lines(t[s], H, W))
-        else:
-            out.append(_unblock_lines(t[s], W, H).transpose(-1, -2))
-    return torch.stack(out).contiguous()

@@ -4,7 +4,6 @@
 
 #include <stdint.h>
 
-#include <mutex>
 
 #include "../../include/gspn.h"
 #include "launch.hpp"
@@ -74,26 +73,7 @@ int hip_status(hipError_t e)
 
 }  // namespace
 
-hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s)
-{
-    // Keep freed scratch in the device's default pool instead of returning it
-    // to the device at the next synchronization, so that repeated calls do not
-    // map their scratch afresh each time (once per device and process).
-    static std::once_flag once[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
-        std::call_once(once[dev], [dev] {
-            hipMemPool_t pool;
-            if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
-                uint64_t keep = UINT64_MAX;
-                (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-            }
-        });
-    }
-    return hipMallocAsync(ptr, bytes, s);
-}
 
-hipError_t scratch_free(void *ptr, hipStream_t s) { return hipFreeAsync(ptr, s); }
 
 }  // namespace gspn
 
@@ -128,113 +108,226 @@ hipError_t dispatch_bwd(const Problem &p, hipStream_t s)
 
 }  // namespace gspn
 
-extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u, void *y,
-                             int direction, int B, int C, int G, int H, int W, int dtype,
-                             void *stream)
+namespace gspn {
+namespace {
+
+constexpr int64_t kNoWorkspace = -1;
+
+// The pieces of one scan call: its checked buffers, its problem, and the
+// workspace check.  A call first runs its dispatch in counting mode (no
+// launch) to learn how much workspace it takes, then checks the caller's
+// workspace against that and runs it for real.
+int scan_buffers(int op, const void *x, const void *w, const void *lam, const void *u,
+                 const void *dy, const void *y, const void *dx, const void *dw, const void *dlam,
+                 const void *du, int direction, int B, int C, int G, int H, int W, int dtype,
+                 Buf *bufs, int *nbuf)
 {
-    int st = check_common(direction, B, C, G, H, W, dtype);
-    if (st != GSPN_OK)
-        return st;
     const int64_t es = dtype == GSPN_F32 ? 4 : 2;
     const int64_t D = __builtin_popcount(direction);
     const int64_t n = (int64_t)B * C * H * W;
     const int64_t nw = D * B * G * 3 * H * W;
-    const Buf bufs[] = {{x, n * es, false},      {w, nw * es, false}, {lam, D * n * es, false},
-                        {u, D * n * es, false},  {y, n * es, true}};
-    st = check_buffers(bufs, 5);
+    const bool bwd = op == GSPN_OP_BWD || op == GSPN_OP_BWD_NORM || op == GSPN_OP_BWD_BLOCKED;
+    int k = 0;
+    bufs[k++] = {x, n * es, false};
+    bufs[k++] = {w, nw * es, false};
+    bufs[k++] = {lam, D * n * es, false};
+    bufs[k++] = {u, D * n * es, false};
+    if (bwd) {
+        bufs[k++] = {dy, n * es, false};
+        bufs[k++] = {dx, n * es, true};
+        bufs[k++] = {dw, nw * es, true};
+        bufs[k++] = {dlam, D * n * es, true};
+        bufs[k++] = {du, D * n * es, true};
+    } else {
+        bufs[k++] = {y, n * es, true};
+    }
+    *nbuf = k;
+    return GSPN_OK;
+}
+
+bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_BLOCKED; }
+
+// The launches of one scan operation on the workspace ws (in counting mode:
+// no launch, ws.used adds up what the call takes).
+hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, hipStream_t s)
+{
+    Problem p = p0;
+    Workspace &ws = *p.ws;
+    const int64_t es = p.dtype == GSPN_F32 ? 4 : 2;
+    const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * p.H * p.W;
+    switch (op) {
+    case GSPN_OP_FWD:
+    case GSPN_OP_FWD_BLOCKED:
+        return dispatch_fwd(p, s);
+    case GSPN_OP_BWD:
+    case GSPN_OP_BWD_BLOCKED:
+        return dispatch_bwd(p, s);
+    case GSPN_OP_FWD_NORM: {
+        // weights from their logits into the workspace, then the scan
+        void *w = nullptr;
+        hipError_t e = ws.take(&w, (size_t)(nw * es));
+        if (e != hipSuccess)
+            return e;
+        p.w = w;
+        if (!ws.counting) {
+            e = launch_norm(p, w_in, nullptr, w, s);
+            if (e != hipSuccess)
+                return e;
+        }
+        return dispatch_fwd(p, s);
+    }
+    default: {   // GSPN_OP_BWD_NORM
+        // the weights, then the gradient with respect to them, then the
+        // logits' gradient
+        void *w = nullptr;
+        hipError_t e = ws.take(&w, (size_t)(2 * nw * es));
+        if (e != hipSuccess)
+            return e;
+        p.w = w;
+        p.dw = static_cast<char *>(w) + nw * es;
+        if (!ws.counting) {
+            e = launch_norm(p, w_in, nullptr, w, s);
+            if (e != hipSuccess)
+                return e;
+        }
+        e = dispatch_bwd(p, s);
+        if (e != hipSuccess || ws.counting)
+            return e;
+        return launch_norm(p, w_in, p.dw, dw_out, s);
+    }
+    }
+}
+
+// Counts the workspace of a checked problem.  GSPN_ERR_HIP if a device query
+// of the plan failed.
+int count_workspace(int op, const Problem &p0, int64_t *bytes)
+{
+    Workspace ws;
+    ws.counting = true;
+    Problem p = p0;
+    p.ws = &ws;
+    const hipError_t e = run_scan(op, p, p0.w, p0.dw, nullptr);
+    if (e != hipSuccess)
+        return hip_status(e);
+    *bytes = (int64_t)ws.used;
+    return GSPN_OK;
+}
+
+int scan_call(int op, const void *x, const void *w, const void *lam, const void *u, const void *dy,
+              void *y, void *dx, void *dw, void *dlam, void *du, int direction, int B, int C,
+              int G, int H, int W, int dtype, void *workspace, int64_t workspace_bytes,
+              void *stream)
+{
+    if (!valid_op(op))
+        return GSPN_ERR_UNSUPPORTED;
+    int st = check_common(direction, B, C, G, H, W, dtype);
     if (st != GSPN_OK)
         return st;
-    Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
-              direction, B, C, G, H, W, dtype};
-    return hip_status(dispatch_fwd(p, static_cast<hipStream_t>(stream)));
+    Buf bufs[11];
+    int nb = 0;
+    scan_buffers(op, x, w, lam, u, dy, y, dx, dw, dlam, du, direction, B, C, G, H, W, dtype, bufs,
+                 &nb);
+    st = check_buffers(bufs, nb);
+    if (st != GSPN_OK)
+        return st;
+    const bool blocked = op == GSPN_OP_FWD_BLOCKED || op == GSPN_OP_BWD_BLOCKED;
+    Problem p{x, w, lam, u, dy, y, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
+              blocked ? kBlocked : kPixelMajor, nullptr};
+    int64_t need = 0;
+    st = count_workspace(op, p, &need);
+    if (st != GSPN_OK)
+        return st;
+    if (workspace_bytes < 0)
+        return GSPN_ERR_WORKSPACE;
+    if (need > 0) {
+        if (workspace == nullptr || workspace_bytes < need)
+            return GSPN_ERR_WORKSPACE;
+        bufs[nb++] = {workspace, need, true};
+        st = check_buffers(bufs, nb);
+        if (st != GSPN_OK)
+            return st;
+    }
+    Workspace ws;
+    ws.base = static_cast<char *>(workspace);
+    ws.size = need > 0 ? (size_t)workspace_bytes : 0;
+    p.ws = &ws;
+    const hipError_t e = run_scan(op, p, w, dw, static_cast<hipStream_t>(stream));
+    return e == hipErrorOutOfMemory ? GSPN_ERR_WORKSPACE : hip_status(e);
+}
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_workspace_size(int op, int direction, int B, int C, int G, int H, int W,
+                                   int dtype, int64_t *bytes)
+{
+    if (bytes == nullptr)
+        return GSPN_ERR_NULL;
+    *bytes = 0;
+    if (!valid_op(op))
+        return GSPN_ERR_UNSUPPORTED;
+    const int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    const bool blocked = op == GSPN_OP_FWD_BLOCKED || op == GSPN_OP_BWD_BLOCKED;
+    Problem p{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+              nullptr, direction, B, C, G, H, W, dtype, blocked ? kBlocked : kPixelMajor, nullptr};
+    return count_workspace(op, p, bytes);
+}
+
+extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u, void *y,
+                             int direction, int B, int C, int G, int H, int W, int dtype,
+                             void *workspace, int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_FWD, x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
+                     direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
 }
 
 extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, const void *u,
                              const void *dy, void *dx, void *dw, void *dlam, void *du,
                              int direction, int B, int C, int G, int H, int W, int dtype,
-                             void *stream)
+                             void *workspace, int64_t workspace_bytes, void *stream)
 {
-    int st = check_common(direction, B, C, G, H, W, dtype);
-    if (st != GSPN_OK)
-        return st;
-    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
-    const int64_t D = __builtin_popcount(direction);
-    const int64_t n = (int64_t)B * C * H * W;
-    const int64_t nw = D * B * G * 3 * H * W;
-    const Buf bufs[] = {{x, n * es, false},      {w, nw * es, false},      {lam, D * n * es, false},
-                        {u, D * n * es, false},  {dy, n * es, false},      {dx, n * es, true},
-                        {dw, nw * es, true},     {dlam, D * n * es, true}, {du, D * n * es, true}};
-    st = check_buffers(bufs, 9);
-    if (st != GSPN_OK)
-        return st;
-    Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
-    return hip_status(dispatch_bwd(p, static_cast<hipStream_t>(stream)));
+    return scan_call(GSPN_OP_BWD, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C,
+                     G, H, W, dtype, workspace, workspace_bytes, stream);
+}
+
+extern "C" int gspn_scan_fwd_blocked(const void *x, const void *w, const void *lam, const void *u,
+                                     void *y, int direction, int B, int C, int G, int H, int W,
+                                     int dtype, void *workspace, int64_t workspace_bytes,
+                                     void *stream)
+{
+    return scan_call(GSPN_OP_FWD_BLOCKED, x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr,
+                     nullptr, direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
+}
+
+extern "C" int gspn_scan_bwd_blocked(const void *x, const void *w, const void *lam,
+                                     const void *u, const void *dy, void *dx, void *dw,
+                                     void *dlam, void *du, int direction, int B, int C, int G,
+                                     int H, int W, int dtype, void *workspace,
+                                     int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_BWD_BLOCKED, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction,
+                     B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
 }
 
 extern "C" int gspn_scan_fwd_norm(const void *x, const void *w_logits, const void *lam,
                                   const void *u, void *y, int direction, int B, int C, int G,
-                                  int H, int W, int dtype, void *stream)
+                                  int H, int W, int dtype, void *workspace,
+                                  int64_t workspace_bytes, void *stream)
 {
-    int st = check_common(direction, B, C, G, H, W, dtype);
-    if (st != GSPN_OK)
-        return st;
-    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
-    const int64_t D = __builtin_popcount(direction);
-    const int64_t n = (int64_t)B * C * H * W;
-    const int64_t nw = D * B * G * 3 * H * W;
-    const Buf bufs[] = {{x, n * es, false},     {w_logits, nw * es, false}, {lam, D * n * es, false},
-                        {u, D * n * es, false}, {y, n * es, true}};
-    st = check_buffers(bufs, 5);
-    if (st != GSPN_OK)
-        return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    void *w = nullptr;
-    hipError_t e = scratch_alloc(&w, (size_t)(nw * es), s);
-    if (e != hipSuccess)
-        return hip_status(e);
-    Problem p{x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr, nullptr,
-              direction, B, C, G, H, W, dtype};
-    e = launch_norm(p, w_logits, nullptr, w, s);
-    if (e == hipSuccess)
-        e = dispatch_fwd(p, s);
-    const hipError_t e2 = scratch_free(w, s);
-    return hip_status(e != hipSuccess ? e : e2);
+    return scan_call(GSPN_OP_FWD_NORM, x, w_logits, lam, u, nullptr, y, nullptr, nullptr, nullptr,
+                     nullptr, direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
 }
 
 extern "C" int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
                                   const void *u, const void *dy, void *dx, void *dw_logits,
                                   void *dlam, void *du, int direction, int B, int C, int G, int H,
-                                  int W, int dtype, void *stream)
+                                  int W, int dtype, void *workspace, int64_t workspace_bytes,
+                                  void *stream)
 {
-    int st = check_common(direction, B, C, G, H, W, dtype);
-    if (st != GSPN_OK)
-        return st;
-    const int64_t es = dtype == GSPN_F32 ? 4 : 2;
-    const int64_t D = __builtin_popcount(direction);
-    const int64_t n = (int64_t)B * C * H * W;
-    const int64_t nw = D * B * G * 3 * H * W;
-    const Buf bufs[] = {{x, n * es, false},         {w_logits, nw * es, false},
-                        {lam, D * n * es, false},   {u, D * n * es, false},
-                        {dy, n * es, false},        {dx, n * es, true},
-                        {dw_logits, nw * es, true}, {dlam, D * n * es, true},
-                        {du, D * n * es, true}};
-    st = check_buffers(bufs, 9);
-    if (st != GSPN_OK)
-        return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    void *w = nullptr;
-    hipError_t e = scratch_alloc(&w, (size_t)(2 * nw * es), s);   // weights, then their gradient
-    if (e != hipSuccess)
-        return hip_status(e);
-    void *dw = static_cast<char *>(w) + nw * es;
-    Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype};
-    e = launch_norm(p, w_logits, nullptr, w, s);
-    if (e == hipSuccess)
-        e = dispatch_bwd(p, s);
-    if (e == hipSuccess)
-        e = launch_norm(p, w_logits, dw, dw_logits, s);
-    const hipError_t e2 = scratch_free(w, s);
-    return hip_status(e != hipSuccess ? e : e2);
+    return scan_call(GSPN_OP_BWD_NORM, x, w_logits, lam, u, dy, nullptr, dx, dw_logits, dlam, du,
+                     direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
 }
 
 namespace gspn {
@@ -314,10 +407,54 @@ extern "C" int gspn_latent_params(const void *xc, const void *l_u, const void *l
                                            static_cast<hipStream_t>(stream)));
 }
 
-extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
-                               const void *l_lam, const void *l_w, const void *p_up, void *y,
-                               int direction, int B, int C, int Cc, int H, int W, int dtype,
-                               void *stream)
+namespace gspn {
+namespace {
+
+// The latent sublayer's launches on the workspace ws (counting mode: none).
+// The latent tensors belong to the call, so the scan may run on a grid padded
+// at the bottom and right to whole 8-line blocks, where the register-streamed
+// and wide kernels apply.  Padded pixels hold x_c = 0, hence u = lambda = 0;
+// the taps of real pixels that point into the padding are normalized as off
+// the grid (weight exactly 0); and a scan that starts in the padding carries
+// h = 0 up to the first real line, which then starts from h = lambda x as on
+// the unpadded grid.  Real pixels therefore see the same recurrence; P_up
+// reads only them.
+hipError_t run_latent(const void *x, const void *p_down, const void *l_u, const void *l_lam,
+                      const void *l_w, const void *p_up, void *y, int direction, int B, int C,
+                      int Cc, int H, int W, Workspace &ws, hipStream_t s)
+{
+    const int64_t D = __builtin_popcount(direction);
+    const auto up8 = [](int v) { return (v + 7) / 8 * 8; };
+    const bool pad = (H % 8 != 0 || W % 8 != 0) && (H > 16 || W > 16) && up8(H) <= 256 &&
+                     up8(W) <= 256;
+    const int Hp = pad ? up8(H) : H, Wp = pad ? up8(W) : W;
+    const int64_t ncp = (int64_t)B * Cc * Hp * Wp;
+    // latent x_c, u, lambda, w and y_c in one block, 16-byte aligned parts
+    const int64_t o_u = round8(ncp), o_l = o_u + round8(D * ncp), o_w = o_l + round8(D * ncp);
+    const int64_t o_y = o_w + round8(3 * D * ncp), total = o_y + round8(ncp);
+    void *scr = nullptr;
+    hipError_t e = ws.take(&scr, (size_t)(total * 2));
+    if (e != hipSuccess)
+        return e;
+    uint16_t *base = static_cast<uint16_t *>(scr);
+    uint16_t *xc = base, *u = base + o_u, *lam = base + o_l, *w = base + o_w, *yc = base + o_y;
+    if (!ws.counting) {
+        e = launch_project(p_down, x, xc, B, Cc, C, Hp, Wp, s, H, W);
+        if (e == hipSuccess)
+            e = launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, Hp, Wp, s,
+                                     H, W);
+        if (e != hipSuccess)
+            return e;
+    }
+    Problem p{xc, w, lam, u, nullptr, yc, nullptr, nullptr, nullptr, nullptr,
+              direction, B, Cc, Cc, Hp, Wp, GSPN_BF16, kBlocked, &ws};
+    e = dispatch_fwd(p, s);
+    if (e != hipSuccess || ws.counting)
+        return e;
+    return launch_project(p_up, yc, y, B, C, Cc, H, W, s, Hp, Wp);
+}
+
+int check_latent_all(int direction, int B, int C, int Cc, int H, int W, int dtype)
 {
     int st = check_latent(direction, B, Cc, H, W, dtype);
     if (st == GSPN_OK)
@@ -327,55 +464,69 @@ extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_
     // the latent grid may be padded by up to 7 lines each way
     if (st == GSPN_OK && H + 7 <= GSPN_MAX_SIDE && W + 7 <= GSPN_MAX_SIDE)
         st = check_latent(direction, B, Cc, H + 7, W + 7, dtype);
+    return st;
+}
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_latent_workspace_size(int direction, int B, int C, int Cc, int H, int W,
+                                          int dtype, int64_t *bytes)
+{
+    if (bytes == nullptr)
+        return GSPN_ERR_NULL;
+    *bytes = 0;
+    const int st = check_latent_all(direction, B, C, Cc, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    Workspace ws;
+    ws.counting = true;
+    const hipError_t e = run_latent(nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                    direction, B, C, Cc, H, W, ws, nullptr);
+    if (e != hipSuccess)
+        return hip_status(e);
+    *bytes = (int64_t)ws.used;
+    return GSPN_OK;
+}
+
+extern "C" int gspn_latent_fwd(const void *x, const void *p_down, const void *l_u,
+                               const void *l_lam, const void *l_w, const void *p_up, void *y,
+                               int direction, int B, int C, int Cc, int H, int W, int dtype,
+                               void *workspace, int64_t workspace_bytes, void *stream)
+{
+    int st = check_latent_all(direction, B, C, Cc, H, W, dtype);
     if (st != GSPN_OK)
         return st;
     const int64_t D = __builtin_popcount(direction);
     const int64_t HW = (int64_t)H * W;
     const int64_t n = (int64_t)B * C * HW;
     const int64_t cc2 = (int64_t)Cc * Cc;
-    const Buf bufs[] = {{x, n * 2, false},           {p_down, (int64_t)Cc * C * 2, false},
-                        {l_u, D * cc2 * 2, false},   {l_lam, D * cc2 * 2, false},
-                        {l_w, 3 * D * cc2 * 2, false}, {p_up, (int64_t)C * Cc * 2, false},
-                        {y, n * 2, true}};
+    Buf bufs[8] = {{x, n * 2, false},           {p_down, (int64_t)Cc * C * 2, false},
+                   {l_u, D * cc2 * 2, false},   {l_lam, D * cc2 * 2, false},
+                   {l_w, 3 * D * cc2 * 2, false}, {p_up, (int64_t)C * Cc * 2, false},
+                   {y, n * 2, true}};
     st = check_buffers(bufs, 7);
     if (st != GSPN_OK)
         return st;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    // The latent tensors belong to this call, so the scan may run on a grid
-    // padded at the bottom and right to whole 8-line blocks, where the
-    // register-streamed and wide kernels apply.  Padded pixels hold x_c = 0,
-    // hence u = lambda = 0; the taps of real pixels that point into the
-    // padding are normalized as off the grid (weight exactly 0); and a scan
-    // that starts in the padding carries h = 0 up to the first real line,
-    // which then starts from h = lambda x as on the unpadded grid.  Real
-    // pixels therefore see the same recurrence; P_up reads only them.
-    const auto up8 = [](int v) { return (v + 7) / 8 * 8; };
-    const bool pad = (H % 8 != 0 || W % 8 != 0) && (H > 16 || W > 16) && up8(H) <= 256 &&
-                     up8(W) <= 256;
-    const int Hp = pad ? up8(H) : H, Wp = pad ? up8(W) : W;
-    const int64_t ncp = (int64_t)B * Cc * Hp * Wp;
-    // latent x_c, u, lambda, w and y_c in one scratch block, 16-byte aligned parts
-    const int64_t o_u = round8(ncp), o_l = o_u + round8(D * ncp), o_w = o_l + round8(D * ncp);
-    const int64_t o_y = o_w + round8(3 * D * ncp), total = o_y + round8(ncp);
-    void *scr = nullptr;
-    hipError_t e = scratch_alloc(&scr, (size_t)(total * 2), s);
+    Workspace cnt;
+    cnt.counting = true;
+    hipError_t e = run_latent(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H, W, cnt,
+                              nullptr);
     if (e != hipSuccess)
         return hip_status(e);
-    uint16_t *base = static_cast<uint16_t *>(scr);
-    uint16_t *xc = base, *u = base + o_u, *lam = base + o_l, *w = base + o_w, *yc = base + o_y;
-    e = launch_project(p_down, x, xc, B, Cc, C, Hp, Wp, s, H, W);
-    if (e == hipSuccess)
-        e = launch_latent_params(xc, l_u, l_lam, l_w, u, lam, w, direction, B, Cc, Hp, Wp, s, H,
-                                 W);
-    if (e == hipSuccess) {
-        Problem p{xc, w, lam, u, nullptr, yc, nullptr, nullptr, nullptr, nullptr,
-                  direction, B, Cc, Cc, Hp, Wp, GSPN_BF16};
-        e = dispatch_fwd(p, s);
-    }
-    if (e == hipSuccess)
-        e = launch_project(p_up, yc, y, B, C, Cc, H, W, s, Hp, Wp);
-    const hipError_t e2 = scratch_free(scr, s);
-    return hip_status(e != hipSuccess ? e : e2);
+    const int64_t need = (int64_t)cnt.used;
+    if (workspace_bytes < need || workspace == nullptr)
+        return GSPN_ERR_WORKSPACE;
+    bufs[7] = {workspace, need, true};
+    st = check_buffers(bufs, 8);
+    if (st != GSPN_OK)
+        return st;
+    Workspace ws;
+    ws.base = static_cast<char *>(workspace);
+    ws.size = (size_t)workspace_bytes;
+    e = run_latent(x, p_down, l_u, l_lam, l_w, p_up, y, direction, B, C, Cc, H, W, ws,
+                   static_cast<hipStream_t>(stream));
+    return e == hipErrorOutOfMemory ? GSPN_ERR_WORKSPACE : hip_status(e);
 }
 
 extern "C" const char *gspn_strerror(int status)
@@ -390,10 +541,11 @@ extern "C" const char *gspn_strerror(int status)
     case GSPN_ERR_ALIAS: return "two buffers of the call overlap";
     case GSPN_ERR_UNSUPPORTED: return "shape beyond the supported limits";
     case GSPN_ERR_HIP: return "a HIP runtime call or kernel launch failed";
+    case GSPN_ERR_WORKSPACE: return "the workspace is missing or smaller than the call needs";
     default: return "unknown status";
     }
 }
 
 extern "C" int gspn_last_hip_error(void) { return g_last_hip_error; }
 
-extern "C" int gspn_version(void) { return 100; }
+extern "C" int gspn_version(void) { return 200; }

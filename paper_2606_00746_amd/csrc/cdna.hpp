@@ -158,6 +158,64 @@ __device__ __forceinline__ void gst128(uint4 *p, uint4 v)
                  : "memory");
 }
 
+// A lane's 16-byte piece of a per-direction plane: the values of storage
+// lines 8q .. 8q+7 at line position j, in line order (two bf16 per dword,
+// the lower line in the low half).  Blocked line-major planes hold it as one
+// 16-byte piece; in a pixel-major plane it is 8 consecutive pixels of row j
+// for a horizontal direction (one 16-byte access) and 8 pixels of column j,
+// one per row, for a vertical one (eight 2-byte accesses, each a full row
+// across the wave).  P: line length; W: image row length.
+__device__ __forceinline__ uint32_t ld16_nt(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 2 /* nt */);
+}
+// `base`: a byte offset added to the plane (e.g. to reach another tap plane).
+template <bool PM, bool VERT, bool NT>
+__device__ __forceinline__ uint4 ld_piece(rsrc_t r, int j, int q, int P, int W, uint32_t base = 0)
+{
+    if constexpr (!PM) {
+        return NT ? ld128_nt(r, 16u * (uint32_t)j, base + 16u * (uint32_t)(P * q))
+                  : ld128(r, 16u * (uint32_t)j, base + 16u * (uint32_t)(P * q));
+    } else if constexpr (!VERT) {
+        return NT ? ld128_nt(r, 2u * (uint32_t)(W * j), base + 16u * (uint32_t)q)
+                  : ld128(r, 2u * (uint32_t)(W * j), base + 16u * (uint32_t)q);
+    } else {
+        uint32_t v[8];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const uint32_t so = base + 2u * (uint32_t)(W * (8 * q + t));
+            v[t] = NT ? ld16_nt(r, 2u * (uint32_t)j, so) : ld16(r, 2u * (uint32_t)j, so);
+        }
+        return make_uint4(__builtin_amdgcn_perm(v[1], v[0], 0x05040100u),
+                          __builtin_amdgcn_perm(v[3], v[2], 0x05040100u),
+                          __builtin_amdgcn_perm(v[5], v[4], 0x05040100u),
+                          __builtin_amdgcn_perm(v[7], v[6], 0x05040100u));
+    }
+}
+// Stores a piece (see ld_piece).  Blocked planes: one full-line 16-byte
+// store (non-temporal if NT); pixel-major horizontal: one 16-byte store into
+// the row, default policy so that the L2 merges the row's pieces; pixel-major
+// vertical: eight 2-byte stores, each a full row across the wave.
+template <bool PM, bool VERT, bool NT>
+__device__ __forceinline__ void st_piece(const u32x4 &d, int j, int q, int P, int W, uint4 v,
+                                         uint32_t base = 0)
+{
+    if constexpr (!PM) {
+        if (NT)
+            st128_nt(d, 16u * (uint32_t)j, base + 16u * (uint32_t)(P * q), v);
+        else
+            st128(d, 16u * (uint32_t)j, base + 16u * (uint32_t)(P * q), v);
+    } else if constexpr (!VERT) {
+        st128(d, 2u * (uint32_t)(W * j), base + 16u * (uint32_t)q, v);
+    } else {
+        const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+            st16(d, 2u * (uint32_t)j, base + 2u * (uint32_t)(W * (8 * q + t)),
+                 (t & 1) ? (w4[t >> 1] >> 16) : w4[t >> 1]);
+    }
+}
+
 __device__ __forceinline__ float widen(uint32_t v, uint32_t sel)
 {
     return __uint_as_float(__builtin_amdgcn_perm(0u, v, sel));

@@ -59,28 +59,48 @@ __host__ __device__ __forceinline__ int lm_offset(int l, int p, int L, int P)
     return 8 * P * q + n * p + (l & 7);
 }
 
+// Offset of (storage line l, line position p) in a per-direction plane of L
+// lines of P positions, in either layout of the per-direction tensors:
+// pixel-major (pm: the plane is the H x W image, row-major, a line being a
+// row for vertical directions and a column for horizontal ones) or blocked
+// line-major.  W: the image's row length.
+__host__ __device__ __forceinline__ int dir_offset(bool pm, bool vert, int l, int p, int L, int P,
+                                                   int W)
+{
+    return pm ? (vert ? l * W + p : p * W + l) : lm_offset(l, p, L, P);
+}
+
 // Direction index d (direction bit 1 << d), frame position (step i, line
 // position j):
 //   pixel offset  e0 + i * es  in an H x W plane whose rows are `pitch`
 //                              elements apart (pitch = W in global memory,
 //                              padded in LDS);
-//   lm(i)                      blocked line-major offset in a per-direction
-//                              plane.
+//   lm(i)                      offset in a per-direction plane (pixel-major
+//                              or blocked line-major, see dir_offset).
 struct Frame {
     int L;        // scan length
     int P;        // line length
     int e0, es;   // pixel offset of (0, j), change per step
     int j;        // line position
+    int W;        // image row length (pixel-major per-direction planes)
     bool rev;     // the scan visits storage lines in decreasing order
+    bool vert;    // the lines are storage rows
+    bool pm;      // per-direction planes are pixel-major
     __device__ __forceinline__ int line(int i) const { return rev ? L - 1 - i : i; }
-    __device__ __forceinline__ int lm(int i) const { return lm_offset(line(i), j, L, P); }
-    __device__ __forceinline__ int lm_at(int i, int jj) const { return lm_offset(line(i), jj, L, P); }
+    __device__ __forceinline__ int lm(int i) const { return dir_offset(pm, vert, line(i), j, L, P, W); }
+    __device__ __forceinline__ int lm_at(int i, int jj) const
+    {
+        return dir_offset(pm, vert, line(i), jj, L, P, W);
+    }
 };
 
-__device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitch)
+__device__ __forceinline__ Frame make_frame(int d, int j, int H, int W, int pitch, bool pm = false)
 {
     Frame f;
     f.j = j;
+    f.W = W;
+    f.pm = pm;
+    f.vert = d < 2;
     f.rev = d == 1 || d == 3;
     switch (d) {
     case 0:  f.L = H; f.P = W; f.e0 = j;                   f.es = pitch; break;  // T2B

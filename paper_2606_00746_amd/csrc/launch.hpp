@@ -6,14 +6,48 @@
 
 namespace gspn {
 
+// Device memory a call may use beyond its inputs and outputs, handed in by
+// the caller.  take() returns 256-byte aligned pieces in order; nothing is
+// ever returned to it within a call.  In counting mode nothing is launched:
+// the launchers only add up what they would take (the workspace-size query
+// runs the same code as the call).
+struct Workspace {
+    char *base = nullptr;
+    size_t size = 0;
+    size_t used = 0;
+    bool counting = false;
+    // hipErrorOutOfMemory when the caller's workspace is too small (the
+    // library never allocates, so this is the only source of that code)
+    hipError_t take(void **p, size_t bytes)
+    {
+        const size_t off = (used + 255) & ~(size_t)255;
+        used = off + bytes;
+        *p = nullptr;
+        if (counting)
+            return hipSuccess;
+        if (used > size)
+            return hipErrorOutOfMemory;
+        *p = base + off;
+        return hipSuccess;
+    }
+};
+
+// Layout of the per-direction tensors (lam, u, w and their gradients).
+enum Layout { kBlocked = 0, kPixelMajor = 1 };
+
 struct Problem {
     const void *x, *w, *lam, *u, *dy;
     void *y, *dx, *dw, *dlam, *du;
     int mask, B, C, G, H, W, dtype;
+    int layout;
+    Workspace *ws;
 };
 
 // Planes whose sides are both <= kSmallSide run on the register-resident path.
 constexpr int kSmallSide = 64;
+
+// LDS a workgroup may use on gfx950 (the only target of this library).
+constexpr int kLdsBytes = 160 * 1024;
 
 hipError_t launch_fwd_small(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_small(const Problem &p, hipStream_t s);
@@ -46,8 +80,5 @@ hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, 
                                 void *u, void *lam, void *w, int mask, int B, int Cc, int H, int W,
                                 hipStream_t s, int Hv = 0, int Wv = 0);
 
-// Stream-ordered scratch from the device's default pool.
-hipError_t scratch_alloc(void **ptr, size_t bytes, hipStream_t s);
-hipError_t scratch_free(void *ptr, hipStream_t s);
 
 }  // namespace gspn

@@ -29,7 +29,8 @@ __device__ __forceinline__ int nth_dir(int mask, int s)
 template <typename S>
 __global__ __launch_bounds__(kThreads) void fwd_general_kernel(
     const S *__restrict__ x, const S *__restrict__ w, const S *__restrict__ lam,
-    const S *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H, int W)
+    const S *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H, int W,
+    int pm)
 {
     extern __shared__ float hb[];  // [3][P]
     int idx = blockIdx.x;
@@ -53,9 +54,9 @@ __global__ __launch_bounds__(kThreads) void fwd_general_kernel(
         float *cur = hb + (i % 3) * P;
         const float *prev = hb + ((i + 2) % 3) * P;
         for (int j = threadIdx.x; j < P; j += blockDim.x) {
-            const Frame f = make_frame(d, j, H, W, W);
+            const Frame f = make_frame(d, j, H, W, W, pm != 0);
             const int e = f.e0 + i * f.es;   // pixel (x, y slots)
-            const int q = f.lm(i);           // line-major (lam, u, w)
+            const int q = f.lm(i);           // per-direction planes (lam, u, w)
             float v = load_f(lp + q) * load_f(xp + e);
             if (i > 0) {
                 v = fmaf(load_f(wp + HW + q), prev[j], v);
@@ -93,7 +94,7 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
     const S *__restrict__ x, const S *__restrict__ w, const S *__restrict__ lam,
     const S *__restrict__ u, const S *__restrict__ dy, float *__restrict__ dxs,
     float *__restrict__ dws, S *__restrict__ dlam, S *__restrict__ du,
-    float *__restrict__ hs_all, int mask, int B, int C, int G, int H, int W)
+    float *__restrict__ hs_all, int mask, int B, int C, int G, int H, int W, int pm)
 {
     extern __shared__ float ab[];  // [3][P] adjoint lines
     int idx = blockIdx.x;
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
 
         for (int i = 0; i < L; ++i) {
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
-                const Frame f = make_frame(d, j, H, W, W);
+                const Frame f = make_frame(d, j, H, W, W, pm != 0);
                 const int e = f.e0 + i * f.es;
                 const int q = f.lm(i);
                 float v = load_f(lp + q) * load_f(xp + e);
@@ -142,9 +143,9 @@ __global__ __launch_bounds__(kThreads) void bwd_general_kernel(
             float *cur = ab + (i % 3) * P;
             const float *next = ab + ((i + 1) % 3) * P;
             for (int j = threadIdx.x; j < P; j += blockDim.x) {
-                const Frame f = make_frame(d, j, H, W, W);
+                const Frame f = make_frame(d, j, H, W, W, pm != 0);
                 const int e = f.e0 + i * f.es;   // pixel (x, dy, dx slots)
-                const int q = f.lm(i);           // line-major (lam, u, w, dlam, du, dw)
+                const int q = f.lm(i);           // per-direction planes (lam, u, w, dlam, du, dw)
                 const float dyv = load_f(dyp + e);
                 float a = load_f(up + q) * dyv;
                 if (i + 1 < L) {
@@ -194,20 +195,20 @@ hipError_t fwd_general_t(const Problem &p, hipStream_t st)
     const int64_t n = (int64_t)p.B * p.C * p.H * p.W;
     const int maxp = p.H > p.W ? p.H : p.W;
     float *ys = nullptr;
-    hipError_t e = scratch_alloc((void **)&ys, (size_t)D * n * sizeof(float), st);
-    if (e != hipSuccess)
+    hipError_t e = p.ws->take((void **)&ys, (size_t)D * n * sizeof(float));
+    if (e != hipSuccess || p.ws->counting)
         return e;
     hipLaunchKernelGGL((fwd_general_kernel<S>), dim3((unsigned)(D * p.B * p.C)), dim3(kThreads),
                        3 * maxp * sizeof(float), st, (const S *)p.x, (const S *)p.w,
-                       (const S *)p.lam, (const S *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W);
+                       (const S *)p.lam, (const S *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
+                       p.layout);
     e = hipGetLastError();
     if (e == hipSuccess) {
         hipLaunchKernelGGL((sum_slots_kernel<S>), dim3(grid_for(n)), dim3(256), 0, st,
                            (const float *)ys, (S *)p.y, n, D);
         e = hipGetLastError();
     }
-    hipError_t e2 = scratch_free(ys, st);
-    return e != hipSuccess ? e : e2;
+    return e;
 }
 
 template <typename S>
@@ -218,19 +219,18 @@ hipError_t bwd_general_t(const Problem &p, hipStream_t st)
     const int64_t HW = (int64_t)p.H * p.W;
     const int64_t units = (int64_t)D * p.B * p.G;
     const int maxp = p.H > p.W ? p.H : p.W;
-    float *dxs = nullptr, *dws = nullptr, *hs = nullptr;
-    hipError_t e = scratch_alloc((void **)&dxs, (size_t)D * n * sizeof(float), st);
-    if (e == hipSuccess)
-        e = scratch_alloc((void **)&dws, (size_t)units * 3 * HW * sizeof(float), st);
-    if (e == hipSuccess)
-        e = scratch_alloc((void **)&hs, (size_t)units * HW * sizeof(float), st);
-    if (e == hipSuccess) {
-        hipLaunchKernelGGL((bwd_general_kernel<S>), dim3((unsigned)units), dim3(kThreads),
-                           3 * maxp * sizeof(float), st, (const S *)p.x, (const S *)p.w,
-                           (const S *)p.lam, (const S *)p.u, (const S *)p.dy, dxs, dws,
-                           (S *)p.dlam, (S *)p.du, hs, p.mask, p.B, p.C, p.G, p.H, p.W);
-        e = hipGetLastError();
-    }
+    // dx terms per direction, the groups' fp32 weight gradients, line states
+    float *dxs = nullptr;
+    const int64_t nf = D * n + units * 3 * HW + units * HW;
+    hipError_t e = p.ws->take((void **)&dxs, (size_t)nf * sizeof(float));
+    if (e != hipSuccess || p.ws->counting)
+        return e;
+    float *dws = dxs + D * n, *hs = dws + units * 3 * HW;
+    hipLaunchKernelGGL((bwd_general_kernel<S>), dim3((unsigned)units), dim3(kThreads),
+                       3 * maxp * sizeof(float), st, (const S *)p.x, (const S *)p.w,
+                       (const S *)p.lam, (const S *)p.u, (const S *)p.dy, dxs, dws,
+                       (S *)p.dlam, (S *)p.du, hs, p.mask, p.B, p.C, p.G, p.H, p.W, p.layout);
+    e = hipGetLastError();
     if (e == hipSuccess) {
         hipLaunchKernelGGL((sum_slots_kernel<S>), dim3(grid_for(n)), dim3(256), 0, st,
                            (const float *)dxs, (S *)p.dx, n, D);
@@ -240,13 +240,6 @@ hipError_t bwd_general_t(const Problem &p, hipStream_t st)
         hipLaunchKernelGGL((cast_kernel<S>), dim3(grid_for(units * 3 * HW)), dim3(256), 0, st,
                            (const float *)dws, (S *)p.dw, units * 3 * HW);
         e = hipGetLastError();
-    }
-    for (float *ptr : {dxs, dws, hs}) {
-        if (ptr) {
-            hipError_t e2 = scratch_free(ptr, st);
-            if (e == hipSuccess)
-                e = e2;
-        }
     }
     return e;
 }

@@ -96,36 +96,33 @@ struct XPlane {
 // One direction's scan over one channel plane.  D: direction index (0 T2B,
 // 1 B2T, 2 L2R, 3 R2L).  lam, u: the channel's blocked line-major planes; w:
 // the 3 tap planes; xs: the bf16 x plane in LDS.
-template <int H, int W, int D>
+template <int H, int W, int D, bool PM>
 __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t w,
                                              const uint8_t *xs, float (&yr)[64])
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;                 // blocks of 8 lines
-    constexpr uint32_t TB = 16 * P;           // bytes of one block of a plane
     constexpr uint32_t PL = 2 * H * W;        // bytes of one plane
     const Sel s = make_sel(j, P);
     const int jc = j < P ? j : P - 1;
-    const uint32_t vo = 16u * (uint32_t)jc;   // this lane's piece of a block
     // frame block fb (steps 8fb..8fb+7) is storage block fb, or NB-1-fb when
     // the scan runs against the storage order
-    auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
     uint4 rl[NB], ru[NB], r0[NB], r1[NB], r2[NB];
     // lam and u come from HBM once, two blocks ahead; the taps, shared by the
     // group's channels and mostly served by L2, one block ahead
 #define FLOADLU(fb)                                                  \
     do {                                                             \
-        const uint32_t so_ = boff(fb);                               \
-        rl[fb] = ld128_nt(lam, vo, so_);                             \
-        ru[fb] = ld128_nt(u, vo, so_);                               \
+        const int sq_ = REV ? NB - 1 - (fb) : (fb);                  \
+        rl[fb] = ld_piece<PM, VERT, true>(lam, jc, sq_, P, W);       \
+        ru[fb] = ld_piece<PM, VERT, true>(u, jc, sq_, P, W);         \
     } while (0)
 #define FLOADW(fb)                                                   \
     do {                                                             \
-        const uint32_t so_ = boff(fb);                               \
-        r0[fb] = ld128(w, vo, so_);                                  \
-        r1[fb] = ld128(w, vo, so_ + PL);                             \
-        r2[fb] = ld128(w, vo, so_ + 2 * PL);                         \
+        const int sq_ = REV ? NB - 1 - (fb) : (fb);                  \
+        r0[fb] = ld_piece<PM, VERT, false>(w, jc, sq_, P, W);        \
+        r1[fb] = ld_piece<PM, VERT, false>(w, jc, sq_, P, W, PL);    \
+        r2[fb] = ld_piece<PM, VERT, false>(w, jc, sq_, P, W, 2 * PL);\
     } while (0)
     FLOADLU(0);
     FLOADW(0);
@@ -161,7 +158,7 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
 #undef FLOADW
 }
 
-template <int H, int W>
+template <int H, int W, bool PM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void fwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G,
@@ -211,13 +208,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
         const rsrc_t ru = make_rsrc(u + pd, 2 * HW);
         const rsrc_t rw = make_rsrc(w + pw, 6 * HW);
         if (d == 0)
-            scan_fwd_dir<H, W, 0>(lane, rl, ru, rw, xs, yr);
+            scan_fwd_dir<H, W, 0, PM>(lane, rl, ru, rw, xs, yr);
         else if (d == 1)
-            scan_fwd_dir<H, W, 1>(lane, rl, ru, rw, xs, yr);
+            scan_fwd_dir<H, W, 1, PM>(lane, rl, ru, rw, xs, yr);
         else if (d == 2)
-            scan_fwd_dir<H, W, 2>(lane, rl, ru, rw, xs, yr);
+            scan_fwd_dir<H, W, 2, PM>(lane, rl, ru, rw, xs, yr);
         else
-            scan_fwd_dir<H, W, 3>(lane, rl, ru, rw, xs, yr);
+            scan_fwd_dir<H, W, 3, PM>(lane, rl, ru, rw, xs, yr);
     }
     lds_barrier();   // the x plane becomes the merge plane
 
@@ -325,21 +322,19 @@ struct BwdArgs {
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM, bool PC, int NS>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;
-    constexpr uint32_t TB = 16 * P;                     // bytes of one block of a bf16 plane
     constexpr uint32_t PL2 = 2 * H * W;                 // bytes of one bf16 plane
     const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
-    const uint32_t vo = 16u * (uint32_t)jj;             // this lane's piece of a block
     const uint32_t vr = 2u * (uint32_t)jj;              // this lane's bf16 of a pixel row
-    auto boff = [](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
+    auto sblk = [](int fb) { return REV ? NB - 1 - fb : fb; };   // storage block of frame block fb
     auto line_of = [](int i) { return REV ? L - 1 - i : i; };   // storage line of step i
     auto rowoff = [&](int i) -> uint32_t { return 2u * (uint32_t)(line_of(i) * W); };
     auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)pidx(jj, line_of(i))); };
@@ -352,11 +347,11 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         uint32_t rd[VERT ? L : 1];
 #define RLOAD(fb)                                                    \
     do {                                                             \
-        const uint32_t so_ = boff(fb);                               \
-        ru[fb] = ld128_nt(A.u, vo, so_);                             \
-        q0[fb] = ld128(A.w, vo, so_);                                \
-        q1[fb] = ld128(A.w, vo, so_ + PL2);                          \
-        q2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+        const int sq_ = sblk(fb);                                    \
+        ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
+        q0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
+        q1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        q2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
         RLOAD(NB - 1);
         if (NB > 1)
@@ -421,11 +416,11 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     uint32_t rx[VERT ? L : 1];
 #define FLOADB(fb)                                                   \
     do {                                                             \
-        const uint32_t so_ = boff(fb);                               \
-        rl[fb] = ld128_nt(A.lam, vo, so_);                           \
-        p0[fb] = ld128(A.w, vo, so_);                                \
-        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
-        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+        const int sq_ = sblk(fb);                                    \
+        rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
+        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
     FLOADB(0);
     if (NB > 1)
@@ -469,7 +464,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 st32(A.dw, 4u * (f + H * W), 0, __float_as_uint(d1));
                 st32(A.dw, 4u * (f + 2 * H * W), 0, __float_as_uint(d2));
             } else {
-                const uint32_t el = 2u * (uint32_t)lm_offset(l, j, L, P);
+                const uint32_t el = 2u * (uint32_t)dir_offset(PM, VERT, l, j, L, P, W);
                 st16(A.dw, el, 0, pack1(d0));
                 st16(A.dw, el + PL2, 0, pack1(d1));
                 st16(A.dw, el + 2 * PL2, 0, pack1(d2));
@@ -580,13 +575,16 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 }
             }
             if (t == 7 && act) {
-                st128_nt(A.du, vo, boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
-                st128_nt(A.dlam, vo, boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                st_piece<PM, VERT, true>(A.du, jj, sblk(fb), P, W,
+                                         make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                st_piece<PM, VERT, true>(A.dlam, jj, sblk(fb), P, W,
+                                         make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
-                        st128_nt(A.dw, vo, boff(fb) + k * PL2,
-                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]));
+                        st_piece<PM, VERT, true>(A.dw, jj, sblk(fb), P, W,
+                                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]),
+                                                 k * PL2);
                 }
             }
             step_fence();
@@ -603,11 +601,10 @@ struct BwdDir {
     static constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     static constexpr int L = VERT ? H : W, P = VERT ? W : H;
     static constexpr int NB = L / 8;
-    static constexpr uint32_t TB = 16 * P;              // bytes of one block of a bf16 plane
     static constexpr uint32_t PL2 = 2 * H * W;          // bytes of one bf16 plane
     static_assert(L % 8 == 0, "whole blocks");
 
-    __device__ static uint32_t boff(int fb) { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); }
+    __device__ static int sblk(int fb) { return REV ? NB - 1 - fb : fb; }   // storage block
     __device__ static int line_of(int i) { return REV ? L - 1 - i : i; }   // storage line of step i
     // the staged (x, dy) dword of step i at position jj
     __device__ static uint32_t stg_at(const uint8_t *stg, int jj, int i)
@@ -618,7 +615,7 @@ struct BwdDir {
 };
 
 // The weight-gradient sum of step i from the slot values read for it.
-template <int H, int W, int D, int NS>
+template <int H, int W, int D, int NS, bool PM>
 __device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const float (&pa)[NS],
                                          const float (&ph)[NS])
 {
@@ -640,7 +637,7 @@ __device__ __forceinline__ void dw_store(const BwdArgs &A, int j, int i, const f
             st32(A.dw, 4u * (f + H * W), 0, __float_as_uint(d1));
             st32(A.dw, 4u * (f + 2 * H * W), 0, __float_as_uint(d2));
         } else {
-            const uint32_t el = 2u * (uint32_t)lm_offset(l, j, F::L, F::P);
+            const uint32_t el = 2u * (uint32_t)dir_offset(PM, F::VERT, l, j, F::L, F::P, W);
             st16(A.dw, el, 0, pack1(d0));
             st16(A.dw, el + F::PL2, 0, pack1(d1));
             st16(A.dw, el + 2 * F::PL2, 0, pack1(d2));
@@ -666,7 +663,7 @@ __device__ __forceinline__ void read_slots(const BwdArgs &A, int j, int buf, int
 // issues the batch's slot reads after the barrier and finishes the sum 1.5
 // steps later; with fewer than kBatch waves (IMM) each wave takes several
 // steps and sums them right after the barrier.
-template <int H, int W, int D, bool IMM, int NS, class StepOf>
+template <int H, int W, int D, bool IMM, int NS, bool PM, class StepOf>
 __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float a, float hp,
                                           float (&pa)[NS], float (&ph)[NS], StepOf step_of)
 {
@@ -674,7 +671,7 @@ __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float 
     // finish the previous batch: its slot reads were issued after the last
     // barrier and overlapped a step of arithmetic
     if (!IMM && (n & 3) == 1 && n >= 5 && reducer)
-        dw_store<H, W, D, NS>(A, j, step_of(n - 5 + A.wave), pa, ph);
+        dw_store<H, W, D, NS, PM>(A, j, step_of(n - 5 + A.wave), pa, ph);
     const int buf = (n >> 2) & 1;
     slot_pair<NS>(A.slots, buf, n & 3, A.wave)[j] = make_float2(a, hp);
     if ((n & 3) == 3) {
@@ -682,7 +679,7 @@ __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float 
         if (IMM) {
             for (int st = A.wave; st < kBatch; st += A.cw) {
                 read_slots<NS>(A, j, buf, st, pa, ph);
-                dw_store<H, W, D, NS>(A, j, step_of(n - 3 + st), pa, ph);
+                dw_store<H, W, D, NS, PM>(A, j, step_of(n - 3 + st), pa, ph);
             }
         } else if (reducer) {
             read_slots<NS>(A, j, buf, A.wave, pa, ph);
@@ -690,12 +687,12 @@ __device__ __forceinline__ void slot_step(const BwdArgs &A, int j, int n, float 
     }
 }
 
-template <int H, int W, int D, bool IMM, int NS, class StepOf>
+template <int H, int W, int D, bool IMM, int NS, bool PM, class StepOf>
 __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float (&pa)[NS],
                                             const float (&ph)[NS], StepOf step_of)
 {
     if (!IMM && A.wave < kBatch)
-        dw_store<H, W, D, NS>(A, j, step_of(BwdDir<H, W, D>::L - 4 + A.wave), pa, ph);
+        dw_store<H, W, D, NS, PM>(A, j, step_of(BwdDir<H, W, D>::L - 4 + A.wave), pa, ph);
 }
 
 // One horizontal direction of the backward without the adjoint history, for
@@ -707,7 +704,7 @@ __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float
 // reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
 // second read of lam and w (the first one leaves them in L2) and one more h
 // recurrence per step.
-template <int H, int W, int D, bool IMM, bool PC, int NS>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM>
 __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                            float (&dxa)[64])
 {
@@ -718,7 +715,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
     const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
-    const uint32_t vo = 16u * (uint32_t)jj;             // this lane's piece of a block
+    constexpr bool VERT = F::VERT;
 
     // --- forward pass: h at the end of every block ------------------------
     float hck[NB];
@@ -726,11 +723,11 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
         uint4 rl[NB], p0[NB], p1[NB], p2[NB];
 #define ALOAD(fb)                                                    \
     do {                                                             \
-        const uint32_t so_ = F::boff(fb);                            \
-        rl[fb] = ld128(A.lam, vo, so_);                              \
-        p0[fb] = ld128(A.w, vo, so_);                                \
-        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
-        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+        const int sq_ = F::sblk(fb);                                 \
+        rl[fb] = ld_piece<PM, VERT, false>(A.lam, jj, sq_, P, W);    \
+        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
         ALOAD(0);
         if (NB > 1)
@@ -769,12 +766,12 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
     uint4 rl[NB], ru[NB], p0[NB], p1[NB], p2[NB];
 #define BLOAD(fb)                                                    \
     do {                                                             \
-        const uint32_t so_ = F::boff(fb);                            \
-        rl[fb] = ld128_nt(A.lam, vo, so_);                           \
-        ru[fb] = ld128_nt(A.u, vo, so_);                             \
-        p0[fb] = ld128(A.w, vo, so_);                                \
-        p1[fb] = ld128(A.w, vo, so_ + PL2);                          \
-        p2[fb] = ld128(A.w, vo, so_ + 2 * PL2);                      \
+        const int sq_ = F::sblk(fb);                                 \
+        rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
+        ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
+        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
     BLOAD(NB - 1);
     uint32_t xd[NB][8];        // staged (x, dy) of a block, read a block ahead
@@ -854,30 +851,33 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
                         dwp[k][e >> 1] = REV ? pack2(dw1[k], dv[k]) : pack2(dv[k], dw1[k]);
                 }
             } else {
-                slot_step<H, W, D, IMM, NS>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
+                slot_step<H, W, D, IMM, NS, PM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
             }
             if (t == 0 && act) {
-                st128_nt(A.du, vo, F::boff(fb), make_uint4(dup[0], dup[1], dup[2], dup[3]));
-                st128_nt(A.dlam, vo, F::boff(fb), make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                st_piece<PM, VERT, true>(A.du, jj, F::sblk(fb), P, W,
+                                         make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                st_piece<PM, VERT, true>(A.dlam, jj, F::sblk(fb), P, W,
+                                         make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
-                        st128_nt(A.dw, vo, F::boff(fb) + k * F::PL2,
-                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]));
+                        st_piece<PM, VERT, true>(A.dw, jj, F::sblk(fb), P, W,
+                                                 make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]),
+                                                 k * F::PL2);
                 }
             }
             step_fence();
         }
     }
     if constexpr (!PC)
-        slot_finish<H, W, D, IMM, NS>(A, j, pa, ph, step_of);
+        slot_finish<H, W, D, IMM, NS, PM>(A, j, pa, ph, step_of);
 #undef BLOAD
 }
 
 // PC: one channel per weight group; a workgroup then takes cw consecutive
 // channels (groups), each wave sums nothing with the others, and nchunk /
 // divChunk count the workgroups per batch.
-template <int H, int W, bool IMM, bool PC, int NS>
+template <int H, int W, bool IMM, bool PC, int NS, bool PM>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -981,15 +981,15 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM, PC, NS>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
         if ((mask & 4) && H >= 64)
-            dir_bwd_ck<H, W, 3, IMM, PC, NS>(A, lane, cvalid, stg, dxr);
+            dir_bwd_ck<H, W, 3, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM, PC, NS>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
@@ -1002,13 +1002,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC, NS>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM, PC, NS>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -1035,11 +1035,12 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     }
 }
 
-// dw (bf16, blocked line-major) = sum over chunks of the fp32 partials, in
-// chunk order.  Partials are line-major per (chunk, unit, tap): storage line l,
-// position j at float l * S + j.  One thread makes the 8 outputs of one
-// (unit, tap, 8-line block, position): eight reads per chunk and one 16-byte
-// store, both contiguous across the wave.
+// dw (bf16) = sum over chunks of the fp32 partials, in chunk order.
+// Partials are line-major per (chunk, unit, tap): storage line l, position j
+// at float l * S + j.
+// Blocked dw: one thread makes the 8 outputs of one (unit, tap, 8-line
+// block, position): eight reads per chunk and one 16-byte store, both
+// contiguous across the wave.
 template <int S>
 __global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ dwp,
                                                      uint4 *__restrict__ dw, int64_t nuk, int nchunk)
@@ -1064,26 +1065,65 @@ __global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ d
     }
 }
 
-template <int H, int W>
+// The same into pixel-major dw: one thread makes 8 consecutive pixels of an
+// image row (one 16-byte store).  A vertical direction's line is that row
+// (eight contiguous partials); a horizontal direction's lines are the 8
+// columns (partials S apart).  vslots: bit s set when direction slot s is
+// vertical; per_slot: units * 3 of one slot.
+template <int S>
+__global__ __launch_bounds__(256) void dw_sum_pm_kernel(const float *__restrict__ dwp,
+                                                        uint4 *__restrict__ dw, int64_t nuk,
+                                                        int nchunk, int vslots, int64_t per_slot)
+{
+    constexpr int NQ = S / 8, HW = S * S;
+    const int64_t n = nuk * S * NQ;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int cq = (int)(o % NQ);
+        const int64_t rr = o / NQ;
+        const int r = (int)(rr % S);                    // image row
+        const int64_t uk = rr / S;                      // unit * 3 + tap
+        const bool vert = (vslots >> (int)(uk / per_slot)) & 1;
+        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        for (int c = 0; c < nchunk; ++c) {
+            const float *pl = dwp + ((int64_t)c * nuk + uk) * HW;
+            if (vert) {
+#pragma unroll
+                for (int t = 0; t < 8; ++t)
+                    v[t] += pl[r * S + 8 * cq + t];
+            } else {
+#pragma unroll
+                for (int t = 0; t < 8; ++t)
+                    v[t] += pl[(8 * cq + t) * S + r];
+            }
+        }
+        gst128(dw + (uk * HW + (int64_t)r * S + 8 * cq) / 8,
+               make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
+    }
+}
+
+template <int H, int W, bool PM>
 hipError_t fwd_med_t(const Problem &p, hipStream_t st)
 {
-    hipLaunchKernelGGL((fwd_med_kernel<H, W>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
+    if (p.ws->counting)
+        return hipSuccess;
+    hipLaunchKernelGGL((fwd_med_kernel<H, W, PM>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
                        (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
     return hipGetLastError();
 }
 
-template <int H, int W, bool IMM, bool PC, int NS>
+template <int H, int W, bool IMM, bool PC, int NS, bool PM>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
     const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS>), dim3(grid),
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -1092,17 +1132,22 @@ hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, 
     return hipGetLastError();
 }
 
-template <int H, int W>
+// Registers the NS = 4 backward holds per lane (for the occupancy estimate of
+// the slot-count choice); 0 if unknown.
+template <int H, int W, bool PM>
+int bwd_ns4_regs()
+{
+    hipFuncAttributes fa;
+    if (hipFuncGetAttributes(&fa, (const void *)bwd_med_kernel<H, W, false, false, 4, PM>) !=
+        hipSuccess)
+        return 0;
+    return fa.numRegs;
+}
+
+template <int H, int W, bool PM>
 hipError_t bwd_med_t(const Problem &p, hipStream_t st)
 {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess)
-        return e;
-    int lds_max = 0;
-    e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-    if (e != hipSuccess)
-        return e;
+    const int lds_max = kLdsBytes;
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
     const int cpg = p.C / p.G;
     if (cpg == 1) {
@@ -1111,8 +1156,10 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         const int nct = (p.C + cw - 1) / cw;
         if ((size_t)cw * per_ch > (size_t)lds_max)
             return hipErrorInvalidConfiguration;
-        return bwd_med_launch<H, W, false, true, kSlots>(p, st, cw, nct, (size_t)cw * per_ch,
-                                                         nullptr);
+        if (p.ws->counting)
+            return hipSuccess;
+        return bwd_med_launch<H, W, false, true, kSlots, PM>(p, st, cw, nct, (size_t)cw * per_ch,
+                                                             nullptr);
     }
     // A group's channels in nchunk workgroups of cw channels, NS slots per
     // step.  NS = 4 (at most 4 channels, a smaller slot area) is taken where
@@ -1140,16 +1187,11 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         return hipErrorInvalidConfiguration;
     bool use4 = false;
     if (p4.nchunk >= 1 && p4.cw == 4 && p4.nchunk <= p8.nchunk + 1) {
-        int lds_cu = 0;
-        if (hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
-                                  dev) != hipSuccess || lds_cu < lds_max)
-            lds_cu = lds_max;
-        hipFuncAttributes fa;
-        if (hipFuncGetAttributes(&fa, (const void *)bwd_med_kernel<H, W, false, false, 4>) ==
-                hipSuccess && fa.numRegs > 0) {
-            const int per_simd = 512 / ((fa.numRegs + 7) / 8 * 8);   // waves a SIMD holds
+        const int regs = bwd_ns4_regs<H, W, PM>();
+        if (regs > 0) {
+            const int per_simd = 512 / ((regs + 7) / 8 * 8);   // waves a SIMD holds
             auto waves = [&](const Plan &q) {
-                const int by_lds = (int)((size_t)lds_cu / q.lds) * q.cw;
+                const int by_lds = (int)((size_t)kLdsBytes / q.lds) * q.cw;
                 return by_lds < 4 * per_simd ? by_lds : 4 * per_simd;
             };
             use4 = waves(p4) > waves(p8);
@@ -1162,31 +1204,55 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * H * W;
 
     float *dwp = nullptr;
+    hipError_t e = hipSuccess;
     if (nchunk > 1) {
-        e = scratch_alloc((void **)&dwp, (size_t)nchunk * ndw * sizeof(float), st);
+        e = p.ws->take((void **)&dwp, (size_t)nchunk * ndw * sizeof(float));
         if (e != hipSuccess)
             return e;
     }
+    if (p.ws->counting)
+        return hipSuccess;
     if (use4)
-        e = bwd_med_launch<H, W, false, false, 4>(p, st, cw, nchunk, lds, dwp);
+        e = bwd_med_launch<H, W, false, false, 4, PM>(p, st, cw, nchunk, lds, dwp);
     else
-        e = cw >= kBatch ? bwd_med_launch<H, W, false, false, kSlots>(p, st, cw, nchunk, lds, dwp)
-                         : bwd_med_launch<H, W, true, false, kSlots>(p, st, cw, nchunk, lds, dwp);
+        e = cw >= kBatch
+                ? bwd_med_launch<H, W, false, false, kSlots, PM>(p, st, cw, nchunk, lds, dwp)
+                : bwd_med_launch<H, W, true, false, kSlots, PM>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
         int64_t blocks = (n8 + 255) / 256;
         blocks = blocks < 16384 ? blocks : 16384;
-        hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
-                           (const float *)dwp, (uint4 *)p.dw, nuk, nchunk);
+        if (PM) {
+            int vslots = 0;
+            for (int d = 0, sl = 0; d < 4; ++d)
+                if ((p.mask >> d) & 1) {
+                    if (d < 2)
+                        vslots |= 1 << sl;
+                    ++sl;
+                }
+            hipLaunchKernelGGL((dw_sum_pm_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
+                               (const float *)dwp, (uint4 *)p.dw, nuk, nchunk, vslots,
+                               (int64_t)p.B * p.G * 3);
+        } else {
+            hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
+                               (const float *)dwp, (uint4 *)p.dw, nuk, nchunk);
+        }
         e = hipGetLastError();
     }
-    if (dwp) {
-        hipError_t e2 = scratch_free(dwp, st);
-        if (e == hipSuccess)
-            e = e2;
-    }
     return e;
+}
+
+template <int H, int W>
+hipError_t fwd_med_l(const Problem &p, hipStream_t st)
+{
+    return p.layout == kPixelMajor ? fwd_med_t<H, W, true>(p, st) : fwd_med_t<H, W, false>(p, st);
+}
+
+template <int H, int W>
+hipError_t bwd_med_l(const Problem &p, hipStream_t st)
+{
+    return p.layout == kPixelMajor ? bwd_med_t<H, W, true>(p, st) : bwd_med_t<H, W, false>(p, st);
 }
 
 }  // namespace
@@ -1200,24 +1266,24 @@ bool med_supported(const Problem &p)
 hipError_t launch_fwd_med(const Problem &p, hipStream_t st)
 {
     switch (p.H) {
-    case 64: return fwd_med_t<64, 64>(p, st);
-    case 56: return fwd_med_t<56, 56>(p, st);
-    case 48: return fwd_med_t<48, 48>(p, st);
-    case 40: return fwd_med_t<40, 40>(p, st);
-    case 32: return fwd_med_t<32, 32>(p, st);
-    default: return fwd_med_t<24, 24>(p, st);
+    case 64: return fwd_med_l<64, 64>(p, st);
+    case 56: return fwd_med_l<56, 56>(p, st);
+    case 48: return fwd_med_l<48, 48>(p, st);
+    case 40: return fwd_med_l<40, 40>(p, st);
+    case 32: return fwd_med_l<32, 32>(p, st);
+    default: return fwd_med_l<24, 24>(p, st);
     }
 }
 
 hipError_t launch_bwd_med(const Problem &p, hipStream_t st)
 {
     switch (p.H) {
-    case 64: return bwd_med_t<64, 64>(p, st);
-    case 56: return bwd_med_t<56, 56>(p, st);
-    case 48: return bwd_med_t<48, 48>(p, st);
-    case 40: return bwd_med_t<40, 40>(p, st);
-    case 32: return bwd_med_t<32, 32>(p, st);
-    default: return bwd_med_t<24, 24>(p, st);
+    case 64: return bwd_med_l<64, 64>(p, st);
+    case 56: return bwd_med_l<56, 56>(p, st);
+    case 48: return bwd_med_l<48, 48>(p, st);
+    case 40: return bwd_med_l<40, 40>(p, st);
+    case 32: return bwd_med_l<32, 32>(p, st);
+    default: return bwd_med_l<24, 24>(p, st);
     }
 }
 

@@ -10,10 +10,10 @@
 // A group's weights serve all C/G of its channels, so they are formed once
 // here rather than in every channel's scan.
 //
-// Planes are blocked line-major: one 16-byte piece of a full 8-line block
-// holds the 8 consecutive lines of one line position, which decides the
-// validity of taps 0 and 2; a last, partial block is taken element by
-// element.
+// Blocked line-major planes: one 16-byte piece of a full 8-line block holds
+// the 8 consecutive lines of one line position, which decides the validity
+// of taps 0 and 2; a last, partial block is taken element by element.
+// Pixel-major planes: 8 consecutive pixels of an image row at a time.
 #include "cdna.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -179,9 +179,98 @@ __global__ __launch_bounds__(256) void norm_kernel(const T *__restrict__ wt, con
     }
 }
 
+// Pixel-major tap planes ([3][H][W] per set): a thread takes 8 consecutive
+// pixels of an image row when rows are whole 16-byte pieces (vec), else one
+// pixel.  The line position deciding taps 0 and 2 is the column for vertical
+// directions and the row for horizontal ones.
+template <typename T>
+__global__ __launch_bounds__(256) void norm_pm_kernel(const T *__restrict__ wt,
+                                                      const T *__restrict__ dw, T *__restrict__ out,
+                                                      int mask, int64_t sets, int H, int W, bool vec)
+{
+    const int HW = H * W;
+    const int E = vec ? 8 : 1;                      // pixels per thread
+    const int per = HW / E;                         // units per tap-plane triple
+    int dirs[4];
+    int nd = 0;
+    for (int d = 0; d < 4; ++d)
+        if ((mask >> d) & 1)
+            dirs[nd++] = d;
+    const int64_t n = (int64_t)nd * sets * per;
+    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
+         o += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t set = o / per;                // slot * sets + (b, g)
+        const int r = (int)(o - set * per);
+        const int d = dirs[set / sets];
+        const int64_t e = (int64_t)r * E;           // first pixel
+        const int row = (int)(e / W), col0 = (int)(e - (int64_t)row * W);
+        const T *src = wt + set * 3 * HW;
+        const T *gsrc = dw ? dw + set * 3 * HW : nullptr;
+        T *dst = out + set * 3 * HW;
+        if (vec) {
+            float t[3][8], v[3][8];
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                load8(src + k * HW + e, t[k]);
+            float g[3][8];
+            if (gsrc) {
+#pragma unroll
+                for (int k = 0; k < 3; ++k)
+                    load8(gsrc + k * HW + e, g[k]);
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int pos = d < 2 ? col0 + q : row;
+                const int len = d < 2 ? W : H;
+                const bool on0 = pos > 0, on2 = pos + 1 < len;
+                const float tq[3] = {t[0][q], t[1][q], t[2][q]};
+                float r3[3];
+                if (gsrc) {
+                    const float gq[3] = {g[0][q], g[1][q], g[2][q]};
+                    norm3_bwd(tq, gq, on0, on2, r3);
+                } else {
+                    norm3(tq, on0, on2, r3);
+                }
+                v[0][q] = r3[0], v[1][q] = r3[1], v[2][q] = r3[2];
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                store8(dst + k * HW + e, v[k]);
+        } else {
+            const int pos = d < 2 ? col0 : row;
+            const int len = d < 2 ? W : H;
+            const bool on0 = pos > 0, on2 = pos + 1 < len;
+            const float tq[3] = {load_f(src + e), load_f(src + HW + e), load_f(src + 2 * HW + e)};
+            float v[3];
+            if (gsrc) {
+                const float gq[3] = {load_f(gsrc + e), load_f(gsrc + HW + e),
+                                     load_f(gsrc + 2 * HW + e)};
+                norm3_bwd(tq, gq, on0, on2, v);
+            } else {
+                norm3(tq, on0, on2, v);
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                store_f(dst + k * HW + e, v[k]);
+        }
+    }
+}
+
 template <typename T>
 hipError_t launch_norm_t(const Problem &p, const void *wt, const void *dw, void *out, hipStream_t st)
 {
+    if (p.layout == kPixelMajor) {
+        const int64_t HW = (int64_t)p.H * p.W;
+        const int64_t sets = (int64_t)p.B * p.G;
+        const bool vec = p.W % 8 == 0;
+        const int64_t n = (int64_t)__builtin_popcount(p.mask) * sets * (vec ? HW / 8 : HW);
+        int64_t blocks = (n + 255) / 256;
+        blocks = blocks < 16384 ? blocks : 16384;
+        hipLaunchKernelGGL((norm_pm_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           static_cast<const T *>(wt), static_cast<const T *>(dw),
+                           static_cast<T *>(out), p.mask, sets, p.H, p.W, vec);
+        return hipGetLastError();
+    }
     const int64_t HW = (int64_t)p.H * p.W;
     const int64_t sets = (int64_t)p.B * p.G;            // tap-plane triples per direction
     const bool vec = HW % 8 == 0;

@@ -29,7 +29,8 @@ namespace {
 template <int T, typename S>
 __global__ __launch_bounds__(256) void fwd_small_kernel(
     const S *__restrict__ x, const S *__restrict__ w, const S *__restrict__ lam,
-    const S *__restrict__ u, S *__restrict__ y, int mask, int B, int C, int G, int H, int W)
+    const S *__restrict__ u, S *__restrict__ y, int mask, int B, int C, int G, int H, int W,
+    int pm)
 {
     constexpr int NL = 64 / T;        // lines (channels) per wave
     constexpr int PITCH = T + 1;      // odd LDS row pitch: column walks are conflict-free
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
 
     float yr[T];
     if (mine) {
-        const Frame f = make_frame(d, jc, H, W, W);
+        const Frame f = make_frame(d, jc, H, W, W, pm != 0);
         const int s = dir_slot(mask, bit);
         const S *xp = x + ((int64_t)b * C + cc) * HW;
         const int64_t pd = (((int64_t)s * B + b) * C + cc) * HW;
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
         for (int i = 0; i < T; ++i) {
             if (i < f.L) {
                 const int e = f.e0 + i * f.es;   // pixel (x)
-                const int q = f.lm(i);           // line-major (lam, u, w)
+                const int q = f.lm(i);           // per-direction planes (lam, u, w)
                 float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
@@ -127,7 +128,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
     const S *__restrict__ x, const S *__restrict__ w, const S *__restrict__ lam,
     const S *__restrict__ u, const S *__restrict__ dy, S *__restrict__ dx,
     S *__restrict__ dw, S *__restrict__ dlam, S *__restrict__ du, float *__restrict__ dwp,
-    int mask, int B, int C, int G, int H, int W, int cw, int nchunk)
+    int mask, int B, int C, int G, int H, int W, int cw, int nchunk, int pm)
 {
     constexpr int NL = 64 / T;
     extern __shared__ float smem[];
@@ -166,7 +167,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
         const int P = line_len(d, H, W);
         const bool active = cvalid && j < P;
         const int jc = active ? j : 0;
-        const Frame f = make_frame(d, jc, H, W, W);
+        const Frame f = make_frame(d, jc, H, W, W, pm != 0);
         const Frame fl = make_frame(d, jc, H, W, pitch);
         const int64_t pd = (((int64_t)s * B + b) * C + c) * HW;
         const S *lp = lam + pd;
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
         for (int i = 0; i < T; ++i) {
             if (i < L) {
                 const int e = f.e0 + i * f.es;   // pixel (x)
-                const int q = f.lm(i);           // line-major (lam, u, w)
+                const int q = f.lm(i);           // per-direction planes (lam, u, w)
                 float inj = load_f(lp + q) * load_f(xp + e);
                 inj = active ? inj : 0.f;
                 float hn = inj;
@@ -213,7 +214,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
         for (int i = T - 1; i >= 0; --i) {
             if (i < L) {
                 const int e = f.e0 + i * f.es;   // pixel (x, dy)
-                const int qd = f.lm(i);          // line-major (lam, u, w, dlam, du)
+                const int qd = f.lm(i);          // per-direction planes (lam, u, w, dlam, du)
                 const float dyv = load_f(dyp + e);
                 float a = load_f(up + qd) * dyv;
                 if (i + 1 < L) {
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(512) void bwd_small_kernel(
                     float sum = 0.f;
                     for (int qq = 0; qq < nvalid; ++qq)
                         sum += src[qq * 3 * T];
-                    const Frame ft = make_frame(d, jj, H, W, W);
+                    const Frame ft = make_frame(d, jj, H, W, W, pm != 0);
                     const int et = k * HW + ft.lm(i);
                     const int64_t unit = ((int64_t)s * B + b) * G + g;
                     if (nchunk == 1)
@@ -308,12 +309,14 @@ __global__ __launch_bounds__(256) void dw_reduce_kernel(const float *__restrict_
 template <int T, typename S>
 hipError_t fwd_small_t(const Problem &p, hipStream_t st)
 {
+    if (p.ws->counting)
+        return hipSuccess;
     constexpr int NL = 64 / T;
     const int nblk = (p.C + NL - 1) / NL;
     const dim3 grid((unsigned)(p.B * nblk));
     hipLaunchKernelGGL((fwd_small_kernel<T, S>), grid, dim3(256), 0, st,
                        (const S *)p.x, (const S *)p.w, (const S *)p.lam, (const S *)p.u, (S *)p.y,
-                       p.mask, p.B, p.C, p.G, p.H, p.W);
+                       p.mask, p.B, p.C, p.G, p.H, p.W, p.layout);
     return hipGetLastError();
 }
 
@@ -321,14 +324,8 @@ template <int T, typename S>
 hipError_t bwd_small_t(const Problem &p, hipStream_t st)
 {
     constexpr int NL = 64 / T;
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess)
-        return e;
-    int lds_max = 0;
-    e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
-    if (e != hipSuccess)
-        return e;
+    hipError_t e = hipSuccess;
+    const int lds_max = kLdsBytes;
     const int pitch = p.W | 1;
     const size_t per_ch = (size_t)p.H * pitch * 4 + 2 * 3 * T * 4;
     const int cpg = p.C / p.G;
@@ -345,21 +342,23 @@ hipError_t bwd_small_t(const Problem &p, hipStream_t st)
     const int D = __builtin_popcount(p.mask);
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * p.H * p.W;
 
+    float *dwp = nullptr;
+    if (nchunk > 1) {
+        e = p.ws->take((void **)&dwp, (size_t)nchunk * ndw * sizeof(float));
+        if (e != hipSuccess)
+            return e;
+    }
+    if (p.ws->counting)
+        return hipSuccess;
     e = hipFuncSetAttribute((const void *)bwd_small_kernel<T, S>,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    float *dwp = nullptr;
-    if (nchunk > 1) {
-        e = scratch_alloc((void **)&dwp, (size_t)nchunk * ndw * sizeof(float), st);
-        if (e != hipSuccess)
-            return e;
-    }
     const dim3 grid((unsigned)(p.B * p.G * nchunk));
     hipLaunchKernelGGL((bwd_small_kernel<T, S>), grid, dim3(64 * nwaves), lds, st,
                        (const S *)p.x, (const S *)p.w, (const S *)p.lam, (const S *)p.u,
                        (const S *)p.dy, (S *)p.dx, (S *)p.dw, (S *)p.dlam, (S *)p.du, dwp,
-                       p.mask, p.B, p.C, p.G, p.H, p.W, cw, nchunk);
+                       p.mask, p.B, p.C, p.G, p.H, p.W, cw, nchunk, p.layout);
     e = hipGetLastError();
     if (e == hipSuccess && nchunk > 1) {
         int64_t blocks = (ndw + 255) / 256;
@@ -367,11 +366,6 @@ hipError_t bwd_small_t(const Problem &p, hipStream_t st)
         hipLaunchKernelGGL((dw_reduce_kernel<S>), dim3((unsigned)blocks), dim3(256), 0, st,
                            (const float *)dwp, (S *)p.dw, ndw, nchunk);
         e = hipGetLastError();
-    }
-    if (dwp) {
-        hipError_t e2 = scratch_free(dwp, st);
-        if (e == hipSuccess)
-            e = e2;
     }
     return e;
 }

@@ -205,7 +205,7 @@ struct TinyLane {
 };
 
 // Forward of one direction for the four channels of this wave.
-template <int H, int W, int D>
+template <int H, int W, int D, bool PM>
 __device__ __forceinline__ void fwd_tiny_dir(const TinyLds<H, W> &S, const TinyLane &t,
                                              float (&yv)[H], float (&yh)[W])
 {
@@ -219,7 +219,7 @@ __device__ __forceinline__ void fwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
 #pragma unroll
     for (int i = 0; i < L; ++i) {
         const int l = REV ? L - 1 - i : i;
-        const int off = lm_offset(l, jc, L, P);
+        const int off = dir_offset(PM, VERT, l, jc, L, P, W);
         const float lamv = act ? bfv(S.lam, cb + off) : 0.f;
         const float xv = bfv(S.x, cb + (VERT ? l * W + jc : jc * W + l));
         const float inj = lamv * xv;
@@ -289,7 +289,7 @@ __device__ __forceinline__ TinyArgs tiny_args(int C, int G, int cpg, int cw, int
     return a;
 }
 
-template <int H, int W>
+template <int H, int W, bool PM>
 __global__ __launch_bounds__(1024) void fwd_tiny_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G, int cpg,
@@ -337,13 +337,13 @@ __global__ __launch_bounds__(1024) void fwd_tiny_kernel(
             issue(k + 1);
         const TinyLds<H, W> Sb = (k & 1) ? S.other() : S;
         if (d == 0)
-            fwd_tiny_dir<H, W, 0>(Sb, t, yv, yh);
+            fwd_tiny_dir<H, W, 0, PM>(Sb, t, yv, yh);
         else if (d == 1)
-            fwd_tiny_dir<H, W, 1>(Sb, t, yv, yh);
+            fwd_tiny_dir<H, W, 1, PM>(Sb, t, yv, yh);
         else if (d == 2)
-            fwd_tiny_dir<H, W, 2>(Sb, t, yv, yh);
+            fwd_tiny_dir<H, W, 2, PM>(Sb, t, yv, yh);
         else
-            fwd_tiny_dir<H, W, 3>(Sb, t, yv, yh);
+            fwd_tiny_dir<H, W, 3, PM>(Sb, t, yv, yh);
     }
     // the merge plane aliases the first buffer
     lds_barrier();
@@ -353,7 +353,7 @@ __global__ __launch_bounds__(1024) void fwd_tiny_kernel(
 // Backward of one direction for the four channels of this wave.  du and dlam
 // replace u and lam in LDS; the weight-gradient terms, summed over the
 // wave's channels, go to this wave's slots.
-template <int H, int W, int D>
+template <int H, int W, int D, bool PM>
 __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyLane &t, int wave,
                                              float (&dxv)[H], float (&dxh)[W])
 {
@@ -372,11 +372,11 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
 #pragma unroll
     for (int i = L - 1; i >= 0; --i) {
         const int l = line(i);
-        const int off = lm_offset(l, jc, L, P);
+        const int off = dir_offset(PM, VERT, l, jc, L, P, W);
         const float uv = act ? bfv(S.u, cb + off) : 0.f;
         float a = uv * bfv(S.dy, pix(l));
         if (i + 1 < L) {
-            const int offn = lm_offset(line(i + 1), jc, L, P);
+            const int offn = dir_offset(PM, VERT, line(i + 1), jc, L, P, W);
             const float w0 = m0 ? bfv(S.wt, offn) : 0.f;
             const float w1 = act ? bfv(S.wt, HW + offn) : 0.f;
             const float w2 = m2 ? bfv(S.wt, 2 * HW + offn) : 0.f;
@@ -394,7 +394,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
 #pragma unroll
     for (int i = 0; i < L; ++i) {
         const int l = line(i);
-        const int off = lm_offset(l, jc, L, P);
+        const int off = dir_offset(PM, VERT, l, jc, L, P, W);
         const float xv = bfv(S.x, pix(l));
         const float dyv = bfv(S.dy, pix(l));
         const float lamv = act ? bfv(S.lam, cb + off) : 0.f;
@@ -435,7 +435,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
     }
 }
 
-template <int H, int W>
+template <int H, int W, bool PM>
 __global__ __launch_bounds__(1024) void bwd_tiny_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -477,13 +477,13 @@ __global__ __launch_bounds__(1024) void bwd_tiny_kernel(
         stage(S.wt, w + unit * 3 * HW, 3 * HW);
         lds_barrier();
         if (d == 0)
-            bwd_tiny_dir<H, W, 0>(S, t, wave, dxv, dxh);
+            bwd_tiny_dir<H, W, 0, PM>(S, t, wave, dxv, dxh);
         else if (d == 1)
-            bwd_tiny_dir<H, W, 1>(S, t, wave, dxv, dxh);
+            bwd_tiny_dir<H, W, 1, PM>(S, t, wave, dxv, dxh);
         else if (d == 2)
-            bwd_tiny_dir<H, W, 2>(S, t, wave, dxv, dxh);
+            bwd_tiny_dir<H, W, 2, PM>(S, t, wave, dxv, dxh);
         else
-            bwd_tiny_dir<H, W, 3>(S, t, wave, dxv, dxh);
+            bwd_tiny_dir<H, W, 3, PM>(S, t, wave, dxv, dxh);
         lds_barrier();
         unstage(du + pd, S.u, a.nvalid * HW);
         unstage(dlam + pd, S.lam, a.nvalid * HW);
@@ -496,7 +496,7 @@ __global__ __launch_bounds__(1024) void bwd_tiny_kernel(
             for (int q = 0; q < nwaves; ++q)
                 v += S.sl[q * 3 * 256 + (k * 16 + i) * 16 + j];
             const int l = rev ? L - 1 - i : i;
-            const int64_t o = k * HW + lm_offset(l, j, L, P);
+            const int64_t o = k * HW + dir_offset(PM, vert, l, j, L, P, W);
             if (a.nchunk > 1)
                 dwp[((int64_t)a.chunk * D * B * G + unit) * 3 * HW + o] = v;
             else
@@ -529,11 +529,7 @@ struct TinyPlan {
 template <int H, int W>
 bool tiny_plan(const Problem &p, bool bwd, TinyPlan &pl)
 {
-    int dev = 0, lds_max = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
-            hipSuccess)
-        return false;
+    const int lds_max = kLdsBytes;
     pl.cpg = p.C / p.G;
     int cap = kMaxCh;
     while (cap > kSlotW && tiny_lds_bytes<H, W>(cap, bwd) > (size_t)lds_max)
@@ -546,18 +542,20 @@ bool tiny_plan(const Problem &p, bool bwd, TinyPlan &pl)
     return true;
 }
 
-template <int H, int W>
+template <int H, int W, bool PM>
 hipError_t fwd_tiny_t(const Problem &p, hipStream_t st)
 {
     TinyPlan pl;
     if (!tiny_plan<H, W>(p, false, pl))
         return hipErrorInvalidConfiguration;
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_tiny_kernel<H, W>,
+    if (p.ws->counting)
+        return hipSuccess;
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_tiny_kernel<H, W, PM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
     if (e != hipSuccess)
         return e;
     const int nw = (pl.cw + kSlotW - 1) / kSlotW;
-    hipLaunchKernelGGL((fwd_tiny_kernel<H, W>), dim3((unsigned)(p.B * p.G * pl.nchunk)),
+    hipLaunchKernelGGL((fwd_tiny_kernel<H, W, PM>), dim3((unsigned)(p.B * p.G * pl.nchunk)),
                        dim3(64 * nw), pl.lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B,
                        p.C, p.G, pl.cpg, pl.cw, pl.nchunk, make_magic((uint32_t)pl.nchunk),
@@ -565,26 +563,29 @@ hipError_t fwd_tiny_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W>
+template <int H, int W, bool PM>
 hipError_t bwd_tiny_t(const Problem &p, hipStream_t st)
 {
     TinyPlan pl;
     if (!tiny_plan<H, W>(p, true, pl))
         return hipErrorInvalidConfiguration;
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_tiny_kernel<H, W>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
-    if (e != hipSuccess)
-        return e;
     const int D = __builtin_popcount(p.mask);
     const int64_t ndw = (int64_t)D * p.B * p.G * 3 * H * W;
     float *dwp = nullptr;
+    hipError_t e = hipSuccess;
     if (pl.nchunk > 1) {
-        e = scratch_alloc((void **)&dwp, (size_t)pl.nchunk * ndw * sizeof(float), st);
+        e = p.ws->take((void **)&dwp, (size_t)pl.nchunk * ndw * sizeof(float));
         if (e != hipSuccess)
             return e;
     }
+    if (p.ws->counting)
+        return hipSuccess;
+    e = hipFuncSetAttribute((const void *)bwd_tiny_kernel<H, W, PM>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)pl.lds);
+    if (e != hipSuccess)
+        return e;
     const int nw = (pl.cw + kSlotW - 1) / kSlotW;
-    hipLaunchKernelGGL((bwd_tiny_kernel<H, W>), dim3((unsigned)(p.B * p.G * pl.nchunk)),
+    hipLaunchKernelGGL((bwd_tiny_kernel<H, W, PM>), dim3((unsigned)(p.B * p.G * pl.nchunk)),
                        dim3(64 * nw), pl.lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -598,12 +599,19 @@ hipError_t bwd_tiny_t(const Problem &p, hipStream_t st)
                            (const float *)dwp, (bf16_t *)p.dw, ndw, pl.nchunk);
         e = hipGetLastError();
     }
-    if (dwp) {
-        hipError_t e2 = scratch_free(dwp, st);
-        if (e == hipSuccess)
-            e = e2;
-    }
     return e;
+}
+
+template <int H, int W>
+hipError_t fwd_tiny_l(const Problem &p, hipStream_t st)
+{
+    return p.layout == kPixelMajor ? fwd_tiny_t<H, W, true>(p, st) : fwd_tiny_t<H, W, false>(p, st);
+}
+
+template <int H, int W>
+hipError_t bwd_tiny_l(const Problem &p, hipStream_t st)
+{
+    return p.layout == kPixelMajor ? bwd_tiny_t<H, W, true>(p, st) : bwd_tiny_t<H, W, false>(p, st);
 }
 
 }  // namespace
@@ -618,20 +626,20 @@ bool tiny_supported(const Problem &p)
 hipError_t launch_fwd_tiny(const Problem &p, hipStream_t st)
 {
     switch (p.H) {
-    case 8: return fwd_tiny_t<8, 8>(p, st);
-    case 12: return fwd_tiny_t<12, 12>(p, st);
-    case 14: return fwd_tiny_t<14, 14>(p, st);
-    default: return fwd_tiny_t<16, 16>(p, st);
+    case 8: return fwd_tiny_l<8, 8>(p, st);
+    case 12: return fwd_tiny_l<12, 12>(p, st);
+    case 14: return fwd_tiny_l<14, 14>(p, st);
+    default: return fwd_tiny_l<16, 16>(p, st);
     }
 }
 
 hipError_t launch_bwd_tiny(const Problem &p, hipStream_t st)
 {
     switch (p.H) {
-    case 8: return bwd_tiny_t<8, 8>(p, st);
-    case 12: return bwd_tiny_t<12, 12>(p, st);
-    case 14: return bwd_tiny_t<14, 14>(p, st);
-    default: return bwd_tiny_t<16, 16>(p, st);
+    case 8: return bwd_tiny_l<8, 8>(p, st);
+    case 12: return bwd_tiny_l<12, 12>(p, st);
+    case 14: return bwd_tiny_l<14, 14>(p, st);
+    default: return bwd_tiny_l<16, 16>(p, st);
     }
 }
 

@@ -24,8 +24,6 @@
 // through w alone, then every chunk again from its carry; wide_chunks picks
 // the chunk count from the shape.
 #include <algorithm>
-#include <mutex>
-#include <vector>
 
 #include "cdna.hpp"
 #include "device.hpp"
@@ -96,7 +94,7 @@ enum PassMode { kStore, kEnd, kHomog };
 // run time); L, P: scan and line length; the x plane sits in LDS with pitch
 // (W / 2) | 1 dwords; ys receives u * h as fp32 in the direction's
 // line-major order (line l, position p at l * P + p).
-template <int NPL, bool VERT, bool REV, int HC, int WC, int MODE>
+template <int NPL, bool VERT, bool REV, int HC, int WC, int MODE, bool PIX>
 __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, rsrc_t u, rsrc_t w,
                                          const uint8_t *xs, u32x4 ys, int fb0, int fb1,
                                          float (&h)[NPL])
@@ -106,7 +104,6 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
     const int pdw = wide_pitch_dw(W);
     const uint32_t wplane = (uint32_t)(2 * H * W);
     Sel s[NPL];
-    uint32_t vo[NPL];
     int jc[NPL];
     bool valid[NPL];
 #pragma unroll
@@ -115,22 +112,19 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
         valid[m] = p < P;
         s[m] = make_sel(p, P);
         jc[m] = p < P ? p : P - 1;
-        vo[m] = 16u * (uint32_t)jc[m];
     }
     const int NB = L / 8;
-    const uint32_t TB = 16u * (uint32_t)P;     // bytes of one block of a bf16 plane
-    auto boff = [&](int fb) -> uint32_t { return TB * (uint32_t)(REV ? NB - 1 - fb : fb); };
     auto load = [&](Pieces<NPL> &pc, int fb) {
-        const uint32_t so = boff(fb);
+        const int sq = REV ? NB - 1 - fb : fb;   // storage block of frame block fb
 #pragma unroll
         for (int m = 0; m < NPL; ++m) {
             if (MODE != kHomog)
-                pc.l[m] = ld128_nt(lam, vo[m], so);
+                pc.l[m] = ld_piece<PIX, VERT, true>(lam, jc[m], sq, P, W);
             if (MODE == kStore)
-                pc.u[m] = ld128_nt(u, vo[m], so);
-            pc.w0[m] = ld128(w, vo[m], so);
-            pc.w1[m] = ld128(w, vo[m], so + wplane);
-            pc.w2[m] = ld128(w, vo[m], so + 2u * wplane);
+                pc.u[m] = ld_piece<PIX, VERT, true>(u, jc[m], sq, P, W);
+            pc.w0[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W);
+            pc.w1[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W, wplane);
+            pc.w2[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W, 2u * wplane);
         }
     };
 
@@ -194,19 +188,19 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
 }
 
 // Direction d's pass over blocks fb0 .. fb1-1 (direction-uniform dispatch).
-template <int NPL, int HC, int WC, int MODE>
+template <int NPL, int HC, int WC, int MODE, bool PIX>
 __device__ __forceinline__ void wide_pass(int d, int lane, int H, int W, rsrc_t rl, rsrc_t ru,
                                           rsrc_t rw, const uint8_t *xs, u32x4 yd, int fb0,
                                           int fb1, float (&h)[NPL])
 {
     if (d == 0)
-        wide_dir<NPL, true, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, true, false, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else if (d == 1)
-        wide_dir<NPL, true, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, true, true, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else if (d == 2)
-        wide_dir<NPL, false, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, false, false, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else
-        wide_dir<NPL, false, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, false, true, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
 }
 
 // x plane of channel plane pc -> LDS: coalesced 16-byte pieces into padded rows.
@@ -230,7 +224,7 @@ __device__ __forceinline__ void stage_x_plane(const bf16_t *x, int64_t pc, int H
     }
 }
 
-template <int NPL, int HC, int WC>
+template <int NPL, int HC, int WC, bool PIX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H_,
@@ -264,7 +258,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int m = 0; m < NPL; ++m)
             h[m] = 0.f;
         const int NB = (d < 2 ? H : W) / 8;
-        wide_pass<NPL, HC, WC, kStore>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
+        wide_pass<NPL, HC, WC, kStore, PIX>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
     }
 }
 
@@ -280,7 +274,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 //     u * h to the fp32 direction planes; then sum_wide_kernel as usual.
 // States are fp32 [plane][direction slot][chunk][max(H, W)], the first P
 // (the direction's line length) of each slot used.
-template <int NPL, int HC, int WC, int MODE>
+template <int NPL, int HC, int WC, int MODE, bool PIX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_chunk_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, float *__restrict__ st, int mask, int B,
@@ -321,8 +315,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             const int p = lane + 64 * m;
             h[m] = (MODE == kStore && k > 0 && p < P) ? sk[p] : 0.f;
         }
-        wide_pass<NPL, HC, WC, MODE>(d, lane, H, W, rl, ru, rw, xs, yd, k * NBc, (k + 1) * NBc,
-                                     h);
+        wide_pass<NPL, HC, WC, MODE, PIX>(d, lane, H, W, rl, ru, rw, xs, yd, k * NBc,
+                                          (k + 1) * NBc, h);
         if (MODE == kEnd) {
 #pragma unroll
             for (int m = 0; m < NPL; ++m) {
@@ -337,7 +331,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // The carries: for each plane and direction, c_{k+1} = Phi_k c_k + e_k,
 // written over e_{k+1}'s slot neighbour: the state array holds e_k after
 // the first pass and c_k (k >= 1; slot 0 unused) after this one.
-template <int NPL, int HC, int WC>
+template <int NPL, int HC, int WC, bool PIX>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void wide_carry_kernel(
     const bf16_t *__restrict__ w, float *__restrict__ st, int mask, int B, int C, int G, int H_,
     int W_, int K, Magic divC, Magic divCpg)
@@ -357,8 +351,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
     const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
     const int P = d < 2 ? W : H, NBc = (d < 2 ? H : W) / 8 / K;
-    const int PM = H > W ? H : W;   // every slot is max(H, W) long
-    float *sp = st + ((int64_t)plane * D + s) * K * PM;
+    const int SL = H > W ? H : W;   // every slot is max(H, W) long
+    float *sp = st + ((int64_t)plane * D + s) * K * SL;
     float h[NPL], e[NPL];
     // c_1 = e_0
 #pragma unroll
@@ -371,13 +365,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
         for (int m = 0; m < NPL; ++m) {
             const int p = lane + 64 * m;
-            e[m] = p < P ? sp[(int64_t)k * PM + p] : 0.f;
+            e[m] = p < P ? sp[(int64_t)k * SL + p] : 0.f;
             if (p < P)
-                sp[(int64_t)k * PM + p] = h[m];
+                sp[(int64_t)k * SL + p] = h[m];
         }
         if (k + 1 < K) {
-            wide_pass<NPL, HC, WC, kHomog>(d, lane, H, W, rw, rw, rw, nullptr, u32x4{}, k * NBc,
-                                           (k + 1) * NBc, h);
+            wide_pass<NPL, HC, WC, kHomog, PIX>(d, lane, H, W, rw, rw, rw, nullptr, u32x4{},
+                                                k * NBc, (k + 1) * NBc, h);
 #pragma unroll
             for (int m = 0; m < NPL; ++m)
                 h[m] += e[m];
@@ -469,15 +463,15 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
     }
 }
 
-template <int NPL, int HC, int WC>
+template <int NPL, int HC, int WC, bool PIX>
 hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, int plane0,
                       int nplanes)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC, PIX>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)nplanes), dim3(256), lds,
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC, PIX>), dim3((unsigned)nplanes), dim3(256), lds,
                        st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
@@ -486,14 +480,14 @@ hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, i
 }
 
 // The three launches of the chunked forward (see fwd_wide_chunk_kernel).
-template <int NPL, int HC, int WC>
+template <int NPL, int HC, int WC, bool PIX>
 hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float *states,
                               size_t lds, int K)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kEnd, PIX>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e == hipSuccess)
-        e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kStore>,
+        e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kStore, PIX>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
@@ -502,12 +496,12 @@ hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float
     const unsigned planes = (unsigned)(p.B * p.C);
     const bf16_t *x = (const bf16_t *)p.x, *w = (const bf16_t *)p.w;
     const bf16_t *lam = (const bf16_t *)p.lam, *u = (const bf16_t *)p.u;
-    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>), dim3(planes * K), dim3(256),
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kEnd, PIX>), dim3(planes * K), dim3(256),
                        lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
                        divCpg, divNq, divK);
-    hipLaunchKernelGGL((wide_carry_kernel<NPL, HC, WC>), dim3(planes), dim3(256), 0, st, w,
+    hipLaunchKernelGGL((wide_carry_kernel<NPL, HC, WC, PIX>), dim3(planes), dim3(256), 0, st, w,
                        states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC, divCpg);
-    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kStore>), dim3(planes * K), dim3(256),
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kStore, PIX>), dim3(planes * K), dim3(256),
                        lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
                        divCpg, divNq, divK);
     return hipGetLastError();
@@ -527,22 +521,6 @@ hipError_t launch_sum_wide(const Problem &p, const float *ys, hipStream_t st, in
     return hipGetLastError();
 }
 
-// A non-blocking stream of default priority per device, created once, for
-// work that overlaps the caller's stream within one call.
-hipError_t side_stream(int dev, hipStream_t *out)
-{
-    static std::once_flag once[64];
-    static hipStream_t streams[64];
-    static hipError_t status[64];
-    if (dev < 0 || dev >= 64)
-        return hipErrorInvalidDevice;
-    std::call_once(once[dev], [dev] {
-        status[dev] = hipStreamCreateWithFlags(&streams[dev], hipStreamNonBlocking);
-    });
-    *out = streams[dev];
-    return status[dev];
-}
-
 size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
 
 // Chunks per scan for the chunked forward, or 1 for the single pass.  The
@@ -556,11 +534,10 @@ size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
 // every chunk keeps at least 2 line blocks.
 int wide_chunks(const Problem &p, size_t lds)
 {
-    int dev = 0, ncu = 0, lds_cu = 0;
+    int dev = 0, ncu = 0;
+    const int lds_cu = kLdsBytes;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
-            hipSuccess)
+        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return 1;
     const int64_t per_cu = std::max<int64_t>(1, (int64_t)lds_cu / (int64_t)std::max<size_t>(lds, 1));
     const int64_t fit = (int64_t)ncu * std::min<int64_t>(per_cu, 8);
@@ -573,6 +550,31 @@ int wide_chunks(const Problem &p, size_t lds)
     return (K >= 8 && nbh >= 32 && nbw >= 32) ? K : 1;
 }
 
+template <bool PIX>
+hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states, size_t lds, int K)
+{
+    const int side = p.H > p.W ? p.H : p.W;
+    const int npl = (side + 63) / 64;
+    // the square planes of 256 and 128 get kernels with their shape built in
+    if (K > 1) {
+        if (p.H == 256 && p.W == 256)
+            return fwd_wide_chunked_t<4, 256, 256, PIX>(p, st, ys, states, lds, K);
+        if (p.H == 128 && p.W == 128)
+            return fwd_wide_chunked_t<2, 128, 128, PIX>(p, st, ys, states, lds, K);
+        return npl <= 2 ? fwd_wide_chunked_t<2, 0, 0, PIX>(p, st, ys, states, lds, K)
+               : npl == 3 ? fwd_wide_chunked_t<3, 0, 0, PIX>(p, st, ys, states, lds, K)
+                          : fwd_wide_chunked_t<4, 0, 0, PIX>(p, st, ys, states, lds, K);
+    }
+    const int planes = p.B * p.C;
+    if (p.H == 256 && p.W == 256)
+        return fwd_wide_t<4, 256, 256, PIX>(p, st, ys, lds, 0, planes);
+    if (p.H == 128 && p.W == 128)
+        return fwd_wide_t<2, 128, 128, PIX>(p, st, ys, lds, 0, planes);
+    return npl <= 2 ? fwd_wide_t<2, 0, 0, PIX>(p, st, ys, lds, 0, planes)
+           : npl == 3 ? fwd_wide_t<3, 0, 0, PIX>(p, st, ys, lds, 0, planes)
+                      : fwd_wide_t<4, 0, 0, PIX>(p, st, ys, lds, 0, planes);
+}
+
 }  // namespace
 
 bool wide_supported(const Problem &p)
@@ -582,12 +584,7 @@ bool wide_supported(const Problem &p)
     const int side = p.H > p.W ? p.H : p.W;
     if (side > 64 * kMaxNpl)
         return false;
-    int dev = 0, lds_max = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) !=
-            hipSuccess)
-        return false;
-    return wide_lds_bytes(p.H, p.W) <= (size_t)lds_max;
+    return wide_lds_bytes(p.H, p.W) <= (size_t)kLdsBytes;
 }
 
 hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
@@ -599,87 +596,15 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     // fp32 direction planes, then (chunked) the chunk states
     const int64_t nst = K > 1 ? (int64_t)p.B * p.C * D * K * std::max(p.H, p.W) : 0;
     float *ys = nullptr;
-    hipError_t e = scratch_alloc((void **)&ys, (size_t)(D * n + nst) * sizeof(float), st);
-    if (e != hipSuccess)
+    hipError_t e = p.ws->take((void **)&ys, (size_t)(D * n + nst) * sizeof(float));
+    if (e != hipSuccess || p.ws->counting)
         return e;
     float *states = ys + D * n;
-    const int side = p.H > p.W ? p.H : p.W;
-    const int npl = (side + 63) / 64;
-    // the square planes of 256 and 128 get kernels with their shape built in
-    if (K > 1) {
-        if (p.H == 256 && p.W == 256)
-            e = fwd_wide_chunked_t<4, 256, 256>(p, st, ys, states, lds, K);
-        else if (p.H == 128 && p.W == 128)
-            e = fwd_wide_chunked_t<2, 128, 128>(p, st, ys, states, lds, K);
-        else
-            e = npl <= 2 ? fwd_wide_chunked_t<2, 0, 0>(p, st, ys, states, lds, K)
-                : npl == 3 ? fwd_wide_chunked_t<3, 0, 0>(p, st, ys, states, lds, K)
-                           : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
-    } else {
-        // Single pass.  With more planes than fit the device at once, the
-        // planes go in rounds, and each round's direction sum runs on a side
-        // stream while the next round scans: the scan leaves HBM bandwidth
-        // unused, and a sum workgroup fits beside a scan workgroup on a CU.
-        // (with two rounds the extra launches cost more than the overlap gains)
-        const int planes = p.B * p.C;
-        int ncu = 0, dev = 0, lds_cu = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor,
-                                  dev) != hipSuccess)
-            ncu = 0;
-        const int round = ncu * std::max(1, lds_cu / (int)std::max<size_t>(lds, 1));
-        hipStream_t side = nullptr;
-        const bool overlap = ncu > 0 && planes >= 4 * round && side_stream(dev, &side) == hipSuccess;
-        const int step = overlap ? round : planes;
-        std::vector<hipEvent_t> evs;
-        for (int p0 = 0; p0 < planes && e == hipSuccess; p0 += step) {
-            const int np = std::min(step, planes - p0);
-            if (p.H == 256 && p.W == 256)
-                e = fwd_wide_t<4, 256, 256>(p, st, ys, lds, p0, np);
-            else if (p.H == 128 && p.W == 128)
-                e = fwd_wide_t<2, 128, 128>(p, st, ys, lds, p0, np);
-            else
-                e = npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds, p0, np)
-                    : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds, p0, np)
-                               : fwd_wide_t<4, 0, 0>(p, st, ys, lds, p0, np);
-            hipStream_t ss = st;
-            if (e == hipSuccess && overlap) {
-                hipEvent_t ev;
-                e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-                if (e == hipSuccess) {
-                    evs.push_back(ev);
-                    e = hipEventRecord(ev, st);
-                }
-                if (e == hipSuccess)
-                    e = hipStreamWaitEvent(side, ev, 0);
-                ss = side;
-            }
-            if (e == hipSuccess)
-                e = launch_sum_wide(p, ys, ss, p0, np);
-        }
-        if (overlap) {
-            // the caller's stream waits for the last sum
-            hipEvent_t done;
-            hipError_t e3 = hipEventCreateWithFlags(&done, hipEventDisableTiming);
-            if (e3 == hipSuccess) {
-                e3 = hipEventRecord(done, side);
-                if (e3 == hipSuccess)
-                    e3 = hipStreamWaitEvent(st, done, 0);
-                evs.push_back(done);
-            }
-            if (e == hipSuccess)
-                e = e3;
-            for (hipEvent_t ev : evs)
-                (void)hipEventDestroy(ev);   // released once complete
-        }
-        hipError_t e2 = scratch_free(ys, st);
-        return e != hipSuccess ? e : e2;
-    }
+    e = p.layout == kPixelMajor ? fwd_wide_l<true>(p, st, ys, states, lds, K)
+                                : fwd_wide_l<false>(p, st, ys, states, lds, K);
     if (e == hipSuccess)
         e = launch_sum_wide(p, ys, st, 0, p.B * p.C);
-    hipError_t e2 = scratch_free(ys, st);
-    return e != hipSuccess ? e : e2;
+    return e;
 }
 
 }  // namespace gspn

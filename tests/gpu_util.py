@@ -27,9 +27,12 @@ def to_host(t) -> np.ndarray:
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def upload(inputs: dict, dtype: str, dirs: int) -> dict:
-    """Device copies of pixel-major inputs, per-direction tensors line-major."""
-    return {k: to_device(v, dtype) for k, v in gi.inputs_line_major(inputs, dirs).items()}
+def upload(inputs: dict, dtype: str, dirs: int, layout: str = "pixel") -> dict:
+    """Device copies of pixel-major inputs; with layout="blocked" the
+    per-direction tensors go in the blocked line-major layout."""
+    if layout == "blocked":
+        inputs = gi.inputs_line_major(inputs, dirs)
+    return {k: to_device(v, dtype) for k, v in inputs.items()}
 
 
 def normwise_err(a: np.ndarray, r: np.ndarray) -> float:
@@ -39,6 +42,25 @@ def normwise_err(a: np.ndarray, r: np.ndarray) -> float:
     if den == 0.0:
         return num
     return num / den
+
+
+def elementwise_err(a: np.ndarray, r: np.ndarray) -> float:
+    """Diagnostic: max_i |a_i - r_i| / (|r_i| + 1e-3 max|r|)."""
+    if r.size == 0:
+        return 0.0
+    scale = float(np.abs(r).max())
+    if scale == 0.0:
+        return float(np.abs(a - r).max())
+    return float((np.abs(a - r) / (np.abs(r) + 1e-3 * scale)).max())
+
+
+def report(tag: str, key: str, a: np.ndarray, r: np.ndarray) -> float:
+    """Prints the normwise and element-wise errors of one output; returns the
+    normwise one."""
+    err = normwise_err(a, r)
+    print(f"[err] {tag} {key}: normwise {err:.3e} elementwise {elementwise_err(a, r):.3e}",
+          flush=True)
+    return err
 
 
 def tolerance(dtype: str) -> float:

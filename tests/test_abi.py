@@ -47,43 +47,42 @@ def P(i, off=0):
     return BASE + i * (1 << 20) + off
 
 
-def fwd(**kw):
-    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), y=P(4), direction=15, B=1, C=4, G=2, H=8, W=8,
-             dtype=g.BF16, stream=None)
-    a.update(kw)
-    return g.gspn_scan_fwd(a["x"], a["w"], a["lam"], a["u"], a["y"], a["direction"], a["B"],
-                           a["C"], a["G"], a["H"], a["W"], a["dtype"], a["stream"])
+def _fwd_call(fn):
+    def call(**kw):
+        a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), y=P(4), direction=15, B=1, C=4, G=2, H=8,
+                 W=8, dtype=g.BF16, ws=None, ws_bytes=0, stream=None)
+        a.update(kw)
+        return fn(a["x"], a["w"], a["lam"], a["u"], a["y"], a["direction"], a["B"], a["C"],
+                  a["G"], a["H"], a["W"], a["dtype"], a["ws"], a["ws_bytes"], a["stream"])
+    call.fwd = True
+    return call
 
 
-def bwd(**kw):
-    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), dy=P(4), dx=P(5), dw=P(6), dlam=P(7), du=P(8),
-             direction=15, B=1, C=4, G=2, H=8, W=8, dtype=g.BF16, stream=None)
-    a.update(kw)
-    return g.gspn_scan_bwd(a["x"], a["w"], a["lam"], a["u"], a["dy"], a["dx"], a["dw"], a["dlam"],
-                           a["du"], a["direction"], a["B"], a["C"], a["G"], a["H"], a["W"],
-                           a["dtype"], a["stream"])
+def _bwd_call(fn):
+    def call(**kw):
+        a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), dy=P(4), dx=P(5), dw=P(6), dlam=P(7),
+                 du=P(8), direction=15, B=1, C=4, G=2, H=8, W=8, dtype=g.BF16, ws=None,
+                 ws_bytes=0, stream=None)
+        a.update(kw)
+        return fn(a["x"], a["w"], a["lam"], a["u"], a["dy"], a["dx"], a["dw"], a["dlam"],
+                  a["du"], a["direction"], a["B"], a["C"], a["G"], a["H"], a["W"], a["dtype"],
+                  a["ws"], a["ws_bytes"], a["stream"])
+    call.fwd = False
+    return call
 
 
-def fwd_norm(**kw):
-    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), y=P(4), direction=15, B=1, C=4, G=2, H=8, W=8,
-             dtype=g.BF16, stream=None)
-    a.update(kw)
-    return g.gspn_scan_fwd_norm(a["x"], a["w"], a["lam"], a["u"], a["y"], a["direction"], a["B"],
-                                a["C"], a["G"], a["H"], a["W"], a["dtype"], a["stream"])
+fwd = _fwd_call(g.gspn_scan_fwd)
+bwd = _bwd_call(g.gspn_scan_bwd)
+fwd_blocked = _fwd_call(g.gspn_scan_fwd_blocked)
+bwd_blocked = _bwd_call(g.gspn_scan_bwd_blocked)
+fwd_norm = _fwd_call(g.gspn_scan_fwd_norm)
+bwd_norm = _bwd_call(g.gspn_scan_bwd_norm)
 
 
-def bwd_norm(**kw):
-    a = dict(x=P(0), w=P(1), lam=P(2), u=P(3), dy=P(4), dx=P(5), dw=P(6), dlam=P(7), du=P(8),
-             direction=15, B=1, C=4, G=2, H=8, W=8, dtype=g.BF16, stream=None)
-    a.update(kw)
-    return g.gspn_scan_bwd_norm(a["x"], a["w"], a["lam"], a["u"], a["dy"], a["dx"], a["dw"],
-                                a["dlam"], a["du"], a["direction"], a["B"], a["C"], a["G"],
-                                a["H"], a["W"], a["dtype"], a["stream"])
-
-
-@pytest.mark.parametrize("call", [fwd, bwd, fwd_norm, bwd_norm])
+@pytest.mark.parametrize("call", [fwd, bwd, fwd_blocked, bwd_blocked, fwd_norm, bwd_norm],
+                         ids=["fwd", "bwd", "fwd_blocked", "bwd_blocked", "fwd_norm", "bwd_norm"])
 def test_invalid_arguments(call):
-    ptrs = ["x", "w", "lam", "u", "y"] if call in (fwd, fwd_norm) else \
+    ptrs = ["x", "w", "lam", "u", "y"] if call.fwd else \
         ["x", "w", "lam", "u", "dy", "dx", "dw", "dlam", "du"]
     for name in ptrs:
         assert call(**{name: None}) == _native.ERR_NULL, name
@@ -118,18 +117,91 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
         _native.load()
 
 
-@pytest.mark.parametrize("H,W", [(5, 6), (16, 24), (13, 20)])
-def test_torch_layout_helpers_match_numpy(H, W):
-    import numpy as np
+def test_workspace_size_query():
+    # planes of 8 x 8 run on the LDS-staged kernels: no workspace, no device query
+    for op in range(6):
+        st, n = g.gspn_workspace_size(op, 15, 1, 4, 2, 8, 8, g.BF16)
+        assert st == _native.OK and n == (0 if op not in (g.OP_FWD_NORM, g.OP_BWD_NORM) else n)
+    # the _norm passes keep the normalized weights (and their gradient) there:
+    # D * B * G * 3 * H * W elements, 256-byte aligned
+    st, n = g.gspn_workspace_size(g.OP_FWD_NORM, 15, 1, 4, 2, 8, 8, g.BF16)
+    assert st == _native.OK and n == 4 * 2 * 3 * 64 * 2
+    st, n = g.gspn_workspace_size(g.OP_BWD_NORM, 15, 1, 4, 2, 8, 8, g.BF16)
+    assert st == _native.OK and n == 2 * 4 * 2 * 3 * 64 * 2
+    # the general planes (a side above 64) go through fp32 direction slots
+    st, n = g.gspn_workspace_size(g.OP_FWD, 5, 1, 3, 1, 70, 100, g.F32)
+    assert st == _native.OK and n == 2 * 3 * 70 * 100 * 4
+    st, n = g.gspn_workspace_size(g.OP_BWD, 5, 1, 4, 2, 70, 100, g.BF16)
+    D, HW = 2, 7000
+    assert st == _native.OK and n == (D * 4 * HW + D * 2 * 3 * HW + D * 2 * HW) * 4
+    # the same checks as the calls
+    assert g.gspn_workspace_size(g.OP_FWD, 0, 1, 4, 2, 8, 8, g.BF16)[0] == _native.ERR_DIRECTION
+    assert g.gspn_workspace_size(g.OP_FWD, 15, 1, 6, 4, 8, 8, g.BF16)[0] == _native.ERR_DIM
+    assert g.gspn_workspace_size(9, 15, 1, 4, 2, 8, 8, g.BF16)[0] == _native.ERR_UNSUPPORTED
+
+
+# one shape per kernel family and storage type (tiny, register-resident small,
+# register-streamed med, wide, general; bf16 and fp32)
+FAMILY_SHAPES = [(1, 1, "bf16"), (5, 7, "bf16"), (8, 8, "bf16"), (14, 14, "bf16"),
+                 (40, 24, "bf16"), (40, 24, "f32"), (64, 64, "bf16"), (56, 56, "bf16"),
+                 (72, 136, "bf16"), (256, 256, "bf16"), (70, 100, "bf16"), (3, 130, "f32")]
+
+
+@pytest.mark.parametrize("H,W,dt", FAMILY_SHAPES)
+def test_workspace_query_launches_nothing(H, W, dt):
+    """The size query runs the call's own dispatch in counting mode; a kernel
+    launched there would fail on this GPU-less host (and, on a GPU, run on
+    null pointers).  Every family, both layouts, every operation and a
+    single-group, a grouped and a per-channel-weight case must come back OK."""
+    dtype = g.BF16 if dt == "bf16" else g.F32
+    for C, G in ((4, 1), (64, 2), (8, 8)):
+        for op in range(6):
+            for dirs in (15, 1, 6):
+                st, n = g.gspn_workspace_size(op, dirs, 2, C, G, H, W, dtype)
+                assert st == _native.OK and n >= 0, (H, W, dt, C, G, op, dirs, st)
+    st, n = g.gspn_latent_workspace_size(15, 1, 32, 16, H, W, g.BF16)
+    assert st in (_native.OK, _native.ERR_UNSUPPORTED), (H, W, st)
+
+
+def test_workspace_checked_before_any_launch():
+    # a shape that needs workspace (general planes): missing, too small,
+    # misaligned or overlapping workspace is rejected on the host
+    kw = dict(direction=5, B=1, C=4, G=2, H=70, W=100)
+    st, need = g.gspn_workspace_size(g.OP_BWD, 5, 1, 4, 2, 70, 100, g.BF16)
+    assert st == _native.OK and need > 0
+    far = lambda i: BASE + (1 << 32) + i * (1 << 26)     # noqa: E731  (room for big buffers)
+    big = dict(x=far(0), w=far(1), lam=far(2), u=far(3), dy=far(4), dx=far(5), dw=far(6),
+               dlam=far(7), du=far(8))
+    assert bwd(**kw, **big) == _native.ERR_WORKSPACE
+    assert bwd(**kw, **big, ws=far(9), ws_bytes=need - 1) == _native.ERR_WORKSPACE
+    assert bwd(**kw, **big, ws=far(9), ws_bytes=-1) == _native.ERR_WORKSPACE
+    assert bwd(**kw, **big, ws=far(9) + 8, ws_bytes=need) == _native.ERR_ALIGN
+    assert bwd(**kw, **big, ws=far(0), ws_bytes=need) == _native.ERR_ALIAS
+    assert bwd(**kw, **big, ws=far(5), ws_bytes=need) == _native.ERR_ALIAS
+
+
+def test_front_end_rejects_mismatched_tensors():
     import torch
-    import gspn_inputs as gi
-    a = np.random.default_rng(0).standard_normal((4, 2, 4, H, W)).astype(np.float32)
-    for dirs in (15, 7, 12, 1):
-        d = bin(dirs).count("1")
-        t = torch.from_numpy(a[:d].copy())
-        lm = g.to_line_major(t, dirs)
-        np.testing.assert_array_equal(lm.numpy(), gi.to_line_major(a[:d], dirs))
-        np.testing.assert_array_equal(g.from_line_major(lm, dirs, H, W).numpy(), a[:d])
+    x = torch.zeros(1, 4, 8, 8, dtype=torch.bfloat16)
+    lam = torch.zeros(4, 1, 4, 8, 8, dtype=torch.bfloat16)
+    w = torch.zeros(4, 1, 2, 3, 8, 8, dtype=torch.bfloat16)
+    dy = torch.zeros_like(x)
+    with pytest.raises(ValueError, match="lam must hold"):
+        g.scan_fwd(x, w, lam[:2], lam, 15)
+    with pytest.raises(ValueError, match="w must hold"):
+        g.scan_fwd(x, torch.zeros(4, 1, 2, 3, 8, 4, dtype=torch.bfloat16), lam, lam, 15)
+    with pytest.raises(ValueError, match="dtype"):
+        g.scan_fwd(x, w, lam.float(), lam, 15)
+    with pytest.raises(ValueError, match="y must hold"):
+        g.scan_fwd(x, w, lam, lam, 15, y=x[:, :2])
+    with pytest.raises(ValueError, match="dy must hold"):
+        g.scan_bwd(x, w, lam, lam, dy[:, :2], 15)
+    with pytest.raises(ValueError, match="du must hold"):
+        g.scan_bwd(x, w, lam, lam, dy, 15, out=(x, w, lam, lam[:3]))
+    with pytest.raises(ValueError, match="contiguous"):
+        g.scan_fwd(x, w, lam, lam.transpose(-1, -2), 15)
+    with pytest.raises(ValueError, match="GPU"):
+        g.scan_fwd(x, w, lam, lam, 15)
 
 
 def project(**kw):
@@ -150,11 +222,21 @@ def latent_params(**kw):
 
 def latent_fwd(**kw):
     a = dict(x=P(0), p_down=P(1), l_u=P(2), l_lam=P(3), l_w=P(4), p_up=P(5), y=P(6),
-             direction=15, B=1, C=32, Cc=16, H=8, W=8, dtype=g.BF16, stream=None)
+             direction=15, B=1, C=32, Cc=16, H=8, W=8, dtype=g.BF16, ws=P(7), ws_bytes=1 << 20,
+             stream=None)
     a.update(kw)
     return g.gspn_latent_fwd(a["x"], a["p_down"], a["l_u"], a["l_lam"], a["l_w"], a["p_up"],
                              a["y"], a["direction"], a["B"], a["C"], a["Cc"], a["H"], a["W"],
-                             a["dtype"], a["stream"])
+                             a["dtype"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+def test_latent_workspace():
+    st, n = g.gspn_latent_workspace_size(15, 1, 32, 16, 8, 8, g.BF16)
+    # x_c, u, lambda, w (3 taps) and y_c: (2 + 5 D) latent maps of bf16
+    assert st == _native.OK and n == (2 + 5 * 4) * 16 * 64 * 2
+    assert latent_fwd(ws=None) == _native.ERR_WORKSPACE
+    assert latent_fwd(ws_bytes=n - 2) == _native.ERR_WORKSPACE
+    assert latent_fwd(ws=P(0)) == _native.ERR_ALIAS
 
 
 @pytest.mark.parametrize("call,ptrs,dims", [

@@ -13,7 +13,7 @@ import pytest
 import gspn_inputs as gi
 import oracle
 import paper_2606_00746_amd as gspn
-from gpu_util import ignored_taps, normwise_err, require_gpu, to_device, to_host, tolerance, upload
+from gpu_util import ignored_taps, report, require_gpu, to_device, to_host, tolerance, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -37,18 +37,16 @@ CASES = [
 
 def run(wl, inputs, wt):
     torch = require_gpu()
+    print(f"[case] norm {wl.name} B={wl.B} C={wl.C} G={wl.G} {wl.H}x{wl.W} dirs={wl.dirs}",
+          flush=True)
     t = upload(inputs, wl.dtype, wl.dirs)
-    wtd = to_device(gi.to_line_major(wt, wl.dirs), wl.dtype)
+    wtd = to_device(wt, wl.dtype)
     out = {"y": gspn.scan_fwd_norm(t["x"], wtd, t["lam"], t["u"], wl.dirs)}
     if wl.backward:
         dx, dwt, dlam, du = gspn.scan_bwd_norm(t["x"], wtd, t["lam"], t["u"], t["dy"], wl.dirs)
         out.update(dx=dx, dwt=dwt, dlam=dlam, du=du)
     torch.cuda.synchronize()
-    res = {k: to_host(v) for k, v in out.items()}
-    for k in ("dwt", "dlam", "du"):
-        if k in res:
-            res[k] = gi.from_line_major(res[k], wl.dirs, wl.H, wl.W)
-    return res
+    return {k: to_host(v) for k, v in out.items()}
 
 
 @pytest.mark.parametrize("wl", CASES, ids=lambda w: w.name)
@@ -59,13 +57,13 @@ def test_norm_parity_against_oracle(wl):
     tol = tolerance(wl.dtype)
     w = oracle.normalize_w(wt, wl.dirs)
     ref_y = oracle.scan_fwd(inputs["x"], w, inputs["lam"], inputs["u"], wl.dirs)
-    err = normwise_err(got["y"], ref_y)
+    err = report(wl.name, "y", got["y"], ref_y)
     assert err <= tol, f"y err {err:.3g}"
     if wl.backward:
         ref = oracle.scan_bwd(inputs["x"], w, inputs["lam"], inputs["u"], inputs["dy"], wl.dirs)
         ref["dwt"] = oracle.normalize_w_bwd(wt, ref["dw"], wl.dirs)
         for k in ("dx", "dwt", "dlam", "du"):
-            err = normwise_err(got[k], ref[k])
+            err = report(wl.name, k, got[k], ref[k])
             assert err <= tol, f"{k} err {err:.3g}"
         # taps off the grid get exactly zero (those on the first line carry
         # the normalization's share of their row, as in the oracle)

@@ -11,40 +11,45 @@ import pytest
 import gspn_inputs as gi
 import oracle
 import paper_2606_00746_amd as gspn
-from gpu_util import ignored_taps, normwise_err, require_gpu, to_host, tolerance, upload
+from gpu_util import ignored_taps, report, require_gpu, to_host, tolerance, upload
 
 pytestmark = pytest.mark.gpu
 
 GRAD_KEYS = ("dx", "dw", "dlam", "du")
 
 
-def run_gpu(inputs, wl, backward):
-    """Run the library on pixel-major host inputs; returns pixel-major results."""
+def run_gpu(inputs, wl, backward, layout="pixel"):
+    """Run the library on pixel-major host inputs (per-direction tensors in
+    `layout` on the device); returns pixel-major results."""
     torch = require_gpu()
-    t = upload(inputs, wl.dtype, wl.dirs)
-    y = gspn.scan_fwd(t["x"], t["w"], t["lam"], t["u"], wl.dirs)
+    print(f"[case] {wl.name} B={wl.B} C={wl.C} G={wl.G} {wl.H}x{wl.W} dirs={wl.dirs} "
+          f"{wl.dtype} layout={layout}", flush=True)
+    t = upload(inputs, wl.dtype, wl.dirs, layout)
+    y = gspn.scan_fwd(t["x"], t["w"], t["lam"], t["u"], wl.dirs, layout=layout)
     out = {"y": y}
     if backward:
-        dx, dw, dlam, du = gspn.scan_bwd(t["x"], t["w"], t["lam"], t["u"], t["dy"], wl.dirs)
+        dx, dw, dlam, du = gspn.scan_bwd(t["x"], t["w"], t["lam"], t["u"], t["dy"], wl.dirs,
+                                         layout=layout)
         out.update(dx=dx, dw=dw, dlam=dlam, du=du)
     torch.cuda.synchronize()
     res = {k: to_host(v) for k, v in out.items()}
-    for k in ("dw", "dlam", "du"):
-        if k in res:
-            res[k] = gi.from_line_major(res[k], wl.dirs, wl.H, wl.W)
+    if layout == "blocked":
+        for k in ("dw", "dlam", "du"):
+            if k in res:
+                res[k] = gi.from_line_major(res[k], wl.dirs, wl.H, wl.W)
     return res
 
 
 def check_against_oracle(inputs, got, wl, backward, tag=""):
     tol = tolerance(wl.dtype)
     ref_y = oracle.scan_fwd(inputs["x"], inputs["w"], inputs["lam"], inputs["u"], wl.dirs)
-    err = normwise_err(got["y"], ref_y)
+    err = report(tag, "y", got["y"], ref_y)
     assert err <= tol, f"{tag} y err {err:.3g} > {tol}"
     if backward:
         ref = oracle.scan_bwd(inputs["x"], inputs["w"], inputs["lam"], inputs["u"], inputs["dy"],
                               wl.dirs)
         for k in GRAD_KEYS:
-            err = normwise_err(got[k], ref[k])
+            err = report(tag, k, got[k], ref[k])
             assert err <= tol, f"{tag} {k} err {err:.3g} > {tol}"
         ign = ignored_taps(wl.dirs, wl.H, wl.W)          # [D,3,H,W]
         dw = got["dw"]                                    # [D,B,G,3,H,W]
@@ -143,6 +148,43 @@ def test_parity_against_oracle(wl):
     inputs = gi.make_inputs(wl, with_dy=wl.backward)
     got = run_gpu(inputs, wl, wl.backward)
     check_against_oracle(inputs, got, wl, wl.backward, wl.name)
+
+
+# the producer layout (blocked line-major per-direction tensors) on every
+# kernel family
+BLOCKED = [
+    gi.workload(0).with_(name="tiny-f32-bwd", backward=True),
+    gi.workload(1).with_(B=2),
+    gi.workload(2).with_(B=2),
+    gi.workload(3).with_(B=1, C=64, G=2),
+    gi.workload(4).with_(C=8, G=2),
+    case("13x7-G=C", 1, 4, 4, 13, 7),
+    case("general-70x100", 1, 4, 2, 70, 100),
+    case("wide-72x136", 1, 4, 2, 72, 136),
+    case("med64-G=C", 1, 16, 16, 64, 64),
+    case("med56-T2B-cpg12", 2, 24, 2, 56, 56, dirs=1),
+    case("chunk-256x256-c8", 1, 8, 2, 256, 256, backward=False),
+]
+
+
+@pytest.mark.parametrize("wl", BLOCKED, ids=lambda w: w.name)
+def test_blocked_layout_parity(wl):
+    inputs = gi.make_inputs(wl, with_dy=wl.backward)
+    got = run_gpu(inputs, wl, wl.backward, layout="blocked")
+    check_against_oracle(inputs, got, wl, wl.backward, wl.name + " blocked")
+
+
+@pytest.mark.parametrize("wl", [gi.workload(3).with_(B=1, C=64, G=2),
+                                case("tiny-14x14-cpg6-dirs6", 2, 12, 2, 14, 14, dirs=6),
+                                case("general-f32-3x130", 1, 3, 1, 3, 130, dtype="f32",
+                                     gate="normal")], ids=lambda w: w.name)
+def test_layouts_agree_bitwise(wl):
+    """Both layouts run the same arithmetic: identical results."""
+    inputs = gi.make_inputs(wl, with_dy=True)
+    a = run_gpu(inputs, wl, True)
+    b = run_gpu(inputs, wl, True, layout="blocked")
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
 
 
 @pytest.mark.parametrize("wl", [case("nan-taps-14x14", 2, 8, 2, 14, 14),
