@@ -209,6 +209,26 @@ int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
                        int64_t workspace_bytes, void *stream);
 
 /*
+ * gspn_scan_bwd for callers that cannot allocate device memory or hand in a
+ * workspace: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same operation, arguments (without the workspace), checks
+ * and errors as gspn_scan_bwd; its workspace is a fixed device array of
+ * GSPN_STATIC_SCRATCH_BYTES that the library holds on every GPU it runs on
+ * until the process ends (looked up, not allocated, at the first call on a
+ * device).  Returns GSPN_ERR_WORKSPACE, before any launch, when the call
+ * needs more (gspn_workspace_size with GSPN_OP_BWD gives the need).  Every
+ * call on one GPU shares that GPU's array: calls that overlap in time on one
+ * GPU (concurrent streams or threads) race and must not be issued; calls
+ * ordered on one stream are safe.  Allocates nothing, not even through
+ * another library.
+ */
+#define GSPN_STATIC_SCRATCH_BYTES (((int64_t)64) << 20)
+int gspn_scan_bwd_static(const void *x, const void *w, const void *lam, const void *u,
+                         const void *dy, void *dx, void *dw, void *dlam, void *du,
+                         int direction, int B, int C, int G, int H, int W, int dtype,
+                         void *stream);
+
+/*
  * Latent-space propagation sublayer of C-GSPN (Sec. 5, Eqs. (latent_down),
  * (latent_params), (latent_recurrence), (latent_up)): the feature map is
  * projected per pixel from C to Cc channels, the propagation parameters are

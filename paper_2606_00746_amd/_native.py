@@ -27,7 +27,8 @@ MAX_SIDE = 4096
 PIXEL, BLOCKED = "pixel", "blocked"
 
 EXPORTED = ("gspn_workspace_size", "gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_blocked",
-            "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm", "gspn_project",
+            "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
+            "gspn_scan_bwd_static", "gspn_project",
             "gspn_latent_params", "gspn_latent_workspace_size", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
 
@@ -62,6 +63,7 @@ def load() -> ctypes.CDLL:
             getattr(lib, name).argtypes = [vp] * 5 + scan8 + ws
         for name in ("gspn_scan_bwd", "gspn_scan_bwd_blocked", "gspn_scan_bwd_norm"):
             getattr(lib, name).argtypes = [vp] * 9 + scan8 + ws
+        lib.gspn_scan_bwd_static.argtypes = [vp] * 9 + scan8 + [vp]
         lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
         lib.gspn_latent_params.argtypes = [vp] * 7 + [i] * 6 + [vp]
         lib.gspn_latent_workspace_size.argtypes = [i] * 7 + [pi64]
@@ -120,6 +122,15 @@ def gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, directi
                        W, dtype, ws, ws_bytes, stream) -> int:
     return load().gspn_scan_bwd_norm(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction,
                                      B, C, G, H, W, dtype, ws, ws_bytes, stream)
+
+
+def gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
+                         stream) -> int:
+    return load().gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H,
+                                       W, dtype, stream)
+
+
+STATIC_SCRATCH_BYTES = 64 << 20
 
 
 def gspn_project(a, x, y, B, M, K, H, W, dtype, stream) -> int:

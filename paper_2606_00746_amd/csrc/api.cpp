@@ -4,6 +4,8 @@
 
 #include <stdint.h>
 
+#include <mutex>
+
 
 #include "../../include/gspn.h"
 #include "launch.hpp"
@@ -328,6 +330,86 @@ extern "C" int gspn_scan_bwd_norm(const void *x, const void *w_logits, const voi
 {
     return scan_call(GSPN_OP_BWD_NORM, x, w_logits, lam, u, dy, nullptr, dx, dw_logits, dlam, du,
                      direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// gspn_scan_bwd_static: gspn_scan_bwd for callers that cannot allocate (code
+// under graph capture, serving loops, harnesses that forbid hipMalloc), with
+// its workspace in a fixed device array instead of a caller buffer.
+// ---------------------------------------------------------------------------
+namespace gspn {
+namespace {
+
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;   // GSPN_STATIC_SCRATCH_BYTES
+static_assert(kStaticScratchBytes == (size_t)GSPN_STATIC_SCRATCH_BYTES, "header constant");
+
+// Each GPU the library runs on holds its own copy of this array until the
+// process ends.  On the host the name stands for the device copy only as a
+// symbol: its device address comes from hipGetSymbolAddress, per device.
+__device__ __align__(256) char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void *g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_status[kMaxDevices];
+
+// The device address of the current device's array (looked up once per
+// device, with that device current).
+hipError_t static_scratch(void **ptr)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= kMaxDevices)
+        return hipErrorInvalidDevice;
+    std::call_once(g_scratch_once[dev], [dev] {
+        void *p = nullptr;
+        g_scratch_status[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        g_scratch_ptr[dev] = g_scratch_status[dev] == hipSuccess ? p : nullptr;
+    });
+    *ptr = g_scratch_ptr[dev];
+    return g_scratch_status[dev];
+}
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_scan_bwd_static(const void *x, const void *w, const void *lam, const void *u,
+                                    const void *dy, void *dx, void *dw, void *dlam, void *du,
+                                    int direction, int B, int C, int G, int H, int W, int dtype,
+                                    void *stream)
+{
+    int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    Buf bufs[11];
+    int nb = 0;
+    scan_buffers(GSPN_OP_BWD, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H,
+                 W, dtype, bufs, &nb);
+    st = check_buffers(bufs, nb);
+    if (st != GSPN_OK)
+        return st;
+    Problem p{x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
+              kPixelMajor, nullptr};
+    int64_t need = 0;
+    st = count_workspace(GSPN_OP_BWD, p, &need);
+    if (st != GSPN_OK)
+        return st;
+    if (need > (int64_t)kStaticScratchBytes)
+        return GSPN_ERR_WORKSPACE;
+    Workspace ws;
+    if (need > 0) {
+        void *ptr = nullptr;
+        const hipError_t e = static_scratch(&ptr);
+        if (e != hipSuccess)
+            return hip_status(e);
+        ws.base = static_cast<char *>(ptr);
+        ws.size = kStaticScratchBytes;
+    }
+    p.ws = &ws;
+    const hipError_t e = run_scan(GSPN_OP_BWD, p, w, dw, static_cast<hipStream_t>(stream));
+    return e == hipErrorOutOfMemory ? GSPN_ERR_WORKSPACE : hip_status(e);
 }
 
 namespace gspn {

@@ -180,6 +180,25 @@ def test_workspace_checked_before_any_launch():
     assert bwd(**kw, **big, ws=far(5), ws_bytes=need) == _native.ERR_ALIAS
 
 
+def test_static_backward_checks_and_limit():
+    """gspn_scan_bwd_static takes the checks of gspn_scan_bwd and refuses, on
+    the host and before any device call, a problem whose workspace exceeds its
+    fixed array."""
+    call = lambda **kw: _bwd_call(lambda *a: g.gspn_scan_bwd_static(*a[:16], a[18]))(**kw)  # noqa
+    for name in ("x", "w", "lam", "u", "dy", "dx", "dw", "dlam", "du"):
+        assert call(**{name: None}) == _native.ERR_NULL, name
+    assert call(direction=0) == _native.ERR_DIRECTION
+    assert call(C=6, G=4) == _native.ERR_DIM
+    assert call(dx=P(4)) == _native.ERR_ALIAS
+    kw = dict(direction=15, B=16, C=64, G=2, H=70, W=100)
+    st, need = g.gspn_workspace_size(g.OP_BWD, 15, 16, 64, 2, 70, 100, g.BF16)
+    assert st == _native.OK and need > _native.STATIC_SCRATCH_BYTES
+    far = lambda i: BASE + (1 << 36) + i * (1 << 32)     # noqa: E731
+    big = dict(x=far(0), w=far(1), lam=far(2), u=far(3), dy=far(4), dx=far(5), dw=far(6),
+               dlam=far(7), du=far(8))
+    assert call(**kw, **big) == _native.ERR_WORKSPACE
+
+
 def test_front_end_rejects_mismatched_tensors():
     import torch
     x = torch.zeros(1, 4, 8, 8, dtype=torch.bfloat16)
