@@ -10,8 +10,8 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgspn.so")
-SOURCES = ["api.cpp", "scan_tiny.hip", "scan_small.hip", "scan_med.hip", "scan_wide.hip",
-           "scan_norm.hip", "scan_general.hip", "latent.hip"]
+SOURCES = ["api.cpp", "scan_tiny.hip", "scan_small.hip", "scan_med.hip", "scan_pm.hip",
+           "scan_wide.hip", "scan_norm.hip", "scan_general.hip", "latent.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -29,13 +29,23 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, jobs: int = 4) -> str:
+def build(verbose: bool = False, jobs: int = 4, incremental: bool = False) -> str:
+    """Compiles every source (incremental: only those older than their object,
+    counting the shared headers) and links libgspn.so in place."""
     cc = hipcc()
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
 
+    headers = [os.path.join(CSRC, h) for h in os.listdir(CSRC) if h.endswith((".hpp", ".h"))]
+    headers.append(os.path.join(HERE, "..", "include", "gspn.h"))
+    newest_header = max(os.path.getmtime(h) for h in headers)
+
     def compile_one(src):
         obj = os.path.join(objdir, os.path.splitext(src)[0] + ".o")
+        if incremental and os.path.exists(obj):
+            t = os.path.getmtime(obj)
+            if t > os.path.getmtime(os.path.join(CSRC, src)) and t > newest_header:
+                return obj
         lang = ["-x", "hip"]
         cmd = [cc, *HIPCC_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
@@ -61,4 +71,4 @@ def build(verbose: bool = False, jobs: int = 4) -> str:
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, jobs=8, incremental="-i" in sys.argv))

@@ -216,6 +216,19 @@ __device__ __forceinline__ void st_piece(const u32x4 &d, int j, int q, int P, in
     }
 }
 
+// Product and sum that the compiler may not fuse into a multiply-add (the
+// direction sums of the forwards round u_d * h_d, then add, in every layout).
+__device__ __forceinline__ float mul_nc(float a, float b)
+{
+#pragma clang fp contract(off)
+    return a * b;
+}
+__device__ __forceinline__ float add_nc(float a, float b)
+{
+#pragma clang fp contract(off)
+    return a + b;
+}
+
 __device__ __forceinline__ float widen(uint32_t v, uint32_t sel)
 {
     return __uint_as_float(__builtin_amdgcn_perm(0u, v, sel));

@@ -62,6 +62,18 @@ bool med_supported(const Problem &p);
 hipError_t launch_fwd_med(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_med(const Problem &p, hipStream_t s);
 bool wide_supported(const Problem &p);
+// Pixel-major problems of the register-streamed shapes: the weights are
+// re-laid out into the blocked order (launch_w_to_blocked, workspace of
+// |w| bytes) when a group has at least kReblockCpg channels, so that the
+// copy costs at most a quarter of the lambda traffic; then the forward is
+// launch_fwd_pm.
+constexpr int kReblockCpg = 4;
+inline bool pm_weights_reblocked(const Problem &p)
+{
+    return p.layout == kPixelMajor && p.C / p.G >= kReblockCpg;
+}
+hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t s);
+hipError_t launch_fwd_pm(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_wide(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_general(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_general(const Problem &p, hipStream_t s);

@@ -150,7 +150,7 @@ __device__ __forceinline__ void scan_fwd_dir(int j, rsrc_t lam, rsrc_t u, rsrc_t
             else
                 h = tri_step(h, elem(r0[fb], e, s.lo0, s.hi0), elem(r1[fb], e, s.lo1, s.hi1),
                              elem(r2[fb], e, s.lo2, s.hi2), inj);
-            yr[i] = uv * h;
+            yr[i] = mul_nc(uv, h);   // rounded product, added in the merge
         }
         step_fence();
     }
@@ -230,7 +230,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
 #pragma unroll
                     for (int i = 0; i < H; ++i) {
                         float *a = Y + (p == 1 ? H - 1 - i : i) * kYPitch + lane;
-                        *a = st ? yr[i] : *a + yr[i];
+                        *a = st ? yr[i] : add_nc(*a, yr[i]);
                     }
                 }
             } else if (lane < H) {
@@ -247,8 +247,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(4))) void f
                     float4 a1 = make_float4(v[4], v[5], v[6], v[7]);
                     if (!st) {
                         const float4 o0 = a[0], o1 = a[1];
-                        a0 = make_float4(o0.x + a0.x, o0.y + a0.y, o0.z + a0.z, o0.w + a0.w);
-                        a1 = make_float4(o1.x + a1.x, o1.y + a1.y, o1.z + a1.z, o1.w + a1.w);
+                        a0 = make_float4(add_nc(o0.x, a0.x), add_nc(o0.y, a0.y),
+                                         add_nc(o0.z, a0.z), add_nc(o0.w, a0.w));
+                        a1 = make_float4(add_nc(o1.x, a1.x), add_nc(o1.y, a1.y),
+                                         add_nc(o1.z, a1.z), add_nc(o1.w, a1.w));
                     }
                     a[0] = a0;
                     a[1] = a1;
@@ -322,7 +324,7 @@ struct BwdArgs {
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
@@ -349,9 +351,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
         ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
-        q0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
-        q1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        q2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        q0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
+        q1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        q2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
         RLOAD(NB - 1);
         if (NB > 1)
@@ -418,9 +420,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
         rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
-        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
-        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
     FLOADB(0);
     if (NB > 1)
@@ -704,7 +706,7 @@ __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float
 // reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
 // second read of lam and w (the first one leaves them in L2) and one more h
 // recurrence per step.
-template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM>
 __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                            float (&dxa)[64])
 {
@@ -725,9 +727,9 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
     do {                                                             \
         const int sq_ = F::sblk(fb);                                 \
         rl[fb] = ld_piece<PM, VERT, false>(A.lam, jj, sq_, P, W);    \
-        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
-        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
         ALOAD(0);
         if (NB > 1)
@@ -769,9 +771,9 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
         const int sq_ = F::sblk(fb);                                 \
         rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
         ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
-        p0[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W);      \
-        p1[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        p2[fb] = ld_piece<PM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
     } while (0)
     BLOAD(NB - 1);
     uint32_t xd[NB][8];        // staged (x, dy) of a block, read a block ahead
@@ -877,7 +879,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
 // PC: one channel per weight group; a workgroup then takes cw consecutive
 // channels (groups), each wave sums nothing with the others, and nchunk /
 // divChunk count the workgroups per batch.
-template <int H, int W, bool IMM, bool PC, int NS, bool PM>
+template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
@@ -981,15 +983,15 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
     }
     if (mask & 8) {
         setup(3);
         if ((mask & 4) && H >= 64)
-            dir_bwd_ck<H, W, 3, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr);
+            dir_bwd_ck<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
     }
     if (horiz && lane < H) {
@@ -1002,13 +1004,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM, PC, NS, PM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -1114,16 +1116,16 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W, bool IMM, bool PC, int NS, bool PM>
+template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
     const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM>), dim3(grid),
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
@@ -1134,17 +1136,19 @@ hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, 
 
 // Registers the NS = 4 backward holds per lane (for the occupancy estimate of
 // the slot-count choice); 0 if unknown.
-template <int H, int W, bool PM>
+template <int H, int W, bool PM, bool WPM>
 int bwd_ns4_regs()
 {
     hipFuncAttributes fa;
-    if (hipFuncGetAttributes(&fa, (const void *)bwd_med_kernel<H, W, false, false, 4, PM>) !=
+    if (hipFuncGetAttributes(&fa, (const void *)bwd_med_kernel<H, W, false, false, 4, PM, WPM>) !=
         hipSuccess)
         return 0;
     return fa.numRegs;
 }
 
-template <int H, int W, bool PM>
+// WPM: the weights are pixel-major (else blocked, e.g. re-laid out by
+// launch_w_to_blocked); the other per-direction tensors follow PM.
+template <int H, int W, bool PM, bool WPM>
 hipError_t bwd_med_t(const Problem &p, hipStream_t st)
 {
     const int lds_max = kLdsBytes;
@@ -1158,8 +1162,8 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
             return hipErrorInvalidConfiguration;
         if (p.ws->counting)
             return hipSuccess;
-        return bwd_med_launch<H, W, false, true, kSlots, PM>(p, st, cw, nct, (size_t)cw * per_ch,
-                                                             nullptr);
+        return bwd_med_launch<H, W, false, true, kSlots, PM, WPM>(p, st, cw, nct,
+                                                                  (size_t)cw * per_ch, nullptr);
     }
     // A group's channels in nchunk workgroups of cw channels, NS slots per
     // step.  NS = 4 (at most 4 channels, a smaller slot area) is taken where
@@ -1187,7 +1191,7 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
         return hipErrorInvalidConfiguration;
     bool use4 = false;
     if (p4.nchunk >= 1 && p4.cw == 4 && p4.nchunk <= p8.nchunk + 1) {
-        const int regs = bwd_ns4_regs<H, W, PM>();
+        const int regs = bwd_ns4_regs<H, W, PM, WPM>();
         if (regs > 0) {
             const int per_simd = 512 / ((regs + 7) / 8 * 8);   // waves a SIMD holds
             auto waves = [&](const Plan &q) {
@@ -1213,11 +1217,11 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     if (p.ws->counting)
         return hipSuccess;
     if (use4)
-        e = bwd_med_launch<H, W, false, false, 4, PM>(p, st, cw, nchunk, lds, dwp);
+        e = bwd_med_launch<H, W, false, false, 4, PM, WPM>(p, st, cw, nchunk, lds, dwp);
     else
         e = cw >= kBatch
-                ? bwd_med_launch<H, W, false, false, kSlots, PM>(p, st, cw, nchunk, lds, dwp)
-                : bwd_med_launch<H, W, true, false, kSlots, PM>(p, st, cw, nchunk, lds, dwp);
+                ? bwd_med_launch<H, W, false, false, kSlots, PM, WPM>(p, st, cw, nchunk, lds, dwp)
+                : bwd_med_launch<H, W, true, false, kSlots, PM, WPM>(p, st, cw, nchunk, lds, dwp);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
@@ -1246,13 +1250,35 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
 template <int H, int W>
 hipError_t fwd_med_l(const Problem &p, hipStream_t st)
 {
-    return p.layout == kPixelMajor ? fwd_med_t<H, W, true>(p, st) : fwd_med_t<H, W, false>(p, st);
+    if (p.layout != kPixelMajor)
+        return fwd_med_t<H, W, false>(p, st);
+    if (pm_weights_reblocked(p))
+        return launch_fwd_pm(p, st);
+    return fwd_med_t<H, W, true>(p, st);
 }
 
 template <int H, int W>
 hipError_t bwd_med_l(const Problem &p, hipStream_t st)
 {
-    return p.layout == kPixelMajor ? bwd_med_t<H, W, true>(p, st) : bwd_med_t<H, W, false>(p, st);
+    if (p.layout != kPixelMajor)
+        return bwd_med_t<H, W, false, false>(p, st);
+    if (!pm_weights_reblocked(p))
+        return bwd_med_t<H, W, true, true>(p, st);
+    // the group's weights re-laid out once into the blocked order of their
+    // direction (workspace), read there as 16-byte pieces
+    const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * H * W;
+    void *wb = nullptr;
+    hipError_t e = p.ws->take(&wb, (size_t)nw * 2);
+    if (e != hipSuccess)
+        return e;
+    if (!p.ws->counting) {
+        e = launch_w_to_blocked(p, wb, st);
+        if (e != hipSuccess)
+            return e;
+    }
+    Problem q = p;
+    q.w = wb;
+    return bwd_med_t<H, W, true, false>(q, st);
 }
 
 }  // namespace

@@ -1,0 +1,366 @@
+// Pixel-major per-direction tensors on the square bf16 planes of side 24 to
+// 64 (multiples of 8): the forward, and the weight re-layout that both
+// passes start from.
+//
+// A horizontal scan needs a column of every per-direction plane at each step,
+// while a pixel-major plane holds rows: one line of the scan touches every
+// 128-byte row of the plane.  On this GPU a load costs what the lines it
+// touches cost, so the kernels move whole rows only and turn them around on
+// chip:
+//  * the weights, shared by the C/G channels of a group, are re-laid out once
+//    per call into the blocked line-major order of their direction (one
+//    workgroup per tap plane, rows staged in LDS) in the caller's workspace,
+//    where the scans read them as 16-byte pieces of 8 steps;
+//  * the forward stages the x plane and each direction's lambda plane in LDS
+//    with coalesced direct-to-LDS loads (no registers), reads rows for
+//    vertical scans and 16-byte column pieces for horizontal ones, keeps
+//    each lane's states h in registers, and applies u afterwards, row by
+//    row: each direction's h plane goes through an fp32 LDS plane and every
+//    thread adds u_d * h_d for 8 pixels of a row, u_d loaded with coalesced
+//    16-byte row pieces (Sec. 3, Eqs. (gspn_recurrence), (gspn_output)).
+#include "cdna.hpp"
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace gspn {
+
+namespace {
+
+using namespace cdna;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void glb_void;
+
+// Row pitch (bytes) of a staged bf16 plane of side S: whole 16-byte pieces,
+// padded so that the pitch in dwords is 4 mod 8; 8 lanes reading 16 bytes of
+// 8 consecutive rows then hit distinct banks.
+template <int S>
+struct PmPlane {
+    static constexpr int kPitch = 2 * S + ((S / 2) % 8 == 4 ? 0 : 16);
+    static constexpr int kSlots = kPitch / 16;          // 16-byte slots per row
+    static constexpr int kBytes = S * kPitch;
+    // fp32 merge plane: row pitch in floats, 4 mod 8
+    static constexpr int kPitchF = S + ((S % 8) == 4 ? 0 : 4);
+    static constexpr int kBytesF = S * kPitchF * 4;
+};
+
+// Starts the copy of one S x S bf16 plane (row-major, rows of 2S bytes) into
+// LDS rows of PmPlane<S>::kPitch bytes, by the nw waves of the workgroup:
+// wave-instruction k covers slots 64k .. 64k+63 (slot s = row s / kSlots,
+// piece s % kSlots; padding slots are skipped).  The bytes land once the
+// issuing wave has waited for its loads.
+template <int S>
+__device__ __forceinline__ void stage_plane(uint8_t *dst, const bf16_t *src, int wave, int nw,
+                                            int lane)
+{
+    using Pl = PmPlane<S>;
+    constexpr int NS = S * Pl::kSlots;
+    constexpr int NI = (NS + 63) / 64;
+    const uint8_t *g = reinterpret_cast<const uint8_t *>(src);
+    for (int k = wave; k < NI; k += nw) {
+        const int s = 64 * k + lane;
+        const int row = s / Pl::kSlots, pc = s - row * Pl::kSlots;
+        if (s < NS && pc < S / 8)
+            __builtin_amdgcn_global_load_lds((glb_void *)(g + row * 2 * S + 16 * pc),
+                                             (lds_void *)(dst + 1024 * k), 16, 0, 0);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// weights: pixel-major -> blocked line-major, one workgroup per tap plane
+// ---------------------------------------------------------------------------
+
+// Plane pl of the [D][B][G][3] planes (direction slot pl / per_slot, whose
+// direction is vertical when bit slot of vslots is set).  The plane's rows
+// are staged in LDS; then each thread writes 16-byte pieces of the blocked
+// layout (piece (q, p): lines 8q..8q+7 at position p, contiguous across the
+// wave).
+template <int S>
+__global__ __launch_bounds__(256) void w_to_blocked_kernel(const bf16_t *__restrict__ w,
+                                                           uint4 *__restrict__ out, int vslots,
+                                                           int per_slot)
+{
+    using Pl = PmPlane<S>;
+    __shared__ uint4 sm[Pl::kBytes / 16];
+    uint8_t *pl = reinterpret_cast<uint8_t *>(sm);
+    const int p0 = blockIdx.x;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    stage_plane<S>(pl, w + (int64_t)p0 * S * S, wave, 4, lane);
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
+    const bool vert = (vslots >> (p0 / per_slot)) & 1;
+    constexpr int NQ = S / 8;
+    uint4 *dst = out + (int64_t)p0 * (S * S / 8);
+    for (int t = threadIdx.x; t < NQ * S; t += 256) {
+        const int q = t / S, p = t - q * S;               // piece (q, p) at 16 bytes * t
+        uint4 v;
+        if (vert) {
+            // lines are rows: the 8 rows 8q.. of column p
+            uint32_t e[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                e[k] = lds_u16(pl, (8 * q + k) * Pl::kPitch + 2 * p);
+            v = make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                           e[6] | (e[7] << 16));
+        } else {
+            // lines are columns: 8 consecutive columns of row p
+            v = *reinterpret_cast<const uint4 *>(pl + p * Pl::kPitch + 16 * q);
+        }
+        gst128(dst + t, v);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// forward
+// ---------------------------------------------------------------------------
+
+// The scan of direction D over one channel plane: h of every step stays in
+// hr (hr[i] = state of this lane's position after step i).  xs, ls: the
+// staged x and lambda planes; w: the direction's blocked tap planes.
+template <int S, int D>
+__device__ __forceinline__ void pm_fwd_dir(int j, const uint8_t *xs, const uint8_t *ls, rsrc_t w,
+                                           float (&hr)[S])
+{
+    using Pl = PmPlane<S>;
+    constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
+    constexpr int NB = S / 8;
+    constexpr uint32_t PL = 2 * S * S;                 // bytes of one tap plane
+    const Sel s = make_sel(j, S);
+    const int jc = j < S ? j : S - 1;
+    uint4 r0[NB], r1[NB], r2[NB];
+    auto wload = [&](int fb) {
+        const int sq = REV ? NB - 1 - fb : fb;
+        r0[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S);
+        r1[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, PL);
+        r2[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, 2 * PL);
+    };
+    wload(0);
+    if (NB > 1)
+        wload(1);
+    float h = 0.f;
+#pragma unroll
+    for (int fb = 0; fb < NB; ++fb) {
+        if (fb + 2 < NB)
+            wload(fb + 2);
+        const int sq = REV ? NB - 1 - fb : fb;             // storage block
+        uint4 xq, lq;
+        if (!VERT) {
+            // this lane's row, the block's 8 columns: one 16-byte piece each
+            xq = *reinterpret_cast<const uint4 *>(xs + jc * Pl::kPitch + 16 * sq);
+            lq = *reinterpret_cast<const uint4 *>(ls + jc * Pl::kPitch + 16 * sq);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int i = 8 * fb + t;
+            const int e = REV ? 7 - t : t;                 // element of the block's piece
+            float xv, lv;
+            if (VERT) {
+                const int row = 8 * sq + e;
+                xv = bf_lo(lds_u16(xs, row * Pl::kPitch + 2 * jc));
+                lv = widen(lds_u16(ls, row * Pl::kPitch + 2 * jc), s.lo1);
+            } else {
+                xv = elem(xq, e);
+                lv = elem(lq, e, s.lo1, s.hi1);
+            }
+            const float inj = lv * xv;
+            if (i == 0) {
+                h = inj;
+            } else {
+                float hn = fmaf(elem(r1[fb], e, s.lo1, s.hi1), h, inj);
+                hn = fmaf(elem(r0[fb], e, s.lo0, s.hi0), from_left<64>(h), hn);
+                hn = fmaf(elem(r2[fb], e, s.lo2, s.hi2), from_right<64>(h), hn);
+                h = hn;
+            }
+            hr[i] = h;
+        }
+        step_fence();
+    }
+}
+
+// One workgroup per (b, c), one wave per direction.  wb: the blocked weights.
+template <int S>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void fwd_pm_kernel(
+    const bf16_t *__restrict__ x, const bf16_t *__restrict__ wb, const bf16_t *__restrict__ lam,
+    const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G,
+    Magic divC, Magic divCpg)
+{
+    using Pl = PmPlane<S>;
+    constexpr int HW = S * S;
+    constexpr int NCH = HW / 8;                           // 8-pixel pieces of a plane
+    constexpr int PER = (NCH + 255) / 256;                // pieces per thread
+    constexpr int STG = 5 * Pl::kBytes;                   // x + 4 lambda planes
+    constexpr int LB = STG > Pl::kBytesF ? STG : Pl::kBytesF;
+    __shared__ uint4 lds4[LB / 16];
+    uint8_t *base = reinterpret_cast<uint8_t *>(lds4);
+    float *M = reinterpret_cast<float *>(lds4);           // merge plane, after the scans
+
+    const int d = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
+    const int lane = threadIdx.x & 63;
+    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int b = mdiv(blk, divC);
+    const int c = blk - b * C;
+    const int g = mdiv(c, divCpg);
+    const int64_t pc = ((int64_t)b * C + c) * HW;
+
+    // x (plane 0) and every present direction's lambda (plane 1 + d)
+    stage_plane<S>(base, x + pc, d, 4, lane);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        if ((mask >> k) & 1) {
+            const int sk = __popc(mask & ((1 << k) - 1));
+            stage_plane<S>(base + (1 + k) * Pl::kBytes,
+                           lam + (((int64_t)sk * B + b) * C + c) * HW, d, 4, lane);
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
+
+    const bool mine = (mask >> d) & 1;
+    const int s = __popc(mask & ((1 << d) - 1));
+    float hr[S];
+    if (mine) {
+        const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
+        const rsrc_t rw = make_rsrc(wb + pw, 6 * HW);
+        const uint8_t *ls = base + (1 + d) * Pl::kBytes;
+        if (d == 0)
+            pm_fwd_dir<S, 0>(lane, base, ls, rw, hr);
+        else if (d == 1)
+            pm_fwd_dir<S, 1>(lane, base, ls, rw, hr);
+        else if (d == 2)
+            pm_fwd_dir<S, 2>(lane, base, ls, rw, hr);
+        else
+            pm_fwd_dir<S, 3>(lane, base, ls, rw, hr);
+    }
+    lds_barrier();   // the staged planes become the merge plane
+
+    // y = sum_d u_d * h_d, directions in bit order, 8 pixels of a row per
+    // thread and piece
+    float acc[PER][8];
+#pragma unroll
+    for (int k = 0; k < PER; ++k)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            acc[k][e] = 0.f;
+    for (int p = 0; p < 4; ++p) {
+        if (!((mask >> p) & 1))
+            continue;
+        const int sp = __popc(mask & ((1 << p) - 1));
+        const rsrc_t ur = make_rsrc(u + (((int64_t)sp * B + b) * C + c) * HW, 2 * HW);
+        uint4 uq[PER];
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int t = threadIdx.x + 256 * k;
+            uq[k] = t < NCH ? ld128_nt(ur, 16u * (uint32_t)t, 0) : make_uint4(0, 0, 0, 0);
+        }
+        if (d == p && lane < S) {
+            if (p < 2) {
+                // column `lane`, row of step i
+#pragma unroll
+                for (int i = 0; i < S; ++i)
+                    M[(p == 1 ? S - 1 - i : i) * Pl::kPitchF + lane] = hr[i];
+            } else {
+                // row `lane`, column of step i, 16-byte stores
+                float4 *row = reinterpret_cast<float4 *>(M + lane * Pl::kPitchF);
+#pragma unroll
+                for (int q = 0; q < S / 4; ++q) {
+                    float v4[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int col = 4 * q + e;
+                        v4[e] = hr[p == 3 ? S - 1 - col : col];
+                    }
+                    row[q] = make_float4(v4[0], v4[1], v4[2], v4[3]);
+                }
+            }
+        }
+        lds_barrier();
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+            const int t = threadIdx.x + 256 * k;
+            if (t < NCH) {
+                const int r = t / (S / 8), cq = t - r * (S / 8);
+                const float4 *src = reinterpret_cast<const float4 *>(M + r * Pl::kPitchF + 8 * cq);
+                const float4 h0 = src[0], h1 = src[1];
+                const float hv[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+                // u_d * h_d rounded, then added (as the blocked-layout
+                // kernels do: both layouts give the same bits)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    acc[k][e] = add_nc(acc[k][e], mul_nc(elem(uq[k], e), hv[e]));
+            }
+        }
+        lds_barrier();
+    }
+    const u32x4 yo = make_sdesc(y + pc, 2 * HW);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int t = threadIdx.x + 256 * k;
+        if (t < NCH)
+            st128_nt(yo, 16u * (uint32_t)t, 0,
+                     make_uint4(pack2(acc[k][0], acc[k][1]), pack2(acc[k][2], acc[k][3]),
+                                pack2(acc[k][4], acc[k][5]), pack2(acc[k][6], acc[k][7])));
+    }
+}
+
+template <int S>
+hipError_t w_to_blocked_t(const Problem &p, void *wb, hipStream_t st)
+{
+    int vslots = 0;
+    for (int d = 0, sl = 0; d < 4; ++d)
+        if ((p.mask >> d) & 1) {
+            if (d < 2)
+                vslots |= 1 << sl;
+            ++sl;
+        }
+    const int per_slot = p.B * p.G * 3;
+    const int planes = __builtin_popcount(p.mask) * per_slot;
+    hipLaunchKernelGGL((w_to_blocked_kernel<S>), dim3((unsigned)planes), dim3(256), 0, st,
+                       (const bf16_t *)p.w, (uint4 *)wb, vslots, per_slot);
+    return hipGetLastError();
+}
+
+template <int S>
+hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
+{
+    const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * S * S;
+    void *wb = nullptr;
+    hipError_t e = p.ws->take(&wb, (size_t)nw * 2);
+    if (e != hipSuccess || p.ws->counting)
+        return e;
+    e = w_to_blocked_t<S>(p, wb, st);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((fwd_pm_kernel<S>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
+                       (const bf16_t *)p.x, (const bf16_t *)wb, (const bf16_t *)p.lam,
+                       (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
+                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t st)
+{
+    switch (p.H) {
+    case 64: return w_to_blocked_t<64>(p, wb, st);
+    case 56: return w_to_blocked_t<56>(p, wb, st);
+    case 48: return w_to_blocked_t<48>(p, wb, st);
+    case 40: return w_to_blocked_t<40>(p, wb, st);
+    case 32: return w_to_blocked_t<32>(p, wb, st);
+    default: return w_to_blocked_t<24>(p, wb, st);
+    }
+}
+
+hipError_t launch_fwd_pm(const Problem &p, hipStream_t st)
+{
+    switch (p.H) {
+    case 64: return fwd_pm_t<64>(p, st);
+    case 56: return fwd_pm_t<56>(p, st);
+    case 48: return fwd_pm_t<48>(p, st);
+    case 40: return fwd_pm_t<40>(p, st);
+    case 32: return fwd_pm_t<32>(p, st);
+    default: return fwd_pm_t<24>(p, st);
+    }
+}
+
+}  // namespace gspn
