@@ -73,6 +73,8 @@ inline bool pm_weights_reblocked(const Problem &p)
     return p.layout == kPixelMajor && p.C / p.G >= kReblockCpg;
 }
 hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t s);
+// lam and u of the horizontal directions into blocked copies [nh][B][C][plane].
+hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipStream_t s);
 hipError_t launch_fwd_pm(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_wide(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_general(const Problem &p, hipStream_t s);

@@ -332,6 +332,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;
     constexpr uint32_t PL2 = 2 * H * W;                 // bytes of one bf16 plane
+    // lam and u: pixel-major, except horizontal ones whose copies were
+    // re-laid out with the weights (WPM false)
+    constexpr bool LPM = PM && (VERT || WPM);
     const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
@@ -350,7 +353,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #define RLOAD(fb)                                                    \
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
-        ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
+        ru[fb] = ld_piece<LPM, VERT, true>(A.u, jj, sq_, P, W);       \
         q0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
         q1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
         q2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
@@ -419,7 +422,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #define FLOADB(fb)                                                   \
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
-        rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
+        rl[fb] = ld_piece<LPM, VERT, true>(A.lam, jj, sq_, P, W);     \
         p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
         p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
         p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
@@ -576,11 +579,19 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                     }
                 }
             }
+            if (PM && !VERT && act) {
+                // pixel-major horizontal outputs: (du, dlam) of this pixel
+                // replace its staged (x, dy), which no later step of this
+                // direction reads; the plane leaves by whole rows afterwards
+                reinterpret_cast<uint32_t *>(A.Xq)[pidx(jj, line_of(i))] = pack2(duv, dlv);
+            }
             if (t == 7 && act) {
-                st_piece<PM, VERT, true>(A.du, jj, sblk(fb), P, W,
-                                         make_uint4(dup[0], dup[1], dup[2], dup[3]));
-                st_piece<PM, VERT, true>(A.dlam, jj, sblk(fb), P, W,
-                                         make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                if (!PM || VERT) {
+                    st_piece<PM, VERT, true>(A.du, jj, sblk(fb), P, W,
+                                             make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                    st_piece<PM, VERT, true>(A.dlam, jj, sblk(fb), P, W,
+                                             make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                }
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
@@ -718,6 +729,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
     constexpr bool VERT = F::VERT;
+    constexpr bool LPM = PM && (VERT || WPM);           // as in dir_bwd
 
     // --- forward pass: h at the end of every block ------------------------
     float hck[NB];
@@ -726,7 +738,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
 #define ALOAD(fb)                                                    \
     do {                                                             \
         const int sq_ = F::sblk(fb);                                 \
-        rl[fb] = ld_piece<PM, VERT, false>(A.lam, jj, sq_, P, W);    \
+        rl[fb] = ld_piece<LPM, VERT, false>(A.lam, jj, sq_, P, W);    \
         p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
         p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
         p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
@@ -769,8 +781,8 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
 #define BLOAD(fb)                                                    \
     do {                                                             \
         const int sq_ = F::sblk(fb);                                 \
-        rl[fb] = ld_piece<PM, VERT, true>(A.lam, jj, sq_, P, W);     \
-        ru[fb] = ld_piece<PM, VERT, true>(A.u, jj, sq_, P, W);       \
+        rl[fb] = ld_piece<LPM, VERT, true>(A.lam, jj, sq_, P, W);     \
+        ru[fb] = ld_piece<LPM, VERT, true>(A.u, jj, sq_, P, W);       \
         p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
         p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
         p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
@@ -855,11 +867,17 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
             } else {
                 slot_step<H, W, D, IMM, NS, PM>(A, j, L - 1 - i, a, hp, pa, ph, step_of);
             }
+            if (PM && act) {
+                // pixel-major outputs in place of the staged (x, dy) (see dir_bwd)
+                reinterpret_cast<uint32_t *>(A.Xq)[pidx(jj, F::line_of(i))] = pack2(duv, dlv);
+            }
             if (t == 0 && act) {
-                st_piece<PM, VERT, true>(A.du, jj, F::sblk(fb), P, W,
-                                         make_uint4(dup[0], dup[1], dup[2], dup[3]));
-                st_piece<PM, VERT, true>(A.dlam, jj, F::sblk(fb), P, W,
-                                         make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                if (!PM) {
+                    st_piece<PM, VERT, true>(A.du, jj, F::sblk(fb), P, W,
+                                             make_uint4(dup[0], dup[1], dup[2], dup[3]));
+                    st_piece<PM, VERT, true>(A.dlam, jj, F::sblk(fb), P, W,
+                                             make_uint4(dlp[0], dlp[1], dlp[2], dlp[3]));
+                }
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
@@ -885,7 +903,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
     bf16_t *__restrict__ dw, bf16_t *__restrict__ dlam, bf16_t *__restrict__ du,
     float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk, Magic divChunk,
-    Magic divG)
+    Magic divG, const bf16_t *__restrict__ lamh, const bf16_t *__restrict__ uh)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
@@ -937,7 +955,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     // registers (this lane's row) and move into the dx plane afterwards.
     const bool horiz = (mask & 12) != 0;
     const uint8_t *stg = reinterpret_cast<const uint8_t *>(A.Xq);
-    if (horiz) {
+    auto stage_xdy = [&]() {
         uint32_t *st = reinterpret_cast<uint32_t *>(A.Xq);
         constexpr int NP = HW / 8;                          // 16-byte pieces per plane
 #pragma unroll
@@ -958,7 +976,36 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
             }
         }
         // the same wave reads what it wrote: LDS keeps its order
-    }
+    };
+    if (horiz)
+        stage_xdy();
+    // Pixel-major horizontal directions leave du and dlam in the plane, one
+    // (du, dlam) pair per pixel: out by whole rows, lane t taking 8
+    // consecutive columns of a row.
+    auto flush_out = [&]() {
+        if (!cvalid)
+            return;
+        constexpr int NP = HW / 8;
+#pragma unroll
+        for (int it = 0; it < (NP + 63) / 64; ++it) {
+            const int t = it * 64 + lane;
+            if (t < NP) {
+                const int r = t / (W / 8), cm = t - r * (W / 8);
+                uint32_t v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    v[e] = reinterpret_cast<const uint32_t *>(A.Xq)[pidx(r, 8 * cm + e)];
+                uint32_t du4[4], dl4[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    du4[e] = __builtin_amdgcn_perm(v[2 * e + 1], v[2 * e], 0x05040100u);
+                    dl4[e] = __builtin_amdgcn_perm(v[2 * e + 1], v[2 * e], 0x07060302u);
+                }
+                st128_nt(A.du, 16u * (uint32_t)t, 0, make_uint4(du4[0], du4[1], du4[2], du4[3]));
+                st128_nt(A.dlam, 16u * (uint32_t)t, 0, make_uint4(dl4[0], dl4[1], dl4[2], dl4[3]));
+            }
+        }
+    };
 
     // Per-direction descriptors.  An idle wave (no channel left in this
     // chunk) still joins every barrier; it reads channel `c` of the chunk,
@@ -967,8 +1014,15 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         const int s = __popc(mask & ((1 << d) - 1));
         const int64_t pd = (((int64_t)s * B + b) * C + c) * HW;
         const int64_t unit = ((int64_t)s * B + b) * G + g;
-        A.lam = make_rsrc(lam + pd, 2 * HW);
-        A.u = make_rsrc(u + pd, 2 * HW);
+        if (PM && !WPM && d >= 2) {
+            // the re-laid-out copies hold the horizontal slots only
+            const int64_t ph = (((int64_t)(s - __popc(mask & 3)) * B + b) * C + c) * HW;
+            A.lam = make_rsrc(lamh + ph, 2 * HW);
+            A.u = make_rsrc(uh + ph, 2 * HW);
+        } else {
+            A.lam = make_rsrc(lam + pd, 2 * HW);
+            A.u = make_rsrc(u + pd, 2 * HW);
+        }
         A.dlam = make_sdesc(dlam + pd, 2 * HW);
         A.du = make_sdesc(du + pd, 2 * HW);
         A.w = make_rsrc(w + unit * 3 * HW, 6 * HW);
@@ -985,6 +1039,11 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         setup(2);
         dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
+        if (PM) {
+            flush_out();
+            if (mask & 8)
+                stage_xdy();   // x and dy again for the other horizontal direction
+        }
     }
     if (mask & 8) {
         setup(3);
@@ -993,6 +1052,8 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         else
             dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
+        if (PM)
+            flush_out();
     }
     if (horiz && lane < H) {
         // the horizontal dx terms (this lane's row) seed the dx plane that the
@@ -1067,40 +1128,49 @@ __global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ d
     }
 }
 
-// The same into pixel-major dw: one thread makes 8 consecutive pixels of an
-// image row (one 16-byte store).  A vertical direction's line is that row
-// (eight contiguous partials); a horizontal direction's lines are the 8
-// columns (partials S apart).  vslots: bit s set when direction slot s is
-// vertical; per_slot: units * 3 of one slot.
+// The same into pixel-major dw, one workgroup per (unit, tap) plane.  A
+// vertical direction's lines are image rows: each thread sums and stores 8
+// consecutive pixels of a row.  A horizontal direction's lines are columns:
+// the partials are read along their lines (coalesced), summed, turned around
+// through LDS, and stored by rows.  vslots: bit s set when direction slot s
+// is vertical; per_slot: units * 3 of one slot.
 template <int S>
 __global__ __launch_bounds__(256) void dw_sum_pm_kernel(const float *__restrict__ dwp,
                                                         uint4 *__restrict__ dw, int64_t nuk,
                                                         int nchunk, int vslots, int64_t per_slot)
 {
-    constexpr int NQ = S / 8, HW = S * S;
-    const int64_t n = nuk * S * NQ;
-    for (int64_t o = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; o < n;
-         o += (int64_t)gridDim.x * blockDim.x) {
-        const int cq = (int)(o % NQ);
-        const int64_t rr = o / NQ;
-        const int r = (int)(rr % S);                    // image row
-        const int64_t uk = rr / S;                      // unit * 3 + tap
-        const bool vert = (vslots >> (int)(uk / per_slot)) & 1;
-        float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-        for (int c = 0; c < nchunk; ++c) {
-            const float *pl = dwp + ((int64_t)c * nuk + uk) * HW;
-            if (vert) {
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    v[t] += pl[r * S + 8 * cq + t];
-            } else {
-#pragma unroll
-                for (int t = 0; t < 8; ++t)
-                    v[t] += pl[(8 * cq + t) * S + r];
+    constexpr int HW = S * S, NQ = S / 8;
+    __shared__ float T[S][S + 1];
+    const int64_t uk = blockIdx.x;
+    const bool vert = (vslots >> (int)(uk / per_slot)) & 1;
+    uint4 *dst = dw + uk * (HW / 8);
+    if (vert) {
+        for (int t = threadIdx.x; t < HW / 8; t += 256) {
+            float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            for (int c = 0; c < nchunk; ++c) {
+                const float4 *src = reinterpret_cast<const float4 *>(dwp + ((int64_t)c * nuk + uk) * HW) + 2 * t;
+                const float4 a = src[0], b = src[1];
+                v[0] += a.x, v[1] += a.y, v[2] += a.z, v[3] += a.w;
+                v[4] += b.x, v[5] += b.y, v[6] += b.z, v[7] += b.w;
             }
+            gst128(dst + t, make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]),
+                                       pack2(v[6], v[7])));
         }
-        gst128(dw + (uk * HW + (int64_t)r * S + 8 * cq) / 8,
-               make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
+        return;
+    }
+    for (int e = threadIdx.x; e < HW; e += 256) {
+        const int l = e / S, pos = e - l * S;             // line (column), position (row)
+        float v = 0.f;
+        for (int c = 0; c < nchunk; ++c)
+            v += dwp[((int64_t)c * nuk + uk) * HW + e];
+        T[pos][l] = v;
+    }
+    __syncthreads();
+    for (int t = threadIdx.x; t < HW / 8; t += 256) {
+        const int r = t / NQ, cq = t - r * NQ;
+        const float *row = &T[r][8 * cq];
+        gst128(dst + t, make_uint4(pack2(row[0], row[1]), pack2(row[2], row[3]),
+                                   pack2(row[4], row[5]), pack2(row[6], row[7])));
     }
 }
 
@@ -1118,7 +1188,7 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
 
 template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
-                          float *dwp)
+                          float *dwp, const void *lamh, const void *uh)
 {
     hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1130,7 +1200,7 @@ hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, 
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
                        p.mask, p.B, p.C, p.G, cw, nchunk, make_magic((uint32_t)nchunk),
-                       make_magic((uint32_t)p.G));
+                       make_magic((uint32_t)p.G), (const bf16_t *)lamh, (const bf16_t *)uh);
     return hipGetLastError();
 }
 
@@ -1149,7 +1219,8 @@ int bwd_ns4_regs()
 // WPM: the weights are pixel-major (else blocked, e.g. re-laid out by
 // launch_w_to_blocked); the other per-direction tensors follow PM.
 template <int H, int W, bool PM, bool WPM>
-hipError_t bwd_med_t(const Problem &p, hipStream_t st)
+hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullptr,
+                     const void *uh = nullptr)
 {
     const int lds_max = kLdsBytes;
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
@@ -1162,8 +1233,8 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
             return hipErrorInvalidConfiguration;
         if (p.ws->counting)
             return hipSuccess;
-        return bwd_med_launch<H, W, false, true, kSlots, PM, WPM>(p, st, cw, nct,
-                                                                  (size_t)cw * per_ch, nullptr);
+        return bwd_med_launch<H, W, false, true, kSlots, PM, WPM>(
+            p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh);
     }
     // A group's channels in nchunk workgroups of cw channels, NS slots per
     // step.  NS = 4 (at most 4 channels, a smaller slot area) is taken where
@@ -1217,11 +1288,12 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
     if (p.ws->counting)
         return hipSuccess;
     if (use4)
-        e = bwd_med_launch<H, W, false, false, 4, PM, WPM>(p, st, cw, nchunk, lds, dwp);
+        e = bwd_med_launch<H, W, false, false, 4, PM, WPM>(p, st, cw, nchunk, lds, dwp, lamh, uh);
     else
-        e = cw >= kBatch
-                ? bwd_med_launch<H, W, false, false, kSlots, PM, WPM>(p, st, cw, nchunk, lds, dwp)
-                : bwd_med_launch<H, W, true, false, kSlots, PM, WPM>(p, st, cw, nchunk, lds, dwp);
+        e = cw >= kBatch ? bwd_med_launch<H, W, false, false, kSlots, PM, WPM>(
+                               p, st, cw, nchunk, lds, dwp, lamh, uh)
+                         : bwd_med_launch<H, W, true, false, kSlots, PM, WPM>(
+                               p, st, cw, nchunk, lds, dwp, lamh, uh);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
@@ -1235,7 +1307,7 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st)
                         vslots |= 1 << sl;
                     ++sl;
                 }
-            hipLaunchKernelGGL((dw_sum_pm_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
+            hipLaunchKernelGGL((dw_sum_pm_kernel<H>), dim3((unsigned)nuk), dim3(256), 0, st,
                                (const float *)dwp, (uint4 *)p.dw, nuk, nchunk, vslots,
                                (int64_t)p.B * p.G * 3);
         } else {
@@ -1264,21 +1336,30 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
         return bwd_med_t<H, W, false, false>(p, st);
     if (!pm_weights_reblocked(p))
         return bwd_med_t<H, W, true, true>(p, st);
-    // the group's weights re-laid out once into the blocked order of their
-    // direction (workspace), read there as 16-byte pieces
+    // the group's weights, and lambda and u of the horizontal directions,
+    // re-laid out once into the blocked order of their direction
+    // (workspace), read there as 16-byte pieces: a horizontal scan would read
+    // each pixel-major piece from 64 rows
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * H * W;
-    void *wb = nullptr;
+    const int64_t nh = (int64_t)__builtin_popcount(p.mask & 12) * p.B * p.C * H * W;
+    void *wb = nullptr, *lamh = nullptr, *uh = nullptr;
     hipError_t e = p.ws->take(&wb, (size_t)nw * 2);
+    if (e == hipSuccess && nh > 0)
+        e = p.ws->take(&lamh, (size_t)nh * 2);
+    if (e == hipSuccess && nh > 0)
+        e = p.ws->take(&uh, (size_t)nh * 2);
     if (e != hipSuccess)
         return e;
     if (!p.ws->counting) {
         e = launch_w_to_blocked(p, wb, st);
+        if (e == hipSuccess && nh > 0)
+            e = launch_horiz_to_blocked(p, lamh, uh, st);
         if (e != hipSuccess)
             return e;
     }
     Problem q = p;
     q.w = wb;
-    return bwd_med_t<H, W, true, false>(q, st);
+    return bwd_med_t<H, W, true, false>(q, st, lamh, uh);
 }
 
 }  // namespace

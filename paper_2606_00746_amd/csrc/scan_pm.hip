@@ -70,15 +70,15 @@ __device__ __forceinline__ void stage_plane(uint8_t *dst, const bf16_t *src, int
 // weights: pixel-major -> blocked line-major, one workgroup per tap plane
 // ---------------------------------------------------------------------------
 
-// Plane pl of the [D][B][G][3] planes (direction slot pl / per_slot, whose
-// direction is vertical when bit slot of vslots is set).  The plane's rows
+// Plane pl of a stack of planes grouped per direction slot (slot pl /
+// per_slot, whose direction is vertical when bit slot of vslots is set).  The plane's rows
 // are staged in LDS; then each thread writes 16-byte pieces of the blocked
 // layout (piece (q, p): lines 8q..8q+7 at position p, contiguous across the
 // wave).
 template <int S>
-__global__ __launch_bounds__(256) void w_to_blocked_kernel(const bf16_t *__restrict__ w,
-                                                           uint4 *__restrict__ out, int vslots,
-                                                           int per_slot)
+__global__ __launch_bounds__(256) void to_blocked_kernel(const bf16_t *__restrict__ w,
+                                                         uint4 *__restrict__ out, int vslots,
+                                                         int per_slot)
 {
     using Pl = PmPlane<S>;
     __shared__ uint4 sm[Pl::kBytes / 16];
@@ -314,8 +314,25 @@ hipError_t w_to_blocked_t(const Problem &p, void *wb, hipStream_t st)
         }
     const int per_slot = p.B * p.G * 3;
     const int planes = __builtin_popcount(p.mask) * per_slot;
-    hipLaunchKernelGGL((w_to_blocked_kernel<S>), dim3((unsigned)planes), dim3(256), 0, st,
+    hipLaunchKernelGGL((to_blocked_kernel<S>), dim3((unsigned)planes), dim3(256), 0, st,
                        (const bf16_t *)p.w, (uint4 *)wb, vslots, per_slot);
+    return hipGetLastError();
+}
+
+// lam and u of the horizontal directions (slots nv .. D-1, nv the vertical
+// directions of the mask) into [D - nv][B][C][plane] blocked copies each.
+template <int S>
+hipError_t horiz_to_blocked_t(const Problem &p, void *lamh, void *uh, hipStream_t st)
+{
+    const int nv = __builtin_popcount(p.mask & 3), nh = __builtin_popcount(p.mask & 12);
+    const int64_t skip = (int64_t)nv * p.B * p.C * S * S;
+    const int planes = nh * p.B * p.C;
+    if (planes == 0)
+        return hipSuccess;
+    hipLaunchKernelGGL((to_blocked_kernel<S>), dim3((unsigned)planes), dim3(256), 0, st,
+                       (const bf16_t *)p.lam + skip, (uint4 *)lamh, 0, planes);
+    hipLaunchKernelGGL((to_blocked_kernel<S>), dim3((unsigned)planes), dim3(256), 0, st,
+                       (const bf16_t *)p.u + skip, (uint4 *)uh, 0, planes);
     return hipGetLastError();
 }
 
@@ -348,6 +365,18 @@ hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t st)
     case 40: return w_to_blocked_t<40>(p, wb, st);
     case 32: return w_to_blocked_t<32>(p, wb, st);
     default: return w_to_blocked_t<24>(p, wb, st);
+    }
+}
+
+hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipStream_t st)
+{
+    switch (p.H) {
+    case 64: return horiz_to_blocked_t<64>(p, lamh, uh, st);
+    case 56: return horiz_to_blocked_t<56>(p, lamh, uh, st);
+    case 48: return horiz_to_blocked_t<48>(p, lamh, uh, st);
+    case 40: return horiz_to_blocked_t<40>(p, lamh, uh, st);
+    case 32: return horiz_to_blocked_t<32>(p, lamh, uh, st);
+    default: return horiz_to_blocked_t<24>(p, lamh, uh, st);
     }
 }
 
