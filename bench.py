@@ -84,6 +84,19 @@ def _cpu_model() -> str:
     return "unknown CPU"
 
 
+CPU_SHARE = 16   # host threads that one GPU's jobs may use on a shared GPU host
+
+
+def cpu_threads() -> int:
+    """Threads of the CPU baseline: the cores this process may run on,
+    at most CPU_SHARE."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, CPU_SHARE))
+
+
 def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool = False,
                  threads: int = 1, runs: int = 3) -> dict:
     """The fp64 oracle on (batch, group) units of the workload.
@@ -151,7 +164,8 @@ def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool =
             "host_nproc": os.cpu_count(),
             "sample": f"{len(units)} (batch, group) units of {wl.name} ({wl.B * wl.G} per step; "
                       f"{len(units) * cpg} channel planes), fwd then bwd, each timed, median of "
-                      f"{runs} runs, fp64, {how} of {os.cpu_count()} host CPUs ({_cpu_model()}), "
+                      f"{runs} runs, fp64, {how} ({os.cpu_count()} host CPUs, at most "
+                      f"{CPU_SHARE} used: one GPU's share; {_cpu_model()}), "
                       f"{sum(tf) + sum(tb):.1f} s"}
 
 
@@ -348,9 +362,10 @@ def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
         log(f"{other['layout']} layout: fwd {other['fwd_ms']:.4f} ms  bwd {other['bwd_ms']:.4f} ms"
             f"  step {o_ms:.4f} ms")
     if not args.no_cpu_baseline:
-        # the oracle on all of the host's cores (the reported baseline), and
-        # on one thread beside it
-        nthr = os.cpu_count() or 1
+        # the oracle on every core this process may use, up to the 16 that
+        # are one GPU's share of the host (the reported baseline), and on one
+        # thread beside it
+        nthr = cpu_threads()
         log(f"timing the CPU oracle on {nthr} threads ...")
         out["cpu_baseline"] = cpu_baseline(wl, inputs, args.cpu_seconds, args.norm,
                                            threads=nthr)
@@ -362,6 +377,11 @@ def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
 
 LATENT_METRIC = ("C-GSPN latent sublayer fwd Gpix·ch/s (input pixel-channels) at 1 MI355X; "
                  "achieved HBM GB/s vs peak")
+
+
+# Sublayer latency of the paper's A100 measurement at batch 32 (Sec. 6, the
+# latency tables over resolutions), by token grid: context, not a target.
+PAPER_A100_SUBLAYER_MS = {37: 0.088, 74: 0.18, 111: 0.299, 147: 0.46, 185: 0.646}
 
 
 def latent_grid(lw: gi.LatentWorkload) -> tuple:
@@ -501,6 +521,10 @@ def run_latent(lw: gi.LatentWorkload, args, torch, gspn) -> dict:
                      "kernel": dom, "avg_ms": round(stage_ms[dom], 5),
                      "algorithmic_bytes": nbytes[dom]},
     }
+    if lw.B == 32 and lw.H == lw.W and lw.H in PAPER_A100_SUBLAYER_MS:
+        out["paper_context"] = {"a100_sublayer_ms": PAPER_A100_SUBLAYER_MS[lw.H],
+                                "note": "A100, the paper's own sublayer latency at this grid "
+                                        "and batch; other hardware, not vs_baseline"}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         out["cpu_baseline"] = latent_cpu_baseline(lw, inp, args.cpu_seconds)

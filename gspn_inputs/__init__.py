@@ -282,12 +282,12 @@ class LatentWorkload:
         return replace(self, **kw)
 
 
-# Token grids of a ViT with 14-pixel patches at 518 and 1022 pixels, width
+# Token grids of a ViT with 14-pixel patches at 518, 1036, 1554, 2058 and
+# 2590 pixels (the sublayer latencies of Sec. 6 are quoted at these), width
 # 1152 compressed to 64 latent channels, batch 32.
-LATENT_WORKLOADS = (
-    LatentWorkload("cgspn-37x37-b32-c1152-cc64", 32, 1152, 64, 37, 37, ALL_DIRS, 21),
-    LatentWorkload("cgspn-73x73-b32-c1152-cc64", 32, 1152, 64, 73, 73, ALL_DIRS, 22),
-)
+LATENT_WORKLOADS = tuple(
+    LatentWorkload(f"cgspn-{n}x{n}-b32-c1152-cc64", 32, 1152, 64, n, n, ALL_DIRS, 21 + i)
+    for i, n in enumerate((37, 74, 111, 147, 185)))
 
 
 def latent_workload(name_or_index) -> LatentWorkload:

@@ -181,12 +181,14 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
     default: {   // GSPN_OP_BWD_NORM
         // the weights, then the gradient with respect to them, then the
         // logits' gradient
-        void *w = nullptr;
-        hipError_t e = ws.take(&w, (size_t)(2 * nw * es));
+        void *w = nullptr, *dw = nullptr;
+        hipError_t e = ws.take(&w, (size_t)(nw * es));
+        if (e == hipSuccess)
+            e = ws.take(&dw, (size_t)(nw * es));
         if (e != hipSuccess)
             return e;
         p.w = w;
-        p.dw = static_cast<char *>(w) + nw * es;
+        p.dw = dw;
         if (!ws.counting) {
             e = launch_norm(p, w_in, nullptr, w, s);
             if (e != hipSuccess)
@@ -518,8 +520,10 @@ hipError_t run_latent(const void *x, const void *p_down, const void *l_u, const 
     hipError_t e = ws.take(&scr, (size_t)(total * 2));
     if (e != hipSuccess)
         return e;
+    // (no pointers into the workspace while counting: it has no base then)
     uint16_t *base = static_cast<uint16_t *>(scr);
-    uint16_t *xc = base, *u = base + o_u, *lam = base + o_l, *w = base + o_w, *yc = base + o_y;
+    const auto at = [&](int64_t o) { return ws.counting ? nullptr : base + o; };
+    uint16_t *xc = base, *u = at(o_u), *lam = at(o_l), *w = at(o_w), *yc = at(o_y);
     if (!ws.counting) {
         e = launch_project(p_down, x, xc, B, Cc, C, Hp, Wp, s, H, W);
         if (e == hipSuccess)

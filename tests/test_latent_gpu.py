@@ -117,11 +117,13 @@ def test_latent_fwd_matches_oracle(lw):
     assert err <= 2e-2, f"{lw.name} y err {err:.3g}"
 
 
-def test_latent_full_size_sampled_images():
-    """The 37 x 37 workload at its full size (B = 32, C = 1152, Cc = 64):
-    every image is independent, so the oracle checks two of them."""
+@pytest.mark.parametrize("lw", gi.LATENT_WORKLOADS, ids=lambda w: w.name)
+def test_latent_full_size_sampled_images(lw):
+    """The paper's token grids at their full size (B = 32, C = 1152, Cc = 64),
+    in the one call the benchmark times: every image is independent, so the
+    oracle checks the first and the last."""
     require_gpu()
-    lw = gi.latent_workload(0)
+    print(f"[case] latent full size {lw.name}", flush=True)
     inp = gi.make_latent_inputs(lw)
     dev = {k: to_device(v, "bf16") for k, v in inp.items()}
     y = gspn.latent_fwd(dev["x"], dev["p_down"], dev["l_u"], dev["l_lam"], dev["l_w"],
@@ -130,4 +132,5 @@ def test_latent_full_size_sampled_images():
         ref = oracle.latent_fwd(inp["x"][b:b + 1], inp["p_down"], inp["l_u"], inp["l_lam"],
                                 inp["l_w"], inp["p_up"], lw.dirs, storage="bf16")
         err = normwise_err(to_host(y[b:b + 1]), ref)
+        print(f"[err] {lw.name} image {b}: normwise {err:.3g}", flush=True)
         assert err <= 2e-2, f"image {b} y err {err:.3g}"
