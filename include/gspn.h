@@ -229,6 +229,31 @@ int gspn_scan_bwd_static(const void *x, const void *w, const void *lam, const vo
                          void *stream);
 
 /*
+ * gspn_scan_bwd with the launch plan of the register-streamed backward (the
+ * bf16 kernels for square planes whose side is a multiple of 8 from 24 to
+ * 64, groups of more than one channel) fixed by the caller, for tests of determinism across
+ * launch shapes and for tuning.  That backward takes the channels of a group
+ * in workgroups of up to `slots` channels, one step's weight-gradient terms
+ * summed over them in LDS, the workgroups' fp32 partials summed afterwards:
+ *   slots  0   the library's choice (the same plan as gspn_scan_bwd)
+ *          4   workgroups of 4 channels, where a group has at least 4
+ *          8   workgroups of up to 8 channels (as many as fit in LDS)
+ * A plan the shape cannot take, and every other kernel family, run as in
+ * gspn_scan_bwd.  dx, dlam and du do not depend on the plan (bit for bit);
+ * dw is summed over a group's channels in another association, so it may
+ * differ in the last bit of the fp32 sum before its one rounding.
+ * gspn_workspace_size_slots gives the workspace of that plan.  Other
+ * values of slots: GSPN_ERR_UNSUPPORTED.  Other arguments, checks and
+ * errors as in gspn_scan_bwd.
+ */
+int gspn_workspace_size_slots(int slots, int direction, int B, int C, int G, int H, int W,
+                              int dtype, int64_t *bytes);
+int gspn_scan_bwd_slots(int slots, const void *x, const void *w, const void *lam,
+                        const void *u, const void *dy, void *dx, void *dw, void *dlam,
+                        void *du, int direction, int B, int C, int G, int H, int W,
+                        int dtype, void *workspace, int64_t workspace_bytes, void *stream);
+
+/*
  * Latent-space propagation sublayer of C-GSPN (Sec. 5, Eqs. (latent_down),
  * (latent_params), (latent_recurrence), (latent_up)): the feature map is
  * projected per pixel from C to Cc channels, the propagation parameters are

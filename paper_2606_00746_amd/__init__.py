@@ -10,7 +10,7 @@ from ._native import (ALL, B2T, BF16, BLOCKED, F32, L2R, LIB_PATH, OP_BWD, OP_BW
                       GspnError, gspn_last_hip_error, gspn_latent_fwd, gspn_latent_params,
                       gspn_latent_workspace_size, gspn_project, gspn_scan_bwd,
                       gspn_scan_bwd_blocked, gspn_scan_bwd_norm, gspn_scan_fwd,
-                      gspn_scan_fwd_blocked, gspn_scan_fwd_norm, gspn_scan_bwd_static, gspn_strerror, gspn_version,
+                      gspn_scan_fwd_blocked, gspn_scan_fwd_norm, gspn_scan_bwd_static, gspn_scan_bwd_slots, gspn_workspace_size_slots, gspn_strerror, gspn_version,
                       gspn_workspace_size, latent_fwd, latent_params, load, project, scan_bwd,
                       scan_bwd_norm, scan_fwd, scan_fwd_norm, workspace_size)
 
@@ -18,7 +18,7 @@ __all__ = ["ALL", "B2T", "BF16", "BLOCKED", "F32", "L2R", "LIB_PATH", "OP_BWD", 
            "OP_BWD_NORM", "OP_FWD", "OP_FWD_BLOCKED", "OP_FWD_NORM", "PIXEL", "R2L", "T2B",
            "GspnError", "gspn_last_hip_error", "gspn_latent_fwd", "gspn_latent_params",
            "gspn_latent_workspace_size", "gspn_project", "gspn_scan_bwd", "gspn_scan_bwd_blocked",
-           "gspn_scan_bwd_norm", "gspn_scan_bwd_static", "gspn_scan_fwd", "gspn_scan_fwd_blocked",
+           "gspn_scan_bwd_norm", "gspn_scan_bwd_static", "gspn_scan_bwd_slots", "gspn_workspace_size_slots", "gspn_scan_fwd", "gspn_scan_fwd_blocked",
            "gspn_scan_fwd_norm",
            "gspn_strerror", "gspn_version", "gspn_workspace_size", "latent_fwd", "latent_params",
            "load", "project", "scan_bwd", "scan_bwd_norm", "scan_fwd", "scan_fwd_norm",

@@ -28,7 +28,8 @@ PIXEL, BLOCKED = "pixel", "blocked"
 
 EXPORTED = ("gspn_workspace_size", "gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_blocked",
             "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
-            "gspn_scan_bwd_static", "gspn_project",
+            "gspn_scan_bwd_static", "gspn_workspace_size_slots", "gspn_scan_bwd_slots",
+            "gspn_project",
             "gspn_latent_params", "gspn_latent_workspace_size", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
 
@@ -64,6 +65,8 @@ def load() -> ctypes.CDLL:
         for name in ("gspn_scan_bwd", "gspn_scan_bwd_blocked", "gspn_scan_bwd_norm"):
             getattr(lib, name).argtypes = [vp] * 9 + scan8 + ws
         lib.gspn_scan_bwd_static.argtypes = [vp] * 9 + scan8 + [vp]
+        lib.gspn_workspace_size_slots.argtypes = [i] + scan8 + [pi64]
+        lib.gspn_scan_bwd_slots.argtypes = [i] + [vp] * 9 + scan8 + ws
         lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
         lib.gspn_latent_params.argtypes = [vp] * 7 + [i] * 6 + [vp]
         lib.gspn_latent_workspace_size.argtypes = [i] * 7 + [pi64]
@@ -128,6 +131,19 @@ def gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G,
                          stream) -> int:
     return load().gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H,
                                        W, dtype, stream)
+
+
+def gspn_workspace_size_slots(slots, direction, B, C, G, H, W, dtype):
+    """(status, bytes) of gspn_workspace_size_slots."""
+    n = ctypes.c_int64(0)
+    st = load().gspn_workspace_size_slots(slots, direction, B, C, G, H, W, dtype, ctypes.byref(n))
+    return st, n.value
+
+
+def gspn_scan_bwd_slots(slots, x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W,
+                        dtype, ws, ws_bytes, stream) -> int:
+    return load().gspn_scan_bwd_slots(slots, x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C,
+                                      G, H, W, dtype, ws, ws_bytes, stream)
 
 
 STATIC_SCRATCH_BYTES = 64 << 20
@@ -232,12 +248,13 @@ def workspace_size(op, x, w, direction) -> int:
     return n
 
 
-def _workspace(op, direction, B, C, G, H, W, dtype, device, given=None):
+def _workspace(op, direction, B, C, G, H, W, dtype, device, given=None, slots=0):
     """The device buffer operation `op` works in: `given` (a uint8 tensor on
     the same device) when it is large enough, else a new one (None if the
     call needs none)."""
     import torch
-    st, n = gspn_workspace_size(op, direction, B, C, G, H, W, dtype)
+    st, n = (gspn_workspace_size_slots(slots, direction, B, C, G, H, W, dtype) if slots
+             else gspn_workspace_size(op, direction, B, C, G, H, W, dtype))
     _check_raise(st)
     if n == 0:
         return None, 0
@@ -249,7 +266,7 @@ def _workspace(op, direction, B, C, G, H, W, dtype, device, given=None):
     return torch.empty(n, dtype=torch.uint8, device=device), n
 
 
-def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=None):
+def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=None, slots=0):
     B, C, G, H, W = _sizes(x, w, direction)
     D = _ndirs(direction)
     n, nd, nw = B * C * H * W, D * B * C * H * W, D * B * G * 3 * H * W
@@ -262,7 +279,7 @@ def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=Non
         named.update(y=(outs[0], n))
     _check_tensors(x, named)
     dt = _dtype_code(x)
-    ws, nbytes = _workspace(op, direction, B, C, G, H, W, dt, x.device, workspace)
+    ws, nbytes = _workspace(op, direction, B, C, G, H, W, dt, x.device, workspace, slots)
     ptrs = [t.data_ptr() for t in (x, w, lam, u)]
     if bwd:
         ptrs += [t.data_ptr() for t in (dy, dx, dw, dlam, du)]
@@ -271,6 +288,8 @@ def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=Non
     fn = {OP_FWD: gspn_scan_fwd, OP_BWD: gspn_scan_bwd, OP_FWD_BLOCKED: gspn_scan_fwd_blocked,
           OP_BWD_BLOCKED: gspn_scan_bwd_blocked, OP_FWD_NORM: gspn_scan_fwd_norm,
           OP_BWD_NORM: gspn_scan_bwd_norm}[op]
+    if slots:
+        fn = lambda *a: gspn_scan_bwd_slots(slots, *a)          # noqa: E731
     status = fn(*ptrs, direction, B, C, G, H, W, dt, ws.data_ptr() if ws is not None else None,
                 nbytes, _stream_handle(x, stream))
     _check_raise(status)
@@ -300,16 +319,20 @@ def scan_fwd(x, w, lam, u, direction: int = ALL, y=None, stream=None, layout: st
 
 
 def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None, layout: str = PIXEL,
-             workspace=None):
+             workspace=None, slots: int = 0):
     """Gradients (dx, dw, dlam, du) of <y, dy> for device tensors, in the
-    layout of the inputs."""
+    layout of the inputs.  `slots` (4 or 8, pixel-major only) forces that
+    plan of the register-streamed backward (gspn_scan_bwd_slots); 0 leaves
+    the choice to the library."""
     import torch
     _check_layout(layout)
+    if slots and layout != PIXEL:
+        raise ValueError("slots applies to the pixel-major backward only")
     if out is None:
         out = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                torch.empty_like(u))
     _scan(OP_BWD if layout == PIXEL else OP_BWD_BLOCKED, x, w, lam, u, direction, out, dy=dy,
-          stream=stream, workspace=workspace)
+          stream=stream, workspace=workspace, slots=slots)
     return out
 
 

@@ -220,7 +220,7 @@ int count_workspace(int op, const Problem &p0, int64_t *bytes)
 int scan_call(int op, const void *x, const void *w, const void *lam, const void *u, const void *dy,
               void *y, void *dx, void *dw, void *dlam, void *du, int direction, int B, int C,
               int G, int H, int W, int dtype, void *workspace, int64_t workspace_bytes,
-              void *stream)
+              void *stream, int slots = 0)
 {
     if (!valid_op(op))
         return GSPN_ERR_UNSUPPORTED;
@@ -236,7 +236,7 @@ int scan_call(int op, const void *x, const void *w, const void *lam, const void 
         return st;
     const bool blocked = op == GSPN_OP_FWD_BLOCKED || op == GSPN_OP_BWD_BLOCKED;
     Problem p{x, w, lam, u, dy, y, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
-              blocked ? kBlocked : kPixelMajor, nullptr};
+              blocked ? kBlocked : kPixelMajor, nullptr, slots};
     int64_t need = 0;
     st = count_workspace(op, p, &need);
     if (st != GSPN_OK)
@@ -262,8 +262,11 @@ int scan_call(int op, const void *x, const void *w, const void *lam, const void 
 }  // namespace
 }  // namespace gspn
 
-extern "C" int gspn_workspace_size(int op, int direction, int B, int C, int G, int H, int W,
-                                   int dtype, int64_t *bytes)
+namespace gspn {
+namespace {
+
+int workspace_query(int op, int direction, int B, int C, int G, int H, int W, int dtype,
+                    int slots, int64_t *bytes)
 {
     if (bytes == nullptr)
         return GSPN_ERR_NULL;
@@ -275,8 +278,42 @@ extern "C" int gspn_workspace_size(int op, int direction, int B, int C, int G, i
         return st;
     const bool blocked = op == GSPN_OP_FWD_BLOCKED || op == GSPN_OP_BWD_BLOCKED;
     Problem p{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-              nullptr, direction, B, C, G, H, W, dtype, blocked ? kBlocked : kPixelMajor, nullptr};
+              nullptr, direction, B, C, G, H, W, dtype, blocked ? kBlocked : kPixelMajor, nullptr,
+              slots};
     return count_workspace(op, p, bytes);
+}
+
+bool valid_slots(int slots) { return slots == 0 || slots == 4 || slots == 8; }
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_workspace_size(int op, int direction, int B, int C, int G, int H, int W,
+                                   int dtype, int64_t *bytes)
+{
+    return workspace_query(op, direction, B, C, G, H, W, dtype, 0, bytes);
+}
+
+extern "C" int gspn_workspace_size_slots(int slots, int direction, int B, int C, int G, int H,
+                                         int W, int dtype, int64_t *bytes)
+{
+    if (bytes != nullptr)
+        *bytes = 0;
+    if (!valid_slots(slots))
+        return GSPN_ERR_UNSUPPORTED;
+    return workspace_query(GSPN_OP_BWD, direction, B, C, G, H, W, dtype, slots, bytes);
+}
+
+extern "C" int gspn_scan_bwd_slots(int slots, const void *x, const void *w, const void *lam,
+                                   const void *u, const void *dy, void *dx, void *dw, void *dlam,
+                                   void *du, int direction, int B, int C, int G, int H, int W,
+                                   int dtype, void *workspace, int64_t workspace_bytes,
+                                   void *stream)
+{
+    if (!valid_slots(slots))
+        return GSPN_ERR_UNSUPPORTED;
+    return scan_call(GSPN_OP_BWD, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C,
+                     G, H, W, dtype, workspace, workspace_bytes, stream, slots);
 }
 
 extern "C" int gspn_scan_fwd(const void *x, const void *w, const void *lam, const void *u, void *y,

@@ -41,6 +41,9 @@ struct Problem {
     int mask, B, C, G, H, W, dtype;
     int layout;
     Workspace *ws;
+    // channel slots per step of the register-streamed backward: 0 the
+    // planner's choice, 4 or 8 that plan where the shape can take it
+    int slots = 0;
 };
 
 // Planes whose sides are both <= kSmallSide run on the register-resident path.

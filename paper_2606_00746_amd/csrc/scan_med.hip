@@ -1261,7 +1261,9 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullpt
     if (p8.nchunk < 1)
         return hipErrorInvalidConfiguration;
     bool use4 = false;
-    if (p4.nchunk >= 1 && p4.cw == 4 && p4.nchunk <= p8.nchunk + 1) {
+    if (p.slots == 4 || p.slots == 8) {
+        use4 = p.slots == 4 && p4.nchunk >= 1 && p4.cw == 4;
+    } else if (p4.nchunk >= 1 && p4.cw == 4 && p4.nchunk <= p8.nchunk + 1) {
         const int regs = bwd_ns4_regs<H, W, PM, WPM>();
         if (regs > 0) {
             const int per_simd = 512 / ((regs + 7) / 8 * 8);   // waves a SIMD holds

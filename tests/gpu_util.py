@@ -93,3 +93,25 @@ def ignored_taps(mask: int, H: int, W: int) -> np.ndarray:
             m[:, :, W - 1] = True
         out.append(m)
     return np.stack(out)
+
+
+def ulp_bf16(v: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 numbers at |v| (8 significant bits), taken at the
+    smallest normal number for |v| below it."""
+    a = np.maximum(np.abs(v), np.finfo(np.float32).tiny)
+    return np.exp2(np.floor(np.log2(a)) - 7)
+
+
+def check_half_ulp(tag, got, ref, mag, K):
+    """Asserts |got - ref| <= 0.5 ulp_bf16(max(|ref|, |got|)) + 2^-24 K mag
+    element by element: one rounding to nearest of a value that fp32
+    arithmetic got within 2^-24 K mag of the exact ref (mag: the element's
+    sum of absolute terms).  Prints the worst ratio to the bound."""
+    bound = 0.5 * ulp_bf16(np.maximum(np.abs(ref), np.abs(got))) + 2.0 ** -24 * K * mag
+    excess = np.abs(got - ref) / bound
+    worst = float(excess.max()) if excess.size else 0.0
+    print(f"[err] {tag}: max |got-ref| / bound {worst:.3f} "
+          f"(elements over half an ulp of r: "
+          f"{float(np.mean(np.abs(got - ref) > 0.5 * ulp_bf16(ref) * (1 + 1e-9))):.2e})",
+          flush=True)
+    assert worst <= 1.0, f"{tag}: {int((excess > 1).sum())} of {excess.size} elements over bound"

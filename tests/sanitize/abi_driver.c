@@ -78,6 +78,15 @@ static void check_fwd(fwd_fn f)
 #undef CALLF
 }
 
+static int bwd_slots4_as_bwd(const void *x, const void *w, const void *lam, const void *u,
+                             const void *dy, void *dx, void *dw, void *dlam, void *du, int dir,
+                             int B, int C, int G, int H, int W, int dt, void *ws, int64_t wsb,
+                             void *s)
+{
+    return gspn_scan_bwd_slots(4, x, w, lam, u, dy, dx, dw, dlam, du, dir, B, C, G, H, W, dt, ws,
+                               wsb, s);
+}
+
 static void check_bwd(bwd_fn f)
 {
     void *p[9];
@@ -109,7 +118,7 @@ static void check_bwd(bwd_fn f)
     for (int i = 0; i < 9; ++i)
         b[i] = fake(i + 16, 1u << 26, 0);
     void *ws = fake(32, 1u << 26, 0);
-    if (f == gspn_scan_bwd || f == gspn_scan_bwd_blocked) {
+    if (f == gspn_scan_bwd || f == gspn_scan_bwd_blocked || f == bwd_slots4_as_bwd) {
         EXPECT(CALLB(b, 5, 1, 4, 2, 70, 100, GSPN_BF16, NULL, 0), GSPN_ERR_WORKSPACE);
         EXPECT(CALLB(b, 5, 1, 4, 2, 70, 100, GSPN_BF16, ws, need - 1), GSPN_ERR_WORKSPACE);
         EXPECT(CALLB(b, 5, 1, 4, 2, 70, 100, GSPN_BF16, ws, -1), GSPN_ERR_WORKSPACE);
@@ -214,6 +223,15 @@ int main(void)
     check_bwd(gspn_scan_bwd_blocked);
     check_bwd(gspn_scan_bwd_norm);
     check_bwd(bwd_static_as_bwd);
+    check_bwd(bwd_slots4_as_bwd);
+    {
+        int64_t n4 = 0, n8 = 0;
+        EXPECT(gspn_workspace_size_slots(4, 15, 1, 64, 2, 64, 64, GSPN_BF16, &n4), GSPN_OK);
+        EXPECT(gspn_workspace_size_slots(8, 15, 1, 64, 2, 64, 64, GSPN_BF16, &n8), GSPN_OK);
+        EXPECT(n4 > n8, 1);
+        EXPECT(gspn_workspace_size_slots(3, 15, 1, 64, 2, 64, 64, GSPN_BF16, &n4),
+               GSPN_ERR_UNSUPPORTED);
+    }
     check_queries();
     for (int s = -20; s < 3; ++s)
         if (gspn_strerror(s) == NULL || gspn_strerror(s)[0] == '\0') {

@@ -282,3 +282,27 @@ def test_latent_invalid_arguments(call, ptrs, dims):
         assert call(C=36) == _native.ERR_UNSUPPORTED
     # an output over an input
     assert call(**{ptrs[-1]: P(0)}) == _native.ERR_ALIAS
+
+
+def test_slot_plan_workspace():
+    """The forced 4-slot plan of the register-streamed backward takes 4 channels
+    per workgroup: a 32-channel group of 64 x 64 planes needs 8 fp32 partials
+    of dw instead of the 4 that 8-slot workgroups (8 channels, as many as fit
+    in LDS) need."""
+    args = (15, 1, 64, 2, 64, 64, g.BF16)
+    st8, n8 = g.gspn_workspace_size_slots(8, *args)
+    st4, n4 = g.gspn_workspace_size_slots(4, *args)
+    st0, n0 = g.gspn_workspace_size_slots(0, *args)
+    assert st8 == st4 == st0 == _native.OK
+    assert n0 == g.gspn_workspace_size(g.OP_BWD, *args)[1]
+    ndw = 4 * 1 * 2 * 3 * 64 * 64                      # D B G 3 H W
+    assert n4 - n8 == (8 - 4) * ndw * 4
+    # per-channel weights (one channel per group) take no plan: same need
+    args1 = (15, 1, 16, 16, 64, 64, g.BF16)
+    assert g.gspn_workspace_size_slots(4, *args1) == g.gspn_workspace_size_slots(8, *args1)
+    for bad in (1, 2, 16, -4):
+        assert g.gspn_workspace_size_slots(bad, *args)[0] == _native.ERR_UNSUPPORTED
+        assert g.gspn_scan_bwd_slots(bad, *[P(i) for i in range(9)], *args, None, 0,
+                                     None) == _native.ERR_UNSUPPORTED
+    assert g.gspn_scan_bwd_slots(4, *[P(i) for i in range(8)], None, *args, None, 0,
+                                 None) == _native.ERR_NULL

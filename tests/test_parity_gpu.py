@@ -11,7 +11,7 @@ import pytest
 import gspn_inputs as gi
 import oracle
 import paper_2606_00746_amd as gspn
-from gpu_util import ignored_taps, report, require_gpu, to_host, tolerance, upload
+from gpu_util import check_half_ulp, ignored_taps, report, require_gpu, to_host, tolerance, upload
 
 pytestmark = pytest.mark.gpu
 
@@ -236,3 +236,41 @@ def test_full_size_sampled_units(idx):
         unit_wl = wl.with_(B=1, C=cpg, G=1)
         check_against_oracle(sl, part, unit_wl, wl.backward, f"{wl.name} unit b={b} g={g}")
     assert np.all(np.isfinite(got["y"]))
+
+
+@pytest.mark.parametrize("wl", [case("med56-cpg12", 1, 24, 2, 56, 56),
+                                case("med64-cpg32", 1, 64, 2, 64, 64),
+                                case("med48-cpg12-dirs6", 2, 24, 2, 48, 48, dirs=6)],
+                         ids=lambda w: w.name)
+def test_slot_plans_agree(wl):
+    """The register-streamed backward under both launch plans (4 channels per
+    workgroup, or up to 8): each plan bitwise reproducible; dx, dlam and du
+    bit for bit the same across plans (nothing there depends on the plan);
+    dw, whose sum over a group's channels the plan associates differently,
+    within half a bf16 ulp of the exact value under both, so at most one ulp
+    apart."""
+    torch = require_gpu()
+    print(f"[case] slot plans {wl.name}", flush=True)
+    inputs = gi.make_inputs(wl, with_dy=True)
+    t = upload(inputs, wl.dtype, wl.dirs)
+    res = {}
+    for slots in (4, 8, 4):
+        out = gspn.scan_bwd(t["x"], t["w"], t["lam"], t["u"], t["dy"], wl.dirs, slots=slots)
+        torch.cuda.synchronize()
+        got = dict(zip(GRAD_KEYS, (to_host(v) for v in out)))
+        if slots in res:
+            for k in GRAD_KEYS:
+                assert np.array_equal(got[k], res[slots][k]), f"slots={slots} {k} not repeatable"
+        res[slots] = got
+    for k in ("dx", "dlam", "du"):
+        assert np.array_equal(res[4][k], res[8][k]), k
+    ref = oracle.scan_bwd(inputs["x"], inputs["w"], inputs["lam"], inputs["u"], inputs["dy"],
+                          wl.dirs)
+    ab = {k: np.abs(v) for k, v in inputs.items()}
+    mag = oracle.scan_bwd(ab["x"], inputs["w"], ab["lam"], ab["u"], ab["dy"], wl.dirs)
+    K = 16 * (wl.H + wl.C // wl.G)
+    for slots in (4, 8):
+        check_half_ulp(f"{wl.name} slots={slots} dw", res[slots]["dw"], ref["dw"], mag["dw"], K)
+    diff = np.abs(res[4]["dw"] - res[8]["dw"])
+    print(f"[err] {wl.name} dw elements differing between plans: "
+          f"{float(np.mean(diff > 0)):.2e}", flush=True)
