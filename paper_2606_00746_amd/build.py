@@ -10,7 +10,8 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libgspn.so")
-SOURCES = ["api.cpp", "scan_tiny.hip", "scan_small.hip", "scan_med.hip", "scan_pm.hip",
+SOURCES = ["api.cpp", "scan_tiny.hip", "scan_small.hip", "scan_med_64.hip", "scan_med_56.hip",
+           "scan_med_48.hip", "scan_med_40_32_24.hip", "scan_med.hip", "scan_pm.hip",
            "scan_wide.hip", "scan_norm.hip", "scan_general.hip", "latent.hip"]
 ARCH = "gfx950"
 
@@ -29,10 +30,12 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose: bool = False, jobs: int = 4, incremental: bool = False) -> str:
+def build(verbose: bool = False, jobs: int = 0, incremental: bool = False) -> str:
     """Compiles every source (incremental: only those older than their object,
     counting the shared headers) and links libgspn.so in place."""
     cc = hipcc()
+    if jobs <= 0:
+        jobs = max(1, min(8, os.cpu_count() or 1))
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
 

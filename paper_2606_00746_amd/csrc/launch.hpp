@@ -64,13 +64,18 @@ hipError_t launch_norm(const Problem &p, const void *wt, const void *dw, void *o
 bool med_supported(const Problem &p);
 hipError_t launch_fwd_med(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_med(const Problem &p, hipStream_t s);
+// one side of the register-streamed path (instantiated per side)
+template <int S>
+hipError_t med_fwd(const Problem &p, hipStream_t s);
+template <int S>
+hipError_t med_bwd(const Problem &p, hipStream_t s);
 bool wide_supported(const Problem &p);
 // Pixel-major problems of the register-streamed shapes: the weights are
 // re-laid out into the blocked order (launch_w_to_blocked, workspace of
 // |w| bytes) when a group has at least kReblockCpg channels, so that the
 // copy costs at most a quarter of the lambda traffic; then the forward is
 // launch_fwd_pm.
-constexpr int kReblockCpg = 4;
+constexpr int kReblockCpg = 1;
 inline bool pm_weights_reblocked(const Problem &p)
 {
     return p.layout == kPixelMajor && p.C / p.G >= kReblockCpg;

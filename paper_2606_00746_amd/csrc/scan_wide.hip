@@ -15,9 +15,15 @@
 // A 256 x 256 fp32 merge plane does not fit in LDS, so each direction writes
 // u_d * h_d to an fp32 plane in its own line-major order (whole lines per
 // store) and a tiled kernel sums the directions in direction-bit order,
-// transposing the horizontal ones through LDS, and stores y once.  With many
-// planes the scan goes in rounds of what fits the device at once, and each
-// round's sum runs on a side stream beside the next round's scan.
+// transposing the horizontal ones through LDS, and stores y once.
+//
+// Pixel-major per-direction tensors are first copied into the blocked order
+// of their direction in the caller's workspace (pieces_kernel: whole rows in
+// through LDS, whole 8-line blocks out), and the scan then runs as on blocked
+// tensors.  Read in place, a vertical scan would take 2 bytes of a row per
+// lane and load (8 loads per 16-byte piece, 40 per block of 8 lines and
+// position group), a horizontal one 16 bytes from each of 64 rows; the copy
+// costs one read and one write of lam, u and w at full bandwidth instead.
 //
 // With few channel planes the same direction pass runs on chunks of the scan
 // (fwd_wide_chunk_kernel, wide_carry_kernel): end states from zero, carries
@@ -94,7 +100,7 @@ enum PassMode { kStore, kEnd, kHomog };
 // run time); L, P: scan and line length; the x plane sits in LDS with pitch
 // (W / 2) | 1 dwords; ys receives u * h as fp32 in the direction's
 // line-major order (line l, position p at l * P + p).
-template <int NPL, bool VERT, bool REV, int HC, int WC, int MODE, bool PIX>
+template <int NPL, bool VERT, bool REV, int HC, int WC, int MODE>
 __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, rsrc_t u, rsrc_t w,
                                          const uint8_t *xs, u32x4 ys, int fb0, int fb1,
                                          float (&h)[NPL])
@@ -119,12 +125,12 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
 #pragma unroll
         for (int m = 0; m < NPL; ++m) {
             if (MODE != kHomog)
-                pc.l[m] = ld_piece<PIX, VERT, true>(lam, jc[m], sq, P, W);
+                pc.l[m] = ld_piece<false, VERT, true>(lam, jc[m], sq, P, W);
             if (MODE == kStore)
-                pc.u[m] = ld_piece<PIX, VERT, true>(u, jc[m], sq, P, W);
-            pc.w0[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W);
-            pc.w1[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W, wplane);
-            pc.w2[m] = ld_piece<PIX, VERT, false>(w, jc[m], sq, P, W, 2u * wplane);
+                pc.u[m] = ld_piece<false, VERT, true>(u, jc[m], sq, P, W);
+            pc.w0[m] = ld_piece<false, VERT, false>(w, jc[m], sq, P, W);
+            pc.w1[m] = ld_piece<false, VERT, false>(w, jc[m], sq, P, W, wplane);
+            pc.w2[m] = ld_piece<false, VERT, false>(w, jc[m], sq, P, W, 2u * wplane);
         }
     };
 
@@ -188,19 +194,19 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
 }
 
 // Direction d's pass over blocks fb0 .. fb1-1 (direction-uniform dispatch).
-template <int NPL, int HC, int WC, int MODE, bool PIX>
+template <int NPL, int HC, int WC, int MODE>
 __device__ __forceinline__ void wide_pass(int d, int lane, int H, int W, rsrc_t rl, rsrc_t ru,
                                           rsrc_t rw, const uint8_t *xs, u32x4 yd, int fb0,
                                           int fb1, float (&h)[NPL])
 {
     if (d == 0)
-        wide_dir<NPL, true, false, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, true, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else if (d == 1)
-        wide_dir<NPL, true, true, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, true, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else if (d == 2)
-        wide_dir<NPL, false, false, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, false, false, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
     else
-        wide_dir<NPL, false, true, HC, WC, MODE, PIX>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
+        wide_dir<NPL, false, true, HC, WC, MODE>(lane, H, W, rl, ru, rw, xs, yd, fb0, fb1, h);
 }
 
 // x plane of channel plane pc -> LDS: coalesced 16-byte pieces into padded rows.
@@ -224,7 +230,7 @@ __device__ __forceinline__ void stage_x_plane(const bf16_t *x, int64_t pc, int H
     }
 }
 
-template <int NPL, int HC, int WC, bool PIX>
+template <int NPL, int HC, int WC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H_,
@@ -258,7 +264,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         for (int m = 0; m < NPL; ++m)
             h[m] = 0.f;
         const int NB = (d < 2 ? H : W) / 8;
-        wide_pass<NPL, HC, WC, kStore, PIX>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
+        wide_pass<NPL, HC, WC, kStore>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
     }
 }
 
@@ -274,7 +280,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 //     u * h to the fp32 direction planes; then sum_wide_kernel as usual.
 // States are fp32 [plane][direction slot][chunk][max(H, W)], the first P
 // (the direction's line length) of each slot used.
-template <int NPL, int HC, int WC, int MODE, bool PIX>
+template <int NPL, int HC, int WC, int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_chunk_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, float *__restrict__ st, int mask, int B,
@@ -315,7 +321,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             const int p = lane + 64 * m;
             h[m] = (MODE == kStore && k > 0 && p < P) ? sk[p] : 0.f;
         }
-        wide_pass<NPL, HC, WC, MODE, PIX>(d, lane, H, W, rl, ru, rw, xs, yd, k * NBc,
+        wide_pass<NPL, HC, WC, MODE>(d, lane, H, W, rl, ru, rw, xs, yd, k * NBc,
                                           (k + 1) * NBc, h);
         if (MODE == kEnd) {
 #pragma unroll
@@ -331,7 +337,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // The carries: for each plane and direction, c_{k+1} = Phi_k c_k + e_k,
 // written over e_{k+1}'s slot neighbour: the state array holds e_k after
 // the first pass and c_k (k >= 1; slot 0 unused) after this one.
-template <int NPL, int HC, int WC, bool PIX>
+template <int NPL, int HC, int WC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void wide_carry_kernel(
     const bf16_t *__restrict__ w, float *__restrict__ st, int mask, int B, int C, int G, int H_,
     int W_, int K, Magic divC, Magic divCpg)
@@ -370,7 +376,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                 sp[(int64_t)k * SL + p] = h[m];
         }
         if (k + 1 < K) {
-            wide_pass<NPL, HC, WC, kHomog, PIX>(d, lane, H, W, rw, rw, rw, nullptr, u32x4{},
+            wide_pass<NPL, HC, WC, kHomog>(d, lane, H, W, rw, rw, rw, nullptr, u32x4{},
                                                 k * NBc, (k + 1) * NBc, h);
 #pragma unroll
             for (int m = 0; m < NPL; ++m)
@@ -463,15 +469,15 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
     }
 }
 
-template <int NPL, int HC, int WC, bool PIX>
+template <int NPL, int HC, int WC>
 hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, int plane0,
                       int nplanes)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC, PIX>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC, PIX>), dim3((unsigned)nplanes), dim3(256), lds,
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)nplanes), dim3(256), lds,
                        st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
@@ -480,14 +486,14 @@ hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, i
 }
 
 // The three launches of the chunked forward (see fwd_wide_chunk_kernel).
-template <int NPL, int HC, int WC, bool PIX>
+template <int NPL, int HC, int WC>
 hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float *states,
                               size_t lds, int K)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kEnd, PIX>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e == hipSuccess)
-        e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kStore, PIX>,
+        e = hipFuncSetAttribute((const void *)fwd_wide_chunk_kernel<NPL, HC, WC, kStore>,
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
@@ -496,12 +502,12 @@ hipError_t fwd_wide_chunked_t(const Problem &p, hipStream_t st, float *ys, float
     const unsigned planes = (unsigned)(p.B * p.C);
     const bf16_t *x = (const bf16_t *)p.x, *w = (const bf16_t *)p.w;
     const bf16_t *lam = (const bf16_t *)p.lam, *u = (const bf16_t *)p.u;
-    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kEnd, PIX>), dim3(planes * K), dim3(256),
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kEnd>), dim3(planes * K), dim3(256),
                        lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
                        divCpg, divNq, divK);
-    hipLaunchKernelGGL((wide_carry_kernel<NPL, HC, WC, PIX>), dim3(planes), dim3(256), 0, st, w,
+    hipLaunchKernelGGL((wide_carry_kernel<NPL, HC, WC>), dim3(planes), dim3(256), 0, st, w,
                        states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC, divCpg);
-    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kStore, PIX>), dim3(planes * K), dim3(256),
+    hipLaunchKernelGGL((fwd_wide_chunk_kernel<NPL, HC, WC, kStore>), dim3(planes * K), dim3(256),
                        lds, st, x, w, lam, u, ys, states, p.mask, p.B, p.C, p.G, p.H, p.W, K, divC,
                        divCpg, divNq, divK);
     return hipGetLastError();
@@ -522,6 +528,91 @@ hipError_t launch_sum_wide(const Problem &p, const float *ys, hipStream_t st, in
 }
 
 size_t wide_lds_bytes(int H, int W) { return (size_t)H * 4 * wide_pitch_dw(W); }
+
+// Pixel-major planes -> blocked line-major.  A row of an H x W plane is nq =
+// W / 8 pieces of 16 bytes (piece q: columns 8q..8q+7).  One workgroup per
+// band of 32 rows of one plane copies the band's rows into LDS with direct
+// 16-byte loads (no registers; rows of nq | 1 pieces, the padding slots
+// skipped), then writes the band's part of the blocked plane:
+//  * vertical direction (lines are rows, positions columns): piece (q, p) of
+//    the output, at q * W + p, holds column p of rows 8q..8q+7, gathered from
+//    8 LDS rows (lanes on consecutive columns: no bank conflict);
+//  * horizontal direction (lines are columns, positions rows): piece (q, p),
+//    at q * H + p, is input piece q of row p, a transpose of 16-byte pieces
+//    (a wave reads one piece column; with an odd pitch 16 consecutive lanes
+//    hit distinct banks).
+// Consecutive lanes write consecutive output pieces.
+constexpr int kBand = 32;
+constexpr int kBandSlots = kBand * ((64 * kMaxNpl / 8) | 1);   // LDS pieces (W <= 256)
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef const __attribute__((address_space(1))) void glb_void;
+
+__global__ __launch_bounds__(256) void pieces_kernel(const uint4 *__restrict__ src,
+                                                     uint4 *__restrict__ dst, int H, int W,
+                                                     int bands, int vert, Magic divBands,
+                                                     Magic divPitch, Magic divW)
+{
+    __shared__ uint4 T[kBandSlots];
+    const int nq = W / 8, pitch = nq | 1;
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int bid = xcd_remap(blockIdx.x, gridDim.x);
+    const int pl = mdiv(bid, divBands);
+    const int r0 = (bid - pl * bands) * kBand;
+    const int rows = H - r0 < kBand ? H - r0 : kBand;     // a multiple of 8
+    const int64_t base = (int64_t)pl * H * nq;
+    const uint4 *band = src + base + (int64_t)r0 * nq;
+    // wave-instruction k fills LDS slots 64k .. 64k+63 (slot: row s / pitch,
+    // piece s % pitch)
+    const int nslots = rows * pitch;
+    for (int k = wave; 64 * k < nslots; k += 4) {
+        const int sl = 64 * k + lane;
+        const int r = mdiv(sl, divPitch), q = sl - r * pitch;
+        if (sl < nslots && q < nq)
+            __builtin_amdgcn_global_load_lds((glb_void *)(band + r * nq + q),
+                                             (lds_void *)(T + 64 * k), 16, 0, 0);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (vert) {
+        const uint16_t *T16 = reinterpret_cast<const uint16_t *>(T);
+        for (int t = threadIdx.x; t < (rows / 8) * W; t += 256) {
+            const int q = mdiv(t, divW), p = t - q * W;
+            uint32_t e[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+                e[k] = T16[(8 * q + k) * (8 * pitch) + p];
+            gst128(dst + base + (int64_t)(r0 / 8 + q) * W + p,
+                   make_uint4(e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                              e[6] | (e[7] << 16)));
+        }
+    } else {
+        for (int t = threadIdx.x; t < kBand * nq; t += 256) {
+            const int q = t / kBand, r = t - q * kBand;
+            if (r < rows)
+                gst128(dst + base + (int64_t)q * H + r0 + r, T[r * pitch + q]);
+        }
+    }
+}
+
+// nv vertical planes, then nh horizontal ones, of H x W at src -> dst.
+hipError_t launch_pieces(const void *src, void *dst, int64_t nv, int64_t nh, int H, int W,
+                         hipStream_t st)
+{
+    const int bands = (H + kBand - 1) / kBand;
+    const Magic divB = make_magic((uint32_t)bands), divP = make_magic((uint32_t)((W / 8) | 1));
+    const Magic divW = make_magic((uint32_t)W);
+    const int64_t HW = (int64_t)H * W;
+    const uint4 *s = (const uint4 *)src;
+    uint4 *d = (uint4 *)dst;
+    if (nv > 0)
+        hipLaunchKernelGGL(pieces_kernel, dim3((unsigned)(nv * bands)), dim3(256), 0, st, s, d, H,
+                           W, bands, 1, divB, divP, divW);
+    if (nh > 0)
+        hipLaunchKernelGGL(pieces_kernel, dim3((unsigned)(nh * bands)), dim3(256), 0, st,
+                           s + nv * HW / 8, d + nv * HW / 8, H, W, bands, 0, divB, divP, divW);
+    return hipGetLastError();
+}
 
 // Chunks per scan for the chunked forward, or 1 for the single pass.  The
 // chunked forward does more than twice the single pass's work (both passes
@@ -550,7 +641,6 @@ int wide_chunks(const Problem &p, size_t lds)
     return (K >= 8 && nbh >= 32 && nbw >= 32) ? K : 1;
 }
 
-template <bool PIX>
 hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states, size_t lds, int K)
 {
     const int side = p.H > p.W ? p.H : p.W;
@@ -558,21 +648,21 @@ hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states
     // the square planes of 256 and 128 get kernels with their shape built in
     if (K > 1) {
         if (p.H == 256 && p.W == 256)
-            return fwd_wide_chunked_t<4, 256, 256, PIX>(p, st, ys, states, lds, K);
+            return fwd_wide_chunked_t<4, 256, 256>(p, st, ys, states, lds, K);
         if (p.H == 128 && p.W == 128)
-            return fwd_wide_chunked_t<2, 128, 128, PIX>(p, st, ys, states, lds, K);
-        return npl <= 2 ? fwd_wide_chunked_t<2, 0, 0, PIX>(p, st, ys, states, lds, K)
-               : npl == 3 ? fwd_wide_chunked_t<3, 0, 0, PIX>(p, st, ys, states, lds, K)
-                          : fwd_wide_chunked_t<4, 0, 0, PIX>(p, st, ys, states, lds, K);
+            return fwd_wide_chunked_t<2, 128, 128>(p, st, ys, states, lds, K);
+        return npl <= 2 ? fwd_wide_chunked_t<2, 0, 0>(p, st, ys, states, lds, K)
+               : npl == 3 ? fwd_wide_chunked_t<3, 0, 0>(p, st, ys, states, lds, K)
+                          : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
     }
     const int planes = p.B * p.C;
     if (p.H == 256 && p.W == 256)
-        return fwd_wide_t<4, 256, 256, PIX>(p, st, ys, lds, 0, planes);
+        return fwd_wide_t<4, 256, 256>(p, st, ys, lds, 0, planes);
     if (p.H == 128 && p.W == 128)
-        return fwd_wide_t<2, 128, 128, PIX>(p, st, ys, lds, 0, planes);
-    return npl <= 2 ? fwd_wide_t<2, 0, 0, PIX>(p, st, ys, lds, 0, planes)
-           : npl == 3 ? fwd_wide_t<3, 0, 0, PIX>(p, st, ys, lds, 0, planes)
-                      : fwd_wide_t<4, 0, 0, PIX>(p, st, ys, lds, 0, planes);
+        return fwd_wide_t<2, 128, 128>(p, st, ys, lds, 0, planes);
+    return npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds, 0, planes)
+           : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds, 0, planes)
+                      : fwd_wide_t<4, 0, 0>(p, st, ys, lds, 0, planes);
 }
 
 }  // namespace
@@ -597,11 +687,39 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     const int64_t nst = K > 1 ? (int64_t)p.B * p.C * D * K * std::max(p.H, p.W) : 0;
     float *ys = nullptr;
     hipError_t e = p.ws->take((void **)&ys, (size_t)(D * n + nst) * sizeof(float));
-    if (e != hipSuccess || p.ws->counting)
+    if (e != hipSuccess)
         return e;
-    float *states = ys + D * n;
-    e = p.layout == kPixelMajor ? fwd_wide_l<true>(p, st, ys, states, lds, K)
-                                : fwd_wide_l<false>(p, st, ys, states, lds, K);
+    if (p.layout != kPixelMajor) {
+        if (p.ws->counting)
+            return hipSuccess;
+        e = fwd_wide_l(p, st, ys, ys + D * n, lds, K);
+    } else {
+        // blocked copies of lam, u and w (workspace), then the blocked scan
+        const int64_t nw = (int64_t)D * p.B * p.G * 3 * p.H * p.W;
+        void *cl = nullptr, *cu = nullptr, *cw = nullptr;
+        e = p.ws->take(&cl, (size_t)(D * n) * 2);
+        if (e == hipSuccess)
+            e = p.ws->take(&cu, (size_t)(D * n) * 2);
+        if (e == hipSuccess)
+            e = p.ws->take(&cw, (size_t)nw * 2);
+        if (e != hipSuccess || p.ws->counting)
+            return e;
+        const int nv = __builtin_popcount(p.mask & 3), nh = D - nv;
+        const int64_t bc = (int64_t)p.B * p.C, bg3 = (int64_t)p.B * p.G * 3;
+        e = launch_pieces(p.lam, cl, nv * bc, nh * bc, p.H, p.W, st);
+        if (e == hipSuccess)
+            e = launch_pieces(p.u, cu, nv * bc, nh * bc, p.H, p.W, st);
+        if (e == hipSuccess)
+            e = launch_pieces(p.w, cw, nv * bg3, nh * bg3, p.H, p.W, st);
+        if (e != hipSuccess)
+            return e;
+        Problem q = p;
+        q.lam = cl;
+        q.u = cu;
+        q.w = cw;
+        q.layout = kBlocked;
+        e = fwd_wide_l(q, st, ys, ys + D * n, lds, K);
+    }
     if (e == hipSuccess)
         e = launch_sum_wide(p, ys, st, 0, p.B * p.C);
     return e;
