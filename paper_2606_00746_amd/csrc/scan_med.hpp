@@ -345,6 +345,19 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     auto rowoff = [&](int i) -> uint32_t { return 2u * (uint32_t)(line_of(i) * W); };
     auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)pidx(jj, line_of(i))); };
 
+    // the forward sweep's pieces: its first two blocks are loaded during the
+    // reverse sweep's last two, so that they arrive while it ends
+    uint4 rl[NB], p0[NB], p1[NB], p2[NB];
+    uint32_t rx[VERT ? L : 1];
+#define FLOADB(fb)                                                   \
+    do {                                                             \
+        const int sq_ = sblk(fb);                                    \
+        rl[fb] = ld_piece<LPM, VERT, true>(A.lam, jj, sq_, P, W);     \
+        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
+        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
+        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+    } while (0)
+
     // --- reverse sweep: adjoint a_i -------------------------------------
     float ahist[L];
     uint32_t pdy[VERT ? L / 2 : 1];
@@ -380,11 +393,18 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         for (int fb = NB - 1; fb >= 0; --fb) {
             if (fb >= 2)
                 RLOAD(fb - 2);
+            else if (fb == 1 || NB == 1)
+                FLOADB(0);
+            else
+                FLOADB(1);
 #pragma unroll
             for (int t = 7; t >= 0; --t) {
                 const int i = 8 * fb + t;
                 if (VERT && i - kPrefetch >= 0)
                     rd[VERT ? i - kPrefetch : 0] = ld16(A.dy, vr, rowoff(i - kPrefetch));
+                else if (VERT)
+                    rx[VERT ? kPrefetch - 1 - i : 0] =
+                        ld16(A.x, vr, rowoff(kPrefetch - 1 - i));
                 float dyv;
                 if (VERT) {
                     dyv = bf_lo(rd[VERT ? i : 0]);
@@ -418,24 +438,6 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     }
 
     // --- forward sweep: states, local gradients, dw terms ---------------
-    uint4 rl[NB], p0[NB], p1[NB], p2[NB];
-    uint32_t rx[VERT ? L : 1];
-#define FLOADB(fb)                                                   \
-    do {                                                             \
-        const int sq_ = sblk(fb);                                    \
-        rl[fb] = ld_piece<LPM, VERT, true>(A.lam, jj, sq_, P, W);     \
-        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
-        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
-    } while (0)
-    FLOADB(0);
-    if (NB > 1)
-        FLOADB(1);
-    if (VERT) {
-#pragma unroll
-        for (int i = 0; i < kPrefetch; ++i)
-            rx[VERT ? i : 0] = ld16(A.x, vr, rowoff(i));
-    }
 
     // Reduction roles: step st of a batch belongs to wave st (waves 0..3, one
     // per SIMD); with fewer than kBatch waves (IMM) each wave takes several
@@ -1343,9 +1345,7 @@ hipError_t fwd_med_l(const Problem &p, hipStream_t st)
 {
     if (p.layout != kPixelMajor)
         return fwd_med_t<H, W, false>(p, st);
-    if (pm_weights_reblocked(p))
-        return launch_fwd_pm(p, st);
-    return fwd_med_t<H, W, true>(p, st);
+    return launch_fwd_pm(p, st);
 }
 
 template <int H, int W>
@@ -1353,8 +1353,6 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
 {
     if (p.layout != kPixelMajor)
         return bwd_med_t<H, W, false, false>(p, st);
-    if (!pm_weights_reblocked(p))
-        return bwd_med_t<H, W, true, true>(p, st);
     // the group's weights, and lambda and u of the horizontal directions,
     // re-laid out once into the blocked order of their direction
     // (workspace), read there as 16-byte pieces: a horizontal scan would read

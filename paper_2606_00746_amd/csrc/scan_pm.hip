@@ -16,8 +16,9 @@
 //    vertical scans and 16-byte column pieces for horizontal ones, keeps
 //    each lane's states h in registers, and applies u afterwards, row by
 //    row: each direction's h plane goes through an fp32 LDS plane and every
-//    thread adds u_d * h_d for 8 pixels of a row, u_d loaded with coalesced
-//    16-byte row pieces (Sec. 3, Eqs. (gspn_recurrence), (gspn_output)).
+//    thread adds u_d * h_d for 8 pixels of a row, u_d loaded into registers
+//    with coalesced 16-byte row pieces while the planes are staged (Sec. 3,
+//    Eqs. (gspn_recurrence), (gspn_output)).
 #include "cdna.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -212,6 +213,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
                            lam + (((int64_t)sk * B + b) * C + c) * HW, d, 4, lane);
         }
     }
+    // every direction's u, 8 pixels of a row per thread and piece, loaded
+    // beside the staging: the merge below waits on no load
+    uint4 uq[4][PER];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        if ((mask >> p) & 1) {
+            const int sp = __popc(mask & ((1 << p) - 1));
+            const rsrc_t ur = make_rsrc(u + (((int64_t)sp * B + b) * C + c) * HW, 2 * HW);
+#pragma unroll
+            for (int k = 0; k < PER; ++k) {
+                const int t = threadIdx.x + 256 * k;
+                uq[p][k] = t < NCH ? ld128_nt(ur, 16u * (uint32_t)t, 0) : make_uint4(0, 0, 0, 0);
+            }
+        }
+    }
     __builtin_amdgcn_s_waitcnt(0);
     lds_barrier();
 
@@ -241,17 +257,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
 #pragma unroll
         for (int e = 0; e < 8; ++e)
             acc[k][e] = 0.f;
+#pragma unroll
     for (int p = 0; p < 4; ++p) {
         if (!((mask >> p) & 1))
             continue;
-        const int sp = __popc(mask & ((1 << p) - 1));
-        const rsrc_t ur = make_rsrc(u + (((int64_t)sp * B + b) * C + c) * HW, 2 * HW);
-        uint4 uq[PER];
-#pragma unroll
-        for (int k = 0; k < PER; ++k) {
-            const int t = threadIdx.x + 256 * k;
-            uq[k] = t < NCH ? ld128_nt(ur, 16u * (uint32_t)t, 0) : make_uint4(0, 0, 0, 0);
-        }
         if (d == p && lane < S) {
             if (p < 2) {
                 // column `lane`, row of step i
@@ -286,7 +295,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
                 // kernels do: both layouts give the same bits)
 #pragma unroll
                 for (int e = 0; e < 8; ++e)
-                    acc[k][e] = add_nc(acc[k][e], mul_nc(elem(uq[k], e), hv[e]));
+                    acc[k][e] = add_nc(acc[k][e], mul_nc(elem(uq[p][k], e), hv[e]));
             }
         }
         lds_barrier();
