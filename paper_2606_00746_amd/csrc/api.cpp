@@ -149,6 +149,12 @@ int scan_buffers(int op, const void *x, const void *w, const void *lam, const vo
 
 bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_BLOCKED; }
 
+// Pixel-major calls on the register-streamed shapes read their weights in
+// the blocked order: the _norm passes form them there directly from the
+// logits (one read of the logits, one write of the weights), instead of
+// writing pixel-major weights that the scan then re-lays out.
+bool norm_fused(const Problem &p) { return p.layout == kPixelMajor && med_supported(p); }
+
 // The launches of one scan operation on the workspace ws (in counting mode:
 // no launch, ws.used adds up what the call takes).
 hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, hipStream_t s)
@@ -171,8 +177,10 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
         if (e != hipSuccess)
             return e;
         p.w = w;
+        p.w_blocked = norm_fused(p);
         if (!ws.counting) {
-            e = launch_norm(p, w_in, nullptr, w, s);
+            e = p.w_blocked ? launch_norm_blocked(p, w_in, w, s)
+                            : launch_norm(p, w_in, nullptr, w, s);
             if (e != hipSuccess)
                 return e;
         }
@@ -189,8 +197,10 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
             return e;
         p.w = w;
         p.dw = dw;
+        p.w_blocked = norm_fused(p);
         if (!ws.counting) {
-            e = launch_norm(p, w_in, nullptr, w, s);
+            e = p.w_blocked ? launch_norm_blocked(p, w_in, w, s)
+                            : launch_norm(p, w_in, nullptr, w, s);
             if (e != hipSuccess)
                 return e;
         }

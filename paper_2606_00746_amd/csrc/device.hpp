@@ -24,6 +24,24 @@ __device__ __forceinline__ void store_f(bf16_t *p, float v)
     *p = __builtin_bit_cast(bf16_t, b);
 }
 
+// Sec. 3, Eq. (row_stochastic_norm) for one pixel: s_k = sigmoid(t_k) on the
+// taps whose neighbour lies on the grid (on0, on2; tap 1 always), 0 on the
+// others, and w_k = s_k / max(s_0 + s_1 + s_2, kNormEps).
+constexpr float kNormEps = 1e-30f;
+
+__device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
+
+__device__ __forceinline__ void norm3(const float (&t)[3], bool on0, bool on2, float (&w)[3])
+{
+    const float s0 = on0 ? sigmoid(t[0]) : 0.f;
+    const float s1 = sigmoid(t[1]);
+    const float s2 = on2 ? sigmoid(t[2]) : 0.f;
+    const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+    w[0] = s0 * inv;
+    w[1] = s1 * inv;
+    w[2] = s2 * inv;
+}
+
 // DPP lane shifts along a line of T lanes (T = 16, 32 or 64).  from_left(v)
 // returns v of lane-1 and from_right(v) v of lane+1; lanes without a source
 // read 0 (bound_ctrl).  For T = 16 the shift stays inside each 16-lane row,

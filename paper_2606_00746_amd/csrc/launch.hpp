@@ -44,6 +44,9 @@ struct Problem {
     // channel slots per step of the register-streamed backward: 0 the
     // planner's choice, 4 or 8 that plan where the shape can take it
     int slots = 0;
+    // w is already in the blocked order of its direction although the call
+    // is pixel-major (weights the library formed itself, launch_norm_blocked)
+    bool w_blocked = false;
 };
 
 // Planes whose sides are both <= kSmallSide run on the register-resident path.
@@ -84,6 +87,10 @@ hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t s);
 // lam and u of the horizontal directions into blocked copies [nh][B][C][plane].
 hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipStream_t s);
 hipError_t launch_fwd_pm(const Problem &p, hipStream_t s);
+// Pixel-major logits -> normalized weights in the blocked order (|w| bytes
+// at wb), for the register-streamed shapes: the normalization of
+// launch_norm and the re-layout of launch_w_to_blocked in one pass.
+hipError_t launch_norm_blocked(const Problem &p, const void *wt, void *wb, hipStream_t s);
 hipError_t launch_fwd_wide(const Problem &p, hipStream_t s);
 hipError_t launch_fwd_general(const Problem &p, hipStream_t s);
 hipError_t launch_bwd_general(const Problem &p, hipStream_t s);

@@ -1359,8 +1359,10 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     // each pixel-major piece from 64 rows
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * H * W;
     const int64_t nh = (int64_t)__builtin_popcount(p.mask & 12) * p.B * p.C * H * W;
-    void *wb = nullptr, *lamh = nullptr, *uh = nullptr;
-    hipError_t e = p.ws->take(&wb, (size_t)nw * 2);
+    void *wb = const_cast<void *>(p.w), *lamh = nullptr, *uh = nullptr;
+    hipError_t e = hipSuccess;
+    if (!p.w_blocked)
+        e = p.ws->take(&wb, (size_t)nw * 2);
     if (e == hipSuccess && nh > 0)
         e = p.ws->take(&lamh, (size_t)nh * 2);
     if (e == hipSuccess && nh > 0)
@@ -1368,7 +1370,8 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     if (e != hipSuccess)
         return e;
     if (!p.ws->counting) {
-        e = launch_w_to_blocked(p, wb, st);
+        if (!p.w_blocked)
+            e = launch_w_to_blocked(p, wb, st);
         if (e == hipSuccess && nh > 0)
             e = launch_horiz_to_blocked(p, lamh, uh, st);
         if (e != hipSuccess)

@@ -24,9 +24,6 @@ namespace {
 
 using namespace cdna;
 
-constexpr float kNormEps = 1e-30f;
-
-__device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
 
 __device__ __forceinline__ void load8(const float *p, float (&v)[8])
 {
@@ -53,18 +50,6 @@ __device__ __forceinline__ void store8(bf16_t *p, const float (&v)[8])
 {
     gst128(reinterpret_cast<uint4 *>(p),
            make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
-}
-
-// Normalized weights of one pixel from its three logits.
-__device__ __forceinline__ void norm3(const float (&t)[3], bool on0, bool on2, float (&w)[3])
-{
-    const float s0 = on0 ? sigmoid(t[0]) : 0.f;
-    const float s1 = sigmoid(t[1]);
-    const float s2 = on2 ? sigmoid(t[2]) : 0.f;
-    const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
-    w[0] = s0 * inv;
-    w[1] = s1 * inv;
-    w[2] = s2 * inv;
 }
 
 // Gradient with respect to the logits of one pixel.

@@ -111,6 +111,69 @@ __global__ __launch_bounds__(256) void to_blocked_kernel(const bf16_t *__restric
     }
 }
 
+// Logits -> normalized weights, pixel-major -> blocked, one workgroup per
+// direction slot, batch and group (three tap planes): the logit planes are
+// staged in LDS, each thread forms the weights of the 8 pixels of one
+// output piece (q, p) from their three logits (Sec. 3,
+// Eq. (row_stochastic_norm)) and writes the piece of every tap.  The line
+// position p decides taps 0 and 2, as in the unfused normalization.
+template <int S>
+__global__ __launch_bounds__(256) void norm_to_blocked_kernel(const bf16_t *__restrict__ wt,
+                                                              uint4 *__restrict__ out, int vslots,
+                                                              int per_slot)
+{
+    using Pl = PmPlane<S>;
+    __shared__ uint4 sm[3 * Pl::kBytes / 16];
+    uint8_t *pl = reinterpret_cast<uint8_t *>(sm);
+    const int set = blockIdx.x;                           // slot * per_slot + (b, g)
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        stage_plane<S>(pl + k * Pl::kBytes, wt + ((int64_t)set * 3 + k) * S * S, wave, 4, lane);
+    __builtin_amdgcn_s_waitcnt(0);
+    lds_barrier();
+    const bool vert = (vslots >> (set / per_slot)) & 1;
+    constexpr int NQ = S / 8;
+    uint4 *dst = out + (int64_t)set * 3 * (S * S / 8);
+    for (int t = threadIdx.x; t < NQ * S; t += 256) {
+        const int q = t / S, p = t - q * S;               // piece (q, p)
+        float lg[3][8];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const uint8_t *pk = pl + k * Pl::kBytes;
+            if (vert) {
+                // rows 8q.. of column p
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    lg[k][e] = __uint_as_float(lds_u16(pk, (8 * q + e) * Pl::kPitch + 2 * p) << 16);
+            } else {
+                // columns 8q.. of row p
+                const uint4 v = *reinterpret_cast<const uint4 *>(pk + p * Pl::kPitch + 16 * q);
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    lg[k][e] = elem(v, e);
+            }
+        }
+        const bool on0 = p > 0, on2 = p + 1 < S;
+        uint32_t pk3[3][4];
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+            float w0[3], w1[3];
+            const float t0[3] = {lg[0][e], lg[1][e], lg[2][e]};
+            const float t1[3] = {lg[0][e + 1], lg[1][e + 1], lg[2][e + 1]};
+            norm3(t0, on0, on2, w0);
+            norm3(t1, on0, on2, w1);
+#pragma unroll
+            for (int k = 0; k < 3; ++k)
+                pk3[k][e / 2] = pack2(w0[k], w1[k]);
+        }
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            gst128(dst + k * (S * S / 8) + t,
+                   make_uint4(pk3[k][0], pk3[k][1], pk3[k][2], pk3[k][3]));
+    }
+}
+
 // ---------------------------------------------------------------------------
 // forward
 // ---------------------------------------------------------------------------
@@ -346,14 +409,34 @@ hipError_t horiz_to_blocked_t(const Problem &p, void *lamh, void *uh, hipStream_
 }
 
 template <int S>
+hipError_t norm_blocked_t(const Problem &p, const void *wt, void *wb, hipStream_t st)
+{
+    int vslots = 0;
+    for (int d = 0, sl = 0; d < 4; ++d)
+        if ((p.mask >> d) & 1) {
+            if (d < 2)
+                vslots |= 1 << sl;
+            ++sl;
+        }
+    const int per_slot = p.B * p.G;
+    const int sets = __builtin_popcount(p.mask) * per_slot;
+    hipLaunchKernelGGL((norm_to_blocked_kernel<S>), dim3((unsigned)sets), dim3(256), 0, st,
+                       (const bf16_t *)wt, (uint4 *)wb, vslots, per_slot);
+    return hipGetLastError();
+}
+
+template <int S>
 hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
 {
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * S * S;
-    void *wb = nullptr;
-    hipError_t e = p.ws->take(&wb, (size_t)nw * 2);
+    void *wb = const_cast<void *>(p.w);
+    hipError_t e = hipSuccess;
+    if (!p.w_blocked)
+        e = p.ws->take(&wb, (size_t)nw * 2);
     if (e != hipSuccess || p.ws->counting)
         return e;
-    e = w_to_blocked_t<S>(p, wb, st);
+    if (!p.w_blocked)
+        e = w_to_blocked_t<S>(p, wb, st);
     if (e != hipSuccess)
         return e;
     hipLaunchKernelGGL((fwd_pm_kernel<S>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
@@ -386,6 +469,18 @@ hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipSt
     case 40: return horiz_to_blocked_t<40>(p, lamh, uh, st);
     case 32: return horiz_to_blocked_t<32>(p, lamh, uh, st);
     default: return horiz_to_blocked_t<24>(p, lamh, uh, st);
+    }
+}
+
+hipError_t launch_norm_blocked(const Problem &p, const void *wt, void *wb, hipStream_t st)
+{
+    switch (p.H) {
+    case 64: return norm_blocked_t<64>(p, wt, wb, st);
+    case 56: return norm_blocked_t<56>(p, wt, wb, st);
+    case 48: return norm_blocked_t<48>(p, wt, wb, st);
+    case 40: return norm_blocked_t<40>(p, wt, wb, st);
+    case 32: return norm_blocked_t<32>(p, wt, wb, st);
+    default: return norm_blocked_t<24>(p, wt, wb, st);
     }
 }
 
