@@ -39,11 +39,17 @@ _ROOT = os.path.dirname(_HERE)
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
-# the source file of each kernel family, by a part of the kernel's name
-_FAMILY_SOURCES = (("_med_", "scan_med.hip"), ("dw_sum", "scan_med.hip"),
-                   ("_wide_", "scan_wide.hip"), ("_tiny_", "scan_tiny.hip"),
-                   ("_small_", "scan_small.hip"), ("_general_", "scan_general.hip"),
-                   ("norm", "scan_norm.hip"))
+# the source files of each kernel family, by a part of the kernel's name
+_MED = ("scan_med.hpp", "scan_med.hip", "scan_med_64.hip", "scan_med_56.hip", "scan_med_48.hip",
+        "scan_med_40_32_24.hip")
+_FAMILY_SOURCES = (("_med_", _MED), ("dw_sum", _MED), ("_pm_", ("scan_pm.hip",)),
+                   ("to_blocked", ("scan_pm.hip",)), ("_wide_", ("scan_wide.hip",)),
+                   ("pieces_kernel", ("scan_wide.hip",)), ("_tiny_", ("scan_tiny.hip",)),
+                   ("_small_", ("scan_small.hip",)), ("_general_", ("scan_general.hip",)),
+                   ("norm", ("scan_norm.hip",)))
+# kernels that run at the start of a call (re-layouts into the blocked order):
+# they belong to the call whose scan kernel follows them
+_PREPASS = ("to_blocked_kernel", "norm_to_blocked_kernel", "pieces_kernel")
 # shared by every family: device helpers, launch declarations, the dispatch
 # and the build flags
 _COMMON_SOURCES = ("cdna.hpp", "device.hpp", "launch.hpp", "api.cpp")
@@ -56,7 +62,7 @@ def source_files(kernels=None) -> list:
     every = sorted(f for f in os.listdir(csrc) if f.endswith((".hip", ".hpp", ".cpp")))
     names = set(_COMMON_SOURCES)
     for k in kernels or ():
-        hit = [f for part, f in _FAMILY_SOURCES if part in k]
+        hit = [f for part, fs in _FAMILY_SOURCES if part in k for f in fs]
         if not hit:
             return [os.path.join(csrc, f) for f in every] + [os.path.join(_HERE, "build.py")]
         names.update(hit)
@@ -119,12 +125,43 @@ def _counter(path: str) -> dict:
     return vals
 
 
+def _dispatches(path: str) -> list:
+    """(kernel, counter value) of every dispatch of a one-counter run, in
+    dispatch order."""
+    d = {}
+    for r in csv.DictReader(open(path)):
+        i = int(r["Dispatch_Id"])
+        k, v = d.get(i, (r["Kernel_Name"], 0.0))
+        d[i] = (k, v + float(r["Counter_Value"]))
+    return [d[i] for i in sorted(d)]
+
+
+def _calls_in_order(disp: list) -> list:
+    """The library call of each dispatch: call_of for the scan kernels and
+    their sums, the next scan kernel's call for a re-layout that precedes it,
+    None for the rest."""
+    out, cur = [None] * len(disp), None
+    for n in range(len(disp) - 1, -1, -1):
+        k = short_name(disp[n][0])
+        c = call_of(k)
+        if c is not None:
+            cur = c
+            out[n] = c
+        elif k.startswith(_PREPASS):
+            out[n] = cur
+    return out
+
+
 def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
                    command: str, calls: int = 3) -> dict:
     """Bytes per call of the library: every dispatch of its kernels counted,
     divided by the number of calls the run made (a call may dispatch a kernel
     several times, e.g. one scan per round of planes)."""
     fetch, write = _counter(fetch_csv), _counter(write_csv)
+    fd, wd = _dispatches(fetch_csv), _dispatches(write_csv)
+    if [k for k, _ in fd] != [k for k, _ in wd]:
+        raise SystemExit("the two counter runs dispatched different kernels")
+    calls_of = _calls_in_order(fd)
     copy = [k for k in fetch if short_name(k) == COPY_KERNEL]
     if not copy:
         raise SystemExit(f"no {COPY_KERNEL} dispatch in {fetch_csv}: run bench.py with "
@@ -137,18 +174,25 @@ def traffic_record(fetch_csv: str, write_csv: str, workload: str, copy_mib: int,
     f_copy = fetch[copy[0]][at] * 1024.0
     w_copy = wl[at] * 1024.0
     scale_f, scale_w = copy_bytes / f_copy, copy_bytes / w_copy
-    kernels, per_call = {}, collections.defaultdict(float)
-    for k, v in fetch.items():
-        call = call_of(k)
+    # per (kernel, call): dispatches and bytes (a re-layout kernel may serve
+    # both calls)
+    acc = collections.defaultdict(lambda: [0, 0.0, 0.0])
+    for (k, fv), (_, wv), call in zip(fd, wd, calls_of):
         if call is None:
             continue
-        fb = sum(v) / len(v) * 1024.0 * scale_f
-        wb = sum(write[k]) / len(write[k]) * 1024.0 * scale_w
-        kernels[short_name(k)] = {"call": call, "fetch_bytes": round(fb), "write_bytes": round(wb),
-                                  "dispatches": len(v), "dispatches_per_call": len(v) / calls}
-        per_call[call] += (fb + wb) * len(v) / calls
-    return {"workload": workload, "source_hash": source_hash(sorted(kernels)),
-            "source_files": [os.path.basename(f) for f in source_files(sorted(kernels))],
+        a = acc[(short_name(k), call)]
+        a[0] += 1
+        a[1] += fv * 1024.0 * scale_f
+        a[2] += wv * 1024.0 * scale_w
+    kernels, per_call = {}, collections.defaultdict(float)
+    for (k, call), (n, fb, wb) in acc.items():
+        name = k if (k, "fwd" if call == "bwd" else "bwd") not in acc else f"{k} [{call}]"
+        kernels[name] = {"call": call, "fetch_bytes": round(fb / n), "write_bytes": round(wb / n),
+                         "dispatches": n, "dispatches_per_call": n / calls}
+        per_call[call] += (fb + wb) / calls
+    names = sorted({k.split(" [")[0] for k in kernels})
+    return {"workload": workload, "source_hash": source_hash(names),
+            "source_files": [os.path.basename(f) for f in source_files(names)],
             "command": command,
             "copy_calibration": {"bytes": copy_bytes, "fetch_kib": f_copy / 1024.0,
                                  "write_kib": w_copy / 1024.0, "fetch_scale": scale_f,
@@ -204,7 +248,8 @@ def load_traffic(path: str, call: str) -> float | None:
         rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if rec.get("source_hash") != source_hash(sorted(rec.get("kernels", {}))):
+    if rec.get("source_hash") != source_hash(sorted({k.split(" [")[0]
+                                                     for k in rec.get("kernels", {})})):
         return None
     return rec.get("bytes_per_call", {}).get(call)
 

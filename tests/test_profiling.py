@@ -99,3 +99,24 @@ def test_waves_summary_shares(tmp_path):
     # kernel name has spaces: read the numeric columns from the right
     wait, valu = float(f[-6]), float(f[-3])
     assert abs(wait - 0.5) < 1e-3 and abs(valu - 0.2) < 1e-3
+
+
+def test_relayout_kernels_belong_to_the_call_they_precede(tmp_path):
+    # pixel-major calls: the weight re-layout precedes the forward scan; the
+    # weight and lambda/u re-layouts precede the backward scan
+    copy = "__amd_rocclr_copyBuffer(char const*, char*)"
+    rel = "void gspn::(anonymous namespace)::to_blocked_kernel<64>(int)"
+    fwd = "void gspn::(anonymous namespace)::fwd_pm_kernel<64>(int)"
+    bwd = "void gspn::(anonymous namespace)::bwd_med_kernel<64, 64, 1>(int)"
+    flush = "void at::native::reduce_kernel<512, 1>(int)"
+    step = [(flush, 999.0), (rel, 10.0), (fwd, 100.0), (flush, 999.0), (rel, 10.0), (rel, 20.0),
+            (rel, 20.0), (bwd, 300.0)]
+    _csv(tmp_path / "f.csv", "FETCH_SIZE", [(copy, 2048.0)] + step * 2)
+    _csv(tmp_path / "w.csv", "WRITE_SIZE", [(copy, 4096.0)] + step * 2)
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd",
+                                   calls=2)
+    assert rec["kernels"]["to_blocked_kernel<64> [fwd]"]["dispatches_per_call"] == 1
+    assert rec["kernels"]["to_blocked_kernel<64> [bwd]"]["dispatches_per_call"] == 3
+    assert rec["bytes_per_call"]["fwd"] == (2 * 10 + 10 + 2 * 100 + 100) * 1024
+    assert rec["bytes_per_call"]["bwd"] == (2 * 50 + 50 + 2 * 300 + 300) * 1024
+    assert "scan_pm.hip" in rec["source_files"]
