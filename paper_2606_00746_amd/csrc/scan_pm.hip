@@ -181,9 +181,11 @@ __global__ __launch_bounds__(256) void norm_to_blocked_kernel(const bf16_t *__re
 // The scan of direction D over one channel plane: h of every step stays in
 // hr (hr[i] = state of this lane's position after step i).  xs, ls: the
 // staged x and lambda planes; w: the direction's blocked tap planes.
-template <int S, int D>
+// WL: the taps too are staged pixel-major planes in LDS (wls, three planes
+// of PmPlane<S>::kBytes), else blocked pieces of w in global memory.
+template <int S, int D, bool WL>
 __device__ __forceinline__ void pm_fwd_dir(int j, const uint8_t *xs, const uint8_t *ls, rsrc_t w,
-                                           float (&hr)[S])
+                                           const uint8_t *wls, float (&hr)[S])
 {
     using Pl = PmPlane<S>;
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
@@ -194,9 +196,19 @@ __device__ __forceinline__ void pm_fwd_dir(int j, const uint8_t *xs, const uint8
     uint4 r0[NB], r1[NB], r2[NB];
     auto wload = [&](int fb) {
         const int sq = REV ? NB - 1 - fb : fb;
-        r0[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S);
-        r1[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, PL);
-        r2[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, 2 * PL);
+        if (WL) {
+            if (!VERT) {
+                // this lane's row, the block's 8 columns, per tap
+                const int o = jc * Pl::kPitch + 16 * sq;
+                r0[fb] = *reinterpret_cast<const uint4 *>(wls + o);
+                r1[fb] = *reinterpret_cast<const uint4 *>(wls + Pl::kBytes + o);
+                r2[fb] = *reinterpret_cast<const uint4 *>(wls + 2 * Pl::kBytes + o);
+            }
+        } else {
+            r0[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S);
+            r1[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, PL);
+            r2[fb] = ld_piece<false, VERT, false>(w, jc, sq, S, S, 2 * PL);
+        }
     };
     wload(0);
     if (NB > 1)
@@ -230,9 +242,20 @@ __device__ __forceinline__ void pm_fwd_dir(int j, const uint8_t *xs, const uint8
             if (i == 0) {
                 h = inj;
             } else {
-                float hn = fmaf(elem(r1[fb], e, s.lo1, s.hi1), h, inj);
-                hn = fmaf(elem(r0[fb], e, s.lo0, s.hi0), from_left<64>(h), hn);
-                hn = fmaf(elem(r2[fb], e, s.lo2, s.hi2), from_right<64>(h), hn);
+                float w0, w1, w2;
+                if (WL && VERT) {
+                    const int o = (8 * sq + e) * Pl::kPitch + 2 * jc;
+                    w0 = widen(lds_u16(wls, o), s.lo0);
+                    w1 = widen(lds_u16(wls + Pl::kBytes, o), s.lo1);
+                    w2 = widen(lds_u16(wls + 2 * Pl::kBytes, o), s.lo2);
+                } else {
+                    w0 = elem(r0[fb], e, s.lo0, s.hi0);
+                    w1 = elem(r1[fb], e, s.lo1, s.hi1);
+                    w2 = elem(r2[fb], e, s.lo2, s.hi2);
+                }
+                float hn = fmaf(w1, h, inj);
+                hn = fmaf(w0, from_left<64>(h), hn);
+                hn = fmaf(w2, from_right<64>(h), hn);
                 h = hn;
             }
             hr[i] = h;
@@ -241,20 +264,30 @@ __device__ __forceinline__ void pm_fwd_dir(int j, const uint8_t *xs, const uint8
     }
 }
 
-// One workgroup per (b, c), one wave per direction.  wb: the blocked weights.
+// LDS of fwd_pm_kernel: x and the 4 lambda planes, with WL also the 12 tap
+// planes; the fp32 merge plane reuses it afterwards.
 template <int S>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void fwd_pm_kernel(
-    const bf16_t *__restrict__ x, const bf16_t *__restrict__ wb, const bf16_t *__restrict__ lam,
-    const bf16_t *__restrict__ u, bf16_t *__restrict__ y, int mask, int B, int C, int G,
-    Magic divC, Magic divCpg)
+constexpr size_t fwd_pm_lds(bool wl)
+{
+    using Pl = PmPlane<S>;
+    const size_t stg = (size_t)(wl ? 17 : 5) * Pl::kBytes;
+    return stg > (size_t)Pl::kBytesF ? stg : (size_t)Pl::kBytesF;
+}
+
+// One workgroup per (b, c), one wave per direction.  w: the blocked weights,
+// or with WL (one channel per group, where a re-layout would copy as much as
+// the lambda planes) the pixel-major weights, staged in LDS with the rest.
+template <int S, bool WL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WL ? 1 : 3))) void
+fwd_pm_kernel(const bf16_t *__restrict__ x, const bf16_t *__restrict__ wb,
+              const bf16_t *__restrict__ lam, const bf16_t *__restrict__ u,
+              bf16_t *__restrict__ y, int mask, int B, int C, int G, Magic divC, Magic divCpg)
 {
     using Pl = PmPlane<S>;
     constexpr int HW = S * S;
     constexpr int NCH = HW / 8;                           // 8-pixel pieces of a plane
     constexpr int PER = (NCH + 255) / 256;                // pieces per thread
-    constexpr int STG = 5 * Pl::kBytes;                   // x + 4 lambda planes
-    constexpr int LB = STG > Pl::kBytesF ? STG : Pl::kBytesF;
-    __shared__ uint4 lds4[LB / 16];
+    extern __shared__ uint4 lds4[];
     uint8_t *base = reinterpret_cast<uint8_t *>(lds4);
     float *M = reinterpret_cast<float *>(lds4);           // merge plane, after the scans
 
@@ -274,6 +307,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
             const int sk = __popc(mask & ((1 << k) - 1));
             stage_plane<S>(base + (1 + k) * Pl::kBytes,
                            lam + (((int64_t)sk * B + b) * C + c) * HW, d, 4, lane);
+            if (WL) {
+                // the three tap planes of direction k (planes 5 + 3k ..)
+                const bf16_t *wk = wb + (((int64_t)sk * B + b) * G + g) * 3 * HW;
+#pragma unroll
+                for (int t = 0; t < 3; ++t)
+                    stage_plane<S>(base + (5 + 3 * k + t) * Pl::kBytes, wk + t * HW, d, 4, lane);
+            }
         }
     }
     // every direction's u, 8 pixels of a row per thread and piece, loaded
@@ -301,14 +341,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void f
         const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
         const rsrc_t rw = make_rsrc(wb + pw, 6 * HW);
         const uint8_t *ls = base + (1 + d) * Pl::kBytes;
+        const uint8_t *wls = base + (5 + 3 * d) * Pl::kBytes;
         if (d == 0)
-            pm_fwd_dir<S, 0>(lane, base, ls, rw, hr);
+            pm_fwd_dir<S, 0, WL>(lane, base, ls, rw, wls, hr);
         else if (d == 1)
-            pm_fwd_dir<S, 1>(lane, base, ls, rw, hr);
+            pm_fwd_dir<S, 1, WL>(lane, base, ls, rw, wls, hr);
         else if (d == 2)
-            pm_fwd_dir<S, 2>(lane, base, ls, rw, hr);
+            pm_fwd_dir<S, 2, WL>(lane, base, ls, rw, wls, hr);
         else
-            pm_fwd_dir<S, 3>(lane, base, ls, rw, hr);
+            pm_fwd_dir<S, 3, WL>(lane, base, ls, rw, wls, hr);
     }
     lds_barrier();   // the staged planes become the merge plane
 
@@ -425,9 +466,28 @@ hipError_t norm_blocked_t(const Problem &p, const void *wt, void *wb, hipStream_
     return hipGetLastError();
 }
 
+template <int S, bool WL>
+hipError_t fwd_pm_launch(const Problem &p, const void *w, hipStream_t st)
+{
+    const size_t lds = fwd_pm_lds<S>(WL);
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_pm_kernel<S, WL>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess)
+        return e;
+    hipLaunchKernelGGL((fwd_pm_kernel<S, WL>), dim3((unsigned)(p.B * p.C)), dim3(256), lds, st,
+                       (const bf16_t *)p.x, (const bf16_t *)w, (const bf16_t *)p.lam,
+                       (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
+                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
+    return hipGetLastError();
+}
+
 template <int S>
 hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
 {
+    // one channel per group: the weights are staged with the channel's
+    // other planes (no copy); else re-laid out once for the group's channels
+    if (p.C == p.G && !p.w_blocked)
+        return p.ws->counting ? hipSuccess : fwd_pm_launch<S, true>(p, p.w, st);
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * S * S;
     void *wb = const_cast<void *>(p.w);
     hipError_t e = hipSuccess;
@@ -439,11 +499,7 @@ hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
         e = w_to_blocked_t<S>(p, wb, st);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_pm_kernel<S>), dim3((unsigned)(p.B * p.C)), dim3(256), 0, st,
-                       (const bf16_t *)p.x, (const bf16_t *)wb, (const bf16_t *)p.lam,
-                       (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
-                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
-    return hipGetLastError();
+    return fwd_pm_launch<S, false>(p, wb, st);
 }
 
 }  // namespace
