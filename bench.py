@@ -144,9 +144,18 @@ def cpu_baseline(wl: gi.Workload, inputs: dict, min_seconds: float, norm: bool =
         probe = order[:threads]
         for bg in probe:
             sl(bg)
+        # (the first pass also warms the oracle and the threads: time the second)
+        phase(ex, fwd, probe)
         t1 = phase(ex, fwd, probe) + (phase(ex, bwd, probe) if wl.backward else 0.0)
         per_round = max(t1, 1e-6)
         rounds = max(1, int(min_seconds / runs / per_round))
+        units = [order[k % len(order)] for k in range(rounds * threads)]
+        for bg in units:
+            sl(bg)
+        # one untimed run at that size corrects the estimate (threads contend
+        # for memory bandwidth more over many units than over one each)
+        t_run = phase(ex, fwd, units) + (phase(ex, bwd, units) if wl.backward else 0.0)
+        rounds = max(1, int(rounds * min_seconds / runs / max(t_run, 1e-6)))
         units = [order[k % len(order)] for k in range(rounds * threads)]
         for bg in units:
             sl(bg)
