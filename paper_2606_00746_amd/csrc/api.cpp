@@ -152,7 +152,7 @@ bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_BLOCKED; }
 // Pixel-major calls on the register-streamed shapes read their weights in
 // the blocked order: the _norm passes form them there directly from the
 // logits (one read of the logits, one write of the weights), instead of
-// writing pixel-major weights that the scan then re-lays out.
+// writing pixel-major weights that the scan then re-lays out or stages.
 bool norm_fused(const Problem &p) { return p.layout == kPixelMajor && med_supported(p); }
 
 // The launches of one scan operation on the workspace ws (in counting mode:

@@ -84,6 +84,9 @@ inline bool pm_weights_reblocked(const Problem &p)
     return p.layout == kPixelMajor && p.C / p.G >= kReblockCpg;
 }
 hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t s);
+// n planes of a horizontal direction (square side S of the register-streamed
+// shapes) into the blocked order of that direction.
+hipError_t launch_planes_to_blocked(const void *src, void *dst, int n, int S, hipStream_t s);
 // lam and u of the horizontal directions into blocked copies [nh][B][C][plane].
 hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipStream_t s);
 hipError_t launch_fwd_pm(const Problem &p, hipStream_t s);

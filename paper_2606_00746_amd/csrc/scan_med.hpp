@@ -325,7 +325,7 @@ struct BwdArgs {
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
 // global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                         float (&dxr)[64], bool dx_first)
 {
@@ -336,9 +336,16 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     // lam and u: pixel-major, except horizontal ones whose copies were
     // re-laid out with the weights (WPM false)
     constexpr bool LPM = PM && (VERT || WPM);
+    // w: blocked, or pixel-major where the call's weights are (WPM); WV:
+    // with one channel per group a vertical direction reads them in place
+    // (rows, as lambda and u; a copy would be as large as lambda)
+    constexpr bool WPD = WPM || (WV && VERT);
     const Sel s = make_sel(cvalid ? j : 64, P);         // an idle wave computes zeros
     const bool act = cvalid && j < P;
     const int jj = j < P ? j : P - 1;
+    auto wpiece = [&](int sq_, uint32_t off) -> uint4 {
+        return ld_piece<WPD, VERT, false>(A.w, jj, sq_, P, W, off);
+    };
     const uint32_t vr = 2u * (uint32_t)jj;              // this lane's bf16 of a pixel row
     auto sblk = [](int fb) { return REV ? NB - 1 - fb : fb; };   // storage block of frame block fb
     auto line_of = [](int i) { return REV ? L - 1 - i : i; };   // storage line of step i
@@ -353,9 +360,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
         rl[fb] = ld_piece<LPM, VERT, true>(A.lam, jj, sq_, P, W);     \
-        p0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
-        p1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        p2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        p0[fb] = wpiece(sq_, 0u);                                     \
+        p1[fb] = wpiece(sq_, PL2);                                    \
+        p2[fb] = wpiece(sq_, 2 * PL2);                                \
     } while (0)
 
     // --- reverse sweep: adjoint a_i -------------------------------------
@@ -368,9 +375,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     do {                                                             \
         const int sq_ = sblk(fb);                                    \
         ru[fb] = ld_piece<LPM, VERT, true>(A.u, jj, sq_, P, W);       \
-        q0[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W);      \
-        q1[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, PL2); \
-        q2[fb] = ld_piece<WPM, VERT, false>(A.w, jj, sq_, P, W, 2 * PL2); \
+        q0[fb] = wpiece(sq_, 0u);                                     \
+        q1[fb] = wpiece(sq_, PL2);                                    \
+        q2[fb] = wpiece(sq_, 2 * PL2);                                \
     } while (0)
         RLOAD(NB - 1);
         if (NB > 1)
@@ -900,13 +907,16 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
 // PC: one channel per weight group; a workgroup then takes cw consecutive
 // channels (groups), each wave sums nothing with the others, and nchunk /
 // divChunk count the workgroups per batch.
-template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM>
+// WV: one channel per group, pixel-major, vertical weights read in place and
+// horizontal ones from the blocked copies wh.
+template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 __global__ __launch_bounds__(512) void bwd_med_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, const bf16_t *__restrict__ dy, bf16_t *__restrict__ dx,
     bf16_t *__restrict__ dw, bf16_t *__restrict__ dlam, bf16_t *__restrict__ du,
     float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk, Magic divChunk,
-    Magic divG, const bf16_t *__restrict__ lamh, const bf16_t *__restrict__ uh)
+    Magic divG, const bf16_t *__restrict__ lamh, const bf16_t *__restrict__ uh,
+    const bf16_t *__restrict__ wh)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
@@ -1028,7 +1038,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         }
         A.dlam = make_sdesc(dlam + pd, 2 * HW);
         A.du = make_sdesc(du + pd, 2 * HW);
-        A.w = make_rsrc(w + unit * 3 * HW, 6 * HW);
+        if (WV && d >= 2) {
+            // one channel per group: blocked copies of the horizontal slots
+            const int64_t uh_ = ((int64_t)(s - __popc(mask & 3)) * B + b) * G + g;
+            A.w = make_rsrc(wh + uh_ * 3 * HW, 6 * HW);
+        } else {
+            A.w = make_rsrc(w + unit * 3 * HW, 6 * HW);
+        }
         if (A.partial)
             A.dw = make_sdesc(dwp + ((int64_t)chunk * D * B * G + unit) * 3 * HW, 12 * HW);
         else
@@ -1040,7 +1056,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, true);
         lds_barrier();   // slot buffers are reused by the next direction
         if (PM) {
             flush_out();
@@ -1053,7 +1069,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         if ((mask & 4) && H >= 64)
             dir_bwd_ck<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
         if (PM)
             flush_out();
@@ -1068,13 +1084,13 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false);
         lds_barrier();
     }
 
@@ -1205,21 +1221,22 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
-template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM>
+template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
-                          float *dwp, const void *lamh, const void *uh)
+                          float *dwp, const void *lamh, const void *uh, const void *wh = nullptr)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM>,
+    hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM, WV>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
     const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
-    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM>), dim3(grid),
+    hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM, WV>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
                        p.mask, p.B, p.C, p.G, cw, nchunk, make_magic((uint32_t)nchunk),
-                       make_magic((uint32_t)p.G), (const bf16_t *)lamh, (const bf16_t *)uh);
+                       make_magic((uint32_t)p.G), (const bf16_t *)lamh, (const bf16_t *)uh,
+                       (const bf16_t *)wh);
     return hipGetLastError();
 }
 
@@ -1239,7 +1256,7 @@ int bwd_ns4_regs()
 // launch_w_to_blocked); the other per-direction tensors follow PM.
 template <int H, int W, bool PM, bool WPM>
 hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullptr,
-                     const void *uh = nullptr)
+                     const void *uh = nullptr, const void *wh = nullptr)
 {
     const int lds_max = kLdsBytes;
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
@@ -1252,6 +1269,9 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullpt
             return hipErrorInvalidConfiguration;
         if (p.ws->counting)
             return hipSuccess;
+        if (PM && !WPM && wh != nullptr)
+            return bwd_med_launch<H, W, false, true, kSlots, PM, WPM, true>(
+                p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh, wh);
         return bwd_med_launch<H, W, false, true, kSlots, PM, WPM>(
             p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh);
     }
@@ -1357,11 +1377,15 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     // re-laid out once into the blocked order of their direction
     // (workspace), read there as 16-byte pieces: a horizontal scan would read
     // each pixel-major piece from 64 rows
-    const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * H * W;
-    const int64_t nh = (int64_t)__builtin_popcount(p.mask & 12) * p.B * p.C * H * W;
+    // One channel per group (weights as large as lambda): only the
+    // horizontal directions' weights are copied, vertical ones read in place.
+    const bool pc = p.C == p.G && !p.w_blocked;   // (formed weights are all blocked)
+    const int nvd = __builtin_popcount(p.mask & 3), nhd = __builtin_popcount(p.mask & 12);
+    const int64_t nw = (int64_t)(pc ? nhd : nvd + nhd) * p.B * p.G * 3 * H * W;
+    const int64_t nh = (int64_t)nhd * p.B * p.C * H * W;
     void *wb = const_cast<void *>(p.w), *lamh = nullptr, *uh = nullptr;
     hipError_t e = hipSuccess;
-    if (!p.w_blocked)
+    if (!p.w_blocked && nw > 0)
         e = p.ws->take(&wb, (size_t)nw * 2);
     if (e == hipSuccess && nh > 0)
         e = p.ws->take(&lamh, (size_t)nh * 2);
@@ -1370,13 +1394,20 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     if (e != hipSuccess)
         return e;
     if (!p.ws->counting) {
-        if (!p.w_blocked)
+        if (pc)
+            e = nw > 0 ? launch_planes_to_blocked(
+                             static_cast<const bf16_t *>(p.w) + (int64_t)nvd * p.B * p.G * 3 * H * W,
+                             wb, (int)(nw / ((int64_t)H * W)), H, st)
+                       : hipSuccess;
+        else if (!p.w_blocked)
             e = launch_w_to_blocked(p, wb, st);
         if (e == hipSuccess && nh > 0)
             e = launch_horiz_to_blocked(p, lamh, uh, st);
         if (e != hipSuccess)
             return e;
     }
+    if (pc)
+        return bwd_med_t<H, W, true, false>(p, st, lamh, uh, wb);
     Problem q = p;
     q.w = wb;
     return bwd_med_t<H, W, true, false>(q, st, lamh, uh);

@@ -516,6 +516,39 @@ hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t st)
     }
 }
 
+hipError_t launch_planes_to_blocked(const void *src, void *dst, int n, int S, hipStream_t st)
+{
+    if (n == 0)
+        return hipSuccess;
+    switch (S) {
+    case 64:
+        hipLaunchKernelGGL((to_blocked_kernel<64>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    case 56:
+        hipLaunchKernelGGL((to_blocked_kernel<56>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    case 48:
+        hipLaunchKernelGGL((to_blocked_kernel<48>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    case 40:
+        hipLaunchKernelGGL((to_blocked_kernel<40>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    case 32:
+        hipLaunchKernelGGL((to_blocked_kernel<32>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    default:
+        hipLaunchKernelGGL((to_blocked_kernel<24>), dim3((unsigned)n), dim3(256), 0, st,
+                           (const bf16_t *)src, (uint4 *)dst, 0, n);
+        break;
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_horiz_to_blocked(const Problem &p, void *lamh, void *uh, hipStream_t st)
 {
     switch (p.H) {

@@ -26,6 +26,10 @@ def case(name, B, C, G, H, W, dirs=15, dtype="bf16", backward=True, sigma=1.0, s
 CASES = [
     case("med64", 1, 64, 2, 64, 64),
     case("med56-dirs6", 2, 24, 2, 56, 56, dirs=6),
+    # one channel per group: weights formed in the blocked order for both
+    # passes (the plain calls read vertical ones in place instead)
+    case("med64-G=C", 1, 16, 16, 64, 64),
+    case("med56-G=C-dirs6", 2, 12, 12, 56, 56, dirs=6, sigma=2.0),
     case("tiny14", 2, 24, 2, 14, 14),
     case("tiny16-R2L", 1, 8, 1, 16, 16, dirs=8, sigma=2.0),
     case("small-f32-40x24", 2, 6, 3, 40, 24, dtype="f32"),
