@@ -84,6 +84,11 @@ inline bool pm_weights_reblocked(const Problem &p)
     return p.layout == kPixelMajor && p.C / p.G >= kReblockCpg;
 }
 hipError_t launch_w_to_blocked(const Problem &p, void *wb, hipStream_t s);
+// nv vertical planes, then nh horizontal ones, of H x W (multiples of 8,
+// W <= 256, or any H with W = 8 * (H's pieces) as a 16-byte piece transpose)
+// pixel-major -> blocked line-major (scan_wide.hip, pieces_kernel).
+hipError_t launch_planes_pieces(const void *src, void *dst, int64_t nv, int64_t nh, int H, int W,
+                                hipStream_t s);
 // n planes of a horizontal direction (square side S of the register-streamed
 // shapes) into the blocked order of that direction.
 hipError_t launch_planes_to_blocked(const void *src, void *dst, int n, int S, hipStream_t s);

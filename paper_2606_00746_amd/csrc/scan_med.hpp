@@ -605,7 +605,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
-                        st_piece<PM, VERT, true>(A.dw, jj, sblk(fb), P, W,
+                        st_piece<PM && (VERT || !WV), VERT, true>(A.dw, jj, sblk(fb), P, W,
                                                  make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]),
                                                  k * PL2);
                 }
@@ -727,7 +727,7 @@ __device__ __forceinline__ void slot_finish(const BwdArgs &A, int j, const float
 // reverse.  The live scan state is 2 x 8 floats instead of L; the price is a
 // second read of lam and w (the first one leaves them in L2) and one more h
 // recurrence per step.
-template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM>
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
                                            float (&dxa)[64])
 {
@@ -891,7 +891,7 @@ __device__ __forceinline__ void dir_bwd_ck(const BwdArgs &A, int j, bool cvalid,
                 if constexpr (PC) {
 #pragma unroll
                     for (int k = 0; k < 3; ++k)
-                        st_piece<PM, VERT, true>(A.dw, jj, F::sblk(fb), P, W,
+                        st_piece<PM && (VERT || !WV), VERT, true>(A.dw, jj, F::sblk(fb), P, W,
                                                  make_uint4(dwp[k][0], dwp[k][1], dwp[k][2], dwp[k][3]),
                                                  k * F::PL2);
                 }
@@ -916,7 +916,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     bf16_t *__restrict__ dw, bf16_t *__restrict__ dlam, bf16_t *__restrict__ du,
     float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk, Magic divChunk,
     Magic divG, const bf16_t *__restrict__ lamh, const bf16_t *__restrict__ uh,
-    const bf16_t *__restrict__ wh)
+    const bf16_t *__restrict__ wh, bf16_t *__restrict__ dwh)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
@@ -1047,6 +1047,11 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         }
         if (A.partial)
             A.dw = make_sdesc(dwp + ((int64_t)chunk * D * B * G + unit) * 3 * HW, 12 * HW);
+        else if (WV && d >= 2)
+            // horizontal weight gradients in the blocked order (whole 16-byte
+            // lines), turned pixel-major by a transpose launch afterwards
+            A.dw = make_sdesc(dwh + (((int64_t)(s - __popc(mask & 3)) * B + b) * G + g) * 3 * HW,
+                              6 * HW);
         else
             A.dw = make_sdesc(dw + unit * 3 * HW, 6 * HW);
     };
@@ -1067,7 +1072,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 8) {
         setup(3);
         if ((mask & 4) && H >= 64)
-            dir_bwd_ck<H, W, 3, IMM, PC, NS, PM, WPM>(A, lane, cvalid, stg, dxr);
+            dir_bwd_ck<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr);
         else
             dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
         lds_barrier();
@@ -1223,7 +1228,8 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
 
 template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
-                          float *dwp, const void *lamh, const void *uh, const void *wh = nullptr)
+                          float *dwp, const void *lamh, const void *uh, const void *wh = nullptr,
+                          void *dwh = nullptr)
 {
     hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM, WV>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -1236,7 +1242,7 @@ hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, 
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
                        p.mask, p.B, p.C, p.G, cw, nchunk, make_magic((uint32_t)nchunk),
                        make_magic((uint32_t)p.G), (const bf16_t *)lamh, (const bf16_t *)uh,
-                       (const bf16_t *)wh);
+                       (const bf16_t *)wh, (bf16_t *)dwh);
     return hipGetLastError();
 }
 
@@ -1256,7 +1262,7 @@ int bwd_ns4_regs()
 // launch_w_to_blocked); the other per-direction tensors follow PM.
 template <int H, int W, bool PM, bool WPM>
 hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullptr,
-                     const void *uh = nullptr, const void *wh = nullptr)
+                     const void *uh = nullptr, const void *wh = nullptr, void *dwh = nullptr)
 {
     const int lds_max = kLdsBytes;
     const size_t per_ch = (size_t)H * kPlanePitch * 4;              // wave plane
@@ -1269,9 +1275,19 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullpt
             return hipErrorInvalidConfiguration;
         if (p.ws->counting)
             return hipSuccess;
-        if (PM && !WPM && wh != nullptr)
-            return bwd_med_launch<H, W, false, true, kSlots, PM, WPM, true>(
-                p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh, wh);
+        if (PM && !WPM && wh != nullptr) {
+            hipError_t e = bwd_med_launch<H, W, false, true, kSlots, PM, WPM, true>(
+                p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh, wh, dwh);
+            const int nvd = __builtin_popcount(p.mask & 3), nhd = __builtin_popcount(p.mask & 12);
+            // the horizontal dw planes, blocked [q][p] pieces -> pixel-major
+            // [p][q]: the piece transpose of a plane of H/8 rows of 8 W
+            // columns
+            if (e == hipSuccess && nhd > 0)
+                e = launch_planes_pieces(dwh,
+                                  static_cast<bf16_t *>(p.dw) + (int64_t)nvd * p.B * p.G * 3 * H * W,
+                                  0, (int64_t)nhd * p.B * p.G * 3, H / 8, 8 * W, st);
+            return e;
+        }
         return bwd_med_launch<H, W, false, true, kSlots, PM, WPM>(
             p, st, cw, nct, (size_t)cw * per_ch, nullptr, lamh, uh);
     }
@@ -1391,6 +1407,9 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
         e = p.ws->take(&lamh, (size_t)nh * 2);
     if (e == hipSuccess && nh > 0)
         e = p.ws->take(&uh, (size_t)nh * 2);
+    void *dwh = nullptr;
+    if (e == hipSuccess && pc && nw > 0)
+        e = p.ws->take(&dwh, (size_t)nw * 2);
     if (e != hipSuccess)
         return e;
     if (!p.ws->counting) {
@@ -1407,7 +1426,7 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
             return e;
     }
     if (pc)
-        return bwd_med_t<H, W, true, false>(p, st, lamh, uh, wb);
+        return bwd_med_t<H, W, true, false>(p, st, lamh, uh, wb, dwh);
     Problem q = p;
     q.w = wb;
     return bwd_med_t<H, W, true, false>(q, st, lamh, uh);

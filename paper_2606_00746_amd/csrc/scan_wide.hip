@@ -667,6 +667,12 @@ hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states
 
 }  // namespace
 
+hipError_t launch_planes_pieces(const void *src, void *dst, int64_t nv, int64_t nh, int H, int W,
+                                hipStream_t st)
+{
+    return launch_pieces(src, dst, nv, nh, H, W, st);
+}
+
 bool wide_supported(const Problem &p)
 {
     if (p.dtype != 1 || p.H % 8 != 0 || p.W % 8 != 0)
