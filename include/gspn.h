@@ -105,7 +105,7 @@ extern "C" {
 #define GSPN_ERR_ALIAS (-6)       /* two buffers of the call overlap            */
 #define GSPN_ERR_UNSUPPORTED (-7) /* H or W > GSPN_MAX_SIDE, or too many elements */
 #define GSPN_ERR_HIP (-8)         /* a HIP runtime call or launch failed        */
-#define GSPN_ERR_WORKSPACE (-9)   /* workspace missing or smaller than needed   */
+#define GSPN_ERR_WORKSPACE (-9)   /* workspace (or reserve) missing or too small */
 
 /* Operations, for gspn_workspace_size. */
 #define GSPN_OP_FWD 0
@@ -114,6 +114,8 @@ extern "C" {
 #define GSPN_OP_BWD_NORM 3
 #define GSPN_OP_FWD_BLOCKED 4
 #define GSPN_OP_BWD_BLOCKED 5
+#define GSPN_OP_FWD_TRAIN 6
+#define GSPN_OP_BWD_RESERVE 7
 
 /* Largest supported H and W, and largest B*C*H*W and B*G*H*W*3*D. */
 #define GSPN_MAX_SIDE 4096
@@ -207,6 +209,44 @@ int gspn_scan_bwd_norm(const void *x, const void *w_logits, const void *lam,
                        void *dlam, void *du, int direction, int B, int C, int G,
                        int H, int W, int dtype, void *workspace,
                        int64_t workspace_bytes, void *stream);
+
+/*
+ * Training pair: the forward and backward passes of gspn_scan_fwd and
+ * gspn_scan_bwd (same operation, results bit for bit), where the forward
+ * also leaves in a caller buffer, the reserve, what the backward of the same
+ * inputs would otherwise have to make again from them -- the analogue of the
+ * tensors an autograd forward saves for its backward.  On the bf16 square
+ * planes of side 24 to 64 (multiples of 8) the backward reads the weights
+ * and the horizontal directions' lambda and u as 16-byte pieces of 8 steps
+ * of one line position; gspn_scan_bwd re-lays them out into that order
+ * first, while gspn_scan_fwd_train writes those copies as it reads its
+ * inputs and gspn_scan_bwd_reserve reads them from the reserve.
+ *   gspn_reserve_size     bytes of the reserve for these sizes (0 where
+ *                         the backward re-lays nothing out; the pair then
+ *                         runs as the plain pair and reserve may be NULL)
+ *   reserve               device buffer of at least that size, 16-byte
+ *                         aligned, overlapping no other buffer of the call;
+ *                         written by gspn_scan_fwd_train, read (not written)
+ *                         by gspn_scan_bwd_reserve
+ * The backward must get the x, w, lam and u that the forward which wrote the
+ * reserve read, unchanged, and the reserve unchanged since; a mismatch is not
+ * detected (the gradients are then those of the inputs the reserve came
+ * from, mixed with the new ones).  GSPN_ERR_WORKSPACE when reserve is NULL or
+ * reserve_bytes below the size.  Workspace: gspn_workspace_size with
+ * GSPN_OP_FWD_TRAIN / GSPN_OP_BWD_RESERVE.  Other arguments, checks and
+ * errors as in gspn_scan_fwd / gspn_scan_bwd.
+ */
+int gspn_reserve_size(int direction, int B, int C, int G, int H, int W, int dtype,
+                      int64_t *bytes);
+int gspn_scan_fwd_train(const void *x, const void *w, const void *lam, const void *u,
+                        void *y, int direction, int B, int C, int G, int H, int W,
+                        int dtype, void *reserve, int64_t reserve_bytes,
+                        void *workspace, int64_t workspace_bytes, void *stream);
+int gspn_scan_bwd_reserve(const void *x, const void *w, const void *lam, const void *u,
+                          const void *dy, void *dx, void *dw, void *dlam, void *du,
+                          int direction, int B, int C, int G, int H, int W, int dtype,
+                          const void *reserve, int64_t reserve_bytes, void *workspace,
+                          int64_t workspace_bytes, void *stream);
 
 /*
  * gspn_scan_bwd for callers that cannot allocate device memory or hand in a

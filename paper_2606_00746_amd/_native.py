@@ -20,7 +20,8 @@ T2B, B2T, L2R, R2L, ALL = 1, 2, 4, 8, 15
 F32, BF16 = 0, 1
 (OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUPPORTED, ERR_HIP,
  ERR_WORKSPACE) = (0, -1, -2, -3, -4, -5, -6, -7, -8, -9)
-OP_FWD, OP_BWD, OP_FWD_NORM, OP_BWD_NORM, OP_FWD_BLOCKED, OP_BWD_BLOCKED = range(6)
+(OP_FWD, OP_BWD, OP_FWD_NORM, OP_BWD_NORM, OP_FWD_BLOCKED, OP_BWD_BLOCKED, OP_FWD_TRAIN,
+ OP_BWD_RESERVE) = range(8)
 MAX_SIDE = 4096
 
 # layouts of the per-direction tensors
@@ -29,6 +30,7 @@ PIXEL, BLOCKED = "pixel", "blocked"
 EXPORTED = ("gspn_workspace_size", "gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_fwd_blocked",
             "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
             "gspn_scan_bwd_static", "gspn_workspace_size_slots", "gspn_scan_bwd_slots",
+            "gspn_reserve_size", "gspn_scan_fwd_train", "gspn_scan_bwd_reserve",
             "gspn_project",
             "gspn_latent_params", "gspn_latent_workspace_size", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
@@ -67,6 +69,9 @@ def load() -> ctypes.CDLL:
         lib.gspn_scan_bwd_static.argtypes = [vp] * 9 + scan8 + [vp]
         lib.gspn_workspace_size_slots.argtypes = [i] + scan8 + [pi64]
         lib.gspn_scan_bwd_slots.argtypes = [i] + [vp] * 9 + scan8 + ws
+        lib.gspn_reserve_size.argtypes = scan8 + [pi64]
+        lib.gspn_scan_fwd_train.argtypes = [vp] * 5 + scan8 + [vp, i64] + ws
+        lib.gspn_scan_bwd_reserve.argtypes = [vp] * 9 + scan8 + [vp, i64] + ws
         lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
         lib.gspn_latent_params.argtypes = [vp] * 7 + [i] * 6 + [vp]
         lib.gspn_latent_workspace_size.argtypes = [i] * 7 + [pi64]
@@ -131,6 +136,25 @@ def gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G,
                          stream) -> int:
     return load().gspn_scan_bwd_static(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H,
                                        W, dtype, stream)
+
+
+def gspn_reserve_size(direction, B, C, G, H, W, dtype):
+    """(status, bytes) of gspn_reserve_size."""
+    n = ctypes.c_int64(0)
+    st = load().gspn_reserve_size(direction, B, C, G, H, W, dtype, ctypes.byref(n))
+    return st, n.value
+
+
+def gspn_scan_fwd_train(x, w, lam, u, y, direction, B, C, G, H, W, dtype, rs, rs_bytes, ws,
+                        ws_bytes, stream) -> int:
+    return load().gspn_scan_fwd_train(x, w, lam, u, y, direction, B, C, G, H, W, dtype, rs,
+                                      rs_bytes, ws, ws_bytes, stream)
+
+
+def gspn_scan_bwd_reserve(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
+                          rs, rs_bytes, ws, ws_bytes, stream) -> int:
+    return load().gspn_scan_bwd_reserve(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G,
+                                        H, W, dtype, rs, rs_bytes, ws, ws_bytes, stream)
 
 
 def gspn_workspace_size_slots(slots, direction, B, C, G, H, W, dtype):
@@ -266,7 +290,8 @@ def _workspace(op, direction, B, C, G, H, W, dtype, device, given=None, slots=0)
     return torch.empty(n, dtype=torch.uint8, device=device), n
 
 
-def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=None, slots=0):
+def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=None, slots=0,
+          reserve=None):
     B, C, G, H, W = _sizes(x, w, direction)
     D = _ndirs(direction)
     n, nd, nw = B * C * H * W, D * B * C * H * W, D * B * G * 3 * H * W
@@ -287,9 +312,14 @@ def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=Non
         ptrs.append(outs[0].data_ptr())
     fn = {OP_FWD: gspn_scan_fwd, OP_BWD: gspn_scan_bwd, OP_FWD_BLOCKED: gspn_scan_fwd_blocked,
           OP_BWD_BLOCKED: gspn_scan_bwd_blocked, OP_FWD_NORM: gspn_scan_fwd_norm,
-          OP_BWD_NORM: gspn_scan_bwd_norm}[op]
+          OP_BWD_NORM: gspn_scan_bwd_norm, OP_FWD_TRAIN: gspn_scan_fwd_train,
+          OP_BWD_RESERVE: gspn_scan_bwd_reserve}[op]
     if slots:
         fn = lambda *a: gspn_scan_bwd_slots(slots, *a)          # noqa: E731
+    if op in (OP_FWD_TRAIN, OP_BWD_RESERVE):
+        rp, rn = (reserve.data_ptr(), reserve.numel()) if reserve is not None else (None, 0)
+        fn0 = fn
+        fn = lambda *a: fn0(*a[:-3], rp, rn, *a[-3:])            # noqa: E731
     status = fn(*ptrs, direction, B, C, G, H, W, dt, ws.data_ptr() if ws is not None else None,
                 nbytes, _stream_handle(x, stream))
     _check_raise(status)
@@ -333,6 +363,48 @@ def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None, layo
                torch.empty_like(u))
     _scan(OP_BWD if layout == PIXEL else OP_BWD_BLOCKED, x, w, lam, u, direction, out, dy=dy,
           stream=stream, workspace=workspace, slots=slots)
+    return out
+
+
+def reserve_size(x, w, direction) -> int:
+    """Bytes of the reserve of the training pair for these tensors."""
+    B, C, G, H, W = _sizes(x, w, direction)
+    st, n = gspn_reserve_size(direction, B, C, G, H, W, _dtype_code(x))
+    _check_raise(st)
+    return n
+
+
+def scan_fwd_train(x, w, lam, u, direction: int = ALL, y=None, reserve=None, stream=None,
+                   workspace=None):
+    """scan_fwd (pixel-major) that also fills the reserve its backward,
+    scan_bwd_reserve, reads.  Returns (y, reserve); `reserve`: a uint8 device
+    tensor of at least reserve_size bytes, or None for a new one (None is
+    returned where the shape needs no reserve)."""
+    import torch
+    if y is None:
+        y = torch.empty_like(x)
+    n = reserve_size(x, w, direction)
+    if n == 0:
+        reserve = None
+    elif reserve is None or reserve.numel() < n:
+        reserve = torch.empty(n, dtype=torch.uint8, device=x.device)
+    elif reserve.device != x.device or reserve.dtype != torch.uint8 or not reserve.is_contiguous():
+        raise ValueError("reserve must be a contiguous uint8 tensor on the inputs' device")
+    _scan(OP_FWD_TRAIN, x, w, lam, u, direction, (y,), stream=stream, workspace=workspace,
+          reserve=reserve)
+    return y, reserve
+
+
+def scan_bwd_reserve(x, w, lam, u, dy, reserve, direction: int = ALL, out=None, stream=None,
+                     workspace=None):
+    """scan_bwd (pixel-major) reading the reserve that scan_fwd_train wrote
+    for the same x, w, lam, u."""
+    import torch
+    if out is None:
+        out = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
+               torch.empty_like(u))
+    _scan(OP_BWD_RESERVE, x, w, lam, u, direction, out, dy=dy, stream=stream,
+          workspace=workspace, reserve=reserve)
     return out
 
 

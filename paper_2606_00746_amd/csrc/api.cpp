@@ -128,7 +128,8 @@ int scan_buffers(int op, const void *x, const void *w, const void *lam, const vo
     const int64_t D = __builtin_popcount(direction);
     const int64_t n = (int64_t)B * C * H * W;
     const int64_t nw = D * B * G * 3 * H * W;
-    const bool bwd = op == GSPN_OP_BWD || op == GSPN_OP_BWD_NORM || op == GSPN_OP_BWD_BLOCKED;
+    const bool bwd = op == GSPN_OP_BWD || op == GSPN_OP_BWD_NORM || op == GSPN_OP_BWD_BLOCKED ||
+                     op == GSPN_OP_BWD_RESERVE;
     int k = 0;
     bufs[k++] = {x, n * es, false};
     bufs[k++] = {w, nw * es, false};
@@ -147,7 +148,10 @@ int scan_buffers(int op, const void *x, const void *w, const void *lam, const vo
     return GSPN_OK;
 }
 
-bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_BLOCKED; }
+bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_RESERVE; }
+
+// The operations of a training pair, which keep blocked copies in a reserve.
+bool reserve_op(int op) { return op == GSPN_OP_FWD_TRAIN || op == GSPN_OP_BWD_RESERVE; }
 
 // Pixel-major calls on the register-streamed shapes read their weights in
 // the blocked order: the _norm passes form them there directly from the
@@ -169,6 +173,12 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
         return dispatch_fwd(p, s);
     case GSPN_OP_BWD:
     case GSPN_OP_BWD_BLOCKED:
+        return dispatch_bwd(p, s);
+    case GSPN_OP_FWD_TRAIN:
+        p.rs_write = true;
+        return dispatch_fwd(p, s);
+    case GSPN_OP_BWD_RESERVE:
+        p.rs_read = true;
         return dispatch_bwd(p, s);
     case GSPN_OP_FWD_NORM: {
         // weights from their logits into the workspace, then the scan
@@ -212,32 +222,36 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
     }
 }
 
-// Counts the workspace of a checked problem.  GSPN_ERR_HIP if a device query
-// of the plan failed.
-int count_workspace(int op, const Problem &p0, int64_t *bytes)
+// Counts the workspace (and for a training pair the reserve) of a checked
+// problem.  GSPN_ERR_HIP if a device query of the plan failed.
+int count_workspace(int op, const Problem &p0, int64_t *bytes, int64_t *reserve_bytes = nullptr)
 {
-    Workspace ws;
+    Workspace ws, rs;
     ws.counting = true;
+    rs.counting = true;
     Problem p = p0;
     p.ws = &ws;
+    p.rs = reserve_op(op) ? &rs : nullptr;
     const hipError_t e = run_scan(op, p, p0.w, p0.dw, nullptr);
     if (e != hipSuccess)
         return hip_status(e);
     *bytes = (int64_t)ws.used;
+    if (reserve_bytes != nullptr)
+        *reserve_bytes = (int64_t)rs.used;
     return GSPN_OK;
 }
 
 int scan_call(int op, const void *x, const void *w, const void *lam, const void *u, const void *dy,
               void *y, void *dx, void *dw, void *dlam, void *du, int direction, int B, int C,
               int G, int H, int W, int dtype, void *workspace, int64_t workspace_bytes,
-              void *stream, int slots = 0)
+              void *stream, int slots = 0, void *reserve = nullptr, int64_t reserve_bytes = 0)
 {
     if (!valid_op(op))
         return GSPN_ERR_UNSUPPORTED;
     int st = check_common(direction, B, C, G, H, W, dtype);
     if (st != GSPN_OK)
         return st;
-    Buf bufs[11];
+    Buf bufs[12];
     int nb = 0;
     scan_buffers(op, x, w, lam, u, dy, y, dx, dw, dlam, du, direction, B, C, G, H, W, dtype, bufs,
                  &nb);
@@ -247,24 +261,35 @@ int scan_call(int op, const void *x, const void *w, const void *lam, const void 
     const bool blocked = op == GSPN_OP_FWD_BLOCKED || op == GSPN_OP_BWD_BLOCKED;
     Problem p{x, w, lam, u, dy, y, dx, dw, dlam, du, direction, B, C, G, H, W, dtype,
               blocked ? kBlocked : kPixelMajor, nullptr, slots};
-    int64_t need = 0;
-    st = count_workspace(op, p, &need);
+    int64_t need = 0, rneed = 0;
+    st = count_workspace(op, p, &need, &rneed);
     if (st != GSPN_OK)
         return st;
-    if (workspace_bytes < 0)
+    if (workspace_bytes < 0 || reserve_bytes < 0)
         return GSPN_ERR_WORKSPACE;
+    if (rneed > 0) {
+        // written by the forward of a training pair, read by its backward
+        if (reserve == nullptr || reserve_bytes < rneed)
+            return GSPN_ERR_WORKSPACE;
+        bufs[nb++] = {reserve, rneed, op == GSPN_OP_FWD_TRAIN};
+    }
     if (need > 0) {
         if (workspace == nullptr || workspace_bytes < need)
             return GSPN_ERR_WORKSPACE;
         bufs[nb++] = {workspace, need, true};
+    }
+    if (need > 0 || rneed > 0) {
         st = check_buffers(bufs, nb);
         if (st != GSPN_OK)
             return st;
     }
-    Workspace ws;
+    Workspace ws, rs;
     ws.base = static_cast<char *>(workspace);
     ws.size = need > 0 ? (size_t)workspace_bytes : 0;
+    rs.base = static_cast<char *>(reserve);
+    rs.size = rneed > 0 ? (size_t)reserve_bytes : 0;
     p.ws = &ws;
+    p.rs = reserve_op(op) ? &rs : nullptr;
     const hipError_t e = run_scan(op, p, w, dw, static_cast<hipStream_t>(stream));
     return e == hipErrorOutOfMemory ? GSPN_ERR_WORKSPACE : hip_status(e);
 }
@@ -341,6 +366,43 @@ extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, cons
 {
     return scan_call(GSPN_OP_BWD, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction, B, C,
                      G, H, W, dtype, workspace, workspace_bytes, stream);
+}
+
+extern "C" int gspn_reserve_size(int direction, int B, int C, int G, int H, int W, int dtype,
+                                 int64_t *bytes)
+{
+    if (bytes == nullptr)
+        return GSPN_ERR_NULL;
+    *bytes = 0;
+    const int st = check_common(direction, B, C, G, H, W, dtype);
+    if (st != GSPN_OK)
+        return st;
+    Problem p{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+              nullptr, direction, B, C, G, H, W, dtype, kPixelMajor, nullptr};
+    int64_t ws = 0;
+    return count_workspace(GSPN_OP_FWD_TRAIN, p, &ws, bytes);
+}
+
+extern "C" int gspn_scan_fwd_train(const void *x, const void *w, const void *lam, const void *u,
+                                   void *y, int direction, int B, int C, int G, int H, int W,
+                                   int dtype, void *reserve, int64_t reserve_bytes,
+                                   void *workspace, int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_FWD_TRAIN, x, w, lam, u, nullptr, y, nullptr, nullptr, nullptr,
+                     nullptr, direction, B, C, G, H, W, dtype, workspace, workspace_bytes, stream,
+                     0, reserve, reserve_bytes);
+}
+
+extern "C" int gspn_scan_bwd_reserve(const void *x, const void *w, const void *lam,
+                                     const void *u, const void *dy, void *dx, void *dw,
+                                     void *dlam, void *du, int direction, int B, int C, int G,
+                                     int H, int W, int dtype, const void *reserve,
+                                     int64_t reserve_bytes, void *workspace,
+                                     int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_BWD_RESERVE, x, w, lam, u, dy, nullptr, dx, dw, dlam, du, direction,
+                     B, C, G, H, W, dtype, workspace, workspace_bytes, stream, 0,
+                     const_cast<void *>(reserve), reserve_bytes);
 }
 
 extern "C" int gspn_scan_fwd_blocked(const void *x, const void *w, const void *lam, const void *u,

@@ -47,7 +47,38 @@ struct Problem {
     // w is already in the blocked order of its direction although the call
     // is pixel-major (weights the library formed itself, launch_norm_blocked)
     bool w_blocked = false;
+    // Reserve of a training pair (pixel-major register-streamed shapes): the
+    // forward writes into it the blocked copies that the backward of the same
+    // inputs would otherwise make (rs_write), the backward reads them from
+    // it (rs_read).  Both take the copies from it in the order of
+    // take_reserve, so that their offsets agree; counting mode sizes it.
+    Workspace *rs = nullptr;
+    bool rs_write = false, rs_read = false;
 };
+
+// The blocked copies a training pair keeps in its reserve: the weights (all
+// directions, or with one channel per group only the horizontal directions'
+// ones), and lambda and u of the horizontal directions.  Null where a piece
+// has no element.
+struct ReserveParts {
+    void *w = nullptr, *lamh = nullptr, *uh = nullptr;
+};
+inline hipError_t take_reserve(const Problem &p, ReserveParts *r)
+{
+    const int64_t HW = (int64_t)p.H * p.W;
+    const int nvd = __builtin_popcount(p.mask & 3), nhd = __builtin_popcount(p.mask & 12);
+    const bool pc = p.C == p.G;
+    const int64_t nw = (int64_t)(pc ? nhd : nvd + nhd) * p.B * p.G * 3 * HW;
+    const int64_t nh = (int64_t)nhd * p.B * p.C * HW;
+    hipError_t e = hipSuccess;
+    if (nw > 0)
+        e = p.rs->take(&r->w, (size_t)nw * 2);
+    if (e == hipSuccess && nh > 0)
+        e = p.rs->take(&r->lamh, (size_t)nh * 2);
+    if (e == hipSuccess && nh > 0)
+        e = p.rs->take(&r->uh, (size_t)nh * 2);
+    return e;
+}
 
 // Planes whose sides are both <= kSmallSide run on the register-resident path.
 constexpr int kSmallSide = 64;

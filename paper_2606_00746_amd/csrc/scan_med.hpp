@@ -1395,24 +1395,35 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     // each pixel-major piece from 64 rows
     // One channel per group (weights as large as lambda): only the
     // horizontal directions' weights are copied, vertical ones read in place.
+    // The backward of a training pair finds these copies in the reserve its
+    // forward wrote (take_reserve: the same pieces in the same order).
     const bool pc = p.C == p.G && !p.w_blocked;   // (formed weights are all blocked)
     const int nvd = __builtin_popcount(p.mask & 3), nhd = __builtin_popcount(p.mask & 12);
     const int64_t nw = (int64_t)(pc ? nhd : nvd + nhd) * p.B * p.G * 3 * H * W;
     const int64_t nh = (int64_t)nhd * p.B * p.C * H * W;
     void *wb = const_cast<void *>(p.w), *lamh = nullptr, *uh = nullptr;
     hipError_t e = hipSuccess;
-    if (!p.w_blocked && nw > 0)
-        e = p.ws->take(&wb, (size_t)nw * 2);
-    if (e == hipSuccess && nh > 0)
-        e = p.ws->take(&lamh, (size_t)nh * 2);
-    if (e == hipSuccess && nh > 0)
-        e = p.ws->take(&uh, (size_t)nh * 2);
+    if (p.rs_read) {
+        ReserveParts r;
+        e = take_reserve(p, &r);
+        if (r.w != nullptr)
+            wb = r.w;
+        lamh = r.lamh;
+        uh = r.uh;
+    } else {
+        if (!p.w_blocked && nw > 0)
+            e = p.ws->take(&wb, (size_t)nw * 2);
+        if (e == hipSuccess && nh > 0)
+            e = p.ws->take(&lamh, (size_t)nh * 2);
+        if (e == hipSuccess && nh > 0)
+            e = p.ws->take(&uh, (size_t)nh * 2);
+    }
     void *dwh = nullptr;
     if (e == hipSuccess && pc && nw > 0)
         e = p.ws->take(&dwh, (size_t)nw * 2);
     if (e != hipSuccess)
         return e;
-    if (!p.ws->counting) {
+    if (!p.ws->counting && !p.rs_read) {
         if (pc)
             e = nw > 0 ? launch_planes_to_blocked(
                              static_cast<const bf16_t *>(p.w) + (int64_t)nvd * p.B * p.G * 3 * H * W,

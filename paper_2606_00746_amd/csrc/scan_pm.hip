@@ -277,11 +277,16 @@ constexpr size_t fwd_pm_lds(bool wl)
 // One workgroup per (b, c), one wave per direction.  w: the blocked weights,
 // or with WL (one channel per group, where a re-layout would copy as much as
 // the lambda planes) the pixel-major weights, staged in LDS with the rest.
+// lamh, uh (wh with WL): where a training forward leaves the blocked copies
+// its backward reads, or null: lambda and u of the horizontal directions
+// [nh][B][C][plane] (with WL their tap planes [nh][B][G][3][plane]), taken
+// from the staged planes and the u pieces already in registers.
 template <int S, bool WL>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WL ? 1 : 3))) void
 fwd_pm_kernel(const bf16_t *__restrict__ x, const bf16_t *__restrict__ wb,
               const bf16_t *__restrict__ lam, const bf16_t *__restrict__ u,
-              bf16_t *__restrict__ y, int mask, int B, int C, int G, Magic divC, Magic divCpg)
+              bf16_t *__restrict__ y, int mask, int B, int C, int G, Magic divC, Magic divCpg,
+              bf16_t *__restrict__ lamh, bf16_t *__restrict__ uh, bf16_t *__restrict__ wh)
 {
     using Pl = PmPlane<S>;
     constexpr int HW = S * S;
@@ -333,6 +338,40 @@ fwd_pm_kernel(const bf16_t *__restrict__ x, const bf16_t *__restrict__ wb,
     }
     __builtin_amdgcn_s_waitcnt(0);
     lds_barrier();
+
+    // the reserve of a training forward: piece (q, p) of a horizontal
+    // direction's blocked plane is columns 8q .. 8q+7 of row p, which this
+    // thread holds (u) or finds staged (lambda, taps) for its row pieces;
+    // the 8 threads of one column block write whole 128-byte lines
+    if (lamh != nullptr) {
+        const int nvd = __popc(mask & 3);
+#pragma unroll
+        for (int p = 2; p < 4; ++p) {
+            if (!((mask >> p) & 1))
+                continue;
+            const int sh = __popc(mask & ((1 << p) - 1)) - nvd;
+            uint4 *lo = reinterpret_cast<uint4 *>(lamh + (((int64_t)sh * B + b) * C + c) * HW);
+            uint4 *uo = reinterpret_cast<uint4 *>(uh + (((int64_t)sh * B + b) * C + c) * HW);
+            uint4 *wo = reinterpret_cast<uint4 *>(WL ? wh + (((int64_t)sh * B + b) * G + g) * 3 * HW
+                                                     : wh);
+#pragma unroll
+            for (int k = 0; k < PER; ++k) {
+                const int t = threadIdx.x + 256 * k;
+                if (t < NCH) {
+                    const int r = t / (S / 8), cq = t - r * (S / 8);
+                    const int o = cq * S + r, so = r * Pl::kPitch + 16 * cq;
+                    gst128(lo + o, *reinterpret_cast<const uint4 *>(base + (1 + p) * Pl::kBytes + so));
+                    gst128(uo + o, uq[p][k]);
+                    if (WL) {
+#pragma unroll
+                        for (int tp = 0; tp < 3; ++tp)
+                            gst128(wo + tp * NCH + o, *reinterpret_cast<const uint4 *>(
+                                                          base + (5 + 3 * p + tp) * Pl::kBytes + so));
+                    }
+                }
+            }
+        }
+    }
 
     const bool mine = (mask >> d) & 1;
     const int s = __popc(mask & ((1 << d) - 1));
@@ -467,7 +506,7 @@ hipError_t norm_blocked_t(const Problem &p, const void *wt, void *wb, hipStream_
 }
 
 template <int S, bool WL>
-hipError_t fwd_pm_launch(const Problem &p, const void *w, hipStream_t st)
+hipError_t fwd_pm_launch(const Problem &p, const void *w, hipStream_t st, const ReserveParts &r)
 {
     const size_t lds = fwd_pm_lds<S>(WL);
     hipError_t e = hipFuncSetAttribute((const void *)fwd_pm_kernel<S, WL>,
@@ -477,29 +516,43 @@ hipError_t fwd_pm_launch(const Problem &p, const void *w, hipStream_t st)
     hipLaunchKernelGGL((fwd_pm_kernel<S, WL>), dim3((unsigned)(p.B * p.C)), dim3(256), lds, st,
                        (const bf16_t *)p.x, (const bf16_t *)w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, (bf16_t *)p.y, p.mask, p.B, p.C, p.G,
-                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)));
+                       make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
+                       (bf16_t *)r.lamh, (bf16_t *)r.uh, (bf16_t *)r.w);
     return hipGetLastError();
 }
 
 template <int S>
 hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
 {
+    // a training forward leaves the blocked copies of its backward in the
+    // reserve: the weights' re-layout writes there, the kernel the rest
+    ReserveParts r;
+    hipError_t e = hipSuccess;
+    if (p.rs_write)
+        e = take_reserve(p, &r);
+    if (e != hipSuccess)
+        return e;
     // one channel per group: the weights are staged with the channel's
     // other planes (no copy); else re-laid out once for the group's channels
     if (p.C == p.G && !p.w_blocked)
-        return p.ws->counting ? hipSuccess : fwd_pm_launch<S, true>(p, p.w, st);
+        return p.ws->counting ? hipSuccess : fwd_pm_launch<S, true>(p, p.w, st, r);
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * S * S;
     void *wb = const_cast<void *>(p.w);
-    hipError_t e = hipSuccess;
-    if (!p.w_blocked)
-        e = p.ws->take(&wb, (size_t)nw * 2);
+    if (!p.w_blocked) {
+        if (p.rs_write)
+            wb = r.w;
+        else
+            e = p.ws->take(&wb, (size_t)nw * 2);
+    }
     if (e != hipSuccess || p.ws->counting)
         return e;
     if (!p.w_blocked)
         e = w_to_blocked_t<S>(p, wb, st);
     if (e != hipSuccess)
         return e;
-    return fwd_pm_launch<S, false>(p, wb, st);
+    ReserveParts k = r;
+    k.w = nullptr;                 // (the weights are written above)
+    return fwd_pm_launch<S, false>(p, wb, st, k);
 }
 
 }  // namespace

@@ -155,7 +155,7 @@ def test_workspace_query_launches_nothing(H, W, dt):
     single-group, a grouped and a per-channel-weight case must come back OK."""
     dtype = g.BF16 if dt == "bf16" else g.F32
     for C, G in ((4, 1), (64, 2), (8, 8)):
-        for op in range(6):
+        for op in range(8):
             for dirs in (15, 1, 6):
                 st, n = g.gspn_workspace_size(op, dirs, 2, C, G, H, W, dtype)
                 assert st == _native.OK and n >= 0, (H, W, dt, C, G, op, dirs, st)
@@ -305,4 +305,53 @@ def test_slot_plan_workspace():
         assert g.gspn_scan_bwd_slots(bad, *[P(i) for i in range(9)], *args, None, 0,
                                      None) == _native.ERR_UNSUPPORTED
     assert g.gspn_scan_bwd_slots(4, *[P(i) for i in range(8)], None, *args, None, 0,
+                                 None) == _native.ERR_NULL
+
+
+def test_training_pair_reserve():
+    """gspn_reserve_size: the blocked weights (horizontal directions only
+    with one channel per group) plus lambda and u of the horizontal
+    directions, 256-byte aligned, on the register-streamed shapes; 0
+    elsewhere.  The reserve is checked on the host like a workspace."""
+    def size(dirs, B, C, G, H, W, dt=g.BF16):
+        st, n = g.gspn_reserve_size(dirs, B, C, G, H, W, dt)
+        assert st == _native.OK
+        return n
+    HW = 64 * 64
+    assert size(15, 1, 64, 2, 64, 64) == 4 * 2 * 3 * HW * 2 + 2 * (2 * 64 * HW * 2)
+    assert size(15, 1, 16, 16, 64, 64) == 2 * 16 * 3 * HW * 2 + 2 * (2 * 16 * HW * 2)
+    assert size(3, 1, 64, 2, 64, 64) == 2 * 2 * 3 * HW * 2            # vertical only
+    assert size(3, 1, 16, 16, 64, 64) == 0                             # read in place
+    for shape in ((14, 14), (8, 8), (70, 100), (256, 256), (64, 48)):
+        assert size(15, 2, 8, 2, *shape) == 0, shape
+    assert size(15, 1, 64, 2, 64, 64, g.F32) == 0
+    assert g.gspn_reserve_size(0, 1, 4, 2, 64, 64, g.BF16)[0] == _native.ERR_DIRECTION
+    assert g.gspn_reserve_size(15, 1, 6, 4, 64, 64, g.BF16)[0] == _native.ERR_DIM
+    # the training pair's own workspace: none for the forward (its copies go
+    # to the reserve), the partials only for the backward
+    args = (15, 1, 64, 2, 64, 64, g.BF16)
+    assert g.gspn_workspace_size(g.OP_FWD_TRAIN, *args) == (_native.OK, 0)
+    st, nb = g.gspn_workspace_size(g.OP_BWD_RESERVE, *args)
+    st0, nb0 = g.gspn_workspace_size(g.OP_BWD, *args)
+    assert st == st0 == _native.OK and nb0 - nb == size(*args)
+    # checks: a missing, small, misaligned or overlapping reserve is refused
+    need = size(*args)
+    far = lambda i: BASE + (1 << 33) + i * (1 << 26)     # noqa: E731
+    fwd_ptrs = [far(i) for i in range(5)]
+    bwd_ptrs = [far(i) for i in range(9)]
+    def fwd(rs, n):
+        return g.gspn_scan_fwd_train(*fwd_ptrs, *args, rs, n, None, 0, None)
+    def bwd(rs, n, ws=None, nws=0):
+        return g.gspn_scan_bwd_reserve(*bwd_ptrs, *args, rs, n, ws, nws, None)
+    assert fwd(None, 0) == _native.ERR_WORKSPACE
+    assert fwd(far(10), need - 1) == _native.ERR_WORKSPACE
+    assert fwd(far(10), -1) == _native.ERR_WORKSPACE
+    assert fwd(far(10) + 8, need) == _native.ERR_ALIGN
+    assert fwd(far(0), need) == _native.ERR_ALIAS          # over an input
+    assert fwd(far(4), need) == _native.ERR_ALIAS          # over the output
+    assert bwd(None, 0, far(11), nb) == _native.ERR_WORKSPACE
+    assert bwd(far(10), need, None, 0) == _native.ERR_WORKSPACE
+    assert bwd(far(5), need, far(11), nb) == _native.ERR_ALIAS     # over an output
+    assert bwd(far(10), need, far(10), nb) == _native.ERR_ALIAS    # over the workspace
+    assert g.gspn_scan_fwd_train(None, *fwd_ptrs[1:], *args, far(10), need, None, 0,
                                  None) == _native.ERR_NULL
