@@ -1,11 +1,14 @@
 #!/usr/bin/env python3
 """Benchmark of the 4-direction GSPN line scan (forward + backward) on one MI355X.
 
-One step = gspn_scan_fwd + gspn_scan_bwd over one batch of the workload, with
-every input already resident in HBM, every tensor pixel-major as the C ABI's
-plain entry points take them; the same step through the _blocked entry
-points (per-direction tensors in their scan order) is timed beside it and
-reported under "blocked".  Prints ONE JSON line on stdout:
+One step = the forward and backward passes over one batch of the workload,
+with every input already resident in HBM and every tensor pixel-major (the
+layout of the C ABI's plain entry points), through the training pair
+gspn_scan_fwd_train + gspn_scan_bwd_reserve (the forward leaves in a reserve
+the blocked copies its backward reads; forward-only workloads use
+gspn_scan_fwd).  The plain pair gspn_scan_fwd + gspn_scan_bwd and the _blocked
+entry points (per-direction tensors in their scan order) are timed beside it
+and reported under "plain" and "blocked".  Prints ONE JSON line on stdout:
 throughput in G pixel-channels per second (B*C*H*W per step), the roofline
 of the dominant kernel (algorithmic bytes / average launch time, from HIP
 events on the launch stream) and the CPU oracle timed on a bounded sample of
@@ -208,22 +211,47 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     stream = torch.cuda.current_stream()
     scrub = (torch.ones(args.flush_mib * (1 << 20) // 4, dtype=torch.float32, device="cuda")
              if args.flush_mib > 0 else None)
-    main = time_step(wl, inputs, args, torch, gspn, args.layout, scrub, stream)
-    other = None
+    train = main_is_train(wl, args, gspn)
+    main = time_step(wl, inputs, args, torch, gspn, args.layout, scrub, stream, train=train)
+    others = []
     if not args.norm and not args.no_blocked:
-        other = time_step(wl, inputs, args, torch, gspn,
-                          gspn.BLOCKED if args.layout == gspn.PIXEL else gspn.PIXEL, scrub, stream)
-    return summarize(wl, inputs, args, torch, main, other, scrub)
+        if train:
+            others.append(time_step(wl, inputs, args, torch, gspn, gspn.PIXEL, scrub, stream))
+        others.append(time_step(wl, inputs, args, torch, gspn,
+                                gspn.BLOCKED if args.layout == gspn.PIXEL else gspn.PIXEL, scrub,
+                                stream))
+    return summarize(wl, inputs, args, torch, main, others, scrub)
 
 
-def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream) -> dict:
-    """Event times of K steps with the per-direction tensors in `layout`."""
+def main_is_train(wl, args, gspn) -> bool:
+    """The headline step runs the training pair: pixel-major, plain weights,
+    a backward pass, and not turned off with --plain."""
+    return wl.backward and args.layout == gspn.PIXEL and not args.norm and not args.plain
+
+
+def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream, train=False) -> dict:
+    """Event times of K steps with the per-direction tensors in `layout`
+    (with `train`, through the training pair and its reserve)."""
     host = gi.inputs_line_major(inputs, wl.dirs) if layout == gspn.BLOCKED else inputs
     dev = {k: to_device(v, wl.dtype, torch) for k, v in host.items()}
     x, w, lam, u = dev["x"], dev["w"], dev["lam"], dev["u"]
     kw = {} if args.norm else {"layout": layout}
     fwd_call = gspn.scan_fwd_norm if args.norm else gspn.scan_fwd
     bwd_call = gspn.scan_bwd_norm if args.norm else gspn.scan_bwd
+    if train:
+        # the reserve, like the workspace, is taken once: a training loop keeps it
+        nrs = gspn.reserve_size(dev["x"], dev["w"], wl.dirs)
+        rsv = torch.empty(max(nrs, 1), dtype=torch.uint8, device="cuda")
+        log(f"training pair: reserve {nrs} bytes")
+
+        def fwd_call(x, w, lam, u, dirs, y, stream, workspace):
+            gspn.scan_fwd_train(x, w, lam, u, dirs, y=y, reserve=rsv, stream=stream,
+                                workspace=workspace)
+
+        def bwd_call(x, w, lam, u, dy, dirs, out, stream, workspace):
+            gspn.scan_bwd_reserve(x, w, lam, u, dy, rsv, dirs, out=out, stream=stream,
+                                  workspace=workspace)
+        kw = {}
     y = torch.empty_like(x)
     if wl.backward:
         dy = dev["dy"]
@@ -231,6 +259,7 @@ def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream) -> dict:
                  torch.empty_like(u))
     # the calls' workspace, taken once (a caller that keeps it allocates nothing per call)
     ops = ((gspn.OP_FWD_NORM, gspn.OP_BWD_NORM) if args.norm else
+           (gspn.OP_FWD_TRAIN, gspn.OP_BWD_RESERVE) if train else
            (gspn.OP_FWD, gspn.OP_BWD) if layout == gspn.PIXEL else
            (gspn.OP_FWD_BLOCKED, gspn.OP_BWD_BLOCKED))
     nws = max(gspn.workspace_size(op, x, w, wl.dirs) for op in ops)
@@ -287,11 +316,12 @@ def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream) -> dict:
     del dev, x, w, lam, u, y, ws
     if wl.backward:
         del dy, grads
-    return {"layout": layout, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms, "fwd_median_ms": fwd_med,
+    name = "train" if train else "plain" if layout == gspn.PIXEL else layout
+    return {"layout": layout, "name": name, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms, "fwd_median_ms": fwd_med,
             "bwd_median_ms": bwd_med, "ms_per_step": ms_per_step}
 
 
-def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
+def summarize(wl, inputs, args, torch, main, others, scrub) -> dict:
     fwd_ms, bwd_ms, ms_per_step = main["fwd_ms"], main["bwd_ms"], main["ms_per_step"]
 
     def flush():
@@ -306,16 +336,20 @@ def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
         f"{value:.2f} Gpix.ch/s  step algorithmic {step_gbs:.0f} GB/s "
         f"({step_gbs / HBM_PEAK_GBS:.1%} of peak)")
 
+    train = main["name"] == "train"
     if bwd_ms > fwd_ms:
-        dom, call, dom_ms, dom_bytes = "gspn_scan_bwd", "bwd", bwd_ms, nbytes["bwd"]
+        dom, call, dom_ms, dom_bytes = ("gspn_scan_bwd_reserve" if train else "gspn_scan_bwd",
+                                        "bwd", bwd_ms, nbytes["bwd"])
     else:
-        dom, call, dom_ms, dom_bytes = "gspn_scan_fwd", "fwd", fwd_ms, nbytes["fwd"]
+        dom, call, dom_ms, dom_bytes = ("gspn_scan_fwd_train" if train else "gspn_scan_fwd",
+                                        "fwd", fwd_ms, nbytes["fwd"])
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     # measured HBM bytes of the same call (FETCH_SIZE + WRITE_SIZE counters, scaled by a
     # plain copy), kept in profiles/ for the current kernel sources only
     from paper_2606_00746_amd import profiling
     traffic = None if args.norm else profiling.load_traffic(
-        os.path.join(ROOT, "profiles", f"traffic_{wl.name}-{args.layout}.txt"), call)
+        os.path.join(ROOT, "profiles",
+                     f"traffic_{wl.name}-{'pair' if train else args.layout}.txt"), call)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
@@ -350,6 +384,10 @@ def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
                    "storage": wl.dtype, "weights": "logits" if args.norm else "normalized",
                    "layout": ("pixel-major [D][B][C][H][W] / [D][B][G][3][H][W]"
                               if args.layout == "pixel" else "blocked line-major"),
+                   "calls": ("gspn_scan_fwd_train + gspn_scan_bwd_reserve" if train else
+                             "gspn_scan_fwd_norm + gspn_scan_bwd_norm" if args.norm else
+                             "gspn_scan_fwd + gspn_scan_bwd" if wl.backward else
+                             "gspn_scan_fwd"),
                    "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
@@ -361,14 +399,14 @@ def summarize(wl, inputs, args, torch, main, other, scrub) -> dict:
         "roofline": roofline,
         "copy_probe": probe,
     }
-    if other is not None:
+    for other in others:
         o_ms = other["ms_per_step"]
-        out[other["layout"]] = {
+        out[other["name"]] = {
             "value": round(pixch / (o_ms * 1e-3) / 1e9, 3), "ms_per_step": round(o_ms, 5),
             "fwd_ms": round(other["fwd_ms"], 5), "bwd_ms": round(other["bwd_ms"], 5),
             "step_hbm_frac": round((nbytes["fwd"] + nbytes["bwd"]) / (o_ms * 1e-3) / 1e9
                                    / HBM_PEAK_GBS, 4)}
-        log(f"{other['layout']} layout: fwd {other['fwd_ms']:.4f} ms  bwd {other['bwd_ms']:.4f} ms"
+        log(f"{other['name']}: fwd {other['fwd_ms']:.4f} ms  bwd {other['bwd_ms']:.4f} ms"
             f"  step {o_ms:.4f} ms")
     if not args.no_cpu_baseline:
         # the oracle on every core this process may use, up to the 16 that
@@ -550,8 +588,10 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layout", default="pixel", choices=("pixel", "blocked"),
                     help="layout of the per-direction tensors of the reported step")
+    ap.add_argument("--plain", action="store_true",
+                    help="time the plain pair gspn_scan_fwd + gspn_scan_bwd as the headline")
     ap.add_argument("--no-blocked", action="store_true",
-                    help="do not time the other layout beside the reported one")
+                    help="time only the headline pair (no plain or blocked entries beside it)")
     ap.add_argument("--norm", action="store_true",
                     help="weights given as logits: time gspn_scan_fwd_norm / gspn_scan_bwd_norm")
     ap.add_argument("--latent", default=None,
