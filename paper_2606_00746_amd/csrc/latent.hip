@@ -17,6 +17,8 @@
 //  * proj_rows_kernel, K <= 64 (P_up, the parameter product): x is staged
 //    once, every wave keeps the B fragments of all 128 pixels in registers
 //    and the waves take the 32-row tiles of A in turn, 4 accumulators each;
+//    a row tile's A rows are loaded while the tile before it is multiplied,
+//    ahead of that tile's stores;
 //  * proj_stage_kernel, K > 64 (P_down): a workgroup owns 64 rows x 128
 //    pixels, wave v pixels 32v .. 32v+31 of both 32-row halves; K runs in
 //    stages of 64 staged in LDS, the next stage's loads in flight while the
@@ -78,6 +80,7 @@ struct ProjArgs {
     int ntiles, mtiles, tiles_w;     // pixel tiles, row tiles, params: tiles across a row
     int Cc, DCc;                     // params: latent channels, D * Cc
     int dirs[4];                     // params: direction index of each stacked slot
+    int vslots;                      // params: bit s set when slot s is a vertical direction
     Magic div_m, div_n, div_cc, div_tw, div_w, div_wi;
 };
 
@@ -299,25 +302,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             po[ct] = 2u * (uint32_t)(pass == 0 ? lm_offset(prow[ct], pcol[ct], A.H, A.W)
                                                 : lm_offset(pcol[ct], prow[ct], A.W, A.H));
     }
-#pragma unroll 1
-    for (int rt = v; rt < RT; rt += 4) {
-        bool is_w = false, vert = true;
-        rsrc_t dd = make_rsrc(A.u, 0);
-        if (fast) {
-            const int m0 = 32 * rt;
-            is_w = m0 >= 2 * A.DCc;
-            const int q0 = is_w ? (m0 - 2 * A.DCc) >> 2 : (m0 < A.DCc ? m0 : m0 - A.DCc);
-            const int sl = mdiv(q0, A.div_cc), c0 = q0 - sl * A.Cc;
-            vert = A.dirs[sl] < 2;
-            if (vert != (pass == 0))
-                continue;
-            const int64_t HW = A.HW;
-            const bf16_t *base =
-                is_w ? A.w + (((int64_t)sl * A.B + b) * A.Cc + c0) * 3 * HW
-                     : (m0 < A.DCc ? A.u : A.lam) + (((int64_t)sl * A.B + b) * A.Cc + c0) * HW;
-            dd = make_rsrc(base, (uint32_t)(2 * (is_w ? 24 : 32) * HW));
-        }
-        bf16x8_t af[kKS / 16];
+    // the row tiles this wave takes in this pass
+    auto in_pass = [&](int rt) {
+        if (!fast)
+            return true;
+        const int m0 = 32 * rt;
+        const bool w_ = m0 >= 2 * A.DCc;
+        const int q0 = w_ ? (m0 - 2 * A.DCc) >> 2 : (m0 < A.DCc ? m0 : m0 - A.DCc);
+        const int sl = mdiv(q0, A.div_cc);
+        return (((A.vslots >> sl) & 1) != 0) == (pass == 0);
+    };
+    auto next_tile = [&](int rt) {
+        while (rt < RT && !in_pass(rt))
+            rt += 4;
+        return rt;
+    };
+    auto load_a = [&](int rt, bf16x8_t (&af)[kKS / 16]) {
         const bf16_t *src = a_row<MODE>(A, 32 * rt + l32);
 #pragma unroll
         for (int s = 0; s < kKS / 16; ++s) {
@@ -325,6 +325,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             if (s < nsteps)
                 af[s] = (src != nullptr && k < A.K) ? *reinterpret_cast<const bf16x8_t *>(src + k)
                                                     : bf16x8_t{};
+        }
+    };
+    // One row tile: the product with af, then the next row tile's A rows
+    // into an, then the stores.  The loop below alternates the two fragment
+    // sets (no run-time index into them, which would go through scratch).
+    auto tile = [&](int rt, int rn, const bf16x8_t (&af)[kKS / 16], bf16x8_t (&an)[kKS / 16]) {
+        bool is_w = false, vert = true;
+        rsrc_t dd = make_rsrc(A.u, 0);
+        if (fast) {
+            const int m0 = 32 * rt;
+            is_w = m0 >= 2 * A.DCc;
+            const int q0 = is_w ? (m0 - 2 * A.DCc) >> 2 : (m0 < A.DCc ? m0 : m0 - A.DCc);
+            const int sl = mdiv(q0, A.div_cc), c0 = q0 - sl * A.Cc;
+            vert = (A.vslots >> sl) & 1;
+            const int64_t HW = A.HW;
+            const bf16_t *base =
+                is_w ? A.w + (((int64_t)sl * A.B + b) * A.Cc + c0) * 3 * HW
+                     : (m0 < A.DCc ? A.u : A.lam) + (((int64_t)sl * A.B + b) * A.Cc + c0) * HW;
+            dd = make_rsrc(base, (uint32_t)(2 * (is_w ? 24 : 32) * HW));
         }
 
         f32x16_t acc[4];
@@ -340,6 +359,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                 for (int ct = 0; ct < 4; ++ct)
                     acc[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s], bfr[ct][s], acc[ct],
                                                                       0, 0, 0);
+        // the next tile's A rows, issued before this tile's stores: a later
+        // wait for them then does not wait for the stores as well
+        if (rn < RT)
+            load_a(rn, an);
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) {
             if (ppix[ct] < 0)
@@ -369,10 +392,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                                   acc[ct][4 * g + 3]};
                     if (is_w) {
                         const int p = vert ? pcol[ct] : prow[ct], P = vert ? A.Wv : A.Hv;
-                        const float s0 = p > 0 ? sigmoid(o[0]) : 0.f;
-                        const float s1 = sigmoid(o[1]);
-                        const float s2 = p < P - 1 ? sigmoid(o[2]) : 0.f;
-                        const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+                        // the sigmoids and the sum's reciprocal with the
+                        // hardware reciprocal (1 ulp): this kernel is bound
+                        // by the instructions it issues per stored value,
+                        // and an IEEE division takes about ten
+                        const float s0 = p > 0 ? __builtin_amdgcn_rcpf(1.f + __expf(-o[0])) : 0.f;
+                        const float s1 = __builtin_amdgcn_rcpf(1.f + __expf(-o[1]));
+                        const float s2 =
+                            p < P - 1 ? __builtin_amdgcn_rcpf(1.f + __expf(-o[2])) : 0.f;
+                        const float inv = __builtin_amdgcn_rcpf(fmaxf((s0 + s1) + s2, kNormEps));
                         o[0] = s0 * inv, o[1] = s1 * inv, o[2] = s2 * inv;
                     }
 #pragma unroll
@@ -385,6 +413,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
                 }
             }
         }
+    };
+    bf16x8_t af0[kKS / 16], af1[kKS / 16];
+    int rt = next_tile(v);
+    if (rt < RT)
+        load_a(rt, af0);
+#pragma unroll 1
+    while (rt < RT) {
+        int rn = next_tile(rt + 4);
+        tile(rt, rn, af0, af1);
+        rt = rn;
+        if (rt >= RT)
+            break;
+        rn = next_tile(rt + 4);
+        tile(rt, rn, af1, af0);
+        rt = rn;
     }
     }
 }
@@ -637,7 +680,11 @@ hipError_t launch_latent_params(const void *xc, const void *lu, const void *ll, 
     int D = 0;
     for (int d = 0; d < 4; ++d)
         if ((mask >> d) & 1)
+        {
+            if (d < 2)
+                A.vslots |= 1 << D;      // slot D scans vertically
             A.dirs[D++] = d;
+        }
     A.B = B, A.K = Cc, A.H = H, A.W = W, A.HW = H * W, A.HWi = A.HW;
     A.Hv = Hv > 0 ? Hv : H, A.Wv = Wv > 0 ? Wv : W;
     A.Cc = Cc, A.DCc = D * Cc, A.M = 6 * D * Cc;
