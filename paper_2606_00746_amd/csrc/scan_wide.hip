@@ -193,6 +193,117 @@ __device__ __forceinline__ void wide_dir(int lane, int H_, int W_, rsrc_t lam, r
     }
 }
 
+template <int AUX>
+__device__ __forceinline__ uint2 ld64(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX);
+    return make_uint2(v[0], v[1]);
+}
+
+// 8 rows of the five streams of a vertical direction, 4 adjacent columns each.
+struct VRows {
+    uint2 l[8], u[8], w0[8], w1[8], w2[8];
+};
+
+// A vertical direction of pixel-major planes (no copy into the blocked
+// order), lane l owning the 4 adjacent columns 4l .. 4l+3 of the row (W up
+// to 256): a step reads 8 bytes per lane of a row of lambda, u and each tap
+// plane (whole rows across the wave), takes the neighbours beyond the lane's
+// 4 columns from lanes l-1 and l+1 by DPP wave shifts, and writes u * h as
+// 16 bytes of the direction's fp32 row.  The same operations in the same
+// order as wide_dir, so the same bits.  Rows come 8 at a time, one block
+// ahead of use.
+template <bool REV, int HC, int WC>
+__device__ __forceinline__ void wide_vert_pm(int lane, int H_, int W_, rsrc_t lam, rsrc_t u,
+                                             rsrc_t w, const uint8_t *xs, u32x4 ys)
+{
+    const int H = HC ? HC : H_, W = WC ? WC : W_;
+    const int pdw = wide_pitch_dw(W);
+    const uint32_t wplane = (uint32_t)(2 * H * W);
+    const int c0 = 4 * lane;
+    const bool act = c0 < W;                         // W is a multiple of 8
+    // idle lanes read column 0 with every weight and lambda selected to 0:
+    // their h stays 0, which is what the last active lane's right neighbour
+    // needs (its tap 2 is ignored anyway)
+    const uint32_t voff = act ? 2u * (uint32_t)c0 : 0u;
+    const uint32_t slo = act ? kSelLo : kSelZero, shi = act ? kSelHi : kSelZero;
+    const uint32_t s0lo = (act && c0 > 0) ? kSelLo : kSelZero;          // tap 0, column c0
+    const uint32_t s2hi = (act && c0 + 4 < W) ? kSelHi : kSelZero;      // tap 2, column c0+3
+    const uint32_t xoff = act ? 2u * (uint32_t)c0 : 0u;
+    auto load = [&](VRows &r, int fb) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int i = 8 * fb + t;
+            const uint32_t ro = 2u * (uint32_t)((REV ? H - 1 - i : i) * W);
+            r.l[t] = ld64<2 /* nt */>(lam, voff, ro);
+            r.u[t] = ld64<2>(u, voff, ro);
+            r.w0[t] = ld64<0>(w, voff, ro);
+            r.w1[t] = ld64<0>(w, voff, ro + wplane);
+            r.w2[t] = ld64<0>(w, voff, ro + 2u * wplane);
+        }
+    };
+    float h[4] = {0.f, 0.f, 0.f, 0.f};
+    auto run = [&](const VRows &r, int fb) {
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int i = 8 * fb + t;
+            const int ln = REV ? H - 1 - i : i;
+            const uint32_t xa = 4u * (uint32_t)(ln * pdw) + xoff;
+            const uint32_t xw0 = lds_u32(xs, xa), xw1 = lds_u32(xs, xa + 4);
+            const float xv[4] = {bf_lo(xw0), bf_hi(xw0), bf_lo(xw1), bf_hi(xw1)};
+            const float lv[4] = {widen(r.l[t].x, slo), widen(r.l[t].x, shi), widen(r.l[t].y, slo),
+                                 widen(r.l[t].y, shi)};
+            const float left = from_left<64>(h[3]), right = from_right<64>(h[0]);
+            float hn[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                hn[e] = lv[e] * xv[e];
+            if (i > 0) {
+                const float w1v[4] = {widen(r.w1[t].x, slo), widen(r.w1[t].x, shi),
+                                      widen(r.w1[t].y, slo), widen(r.w1[t].y, shi)};
+                const float w0v[4] = {widen(r.w0[t].x, s0lo), widen(r.w0[t].x, shi),
+                                      widen(r.w0[t].y, slo), widen(r.w0[t].y, shi)};
+                const float w2v[4] = {widen(r.w2[t].x, slo), widen(r.w2[t].x, shi),
+                                      widen(r.w2[t].y, slo), widen(r.w2[t].y, s2hi)};
+                const float lf[4] = {left, h[0], h[1], h[2]};
+                const float rt[4] = {h[1], h[2], h[3], right};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    hn[e] = fmaf(w1v[e], h[e], hn[e]);
+                    hn[e] = fmaf(w0v[e], lf[e], hn[e]);
+                    hn[e] = fmaf(w2v[e], rt[e], hn[e]);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                h[e] = hn[e];
+            if (act) {
+                const uint2 uu = r.u[t];
+                st128_nt(ys, 4u * (uint32_t)c0, 4u * (uint32_t)(ln * W),
+                         make_uint4(__float_as_uint(bf_lo(uu.x) * h[0]),
+                                    __float_as_uint(bf_hi(uu.x) * h[1]),
+                                    __float_as_uint(bf_lo(uu.y) * h[2]),
+                                    __float_as_uint(bf_hi(uu.y) * h[3])));
+            }
+        }
+        step_fence();
+    };
+    const int NB = H / 8;
+    VRows A, B;
+    load(A, 0);
+#pragma unroll 1
+    for (int fb = 0; fb < NB; fb += 2) {
+        if (fb + 1 < NB)
+            load(B, fb + 1);
+        run(A, fb);
+        if (fb + 1 < NB) {
+            if (fb + 2 < NB)
+                load(A, fb + 2);
+            run(B, fb + 1);
+        }
+    }
+}
+
 // Direction d's pass over blocks fb0 .. fb1-1 (direction-uniform dispatch).
 template <int NPL, int HC, int WC, int MODE>
 __device__ __forceinline__ void wide_pass(int d, int lane, int H, int W, rsrc_t rl, rsrc_t ru,
@@ -230,11 +341,15 @@ __device__ __forceinline__ void stage_x_plane(const bf16_t *x, int64_t pc, int H
     }
 }
 
-template <int NPL, int HC, int WC>
+// VPM: the call is pixel-major and lam, u, w hold blocked copies of the
+// horizontal directions only ([nh][B][C][plane], [nh][B][G][3][plane]); the
+// vertical ones are read in place from lam_v, u_v, w_v (the call's tensors).
+template <int NPL, int HC, int WC, bool VPM>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void fwd_wide_kernel(
     const bf16_t *__restrict__ x, const bf16_t *__restrict__ w, const bf16_t *__restrict__ lam,
     const bf16_t *__restrict__ u, float *__restrict__ ys, int mask, int B, int C, int G, int H_,
-    int W_, Magic divC, Magic divCpg, Magic divNq, int plane0)
+    int W_, Magic divC, Magic divCpg, Magic divNq, int plane0, const bf16_t *__restrict__ lam_v,
+    const bf16_t *__restrict__ u_v, const bf16_t *__restrict__ w_v)
 {
     const int H = HC ? HC : H_, W = WC ? WC : W_;
     extern __shared__ uint32_t xs32[];
@@ -254,17 +369,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     if ((mask >> d) & 1) {
         const int s = __popc(mask & ((1 << d) - 1));
         const int64_t pd = (((int64_t)s * B + b) * C + c) * HW;
-        const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
-        const rsrc_t rl = make_rsrc(lam + pd, (uint32_t)(2 * HW));
-        const rsrc_t ru = make_rsrc(u + pd, (uint32_t)(2 * HW));
-        const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
         const u32x4 yd = make_sdesc(ys + pd, (uint32_t)(4 * HW));
-        float h[NPL];
+        if (VPM && d < 2) {
+            const int64_t pw = (((int64_t)s * B + b) * G + g) * 3 * HW;
+            const rsrc_t rl = make_rsrc(lam_v + pd, (uint32_t)(2 * HW));
+            const rsrc_t ru = make_rsrc(u_v + pd, (uint32_t)(2 * HW));
+            const rsrc_t rw = make_rsrc(w_v + pw, (uint32_t)(6 * HW));
+            if (d == 0)
+                wide_vert_pm<false, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
+            else
+                wide_vert_pm<true, HC, WC>(lane, H, W, rl, ru, rw, xs, yd);
+        } else {
+            const int sc = VPM ? s - __popc(mask & 3) : s;   // slot among the copies
+            const int64_t pdc = (((int64_t)sc * B + b) * C + c) * HW;
+            const int64_t pw = (((int64_t)sc * B + b) * G + g) * 3 * HW;
+            const rsrc_t rl = make_rsrc(lam + pdc, (uint32_t)(2 * HW));
+            const rsrc_t ru = make_rsrc(u + pdc, (uint32_t)(2 * HW));
+            const rsrc_t rw = make_rsrc(w + pw, (uint32_t)(6 * HW));
+            float h[NPL];
 #pragma unroll
-        for (int m = 0; m < NPL; ++m)
-            h[m] = 0.f;
-        const int NB = (d < 2 ? H : W) / 8;
-        wide_pass<NPL, HC, WC, kStore>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
+            for (int m = 0; m < NPL; ++m)
+                h[m] = 0.f;
+            const int NB = (d < 2 ? H : W) / 8;
+            wide_pass<NPL, HC, WC, kStore>(d, lane, H, W, rl, ru, rw, xs, yd, 0, NB, h);
+        }
     }
 }
 
@@ -469,19 +597,23 @@ __global__ __launch_bounds__(256) void sum_wide_kernel(const float *__restrict__
     }
 }
 
-template <int NPL, int HC, int WC>
+// v: with the vertical directions read in place, the call's pixel-major
+// tensors (p then holds the horizontal directions' blocked copies).
+template <int NPL, int HC, int WC, bool VPM>
 hipError_t fwd_wide_t(const Problem &p, hipStream_t st, float *ys, size_t lds, int plane0,
-                      int nplanes)
+                      int nplanes, const Problem *v)
 {
-    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC>,
+    hipError_t e = hipFuncSetAttribute((const void *)fwd_wide_kernel<NPL, HC, WC, VPM>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC>), dim3((unsigned)nplanes), dim3(256), lds,
-                       st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
+    hipLaunchKernelGGL((fwd_wide_kernel<NPL, HC, WC, VPM>), dim3((unsigned)nplanes), dim3(256),
+                       lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w, (const bf16_t *)p.lam,
                        (const bf16_t *)p.u, ys, p.mask, p.B, p.C, p.G, p.H, p.W,
                        make_magic((uint32_t)p.C), make_magic((uint32_t)(p.C / p.G)),
-                       make_magic((uint32_t)(p.W / 8)), plane0);
+                       make_magic((uint32_t)(p.W / 8)), plane0,
+                       (const bf16_t *)(v ? v->lam : nullptr), (const bf16_t *)(v ? v->u : nullptr),
+                       (const bf16_t *)(v ? v->w : nullptr));
     return hipGetLastError();
 }
 
@@ -641,7 +773,8 @@ int wide_chunks(const Problem &p, size_t lds)
     return (K >= 8 && nbh >= 32 && nbw >= 32) ? K : 1;
 }
 
-hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states, size_t lds, int K)
+hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states, size_t lds, int K,
+                      const Problem *v = nullptr)
 {
     const int side = p.H > p.W ? p.H : p.W;
     const int npl = (side + 63) / 64;
@@ -656,13 +789,20 @@ hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states
                           : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
     }
     const int planes = p.B * p.C;
+    if (v != nullptr) {
+        if (p.H == 256 && p.W == 256)
+            return fwd_wide_t<4, 256, 256, true>(p, st, ys, lds, 0, planes, v);
+        return npl <= 2 ? fwd_wide_t<2, 0, 0, true>(p, st, ys, lds, 0, planes, v)
+               : npl == 3 ? fwd_wide_t<3, 0, 0, true>(p, st, ys, lds, 0, planes, v)
+                          : fwd_wide_t<4, 0, 0, true>(p, st, ys, lds, 0, planes, v);
+    }
     if (p.H == 256 && p.W == 256)
-        return fwd_wide_t<4, 256, 256>(p, st, ys, lds, 0, planes);
+        return fwd_wide_t<4, 256, 256, false>(p, st, ys, lds, 0, planes, nullptr);
     if (p.H == 128 && p.W == 128)
-        return fwd_wide_t<2, 128, 128>(p, st, ys, lds, 0, planes);
-    return npl <= 2 ? fwd_wide_t<2, 0, 0>(p, st, ys, lds, 0, planes)
-           : npl == 3 ? fwd_wide_t<3, 0, 0>(p, st, ys, lds, 0, planes)
-                      : fwd_wide_t<4, 0, 0>(p, st, ys, lds, 0, planes);
+        return fwd_wide_t<2, 128, 128, false>(p, st, ys, lds, 0, planes, nullptr);
+    return npl <= 2 ? fwd_wide_t<2, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr)
+           : npl == 3 ? fwd_wide_t<3, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr)
+                      : fwd_wide_t<4, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr);
 }
 
 }  // namespace
@@ -700,31 +840,44 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
             return hipSuccess;
         e = fwd_wide_l(p, st, ys, ys + D * n, lds, K);
     } else {
-        // blocked copies of lam, u and w (workspace), then the blocked scan
-        const int64_t nw = (int64_t)D * p.B * p.G * 3 * p.H * p.W;
+        // Blocked copies (workspace) of lam, u and w, then the blocked scan.
+        // The single pass reads the vertical directions in place (whole rows,
+        // wide_vert_pm), so only the horizontal ones are copied; the chunked
+        // passes take every direction from copies.
+        const int nv = __builtin_popcount(p.mask & 3), nh = D - nv;
+        const int nc = K > 1 ? D : nh;                    // directions copied
+        const int64_t bc = (int64_t)p.B * p.C, bg3 = (int64_t)p.B * p.G * 3;
+        const int64_t HW = (int64_t)p.H * p.W;
         void *cl = nullptr, *cu = nullptr, *cw = nullptr;
-        e = p.ws->take(&cl, (size_t)(D * n) * 2);
-        if (e == hipSuccess)
-            e = p.ws->take(&cu, (size_t)(D * n) * 2);
-        if (e == hipSuccess)
-            e = p.ws->take(&cw, (size_t)nw * 2);
+        if (nc > 0) {
+            e = p.ws->take(&cl, (size_t)(nc * bc * HW) * 2);
+            if (e == hipSuccess)
+                e = p.ws->take(&cu, (size_t)(nc * bc * HW) * 2);
+            if (e == hipSuccess)
+                e = p.ws->take(&cw, (size_t)(nc * bg3 * HW) * 2);
+        }
         if (e != hipSuccess || p.ws->counting)
             return e;
-        const int nv = __builtin_popcount(p.mask & 3), nh = D - nv;
-        const int64_t bc = (int64_t)p.B * p.C, bg3 = (int64_t)p.B * p.G * 3;
-        e = launch_pieces(p.lam, cl, nv * bc, nh * bc, p.H, p.W, st);
-        if (e == hipSuccess)
-            e = launch_pieces(p.u, cu, nv * bc, nh * bc, p.H, p.W, st);
-        if (e == hipSuccess)
-            e = launch_pieces(p.w, cw, nv * bg3, nh * bg3, p.H, p.W, st);
-        if (e != hipSuccess)
-            return e;
+        const int cv = nc - nh;                           // vertical directions copied
+        const int64_t skip = (int64_t)(nv - cv);          // vertical slots not copied
+        if (nc > 0) {
+            e = launch_pieces(static_cast<const bf16_t *>(p.lam) + skip * bc * HW, cl, cv * bc,
+                              nh * bc, p.H, p.W, st);
+            if (e == hipSuccess)
+                e = launch_pieces(static_cast<const bf16_t *>(p.u) + skip * bc * HW, cu, cv * bc,
+                                  nh * bc, p.H, p.W, st);
+            if (e == hipSuccess)
+                e = launch_pieces(static_cast<const bf16_t *>(p.w) + skip * bg3 * HW, cw,
+                                  cv * bg3, nh * bg3, p.H, p.W, st);
+            if (e != hipSuccess)
+                return e;
+        }
         Problem q = p;
         q.lam = cl;
         q.u = cu;
         q.w = cw;
         q.layout = kBlocked;
-        e = fwd_wide_l(q, st, ys, ys + D * n, lds, K);
+        e = fwd_wide_l(q, st, ys, ys + D * n, lds, K, K > 1 ? nullptr : &p);
     }
     if (e == hipSuccess)
         e = launch_sum_wide(p, ys, st, 0, p.B * p.C);
