@@ -303,6 +303,11 @@ def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=Non
     else:
         named.update(y=(outs[0], n))
     _check_tensors(x, named)
+    if reserve is not None:
+        import torch
+        if (reserve.dtype != torch.uint8 or not reserve.is_contiguous() or not reserve.is_cuda
+                or reserve.device != x.device):
+            raise ValueError("reserve must be a contiguous uint8 tensor on the inputs' device")
     dt = _dtype_code(x)
     ws, nbytes = _workspace(op, direction, B, C, G, H, W, dt, x.device, workspace, slots)
     ptrs = [t.data_ptr() for t in (x, w, lam, u)]

@@ -736,7 +736,7 @@ extern "C" const char *gspn_strerror(int status)
     case GSPN_ERR_ALIAS: return "two buffers of the call overlap";
     case GSPN_ERR_UNSUPPORTED: return "shape beyond the supported limits";
     case GSPN_ERR_HIP: return "a HIP runtime call or kernel launch failed";
-    case GSPN_ERR_WORKSPACE: return "the workspace is missing or smaller than the call needs";
+    case GSPN_ERR_WORKSPACE: return "the workspace or the reserve is missing or smaller than the call needs";
     default: return "unknown status";
     }
 }

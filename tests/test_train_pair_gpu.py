@@ -138,3 +138,22 @@ def test_pair_full_size(idx):
     check_same(wl, plain, train)
     del plain, train, rs, t
     torch.cuda.empty_cache()
+
+
+def test_front_end_checks_the_reserve():
+    """A reserve on another device, of another dtype or not contiguous is
+    refused by the binding before any call; a short one by the library."""
+    torch = require_gpu()
+    wl = CASES[0].with_(C=4, G=2)
+    print(f"[case] train pair reserve checks {wl.name}", flush=True)
+    t = upload(gi.make_inputs(wl, with_dy=True), wl.dtype, wl.dirs)
+    y, rs = gspn.scan_fwd_train(t["x"], t["w"], t["lam"], t["u"], wl.dirs)
+    args = (t["x"], t["w"], t["lam"], t["u"], t["dy"])
+    for bad in (rs.cpu(), rs.view(torch.int8), rs.view(-1, 2)[:, 0]):
+        with pytest.raises(ValueError, match="reserve"):
+            gspn.scan_bwd_reserve(*args, bad, wl.dirs)
+    with pytest.raises(gspn.GspnError, match="workspace"):
+        gspn.scan_bwd_reserve(*args, rs[: rs.numel() - 1], wl.dirs)
+    with pytest.raises(gspn.GspnError, match="workspace"):
+        gspn.scan_bwd_reserve(*args, None, wl.dirs)
+    torch.cuda.synchronize()
