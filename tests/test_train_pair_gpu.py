@@ -30,6 +30,7 @@ CASES = [
     case("32-T2B+L2R", 1, 16, 4, 32, 32, dirs=5),
     case("64-G=C-R2L", 1, 8, 8, 64, 64, dirs=8),
     case("56-G=C-B2T+R2L", 1, 8, 8, 56, 56, dirs=10),
+    case("48-G=C-vertical-only", 1, 8, 8, 48, 48, dirs=3),   # nothing to keep: reserve 0
 ]
 NO_RESERVE = [
     case("14x14", 2, 24, 3, 14, 14),
