@@ -110,6 +110,10 @@ EDGE = [
     case("wide-96x80-R2L", 2, 4, 4, 96, 80, dirs=8),
     case("wide-128x192-dirs6", 1, 4, 4, 128, 192, dirs=6, backward=False),
     case("wide-256x128-dirs9-peaky", 1, 2, 1, 256, 128, dirs=9, sigma=2.0, backward=False),
+    # pixel-major vertical directions read in place, 4 columns per lane: 2
+    # lanes active (W = 8), 50 lanes (W = 200)
+    case("wide-200x8-fwd", 2, 3, 3, 200, 8, backward=False),
+    case("wide-8x200-dirs3", 1, 4, 2, 8, 200, dirs=3, backward=False),
     # few channel planes of 256 x 256: the forward cuts every scan into
     # chunks of whole line blocks, end states from zero, carries through w,
     # then the chunks again from their carries (16, 16 and 8 chunks)
