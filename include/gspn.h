@@ -116,6 +116,8 @@ extern "C" {
 #define GSPN_OP_BWD_BLOCKED 5
 #define GSPN_OP_FWD_TRAIN 6
 #define GSPN_OP_BWD_RESERVE 7
+#define GSPN_OP_FWD_NORM_TRAIN 8
+#define GSPN_OP_BWD_NORM_RESERVE 9
 
 /* Largest supported H and W, and largest B*C*H*W and B*G*H*W*3*D. */
 #define GSPN_MAX_SIDE 4096
@@ -247,6 +249,29 @@ int gspn_scan_bwd_reserve(const void *x, const void *w, const void *lam, const v
                           int direction, int B, int C, int G, int H, int W, int dtype,
                           const void *reserve, int64_t reserve_bytes, void *workspace,
                           int64_t workspace_bytes, void *stream);
+
+/*
+ * The training pair of the _norm entry points (weights given as logits):
+ * gspn_scan_fwd_norm and gspn_scan_bwd_norm, bit for bit, where the forward
+ * keeps in the reserve the weights it forms from the logits (in the blocked
+ * order, every direction) and the horizontal directions' lambda and u
+ * copies, and the backward takes them from there instead of forming and
+ * copying them again.  gspn_reserve_size_norm gives the reserve's bytes;
+ * arguments, rules and errors otherwise as for gspn_scan_fwd_train /
+ * gspn_scan_bwd_reserve and the _norm entry points (workspace:
+ * gspn_workspace_size with GSPN_OP_FWD_NORM_TRAIN / GSPN_OP_BWD_NORM_RESERVE).
+ */
+int gspn_reserve_size_norm(int direction, int B, int C, int G, int H, int W, int dtype,
+                           int64_t *bytes);
+int gspn_scan_fwd_norm_train(const void *x, const void *w_logits, const void *lam,
+                             const void *u, void *y, int direction, int B, int C, int G,
+                             int H, int W, int dtype, void *reserve, int64_t reserve_bytes,
+                             void *workspace, int64_t workspace_bytes, void *stream);
+int gspn_scan_bwd_norm_reserve(const void *x, const void *w_logits, const void *lam,
+                               const void *u, const void *dy, void *dx, void *dw_logits,
+                               void *dlam, void *du, int direction, int B, int C, int G, int H,
+                               int W, int dtype, const void *reserve, int64_t reserve_bytes,
+                               void *workspace, int64_t workspace_bytes, void *stream);
 
 /*
  * gspn_scan_bwd for callers that cannot allocate device memory or hand in a

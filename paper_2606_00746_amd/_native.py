@@ -21,7 +21,7 @@ F32, BF16 = 0, 1
 (OK, ERR_NULL, ERR_DIM, ERR_DIRECTION, ERR_DTYPE, ERR_ALIGN, ERR_ALIAS, ERR_UNSUPPORTED, ERR_HIP,
  ERR_WORKSPACE) = (0, -1, -2, -3, -4, -5, -6, -7, -8, -9)
 (OP_FWD, OP_BWD, OP_FWD_NORM, OP_BWD_NORM, OP_FWD_BLOCKED, OP_BWD_BLOCKED, OP_FWD_TRAIN,
- OP_BWD_RESERVE) = range(8)
+ OP_BWD_RESERVE, OP_FWD_NORM_TRAIN, OP_BWD_NORM_RESERVE) = range(10)
 MAX_SIDE = 4096
 
 # layouts of the per-direction tensors
@@ -31,6 +31,7 @@ EXPORTED = ("gspn_workspace_size", "gspn_scan_fwd", "gspn_scan_bwd", "gspn_scan_
             "gspn_scan_bwd_blocked", "gspn_scan_fwd_norm", "gspn_scan_bwd_norm",
             "gspn_scan_bwd_static", "gspn_workspace_size_slots", "gspn_scan_bwd_slots",
             "gspn_reserve_size", "gspn_scan_fwd_train", "gspn_scan_bwd_reserve",
+            "gspn_reserve_size_norm", "gspn_scan_fwd_norm_train", "gspn_scan_bwd_norm_reserve",
             "gspn_project",
             "gspn_latent_params", "gspn_latent_workspace_size", "gspn_latent_fwd",
             "gspn_strerror", "gspn_last_hip_error", "gspn_version")
@@ -69,9 +70,12 @@ def load() -> ctypes.CDLL:
         lib.gspn_scan_bwd_static.argtypes = [vp] * 9 + scan8 + [vp]
         lib.gspn_workspace_size_slots.argtypes = [i] + scan8 + [pi64]
         lib.gspn_scan_bwd_slots.argtypes = [i] + [vp] * 9 + scan8 + ws
-        lib.gspn_reserve_size.argtypes = scan8 + [pi64]
-        lib.gspn_scan_fwd_train.argtypes = [vp] * 5 + scan8 + [vp, i64] + ws
-        lib.gspn_scan_bwd_reserve.argtypes = [vp] * 9 + scan8 + [vp, i64] + ws
+        for name in ("gspn_reserve_size", "gspn_reserve_size_norm"):
+            getattr(lib, name).argtypes = scan8 + [pi64]
+        for name in ("gspn_scan_fwd_train", "gspn_scan_fwd_norm_train"):
+            getattr(lib, name).argtypes = [vp] * 5 + scan8 + [vp, i64] + ws
+        for name in ("gspn_scan_bwd_reserve", "gspn_scan_bwd_norm_reserve"):
+            getattr(lib, name).argtypes = [vp] * 9 + scan8 + [vp, i64] + ws
         lib.gspn_project.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
         lib.gspn_latent_params.argtypes = [vp] * 7 + [i] * 6 + [vp]
         lib.gspn_latent_workspace_size.argtypes = [i] * 7 + [pi64]
@@ -155,6 +159,26 @@ def gspn_scan_bwd_reserve(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G
                           rs, rs_bytes, ws, ws_bytes, stream) -> int:
     return load().gspn_scan_bwd_reserve(x, w, lam, u, dy, dx, dw, dlam, du, direction, B, C, G,
                                         H, W, dtype, rs, rs_bytes, ws, ws_bytes, stream)
+
+
+def gspn_reserve_size_norm(direction, B, C, G, H, W, dtype):
+    """(status, bytes) of gspn_reserve_size_norm."""
+    n = ctypes.c_int64(0)
+    st = load().gspn_reserve_size_norm(direction, B, C, G, H, W, dtype, ctypes.byref(n))
+    return st, n.value
+
+
+def gspn_scan_fwd_norm_train(x, w_logits, lam, u, y, direction, B, C, G, H, W, dtype, rs,
+                             rs_bytes, ws, ws_bytes, stream) -> int:
+    return load().gspn_scan_fwd_norm_train(x, w_logits, lam, u, y, direction, B, C, G, H, W,
+                                           dtype, rs, rs_bytes, ws, ws_bytes, stream)
+
+
+def gspn_scan_bwd_norm_reserve(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du, direction, B,
+                               C, G, H, W, dtype, rs, rs_bytes, ws, ws_bytes, stream) -> int:
+    return load().gspn_scan_bwd_norm_reserve(x, w_logits, lam, u, dy, dx, dw_logits, dlam, du,
+                                             direction, B, C, G, H, W, dtype, rs, rs_bytes, ws,
+                                             ws_bytes, stream)
 
 
 def gspn_workspace_size_slots(slots, direction, B, C, G, H, W, dtype):
@@ -318,10 +342,11 @@ def _scan(op, x, w, lam, u, direction, outs, dy=None, stream=None, workspace=Non
     fn = {OP_FWD: gspn_scan_fwd, OP_BWD: gspn_scan_bwd, OP_FWD_BLOCKED: gspn_scan_fwd_blocked,
           OP_BWD_BLOCKED: gspn_scan_bwd_blocked, OP_FWD_NORM: gspn_scan_fwd_norm,
           OP_BWD_NORM: gspn_scan_bwd_norm, OP_FWD_TRAIN: gspn_scan_fwd_train,
-          OP_BWD_RESERVE: gspn_scan_bwd_reserve}[op]
+          OP_BWD_RESERVE: gspn_scan_bwd_reserve, OP_FWD_NORM_TRAIN: gspn_scan_fwd_norm_train,
+          OP_BWD_NORM_RESERVE: gspn_scan_bwd_norm_reserve}[op]
     if slots:
         fn = lambda *a: gspn_scan_bwd_slots(slots, *a)          # noqa: E731
-    if op in (OP_FWD_TRAIN, OP_BWD_RESERVE):
+    if op in (OP_FWD_TRAIN, OP_BWD_RESERVE, OP_FWD_NORM_TRAIN, OP_BWD_NORM_RESERVE):
         rp, rn = (reserve.data_ptr(), reserve.numel()) if reserve is not None else (None, 0)
         fn0 = fn
         fn = lambda *a: fn0(*a[:-3], rp, rn, *a[-3:])            # noqa: E731
@@ -371,12 +396,28 @@ def scan_bwd(x, w, lam, u, dy, direction: int = ALL, out=None, stream=None, layo
     return out
 
 
-def reserve_size(x, w, direction) -> int:
-    """Bytes of the reserve of the training pair for these tensors."""
+def reserve_size(x, w, direction, norm: bool = False) -> int:
+    """Bytes of the reserve of the training pair for these tensors (norm: the
+    pair of the _norm entry points, w holding the logits)."""
     B, C, G, H, W = _sizes(x, w, direction)
-    st, n = gspn_reserve_size(direction, B, C, G, H, W, _dtype_code(x))
+    st, n = (gspn_reserve_size_norm if norm else gspn_reserve_size)(direction, B, C, G, H, W,
+                                                                     _dtype_code(x))
     _check_raise(st)
     return n
+
+
+def _train_fwd(op, x, w, lam, u, direction, y, reserve, stream, workspace):
+    import torch
+    if y is None:
+        y = torch.empty_like(x)
+    n = reserve_size(x, w, direction, norm=op == OP_FWD_NORM_TRAIN)
+    if n == 0:
+        reserve = None
+    elif reserve is None or reserve.numel() < n:
+        reserve = torch.empty(n, dtype=torch.uint8, device=x.device)
+    _scan(op, x, w, lam, u, direction, (y,), stream=stream, workspace=workspace,
+          reserve=reserve)
+    return y, reserve
 
 
 def scan_fwd_train(x, w, lam, u, direction: int = ALL, y=None, reserve=None, stream=None,
@@ -385,19 +426,28 @@ def scan_fwd_train(x, w, lam, u, direction: int = ALL, y=None, reserve=None, str
     scan_bwd_reserve, reads.  Returns (y, reserve); `reserve`: a uint8 device
     tensor of at least reserve_size bytes, or None for a new one (None is
     returned where the shape needs no reserve)."""
+    return _train_fwd(OP_FWD_TRAIN, x, w, lam, u, direction, y, reserve, stream, workspace)
+
+
+def scan_fwd_norm_train(x, w_logits, lam, u, direction: int = ALL, y=None, reserve=None,
+                        stream=None, workspace=None):
+    """scan_fwd_norm that also fills the reserve scan_bwd_norm_reserve reads
+    (the formed weights among it).  Returns (y, reserve) as scan_fwd_train."""
+    return _train_fwd(OP_FWD_NORM_TRAIN, x, w_logits, lam, u, direction, y, reserve, stream,
+                      workspace)
+
+
+def scan_bwd_norm_reserve(x, w_logits, lam, u, dy, reserve, direction: int = ALL, out=None,
+                          stream=None, workspace=None):
+    """scan_bwd_norm reading the reserve that scan_fwd_norm_train wrote for
+    the same x, logits, lam, u; returns (dx, dw_logits, dlam, du)."""
     import torch
-    if y is None:
-        y = torch.empty_like(x)
-    n = reserve_size(x, w, direction)
-    if n == 0:
-        reserve = None
-    elif reserve is None or reserve.numel() < n:
-        reserve = torch.empty(n, dtype=torch.uint8, device=x.device)
-    elif reserve.device != x.device or reserve.dtype != torch.uint8 or not reserve.is_contiguous():
-        raise ValueError("reserve must be a contiguous uint8 tensor on the inputs' device")
-    _scan(OP_FWD_TRAIN, x, w, lam, u, direction, (y,), stream=stream, workspace=workspace,
-          reserve=reserve)
-    return y, reserve
+    if out is None:
+        out = (torch.empty_like(x), torch.empty_like(w_logits), torch.empty_like(lam),
+               torch.empty_like(u))
+    _scan(OP_BWD_NORM_RESERVE, x, w_logits, lam, u, direction, out, dy=dy, stream=stream,
+          workspace=workspace, reserve=reserve)
+    return out
 
 
 def scan_bwd_reserve(x, w, lam, u, dy, reserve, direction: int = ALL, out=None, stream=None,

@@ -129,7 +129,7 @@ int scan_buffers(int op, const void *x, const void *w, const void *lam, const vo
     const int64_t n = (int64_t)B * C * H * W;
     const int64_t nw = D * B * G * 3 * H * W;
     const bool bwd = op == GSPN_OP_BWD || op == GSPN_OP_BWD_NORM || op == GSPN_OP_BWD_BLOCKED ||
-                     op == GSPN_OP_BWD_RESERVE;
+                     op == GSPN_OP_BWD_RESERVE || op == GSPN_OP_BWD_NORM_RESERVE;
     int k = 0;
     bufs[k++] = {x, n * es, false};
     bufs[k++] = {w, nw * es, false};
@@ -148,10 +148,14 @@ int scan_buffers(int op, const void *x, const void *w, const void *lam, const vo
     return GSPN_OK;
 }
 
-bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_RESERVE; }
+bool valid_op(int op) { return op >= GSPN_OP_FWD && op <= GSPN_OP_BWD_NORM_RESERVE; }
 
 // The operations of a training pair, which keep blocked copies in a reserve.
-bool reserve_op(int op) { return op == GSPN_OP_FWD_TRAIN || op == GSPN_OP_BWD_RESERVE; }
+bool reserve_op(int op)
+{
+    return op == GSPN_OP_FWD_TRAIN || op == GSPN_OP_BWD_RESERVE || op == GSPN_OP_FWD_NORM_TRAIN ||
+           op == GSPN_OP_BWD_NORM_RESERVE;
+}
 
 // Pixel-major calls on the register-streamed shapes read their weights in
 // the blocked order: the _norm passes form them there directly from the
@@ -167,59 +171,52 @@ hipError_t run_scan(int op, const Problem &p0, const void *w_in, void *dw_out, h
     Workspace &ws = *p.ws;
     const int64_t es = p.dtype == GSPN_F32 ? 4 : 2;
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * p.H * p.W;
-    switch (op) {
-    case GSPN_OP_FWD:
-    case GSPN_OP_FWD_BLOCKED:
-        return dispatch_fwd(p, s);
-    case GSPN_OP_BWD:
-    case GSPN_OP_BWD_BLOCKED:
-        return dispatch_bwd(p, s);
-    case GSPN_OP_FWD_TRAIN:
-        p.rs_write = true;
-        return dispatch_fwd(p, s);
-    case GSPN_OP_BWD_RESERVE:
-        p.rs_read = true;
-        return dispatch_bwd(p, s);
-    case GSPN_OP_FWD_NORM: {
-        // weights from their logits into the workspace, then the scan
-        void *w = nullptr;
-        hipError_t e = ws.take(&w, (size_t)(nw * es));
-        if (e != hipSuccess)
-            return e;
-        p.w = w;
+    const bool bwd = op == GSPN_OP_BWD || op == GSPN_OP_BWD_BLOCKED || op == GSPN_OP_BWD_NORM ||
+                     op == GSPN_OP_BWD_RESERVE || op == GSPN_OP_BWD_NORM_RESERVE;
+    const bool norm = op == GSPN_OP_FWD_NORM || op == GSPN_OP_BWD_NORM ||
+                      op == GSPN_OP_FWD_NORM_TRAIN || op == GSPN_OP_BWD_NORM_RESERVE;
+    if (norm)
         p.w_blocked = norm_fused(p);
-        if (!ws.counting) {
-            e = p.w_blocked ? launch_norm_blocked(p, w_in, w, s)
-                            : launch_norm(p, w_in, nullptr, w, s);
-            if (e != hipSuccess)
-                return e;
-        }
-        return dispatch_fwd(p, s);
-    }
-    default: {   // GSPN_OP_BWD_NORM
-        // the weights, then the gradient with respect to them, then the
-        // logits' gradient
-        void *w = nullptr, *dw = nullptr;
-        hipError_t e = ws.take(&w, (size_t)(nw * es));
-        if (e == hipSuccess)
-            e = ws.take(&dw, (size_t)(nw * es));
+    // A training pair on the shapes whose backward re-lays out its inputs
+    // keeps the copies in its reserve; the parts are taken here, once, in
+    // the same order for both calls.
+    ReserveParts r;
+    if (p.rs != nullptr && p.layout == kPixelMajor && med_supported(p)) {
+        const hipError_t e = take_reserve(p, &r);
         if (e != hipSuccess)
             return e;
-        p.w = w;
+        p.rsp = &r;
+        (bwd ? p.rs_read : p.rs_write) = true;
+    }
+    if (!norm)
+        return bwd ? dispatch_bwd(p, s) : dispatch_fwd(p, s);
+
+    // Weights from their logits: formed into the reserve where a training
+    // pair keeps them (its backward then finds them formed), else into the
+    // workspace; the backward's weight gradient, then the logits' gradient.
+    const bool kept = p.rsp != nullptr && p.w_blocked;
+    void *w = kept ? r.w : nullptr, *dw = nullptr;
+    hipError_t e = hipSuccess;
+    if (!kept)
+        e = ws.take(&w, (size_t)(nw * es));
+    if (e == hipSuccess && bwd)
+        e = ws.take(&dw, (size_t)(nw * es));
+    if (e != hipSuccess)
+        return e;
+    p.w = w;
+    if (bwd)
         p.dw = dw;
-        p.w_blocked = norm_fused(p);
-        if (!ws.counting) {
-            e = p.w_blocked ? launch_norm_blocked(p, w_in, w, s)
-                            : launch_norm(p, w_in, nullptr, w, s);
-            if (e != hipSuccess)
-                return e;
-        }
-        e = dispatch_bwd(p, s);
-        if (e != hipSuccess || ws.counting)
+    if (!ws.counting && !(kept && bwd)) {
+        e = p.w_blocked ? launch_norm_blocked(p, w_in, w, s) : launch_norm(p, w_in, nullptr, w, s);
+        if (e != hipSuccess)
             return e;
-        return launch_norm(p, w_in, p.dw, dw_out, s);
     }
-    }
+    if (!bwd)
+        return dispatch_fwd(p, s);
+    e = dispatch_bwd(p, s);
+    if (e != hipSuccess || ws.counting)
+        return e;
+    return launch_norm(p, w_in, p.dw, dw_out, s);
 }
 
 // Counts the workspace (and for a training pair the reserve) of a checked
@@ -271,7 +268,7 @@ int scan_call(int op, const void *x, const void *w, const void *lam, const void 
         // written by the forward of a training pair, read by its backward
         if (reserve == nullptr || reserve_bytes < rneed)
             return GSPN_ERR_WORKSPACE;
-        bufs[nb++] = {reserve, rneed, op == GSPN_OP_FWD_TRAIN};
+        bufs[nb++] = {reserve, rneed, op == GSPN_OP_FWD_TRAIN || op == GSPN_OP_FWD_NORM_TRAIN};
     }
     if (need > 0) {
         if (workspace == nullptr || workspace_bytes < need)
@@ -368,8 +365,11 @@ extern "C" int gspn_scan_bwd(const void *x, const void *w, const void *lam, cons
                      G, H, W, dtype, workspace, workspace_bytes, stream);
 }
 
-extern "C" int gspn_reserve_size(int direction, int B, int C, int G, int H, int W, int dtype,
-                                 int64_t *bytes)
+namespace gspn {
+namespace {
+
+int reserve_query(int op, int direction, int B, int C, int G, int H, int W, int dtype,
+                  int64_t *bytes)
 {
     if (bytes == nullptr)
         return GSPN_ERR_NULL;
@@ -380,7 +380,45 @@ extern "C" int gspn_reserve_size(int direction, int B, int C, int G, int H, int 
     Problem p{nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
               nullptr, direction, B, C, G, H, W, dtype, kPixelMajor, nullptr};
     int64_t ws = 0;
-    return count_workspace(GSPN_OP_FWD_TRAIN, p, &ws, bytes);
+    return count_workspace(op, p, &ws, bytes);
+}
+
+}  // namespace
+}  // namespace gspn
+
+extern "C" int gspn_reserve_size(int direction, int B, int C, int G, int H, int W, int dtype,
+                                 int64_t *bytes)
+{
+    return reserve_query(GSPN_OP_FWD_TRAIN, direction, B, C, G, H, W, dtype, bytes);
+}
+
+extern "C" int gspn_reserve_size_norm(int direction, int B, int C, int G, int H, int W, int dtype,
+                                      int64_t *bytes)
+{
+    return reserve_query(GSPN_OP_FWD_NORM_TRAIN, direction, B, C, G, H, W, dtype, bytes);
+}
+
+extern "C" int gspn_scan_fwd_norm_train(const void *x, const void *w_logits, const void *lam,
+                                        const void *u, void *y, int direction, int B, int C,
+                                        int G, int H, int W, int dtype, void *reserve,
+                                        int64_t reserve_bytes, void *workspace,
+                                        int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_FWD_NORM_TRAIN, x, w_logits, lam, u, nullptr, y, nullptr, nullptr,
+                     nullptr, nullptr, direction, B, C, G, H, W, dtype, workspace,
+                     workspace_bytes, stream, 0, reserve, reserve_bytes);
+}
+
+extern "C" int gspn_scan_bwd_norm_reserve(const void *x, const void *w_logits, const void *lam,
+                                          const void *u, const void *dy, void *dx,
+                                          void *dw_logits, void *dlam, void *du, int direction,
+                                          int B, int C, int G, int H, int W, int dtype,
+                                          const void *reserve, int64_t reserve_bytes,
+                                          void *workspace, int64_t workspace_bytes, void *stream)
+{
+    return scan_call(GSPN_OP_BWD_NORM_RESERVE, x, w_logits, lam, u, dy, nullptr, dx, dw_logits,
+                     dlam, du, direction, B, C, G, H, W, dtype, workspace, workspace_bytes,
+                     stream, 0, const_cast<void *>(reserve), reserve_bytes);
 }
 
 extern "C" int gspn_scan_fwd_train(const void *x, const void *w, const void *lam, const void *u,

@@ -35,6 +35,14 @@ struct Workspace {
 // Layout of the per-direction tensors (lam, u, w and their gradients).
 enum Layout { kBlocked = 0, kPixelMajor = 1 };
 
+// The blocked copies a training pair keeps in its reserve (take_reserve):
+// the weights (all directions, or with one channel per group only the
+// horizontal directions' ones), and lambda and u of the horizontal
+// directions.  Null where a piece has no element.
+struct ReserveParts {
+    void *w = nullptr, *lamh = nullptr, *uh = nullptr;
+};
+
 struct Problem {
     const void *x, *w, *lam, *u, *dy;
     void *y, *dx, *dw, *dlam, *du;
@@ -50,24 +58,21 @@ struct Problem {
     // Reserve of a training pair (pixel-major register-streamed shapes): the
     // forward writes into it the blocked copies that the backward of the same
     // inputs would otherwise make (rs_write), the backward reads them from
-    // it (rs_read).  Both take the copies from it in the order of
-    // take_reserve, so that their offsets agree; counting mode sizes it.
+    // it (rs_read).  The entry point takes the parts once (take_reserve, the
+    // same order for both calls, so that their offsets agree; counting mode
+    // sizes it) and hands them over in rsp.
     Workspace *rs = nullptr;
     bool rs_write = false, rs_read = false;
+    const ReserveParts *rsp = nullptr;
 };
 
-// The blocked copies a training pair keeps in its reserve: the weights (all
-// directions, or with one channel per group only the horizontal directions'
-// ones), and lambda and u of the horizontal directions.  Null where a piece
-// has no element.
-struct ReserveParts {
-    void *w = nullptr, *lamh = nullptr, *uh = nullptr;
-};
+// Takes the reserve's parts from p.rs.  Weights the library forms itself
+// (w_blocked) are kept for every direction.
 inline hipError_t take_reserve(const Problem &p, ReserveParts *r)
 {
     const int64_t HW = (int64_t)p.H * p.W;
     const int nvd = __builtin_popcount(p.mask & 3), nhd = __builtin_popcount(p.mask & 12);
-    const bool pc = p.C == p.G;
+    const bool pc = p.C == p.G && !p.w_blocked;
     const int64_t nw = (int64_t)(pc ? nhd : nvd + nhd) * p.B * p.G * 3 * HW;
     const int64_t nh = (int64_t)nhd * p.B * p.C * HW;
     hipError_t e = hipSuccess;

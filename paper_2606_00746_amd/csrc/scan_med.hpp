@@ -1403,13 +1403,11 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
     const int64_t nh = (int64_t)nhd * p.B * p.C * H * W;
     void *wb = const_cast<void *>(p.w), *lamh = nullptr, *uh = nullptr;
     hipError_t e = hipSuccess;
-    if (p.rs_read) {
-        ReserveParts r;
-        e = take_reserve(p, &r);
-        if (r.w != nullptr)
-            wb = r.w;
-        lamh = r.lamh;
-        uh = r.uh;
+    if (p.rs_read && p.rsp != nullptr) {
+        if (p.rsp->w != nullptr)
+            wb = p.rsp->w;
+        lamh = p.rsp->lamh;
+        uh = p.rsp->uh;
     } else {
         if (!p.w_blocked && nw > 0)
             e = p.ws->take(&wb, (size_t)nw * 2);
@@ -1423,7 +1421,7 @@ hipError_t bwd_med_l(const Problem &p, hipStream_t st)
         e = p.ws->take(&dwh, (size_t)nw * 2);
     if (e != hipSuccess)
         return e;
-    if (!p.ws->counting && !p.rs_read) {
+    if (!p.ws->counting && !(p.rs_read && p.rsp != nullptr)) {
         if (pc)
             e = nw > 0 ? launch_planes_to_blocked(
                              static_cast<const bf16_t *>(p.w) + (int64_t)nvd * p.B * p.G * 3 * H * W,

@@ -525,13 +525,12 @@ template <int S>
 hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
 {
     // a training forward leaves the blocked copies of its backward in the
-    // reserve: the weights' re-layout writes there, the kernel the rest
+    // reserve (parts taken by the entry point): the weights' re-layout
+    // writes there, the kernel the rest
     ReserveParts r;
     hipError_t e = hipSuccess;
-    if (p.rs_write)
-        e = take_reserve(p, &r);
-    if (e != hipSuccess)
-        return e;
+    if (p.rs_write && p.rsp != nullptr)
+        r = *p.rsp;
     // one channel per group: the weights are staged with the channel's
     // other planes (no copy); else re-laid out once for the group's channels
     if (p.C == p.G && !p.w_blocked)
@@ -539,7 +538,7 @@ hipError_t fwd_pm_t(const Problem &p, hipStream_t st)
     const int64_t nw = (int64_t)__builtin_popcount(p.mask) * p.B * p.G * 3 * S * S;
     void *wb = const_cast<void *>(p.w);
     if (!p.w_blocked) {
-        if (p.rs_write)
+        if (p.rs_write && p.rsp != nullptr)
             wb = r.w;
         else
             e = p.ws->take(&wb, (size_t)nw * 2);

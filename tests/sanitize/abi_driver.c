@@ -151,7 +151,7 @@ static void check_queries(void)
     static const int dirs[] = {15, 1, 2, 4, 8, 6, 9};
     for (size_t s = 0; s < sizeof(shapes) / sizeof(shapes[0]); ++s)
         for (int c = 0; c < 5; ++c)
-            for (int op = 0; op < 6; ++op)
+            for (int op = 0; op <= GSPN_OP_BWD_NORM_RESERVE; ++op)
                 for (size_t d = 0; d < sizeof(dirs) / sizeof(dirs[0]); ++d) {
                     int64_t n1 = -1, n2 = -2;
                     const int st = gspn_workspace_size(op, dirs[d], 2, groups[c][0], groups[c][1],
@@ -167,7 +167,46 @@ static void check_queries(void)
                     }
                 }
     int64_t n = 0;
-    EXPECT(gspn_workspace_size(9, 15, 1, 4, 2, 8, 8, GSPN_BF16, &n), GSPN_ERR_UNSUPPORTED);
+    EXPECT(gspn_workspace_size(GSPN_OP_BWD_NORM_RESERVE + 1, 15, 1, 4, 2, 8, 8, GSPN_BF16, &n),
+           GSPN_ERR_UNSUPPORTED);
+    /* the training pairs' reserves: sizes and host checks */
+    for (size_t s = 0; s < sizeof(shapes) / sizeof(shapes[0]); ++s)
+        for (int c = 0; c < 5; ++c) {
+            int64_t r1 = -1, r2 = -1;
+            EXPECT(gspn_reserve_size(15, 2, groups[c][0], groups[c][1], shapes[s][0],
+                                     shapes[s][1], shapes[s][2], &r1),
+                   GSPN_OK);
+            EXPECT(gspn_reserve_size_norm(15, 2, groups[c][0], groups[c][1], shapes[s][0],
+                                          shapes[s][1], shapes[s][2], &r2),
+                   GSPN_OK);
+            if (r1 < 0 || r2 < r1) {
+                fprintf(stderr, "reserve %dx%d: %lld, norm %lld\n", shapes[s][0], shapes[s][1],
+                        (long long)r1, (long long)r2);
+                ++failures;
+            }
+        }
+    {
+        int64_t rn = 0, wn = 0;
+        EXPECT(gspn_reserve_size(15, 1, 64, 2, 64, 64, GSPN_BF16, &rn), GSPN_OK);
+        EXPECT(gspn_workspace_size(GSPN_OP_BWD_RESERVE, 15, 1, 64, 2, 64, 64, GSPN_BF16, &wn),
+               GSPN_OK);
+        void *t[12];
+        for (int i = 0; i < 12; ++i)
+            t[i] = fake(i + 128, 1u << 26, 0);
+        EXPECT(gspn_scan_fwd_train(t[0], t[1], t[2], t[3], t[4], 15, 1, 64, 2, 64, 64, GSPN_BF16,
+                                   NULL, 0, NULL, 0, NULL),
+               GSPN_ERR_WORKSPACE);
+        EXPECT(gspn_scan_fwd_train(t[0], t[1], t[2], t[3], t[4], 15, 1, 64, 2, 64, 64, GSPN_BF16,
+                                   t[0], rn, NULL, 0, NULL),
+               GSPN_ERR_ALIAS);
+        EXPECT(gspn_scan_bwd_reserve(t[0], t[1], t[2], t[3], t[4], t[5], t[6], t[7], t[8], 15, 1,
+                                     64, 2, 64, 64, GSPN_BF16, t[9], rn - 16, t[10], wn, NULL),
+               GSPN_ERR_WORKSPACE);
+        EXPECT(gspn_scan_bwd_norm_reserve(t[0], t[1], t[2], t[3], t[4], t[5], t[6], t[7], t[8],
+                                          15, 1, 64, 2, 64, 64, GSPN_BF16, t[9], -1, t[10], wn,
+                                          NULL),
+               GSPN_ERR_WORKSPACE);
+    }
     EXPECT(gspn_workspace_size(GSPN_OP_FWD, 15, 1, 4, 2, 8, 8, GSPN_BF16, NULL), GSPN_ERR_NULL);
     EXPECT(gspn_workspace_size(GSPN_OP_BWD, 15, 1 << 20, 1 << 10, 1, 4096, 4096, GSPN_BF16, &n),
            GSPN_ERR_UNSUPPORTED);

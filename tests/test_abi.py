@@ -137,7 +137,8 @@ def test_workspace_size_query():
     # the same checks as the calls
     assert g.gspn_workspace_size(g.OP_FWD, 0, 1, 4, 2, 8, 8, g.BF16)[0] == _native.ERR_DIRECTION
     assert g.gspn_workspace_size(g.OP_FWD, 15, 1, 6, 4, 8, 8, g.BF16)[0] == _native.ERR_DIM
-    assert g.gspn_workspace_size(9, 15, 1, 4, 2, 8, 8, g.BF16)[0] == _native.ERR_UNSUPPORTED
+    for bad in (10, -1):
+        assert g.gspn_workspace_size(bad, 15, 1, 4, 2, 8, 8, g.BF16)[0] == _native.ERR_UNSUPPORTED
 
 
 # one shape per kernel family and storage type (tiny, register-resident small,
@@ -155,7 +156,7 @@ def test_workspace_query_launches_nothing(H, W, dt):
     single-group, a grouped and a per-channel-weight case must come back OK."""
     dtype = g.BF16 if dt == "bf16" else g.F32
     for C, G in ((4, 1), (64, 2), (8, 8)):
-        for op in range(8):
+        for op in range(10):
             for dirs in (15, 1, 6):
                 st, n = g.gspn_workspace_size(op, dirs, 2, C, G, H, W, dtype)
                 assert st == _native.OK and n >= 0, (H, W, dt, C, G, op, dirs, st)
@@ -355,3 +356,32 @@ def test_training_pair_reserve():
     assert bwd(far(10), need, far(10), nb) == _native.ERR_ALIAS    # over the workspace
     assert g.gspn_scan_fwd_train(None, *fwd_ptrs[1:], *args, far(10), need, None, 0,
                                  None) == _native.ERR_NULL
+
+
+def test_norm_training_pair_reserve():
+    """The _norm pair keeps the weights it forms for every direction (also
+    with one channel per group, where the plain pair copies only the
+    horizontal ones) plus the horizontal lambda and u; its forward takes no
+    workspace, its backward only the weight gradient and the partials."""
+    def size(dirs, B, C, G, H, W):
+        st, n = g.gspn_reserve_size_norm(dirs, B, C, G, H, W, g.BF16)
+        assert st == _native.OK
+        return n
+    HW = 64 * 64
+    assert size(15, 1, 64, 2, 64, 64) == g.gspn_reserve_size(15, 1, 64, 2, 64, 64, g.BF16)[1]
+    assert size(15, 1, 16, 16, 64, 64) == 4 * 16 * 3 * HW * 2 + 2 * (2 * 16 * HW * 2)
+    assert size(3, 1, 16, 16, 64, 64) == 2 * 16 * 3 * HW * 2
+    assert size(15, 2, 8, 2, 14, 14) == 0
+    args = (15, 1, 64, 2, 64, 64, g.BF16)
+    assert g.gspn_workspace_size(g.OP_FWD_NORM_TRAIN, *args) == (_native.OK, 0)
+    st, nb = g.gspn_workspace_size(g.OP_BWD_NORM_RESERVE, *args)
+    st0, nb0 = g.gspn_workspace_size(g.OP_BWD_NORM, *args)
+    assert st == st0 == _native.OK and nb0 - nb == size(*args[:6])
+    far = lambda i: BASE + (1 << 34) + i * (1 << 26)     # noqa: E731
+    need = size(*args[:6])
+    assert g.gspn_scan_fwd_norm_train(*[far(i) for i in range(5)], *args, None, 0, None, 0,
+                                      None) == _native.ERR_WORKSPACE
+    assert g.gspn_scan_bwd_norm_reserve(*[far(i) for i in range(9)], *args, far(10), need - 1,
+                                        far(11), nb, None) == _native.ERR_WORKSPACE
+    assert g.gspn_scan_bwd_norm_reserve(*[far(i) for i in range(9)], *args, far(6), need,
+                                        far(11), nb, None) == _native.ERR_ALIAS

@@ -158,3 +158,48 @@ def test_front_end_checks_the_reserve():
     with pytest.raises(gspn.GspnError, match="workspace"):
         gspn.scan_bwd_reserve(*args, None, wl.dirs)
     torch.cuda.synchronize()
+
+
+NORM_CASES = [CASES[0], CASES[1], CASES[2], CASES[4], CASES[7],
+              case("24-G=C-dirs5", 2, 5, 5, 24, 24, dirs=5), NO_RESERVE[0]]
+
+
+def run_norm_pairs(t, wt, wl, torch):
+    y0 = gspn.scan_fwd_norm(t["x"], wt, t["lam"], t["u"], wl.dirs)
+    g0 = gspn.scan_bwd_norm(t["x"], wt, t["lam"], t["u"], t["dy"], wl.dirs)
+    y1, rs = gspn.scan_fwd_norm_train(t["x"], wt, t["lam"], t["u"], wl.dirs)
+    n = gspn.workspace_size(gspn.OP_BWD_NORM_RESERVE, t["x"], wt, wl.dirs)
+    ws = torch.full((max(n, 1),), 0xFF, dtype=torch.uint8, device="cuda")
+    g1 = gspn.scan_bwd_norm_reserve(t["x"], wt, t["lam"], t["u"], t["dy"], rs, wl.dirs,
+                                    workspace=ws)
+    torch.cuda.synchronize()
+    return (y0, *g0), (y1, *g1), rs
+
+
+@pytest.mark.parametrize("wl", NORM_CASES, ids=lambda w: w.name)
+def test_norm_pair_matches_plain(wl):
+    """The _norm training pair (weights given as logits, the formed weights
+    kept in the reserve) against gspn_scan_fwd_norm / gspn_scan_bwd_norm, bit
+    for bit, including the logits' gradient."""
+    torch = require_gpu()
+    print(f"[case] norm train pair {wl.name} B={wl.B} C={wl.C} G={wl.G} {wl.H}x{wl.W} "
+          f"dirs={wl.dirs}", flush=True)
+    t = upload(gi.make_inputs(wl, with_dy=True), wl.dtype, wl.dirs)
+    wt = upload({"w": gi.make_logits(wl)}, wl.dtype, wl.dirs)["w"]
+    plain, train, rs = run_norm_pairs(t, wt, wl, torch)
+    n = gspn.reserve_size(t["x"], wt, wl.dirs, norm=True)
+    assert (rs is None) == (n == 0)
+    check_same(wl, plain, train)
+
+
+@pytest.mark.parametrize("idx", [3, 5], ids=["hires-64x64-b8-c768", "g768"])
+def test_norm_pair_full_size(idx):
+    torch = require_gpu()
+    wl = gi.workload(idx)
+    print(f"[case] norm train pair full size {wl.name}", flush=True)
+    t = upload(gi.make_inputs(wl, with_dy=True), wl.dtype, wl.dirs)
+    wt = upload({"w": gi.make_logits(wl)}, wl.dtype, wl.dirs)["w"]
+    plain, train, rs = run_norm_pairs(t, wt, wl, torch)
+    check_same(wl, plain, train)
+    del plain, train, rs, t, wt
+    torch.cuda.empty_cache()
