@@ -8,7 +8,10 @@ gspn_scan_fwd_train + gspn_scan_bwd_reserve (the forward leaves in a reserve
 the blocked copies its backward reads; forward-only workloads use
 gspn_scan_fwd).  The plain pair gspn_scan_fwd + gspn_scan_bwd and the _blocked
 entry points (per-direction tensors in their scan order) are timed beside it
-and reported under "plain" and "blocked".  Prints ONE JSON line on stdout:
+and reported under "plain" and "blocked".  With --norm the weights are given
+as logits and the calls are the _norm pairs (gspn_scan_fwd_norm_train +
+gspn_scan_bwd_norm_reserve, the plain _norm pair beside it).  Prints ONE
+JSON line on stdout:
 throughput in G pixel-channels per second (B*C*H*W per step), the roofline
 of the dominant kernel (algorithmic bytes / average launch time, from HIP
 events on the launch stream) and the CPU oracle timed on a bounded sample of
@@ -214,9 +217,10 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
     train = main_is_train(wl, args, gspn)
     main = time_step(wl, inputs, args, torch, gspn, args.layout, scrub, stream, train=train)
     others = []
-    if not args.norm and not args.no_blocked:
+    if not args.no_blocked:
         if train:
             others.append(time_step(wl, inputs, args, torch, gspn, gspn.PIXEL, scrub, stream))
+    if not args.norm and not args.no_blocked:
         others.append(time_step(wl, inputs, args, torch, gspn,
                                 gspn.BLOCKED if args.layout == gspn.PIXEL else gspn.PIXEL, scrub,
                                 stream))
@@ -224,9 +228,10 @@ def run_workload(wl: gi.Workload, args, torch, gspn) -> dict:
 
 
 def main_is_train(wl, args, gspn) -> bool:
-    """The headline step runs the training pair: pixel-major, plain weights,
-    a backward pass, and not turned off with --plain."""
-    return wl.backward and args.layout == gspn.PIXEL and not args.norm and not args.plain
+    """The headline step runs the training pair (with --norm, the one that
+    takes logits): pixel-major, a backward pass, and not turned off with
+    --plain."""
+    return wl.backward and args.layout == gspn.PIXEL and not args.plain
 
 
 def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream, train=False) -> dict:
@@ -240,17 +245,17 @@ def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream, train=False)
     bwd_call = gspn.scan_bwd_norm if args.norm else gspn.scan_bwd
     if train:
         # the reserve, like the workspace, is taken once: a training loop keeps it
-        nrs = gspn.reserve_size(dev["x"], dev["w"], wl.dirs)
+        nrs = gspn.reserve_size(dev["x"], dev["w"], wl.dirs, norm=args.norm)
         rsv = torch.empty(max(nrs, 1), dtype=torch.uint8, device="cuda")
         log(f"training pair: reserve {nrs} bytes")
+        fwd_train = gspn.scan_fwd_norm_train if args.norm else gspn.scan_fwd_train
+        bwd_reserve = gspn.scan_bwd_norm_reserve if args.norm else gspn.scan_bwd_reserve
 
         def fwd_call(x, w, lam, u, dirs, y, stream, workspace):
-            gspn.scan_fwd_train(x, w, lam, u, dirs, y=y, reserve=rsv, stream=stream,
-                                workspace=workspace)
+            fwd_train(x, w, lam, u, dirs, y=y, reserve=rsv, stream=stream, workspace=workspace)
 
         def bwd_call(x, w, lam, u, dy, dirs, out, stream, workspace):
-            gspn.scan_bwd_reserve(x, w, lam, u, dy, rsv, dirs, out=out, stream=stream,
-                                  workspace=workspace)
+            bwd_reserve(x, w, lam, u, dy, rsv, dirs, out=out, stream=stream, workspace=workspace)
         kw = {}
     y = torch.empty_like(x)
     if wl.backward:
@@ -258,7 +263,8 @@ def time_step(wl, inputs, args, torch, gspn, layout, scrub, stream, train=False)
         grads = (torch.empty_like(x), torch.empty_like(w), torch.empty_like(lam),
                  torch.empty_like(u))
     # the calls' workspace, taken once (a caller that keeps it allocates nothing per call)
-    ops = ((gspn.OP_FWD_NORM, gspn.OP_BWD_NORM) if args.norm else
+    ops = ((gspn.OP_FWD_NORM_TRAIN, gspn.OP_BWD_NORM_RESERVE) if args.norm and train else
+           (gspn.OP_FWD_NORM, gspn.OP_BWD_NORM) if args.norm else
            (gspn.OP_FWD_TRAIN, gspn.OP_BWD_RESERVE) if train else
            (gspn.OP_FWD, gspn.OP_BWD) if layout == gspn.PIXEL else
            (gspn.OP_FWD_BLOCKED, gspn.OP_BWD_BLOCKED))
@@ -337,19 +343,18 @@ def summarize(wl, inputs, args, torch, main, others, scrub) -> dict:
         f"({step_gbs / HBM_PEAK_GBS:.1%} of peak)")
 
     train = main["name"] == "train"
+    fwd_name, bwd_name = call_names(args.norm, train, wl.backward)
     if bwd_ms > fwd_ms:
-        dom, call, dom_ms, dom_bytes = ("gspn_scan_bwd_reserve" if train else "gspn_scan_bwd",
-                                        "bwd", bwd_ms, nbytes["bwd"])
+        dom, call, dom_ms, dom_bytes = bwd_name, "bwd", bwd_ms, nbytes["bwd"]
     else:
-        dom, call, dom_ms, dom_bytes = ("gspn_scan_fwd_train" if train else "gspn_scan_fwd",
-                                        "fwd", fwd_ms, nbytes["fwd"])
+        dom, call, dom_ms, dom_bytes = fwd_name, "fwd", fwd_ms, nbytes["fwd"]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     # measured HBM bytes of the same call (FETCH_SIZE + WRITE_SIZE counters, scaled by a
     # plain copy), kept in profiles/ for the current kernel sources only
     from paper_2606_00746_amd import profiling
-    traffic = None if args.norm else profiling.load_traffic(
-        os.path.join(ROOT, "profiles",
-                     f"traffic_{wl.name}-{'pair' if train else args.layout}.txt"), call)
+    tag = ("logits-" if args.norm else "") + ("pair" if train else args.layout)
+    traffic = profiling.load_traffic(
+        os.path.join(ROOT, "profiles", f"traffic_{wl.name}-{tag}.txt"), call)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                 "traffic": traffic,
@@ -384,10 +389,7 @@ def summarize(wl, inputs, args, torch, main, others, scrub) -> dict:
                    "storage": wl.dtype, "weights": "logits" if args.norm else "normalized",
                    "layout": ("pixel-major [D][B][C][H][W] / [D][B][G][3][H][W]"
                               if args.layout == "pixel" else "blocked line-major"),
-                   "calls": ("gspn_scan_fwd_train + gspn_scan_bwd_reserve" if train else
-                             "gspn_scan_fwd_norm + gspn_scan_bwd_norm" if args.norm else
-                             "gspn_scan_fwd + gspn_scan_bwd" if wl.backward else
-                             "gspn_scan_fwd"),
+                   "calls": " + ".join(c for c in (fwd_name, bwd_name) if c),
                    "parallelism": "single GPU"},
         "fwd_ms": round(fwd_ms, 5),
         "bwd_ms": round(bwd_ms, 5),
@@ -420,6 +422,17 @@ def summarize(wl, inputs, args, torch, main, others, scrub) -> dict:
         out["cpu_baseline_single_thread"] = cpu_baseline(wl, inputs, args.cpu_seconds / 2,
                                                          args.norm)
     return out
+
+
+def call_names(norm: bool, train: bool, backward: bool):
+    """The entry points of the headline step: (forward, backward or None)."""
+    if train:
+        pair = (("gspn_scan_fwd_norm_train", "gspn_scan_bwd_norm_reserve") if norm else
+                ("gspn_scan_fwd_train", "gspn_scan_bwd_reserve"))
+    else:
+        pair = (("gspn_scan_fwd_norm", "gspn_scan_bwd_norm") if norm else
+                ("gspn_scan_fwd", "gspn_scan_bwd"))
+    return pair[0], (pair[1] if backward else None)
 
 
 LATENT_METRIC = ("C-GSPN latent sublayer fwd Gpix·ch/s (input pixel-channels) at 1 MI355X; "
@@ -593,7 +606,8 @@ def main() -> int:
     ap.add_argument("--no-blocked", action="store_true",
                     help="time only the headline pair (no plain or blocked entries beside it)")
     ap.add_argument("--norm", action="store_true",
-                    help="weights given as logits: time gspn_scan_fwd_norm / gspn_scan_bwd_norm")
+                    help="weights given as logits: time the _norm training pair (and the "
+                         "plain gspn_scan_fwd_norm / gspn_scan_bwd_norm beside it)")
     ap.add_argument("--latent", default=None,
                     help="time the latent sublayer instead: index or name of the latent "
                          "workload, or 'all'")

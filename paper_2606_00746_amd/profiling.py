@@ -50,6 +50,9 @@ _FAMILY_SOURCES = (("_med_", _MED), ("dw_sum", _MED), ("_pm_", ("scan_pm.hip",))
 # kernels that run at the start of a call (re-layouts into the blocked order):
 # they belong to the call whose scan kernel follows them
 _PREPASS = ("to_blocked_kernel", "norm_to_blocked_kernel", "pieces_kernel")
+# the normalization kernels of the _norm calls: forming the weights at the
+# start of a call, or the logits' gradient at the end of a backward
+_NORM = ("norm_kernel", "norm_pm_kernel")
 # shared by every family: device helpers, launch declarations, the dispatch
 # and the build flags
 _COMMON_SOURCES = ("cdna.hpp", "device.hpp", "launch.hpp", "api.cpp")
@@ -137,18 +140,37 @@ def _dispatches(path: str) -> list:
 
 
 def _calls_in_order(disp: list) -> list:
-    """The library call of each dispatch: call_of for the scan kernels and
-    their sums, the next scan kernel's call for a re-layout that precedes it,
-    None for the rest."""
-    out, cur = [None] * len(disp), None
-    for n in range(len(disp) - 1, -1, -1):
-        k = short_name(disp[n][0])
-        c = call_of(k)
-        if c is not None:
-            cur = c
-            out[n] = c
-        elif k.startswith(_PREPASS):
-            out[n] = cur
+    """The library call of each dispatch, None for other kernels.  The
+    library's dispatches come in runs between other kernels (the benchmark's
+    cache flush before each step); within a run a scan kernel (call_of)
+    names its call, a kernel before a scan kernel belongs to that scan's
+    call (a re-layout or the weights' normalization at the start of a call),
+    and one after the run's last scan kernel to that kernel's call (the
+    transpose of a weight gradient, the logits' gradient at the end of a
+    backward)."""
+    def library(k):
+        return call_of(k) is not None or k.startswith(_PREPASS) or k.startswith(_NORM)
+
+    names = [short_name(k) for k, _ in disp]
+    out = [None] * len(disp)
+    n = 0
+    while n < len(names):
+        if not library(names[n]):
+            n += 1
+            continue
+        m = n
+        while m < len(names) and library(names[m]):
+            m += 1
+        nxt = None
+        for i in range(m - 1, n - 1, -1):
+            nxt = call_of(names[i]) or nxt
+            out[i] = nxt
+        last = None
+        for i in range(n, m):
+            last = call_of(names[i]) or last
+            if out[i] is None:
+                out[i] = last
+        n = m
     return out
 
 

@@ -120,3 +120,47 @@ def test_relayout_kernels_belong_to_the_call_they_precede(tmp_path):
     assert rec["bytes_per_call"]["fwd"] == (2 * 10 + 10 + 2 * 100 + 100) * 1024
     assert rec["bytes_per_call"]["bwd"] == (2 * 50 + 50 + 2 * 300 + 300) * 1024
     assert "scan_pm.hip" in rec["source_files"]
+
+
+def test_normalization_kernels_belong_to_their_calls(tmp_path):
+    # _norm calls: the weights are formed at the start of each call; the
+    # logits' gradient ends the backward (it follows the backward's scans and
+    # precedes the next step's forward, which forms its weights again)
+    copy = "__amd_rocclr_copyBuffer(char const*, char*)"
+    norm = "void gspn::(anonymous namespace)::norm_pm_kernel<unsigned short>(int)"
+    fwd = "void gspn::(anonymous namespace)::fwd_pm_kernel<64>(int)"
+    bwd = "void gspn::(anonymous namespace)::bwd_med_kernel<64, 64, 1>(int)"
+    dws = "void gspn::(anonymous namespace)::dw_sum_pm_kernel<64>(int)"
+    flush = "void at::native::reduce_kernel<512, 1>(int)"
+    step = [(flush, 999.0), (norm, 5.0), (fwd, 100.0), (norm, 7.0), (bwd, 300.0), (dws, 30.0),
+            (norm, 11.0)]
+    _csv(tmp_path / "f.csv", "FETCH_SIZE", [(copy, 2048.0)] + step * 2)
+    _csv(tmp_path / "w.csv", "WRITE_SIZE", [(copy, 4096.0)] + step * 2)
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd",
+                                   calls=2)
+    assert rec["kernels"]["norm_pm_kernel<unsigned short> [fwd]"]["dispatches_per_call"] == 1
+    assert rec["kernels"]["norm_pm_kernel<unsigned short> [bwd]"]["dispatches_per_call"] == 2
+    assert rec["bytes_per_call"]["fwd"] == (2 * 105 + 105) * 1024
+    assert rec["bytes_per_call"]["bwd"] == (2 * 348 + 348) * 1024
+    assert "scan_norm.hip" in rec["source_files"]
+
+
+def test_kernels_after_the_last_scan_belong_to_its_call(tmp_path):
+    # one channel per group: the horizontal weight gradients leave the
+    # backward's scan in the blocked order and are turned pixel-major by a
+    # re-layout launch that ends the backward; the next step's forward starts
+    # with the same kind of launch
+    copy = "__amd_rocclr_copyBuffer(char const*, char*)"
+    rel = "void gspn::(anonymous namespace)::pieces_kernel(int)"
+    fwd = "void gspn::(anonymous namespace)::fwd_pm_kernel<64>(int)"
+    bwd = "void gspn::(anonymous namespace)::bwd_med_kernel<64, 64, 1>(int)"
+    flush = "void at::native::reduce_kernel<512, 1>(int)"
+    step = [(flush, 999.0), (rel, 3.0), (fwd, 100.0), (bwd, 300.0), (rel, 20.0)]
+    _csv(tmp_path / "f.csv", "FETCH_SIZE", [(copy, 2048.0)] + step * 3)
+    _csv(tmp_path / "w.csv", "WRITE_SIZE", [(copy, 4096.0)] + step * 3)
+    rec = profiling.traffic_record(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), "wl", 4, "cmd",
+                                   calls=3)
+    assert rec["kernels"]["pieces_kernel [fwd]"]["dispatches_per_call"] == 1
+    assert rec["kernels"]["pieces_kernel [bwd]"]["dispatches_per_call"] == 1
+    assert rec["bytes_per_call"]["fwd"] == (2 * 103 + 103) * 1024
+    assert rec["bytes_per_call"]["bwd"] == (2 * 320 + 320) * 1024
