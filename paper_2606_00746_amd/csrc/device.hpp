@@ -26,20 +26,45 @@ __device__ __forceinline__ void store_f(bf16_t *p, float v)
 
 // Sec. 3, Eq. (row_stochastic_norm) for one pixel: s_k = sigmoid(t_k) on the
 // taps whose neighbour lies on the grid (on0, on2; tap 1 always), 0 on the
-// others, and w_k = s_k / max(s_0 + s_1 + s_2, kNormEps).
+// others, and w_k = s_k / max(s_0 + s_1 + s_2, kNormEps).  The reciprocals
+// are the hardware's (v_rcp_f32, within one fp32 ulp): a correctly rounded
+// division takes about ten instructions, and every kernel that normalizes
+// (the weights, their gradient, separately or inside a scan) calls these
+// same functions, so all of them agree bit for bit.
 constexpr float kNormEps = 1e-30f;
 
-__device__ __forceinline__ float sigmoid(float t) { return 1.f / (1.f + __expf(-t)); }
+__device__ __forceinline__ float sigmoid(float t)
+{
+    return __builtin_amdgcn_rcpf(1.f + __expf(-t));
+}
 
 __device__ __forceinline__ void norm3(const float (&t)[3], bool on0, bool on2, float (&w)[3])
 {
     const float s0 = on0 ? sigmoid(t[0]) : 0.f;
     const float s1 = sigmoid(t[1]);
     const float s2 = on2 ? sigmoid(t[2]) : 0.f;
-    const float inv = 1.f / fmaxf((s0 + s1) + s2, kNormEps);
+    const float inv = __builtin_amdgcn_rcpf(fmaxf((s0 + s1) + s2, kNormEps));
     w[0] = s0 * inv;
     w[1] = s1 * inv;
     w[2] = s2 * inv;
+}
+
+// Gradient with respect to the logits t of one pixel, from the gradient g
+// with respect to its weights: dt_m = s_m (1 - s_m) (g_m - sum_k w_k g_k) / S
+// (the sum term drops where the clamp holds S at kNormEps); 0 on the taps
+// off the grid.
+__device__ __forceinline__ void norm3_bwd(const float (&t)[3], const float (&g)[3], bool on0,
+                                          bool on2, float (&dt)[3])
+{
+    const float s[3] = {on0 ? sigmoid(t[0]) : 0.f, sigmoid(t[1]), on2 ? sigmoid(t[2]) : 0.f};
+    const float sum = (s[0] + s[1]) + s[2];
+    const bool clamped = sum < kNormEps;
+    const float inv = __builtin_amdgcn_rcpf(clamped ? kNormEps : sum);
+    const float inner = clamped ? 0.f : ((s[0] * inv) * g[0] + (s[1] * inv) * g[1]) + (s[2] * inv) * g[2];
+    const bool on[3] = {on0, true, on2};
+#pragma unroll
+    for (int k = 0; k < 3; ++k)
+        dt[k] = on[k] ? s[k] * (1.f - s[k]) * (g[k] - inner) * inv : 0.f;
 }
 
 // DPP lane shifts along a line of T lanes (T = 16, 32 or 64).  from_left(v)

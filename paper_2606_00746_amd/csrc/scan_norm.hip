@@ -52,21 +52,6 @@ __device__ __forceinline__ void store8(bf16_t *p, const float (&v)[8])
            make_uint4(pack2(v[0], v[1]), pack2(v[2], v[3]), pack2(v[4], v[5]), pack2(v[6], v[7])));
 }
 
-// Gradient with respect to the logits of one pixel.
-__device__ __forceinline__ void norm3_bwd(const float (&t)[3], const float (&g)[3], bool on0,
-                                          bool on2, float (&dt)[3])
-{
-    const float s[3] = {on0 ? sigmoid(t[0]) : 0.f, sigmoid(t[1]), on2 ? sigmoid(t[2]) : 0.f};
-    const float sum = (s[0] + s[1]) + s[2];
-    const bool clamped = sum < kNormEps;
-    const float inv = 1.f / (clamped ? kNormEps : sum);
-    const float inner = clamped ? 0.f : ((s[0] * inv) * g[0] + (s[1] * inv) * g[1]) + (s[2] * inv) * g[2];
-    const bool on[3] = {on0, true, on2};
-#pragma unroll
-    for (int k = 0; k < 3; ++k)
-        dt[k] = on[k] ? s[k] * (1.f - s[k]) * (g[k] - inner) * inv : 0.f;
-}
-
 // Every direction of the mask in one launch: for direction slot s, the B*G
 // tap-plane triples of HW elements, lines of P positions, L lines.
 // dw == nullptr: write the weights; else the logits' gradient.  vec: the

@@ -91,6 +91,7 @@ def _ws_bf16(ws, offset, shape):
 
 
 @pytest.mark.parametrize("wl", [case("norm-med-64x64", 1, 64, 2, 64, 64),
+                                case("norm-med-56x56-G=C-dirs13", 1, 8, 8, 56, 56, dirs=13),
                                 case("norm-tiny-14x14", 2, 12, 2, 14, 14)],
                          ids=lambda w: w.name)
 def test_norm_stores_and_outputs_within_half_ulp(wl):

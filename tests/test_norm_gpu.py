@@ -30,6 +30,11 @@ CASES = [
     # passes (the plain calls read vertical ones in place instead)
     case("med64-G=C", 1, 16, 16, 64, 64),
     case("med56-G=C-dirs6", 2, 12, 12, 56, 56, dirs=6, sigma=2.0),
+    # ... at every side of the register-streamed kernels
+    case("med48-G=C-dirs9", 1, 8, 8, 48, 48, dirs=9),
+    case("med40-G=C", 1, 8, 8, 40, 40),
+    case("med32-G=C-dirs12", 2, 6, 6, 32, 32, dirs=12, sigma=2.0),
+    case("med24-G=C-dirs3", 2, 8, 8, 24, 24, dirs=3),
     case("tiny14", 2, 24, 2, 14, 14),
     case("tiny16-R2L", 1, 8, 1, 16, 16, dirs=8, sigma=2.0),
     case("small-f32-40x24", 2, 6, 3, 40, 24, dtype="f32"),
