@@ -15,7 +15,9 @@
 // A 256 x 256 fp32 merge plane does not fit in LDS, so each direction writes
 // u_d * h_d to an fp32 plane in its own line-major order (whole lines per
 // store) and a tiled kernel sums the directions in direction-bit order,
-// transposing the horizontal ones through LDS, and stores y once.
+// transposing the horizontal ones through LDS, and stores y once.  The scan
+// and the sum alternate in rounds of planes, so that the sum finds much of
+// its round's planes still in the Infinity Cache (wide_round).
 //
 // Pixel-major per-direction tensors are first copied into the blocked order
 // of their direction in the caller's workspace (pieces_kernel: whole rows in
@@ -755,15 +757,24 @@ hipError_t launch_pieces(const void *src, void *dst, int64_t nv, int64_t nh, int
 // scans of at least 256 lines in both orientations, and at least 8 chunks,
 // the count doubling while B*C*K workgroups still fit the device at once and
 // every chunk keeps at least 2 line blocks.
-int wide_chunks(const Problem &p, size_t lds)
+// Workgroups of the single-pass forward that the device runs at once (LDS
+// bound), 0 if the device cannot be queried.
+int64_t wide_fit(size_t lds)
 {
     int dev = 0, ncu = 0;
-    const int lds_cu = kLdsBytes;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return 0;
+    const int64_t per_cu =
+        std::max<int64_t>(1, (int64_t)kLdsBytes / (int64_t)std::max<size_t>(lds, 1));
+    return (int64_t)ncu * std::min<int64_t>(per_cu, 8);
+}
+
+int wide_chunks(const Problem &p, size_t lds)
+{
+    const int64_t fit = wide_fit(lds);
+    if (fit == 0)
         return 1;
-    const int64_t per_cu = std::max<int64_t>(1, (int64_t)lds_cu / (int64_t)std::max<size_t>(lds, 1));
-    const int64_t fit = (int64_t)ncu * std::min<int64_t>(per_cu, 8);
     const int64_t planes = (int64_t)p.B * p.C;
     const int nbh = p.H / 8, nbw = p.W / 8;
     int K = 1;
@@ -773,8 +784,10 @@ int wide_chunks(const Problem &p, size_t lds)
     return (K >= 8 && nbh >= 32 && nbw >= 32) ? K : 1;
 }
 
+// The forward of planes plane0 .. plane0 + nplanes - 1 (single pass; the
+// chunked forward takes every plane).
 hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states, size_t lds, int K,
-                      const Problem *v = nullptr)
+                      int plane0, int nplanes, const Problem *v = nullptr)
 {
     const int side = p.H > p.W ? p.H : p.W;
     const int npl = (side + 63) / 64;
@@ -788,21 +801,41 @@ hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states
                : npl == 3 ? fwd_wide_chunked_t<3, 0, 0>(p, st, ys, states, lds, K)
                           : fwd_wide_chunked_t<4, 0, 0>(p, st, ys, states, lds, K);
     }
-    const int planes = p.B * p.C;
+    const int p0 = plane0, n = nplanes;
     if (v != nullptr) {
         if (p.H == 256 && p.W == 256)
-            return fwd_wide_t<4, 256, 256, true>(p, st, ys, lds, 0, planes, v);
-        return npl <= 2 ? fwd_wide_t<2, 0, 0, true>(p, st, ys, lds, 0, planes, v)
-               : npl == 3 ? fwd_wide_t<3, 0, 0, true>(p, st, ys, lds, 0, planes, v)
-                          : fwd_wide_t<4, 0, 0, true>(p, st, ys, lds, 0, planes, v);
+            return fwd_wide_t<4, 256, 256, true>(p, st, ys, lds, p0, n, v);
+        return npl <= 2 ? fwd_wide_t<2, 0, 0, true>(p, st, ys, lds, p0, n, v)
+               : npl == 3 ? fwd_wide_t<3, 0, 0, true>(p, st, ys, lds, p0, n, v)
+                          : fwd_wide_t<4, 0, 0, true>(p, st, ys, lds, p0, n, v);
     }
     if (p.H == 256 && p.W == 256)
-        return fwd_wide_t<4, 256, 256, false>(p, st, ys, lds, 0, planes, nullptr);
+        return fwd_wide_t<4, 256, 256, false>(p, st, ys, lds, p0, n, nullptr);
     if (p.H == 128 && p.W == 128)
-        return fwd_wide_t<2, 128, 128, false>(p, st, ys, lds, 0, planes, nullptr);
-    return npl <= 2 ? fwd_wide_t<2, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr)
-           : npl == 3 ? fwd_wide_t<3, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr)
-                      : fwd_wide_t<4, 0, 0, false>(p, st, ys, lds, 0, planes, nullptr);
+        return fwd_wide_t<2, 128, 128, false>(p, st, ys, lds, p0, n, nullptr);
+    return npl <= 2 ? fwd_wide_t<2, 0, 0, false>(p, st, ys, lds, p0, n, nullptr)
+           : npl == 3 ? fwd_wide_t<3, 0, 0, false>(p, st, ys, lds, p0, n, nullptr)
+                      : fwd_wide_t<4, 0, 0, false>(p, st, ys, lds, p0, n, nullptr);
+}
+
+// Planes per round of the single-pass forward.  Each round's direction sum
+// runs right after its scan, while much of the round's fp32 direction planes
+// is still in the 256 MB Infinity Cache: a round holds a whole number of
+// device-fulls of planes (so that no round leaves CUs idle) whose planes fit
+// that size.  Where one device-full does not fit, the rounds measured slower
+// (their drains cost more than the cache saves: the latent grids of 147 and
+// 185, 300 MB per device-full, 2% slower) and the forward runs as one pass.
+// At 256 x 256, B = 1, C = 1024: rounds of 256 planes (1 MB each), the
+// pixel-major forward 1064 -> 958 us, the blocked one 862 -> 721 us.
+int wide_round(const Problem &p, size_t lds)
+{
+    const int64_t planes = (int64_t)p.B * p.C;
+    const int64_t fit = wide_fit(lds);
+    const int64_t bytes = (int64_t)__builtin_popcount(p.mask) * p.H * p.W * 4;
+    const int64_t budget = (int64_t)256 << 20;
+    if (fit == 0 || fit >= planes || fit * bytes > budget)
+        return (int)planes;
+    return (int)std::min(planes, fit * (budget / (fit * bytes)));
 }
 
 }  // namespace
@@ -835,10 +868,25 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     hipError_t e = p.ws->take((void **)&ys, (size_t)(D * n + nst) * sizeof(float));
     if (e != hipSuccess)
         return e;
+    const int planes = p.B * p.C;
+    // the single pass in rounds of planes, each followed by its direction sum
+    auto rounds = [&](const Problem &q, const Problem *v) -> hipError_t {
+        const int R = wide_round(p, lds);
+        hipError_t r = hipSuccess;
+        for (int r0 = 0; r0 < planes && r == hipSuccess; r0 += R) {
+            const int nr = std::min(R, planes - r0);
+            r = fwd_wide_l(q, st, ys, nullptr, lds, 1, r0, nr, v);
+            if (r == hipSuccess)
+                r = launch_sum_wide(p, ys, st, r0, nr);
+        }
+        return r;
+    };
     if (p.layout != kPixelMajor) {
         if (p.ws->counting)
             return hipSuccess;
-        e = fwd_wide_l(p, st, ys, ys + D * n, lds, K);
+        if (K == 1)
+            return rounds(p, nullptr);
+        e = fwd_wide_l(p, st, ys, ys + D * n, lds, K, 0, planes);
     } else {
         // Blocked copies (workspace) of lam, u and w, then the blocked scan.
         // The single pass reads the vertical directions in place (whole rows,
@@ -877,10 +925,12 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
         q.u = cu;
         q.w = cw;
         q.layout = kBlocked;
-        e = fwd_wide_l(q, st, ys, ys + D * n, lds, K, K > 1 ? nullptr : &p);
+        if (K == 1)
+            return rounds(q, &p);
+        e = fwd_wide_l(q, st, ys, ys + D * n, lds, K, 0, planes);
     }
     if (e == hipSuccess)
-        e = launch_sum_wide(p, ys, st, 0, p.B * p.C);
+        e = launch_sum_wide(p, ys, st, 0, planes);
     return e;
 }
 
