@@ -242,6 +242,24 @@ def test_full_size_sampled_units(idx):
     assert np.all(np.isfinite(got["y"]))
 
 
+def test_wide_rounds_ragged():
+    """The 256 x 256 forward takes its planes in rounds of as many as the
+    device runs at once (256 on this GPU); 300 planes end with a short round,
+    and the weight group of planes 250..274 spans the boundary between the
+    rounds.  Units on both sides of it and in the last round, against the
+    oracle."""
+    wl = case("wide256-300planes", 3, 100, 4, 256, 256, backward=False)
+    inputs = gi.make_inputs(wl)
+    got = run_gpu(inputs, wl, False)
+    cpg = wl.C // wl.G
+    for b, g in [(0, 0), (2, 1), (2, 2), (2, 3)]:
+        sl = oracle.slice_group(inputs, b, g, wl.G)
+        cs = slice(g * cpg, (g + 1) * cpg)
+        check_against_oracle(sl, {"y": got["y"][b:b + 1, cs]}, wl.with_(B=1, C=cpg, G=1), False,
+                             f"{wl.name} unit b={b} g={g}")
+    assert np.all(np.isfinite(got["y"]))
+
+
 @pytest.mark.parametrize("wl", [case("med56-cpg12", 1, 24, 2, 56, 56),
                                 case("med64-cpg32", 1, 64, 2, 64, 64),
                                 case("med48-cpg12-dirs6", 2, 24, 2, 48, 48, dirs=6)],
