@@ -748,17 +748,8 @@ hipError_t launch_pieces(const void *src, void *dst, int64_t nv, int64_t nh, int
     return hipGetLastError();
 }
 
-// Chunks per scan for the chunked forward, or 1 for the single pass.  The
-// chunked forward does more than twice the single pass's work (both passes
-// over every line, and the carries), and its carry chain still takes every
-// line block of a scan in turn, each step bound by issue latency at one wave
-// per SIMD (about 380 cycles for the w-only step against about 890 for the
-// full one at 256 positions).  It is chosen only where it measured faster:
-// scans of at least 256 lines in both orientations, and at least 8 chunks,
-// the count doubling while B*C*K workgroups still fit the device at once and
-// every chunk keeps at least 2 line blocks.
 // Workgroups of the single-pass forward that the device runs at once (LDS
-// bound), 0 if the device cannot be queried.
+// bound), 0 if the device cannot be queried (then neither chunks nor rounds).
 int64_t wide_fit(size_t lds)
 {
     int dev = 0, ncu = 0;
@@ -770,9 +761,17 @@ int64_t wide_fit(size_t lds)
     return (int64_t)ncu * std::min<int64_t>(per_cu, 8);
 }
 
-int wide_chunks(const Problem &p, size_t lds)
+// Chunks per scan for the chunked forward, or 1 for the single pass.  The
+// chunked forward does more than twice the single pass's work (both passes
+// over every line, and the carries), and its carry chain still takes every
+// line block of a scan in turn, each step bound by issue latency at one wave
+// per SIMD (about 380 cycles for the w-only step against about 890 for the
+// full one at 256 positions).  It is chosen only where it measured faster:
+// scans of at least 256 lines in both orientations, and at least 8 chunks,
+// the count doubling while B*C*K workgroups still fit the device at once and
+// every chunk keeps at least 2 line blocks.
+int wide_chunks(const Problem &p, int64_t fit)
 {
-    const int64_t fit = wide_fit(lds);
     if (fit == 0)
         return 1;
     const int64_t planes = (int64_t)p.B * p.C;
@@ -827,10 +826,9 @@ hipError_t fwd_wide_l(const Problem &p, hipStream_t st, float *ys, float *states
 // 185, 300 MB per device-full, 2% slower) and the forward runs as one pass.
 // At 256 x 256, B = 1, C = 1024: rounds of 256 planes (1 MB each), the
 // pixel-major forward 1064 -> 958 us, the blocked one 862 -> 721 us.
-int wide_round(const Problem &p, size_t lds)
+int wide_round(const Problem &p, int64_t fit)
 {
     const int64_t planes = (int64_t)p.B * p.C;
-    const int64_t fit = wide_fit(lds);
     const int64_t bytes = (int64_t)__builtin_popcount(p.mask) * p.H * p.W * 4;
     const int64_t budget = (int64_t)256 << 20;
     if (fit == 0 || fit >= planes || fit * bytes > budget)
@@ -861,7 +859,8 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     const int D = __builtin_popcount(p.mask);
     const int64_t n = (int64_t)p.B * p.C * p.H * p.W;
     const size_t lds = wide_lds_bytes(p.H, p.W);
-    const int K = wide_chunks(p, lds);
+    const int64_t fit = wide_fit(lds);     // one device query per call
+    const int K = wide_chunks(p, fit);
     // fp32 direction planes, then (chunked) the chunk states
     const int64_t nst = K > 1 ? (int64_t)p.B * p.C * D * K * std::max(p.H, p.W) : 0;
     float *ys = nullptr;
@@ -871,7 +870,7 @@ hipError_t launch_fwd_wide(const Problem &p, hipStream_t st)
     const int planes = p.B * p.C;
     // the single pass in rounds of planes, each followed by its direction sum
     auto rounds = [&](const Problem &q, const Problem *v) -> hipError_t {
-        const int R = wide_round(p, lds);
+        const int R = wide_round(p, fit);
         hipError_t r = hipSuccess;
         for (int r0 = 0; r0 < planes && r == hipSuccess; r0 += R) {
             const int nr = std::min(R, planes - r0);
