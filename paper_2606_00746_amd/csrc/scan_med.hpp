@@ -38,6 +38,8 @@
 //    through double-buffered LDS slots, one barrier per two steps; when a
 //    group spans several workgroups the sums go to fp32 partials that a
 //    second kernel adds in fixed order.
+#include <algorithm>
+
 #include "cdna.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -916,7 +918,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     bf16_t *__restrict__ dw, bf16_t *__restrict__ dlam, bf16_t *__restrict__ du,
     float *__restrict__ dwp, int mask, int B, int C, int G, int cw, int nchunk, Magic divChunk,
     Magic divG, const bf16_t *__restrict__ lamh, const bf16_t *__restrict__ uh,
-    const bf16_t *__restrict__ wh, bf16_t *__restrict__ dwh)
+    const bf16_t *__restrict__ wh, bf16_t *__restrict__ dwh, int blk0)
 {
     static_assert(H <= 64 && W <= 64 && H % 8 == 0 && W % 8 == 0 && H == W, "shape");
     constexpr int HW = H * W;
@@ -925,7 +927,7 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     float *smem = reinterpret_cast<float *>(smem4);
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int lane = threadIdx.x & 63;
-    const int blk = xcd_remap(blockIdx.x, gridDim.x);
+    const int blk = blk0 + xcd_remap(blockIdx.x, gridDim.x);   // this launch: blk0 ..
     int b, g, c, chunk;
     bool cvalid;
     if constexpr (PC) {
@@ -1157,15 +1159,18 @@ __global__ __launch_bounds__(256) void dw_sum_kernel(const float *__restrict__ d
 // consecutive pixels of a row.  A horizontal direction's lines are columns:
 // the partials are read along their lines (coalesced), summed, turned around
 // through LDS, and stored by rows.  vslots: bit s set when direction slot s
-// is vertical; per_slot: units * 3 of one slot.
+// is vertical; per_slot: units * 3 of one slot.  This launch takes, in every
+// slot, the (unit, tap) planes r0 .. r0 + rn - 1 of the slot.
 template <int S>
 __global__ __launch_bounds__(256) void dw_sum_pm_kernel(const float *__restrict__ dwp,
                                                         uint4 *__restrict__ dw, int64_t nuk,
-                                                        int nchunk, int vslots, int64_t per_slot)
+                                                        int nchunk, int vslots, int64_t per_slot,
+                                                        int64_t r0, int64_t rn)
 {
     constexpr int HW = S * S, NQ = S / 8;
     __shared__ float T[S][S + 1];
-    const int64_t uk = blockIdx.x;
+    const int64_t sl = blockIdx.x / rn;
+    const int64_t uk = sl * per_slot + r0 + (blockIdx.x - sl * rn);
     const bool vert = (vslots >> (int)(uk / per_slot)) & 1;   // uniform over the workgroup
     uint4 *dst = dw + uk * (HW / 8);
     const float4 *src = reinterpret_cast<const float4 *>(dwp + uk * HW);
@@ -1226,23 +1231,25 @@ hipError_t fwd_med_t(const Problem &p, hipStream_t st)
     return hipGetLastError();
 }
 
+// Workgroups blk0 .. blk0 + nblk - 1 (nblk < 0: all of them).
 template <int H, int W, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
 hipError_t bwd_med_launch(const Problem &p, hipStream_t st, int cw, int nchunk, size_t lds,
                           float *dwp, const void *lamh, const void *uh, const void *wh = nullptr,
-                          void *dwh = nullptr)
+                          void *dwh = nullptr, int blk0 = 0, int nblk = -1)
 {
     hipError_t e = hipFuncSetAttribute((const void *)bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM, WV>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
         return e;
-    const unsigned grid = (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
+    const unsigned grid = nblk >= 0 ? (unsigned)nblk
+                                    : (unsigned)(PC ? p.B * nchunk : p.B * p.G * nchunk);
     hipLaunchKernelGGL((bwd_med_kernel<H, W, IMM, PC, NS, PM, WPM, WV>), dim3(grid),
                        dim3(64 * cw), lds, st, (const bf16_t *)p.x, (const bf16_t *)p.w,
                        (const bf16_t *)p.lam, (const bf16_t *)p.u, (const bf16_t *)p.dy,
                        (bf16_t *)p.dx, (bf16_t *)p.dw, (bf16_t *)p.dlam, (bf16_t *)p.du, dwp,
                        p.mask, p.B, p.C, p.G, cw, nchunk, make_magic((uint32_t)nchunk),
                        make_magic((uint32_t)p.G), (const bf16_t *)lamh, (const bf16_t *)uh,
-                       (const bf16_t *)wh, (bf16_t *)dwh);
+                       (const bf16_t *)wh, (bf16_t *)dwh, blk0);
     return hipGetLastError();
 }
 
@@ -1344,33 +1351,63 @@ hipError_t bwd_med_t(const Problem &p, hipStream_t st, const void *lamh = nullpt
     }
     if (p.ws->counting)
         return hipSuccess;
-    if (use4)
-        e = bwd_med_launch<H, W, false, false, 4, PM, WPM>(p, st, cw, nchunk, lds, dwp, lamh, uh);
-    else
-        e = cw >= kBatch ? bwd_med_launch<H, W, false, false, kSlots, PM, WPM>(
-                               p, st, cw, nchunk, lds, dwp, lamh, uh)
-                         : bwd_med_launch<H, W, true, false, kSlots, PM, WPM>(
-                               p, st, cw, nchunk, lds, dwp, lamh, uh);
+    auto scan = [&](int blk0, int nblk) {
+        if (use4)
+            return bwd_med_launch<H, W, false, false, 4, PM, WPM>(p, st, cw, nchunk, lds, dwp, lamh,
+                                                                  uh, nullptr, nullptr, blk0, nblk);
+        return cw >= kBatch ? bwd_med_launch<H, W, false, false, kSlots, PM, WPM>(
+                                  p, st, cw, nchunk, lds, dwp, lamh, uh, nullptr, nullptr, blk0, nblk)
+                            : bwd_med_launch<H, W, true, false, kSlots, PM, WPM>(
+                                  p, st, cw, nchunk, lds, dwp, lamh, uh, nullptr, nullptr, blk0, nblk);
+    };
+    const int64_t units = (int64_t)p.B * p.G;          // (b, g), nchunk workgroups each
+    if (PM && nchunk > 1) {
+        // Rounds of whole units, each exactly as many workgroups as the device
+        // runs at once, the partial sum of a round right after its scan: the
+        // round's partials (50 MB at 64 x 64) are then mostly still in the
+        // Infinity Cache when the sum reads them (64 x 64, B = 8, C = 768,
+        // G = 24: three rounds, backward 373 -> 363 us).  Only where the
+        // rounds come out even: each boundary drains the device, and at
+        // 56 x 56 (512 workgroups at once, units of 3) four uneven rounds
+        // took the backward from 360 to 423 us.
+        int vslots = 0;
+        for (int d = 0, sl = 0; d < 4; ++d)
+            if ((p.mask >> d) & 1) {
+                if (d < 2)
+                    vslots |= 1 << sl;
+                ++sl;
+            }
+        int dev = 0, ncu = 0;
+        int64_t ru = units;                              // units per round
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+            ncu > 0) {
+            const int per_cu = std::max(1, std::min((int)((size_t)kLdsBytes / lds), 8 / cw));
+            const int64_t fit = (int64_t)ncu * per_cu;
+            if (fit % nchunk == 0 && units % (fit / nchunk) == 0)
+                ru = fit / nchunk;
+        }
+        const int64_t nuk = (int64_t)D * units * 3;
+        for (int64_t u0 = 0; u0 < units && e == hipSuccess; u0 += ru) {
+            const int64_t nu = std::min(ru, units - u0);
+            e = scan((int)(u0 * nchunk), (int)(nu * nchunk));
+            if (e == hipSuccess) {
+                hipLaunchKernelGGL((dw_sum_pm_kernel<H>), dim3((unsigned)(D * nu * 3)), dim3(256), 0,
+                                   st, (const float *)dwp, (uint4 *)p.dw, nuk, nchunk, vslots,
+                                   units * 3, u0 * 3, nu * 3);
+                e = hipGetLastError();
+            }
+        }
+        return e;
+    }
+    e = scan(0, -1);
     if (e == hipSuccess && nchunk > 1) {
         const int64_t nuk = (int64_t)D * p.B * p.G * 3;
         const int64_t n8 = ndw / 8;
         int64_t blocks = (n8 + 255) / 256;
         blocks = blocks < 16384 ? blocks : 16384;
-        if (PM) {
-            int vslots = 0;
-            for (int d = 0, sl = 0; d < 4; ++d)
-                if ((p.mask >> d) & 1) {
-                    if (d < 2)
-                        vslots |= 1 << sl;
-                    ++sl;
-                }
-            hipLaunchKernelGGL((dw_sum_pm_kernel<H>), dim3((unsigned)nuk), dim3(256), 0, st,
-                               (const float *)dwp, (uint4 *)p.dw, nuk, nchunk, vslots,
-                               (int64_t)p.B * p.G * 3);
-        } else {
-            hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
-                               (const float *)dwp, (uint4 *)p.dw, nuk, nchunk);
-        }
+        hipLaunchKernelGGL((dw_sum_kernel<H>), dim3((unsigned)blocks), dim3(256), 0, st,
+                           (const float *)dwp, (uint4 *)p.dw, nuk, nchunk);
         e = hipGetLastError();
     }
     return e;
