@@ -48,10 +48,9 @@ __device__ __forceinline__ float bfv(const uint16_t *p, int i)
 // planes (line positions are clamped to the line, an idle channel slot reads
 // channel 0) -- so that a step's reads issue together: a read under the
 // condition compiles to a branch around it and a wait right after it.  The
-// backward's sweeps use it (14 x 14, B = 32, C = 384: 55.5 -> 51.4 us); the
-// forward keeps the conditional reads, which measured faster there (25.3
-// against 27.1 us), its next direction's planes arriving by direct-to-LDS
-// copies meanwhile.
+// sweeps also keep each step's reads within the step (a scheduling barrier
+// per step).  14 x 14, B = 32, C = 384: forward 25.3 -> 21.0 us, backward
+// 55.5 -> 47.9 us.
 __device__ __forceinline__ float bfv_if(const uint16_t *p, int i, bool on)
 {
     const float v = bfv(p, i);
@@ -234,15 +233,15 @@ __device__ __forceinline__ void fwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
     for (int i = 0; i < L; ++i) {
         const int l = REV ? L - 1 - i : i;
         const int off = dir_offset(PM, VERT, l, jc, L, P, W);
-        const float lamv = act ? bfv(S.lam, cb + off) : 0.f;
+        const float lamv = bfv_if(S.lam, cb + off, act);
         const float xv = bfv(S.x, cb + (VERT ? l * W + jc : jc * W + l));
         const float inj = lamv * xv;
         if (i == 0) {
             h = inj;
         } else {
-            const float w0 = m0 ? bfv(S.wt, off) : 0.f;
-            const float w1 = act ? bfv(S.wt, HW + off) : 0.f;
-            const float w2 = m2 ? bfv(S.wt, 2 * HW + off) : 0.f;
+            const float w0 = bfv_if(S.wt, off, m0);
+            const float w1 = bfv_if(S.wt, HW + off, act);
+            const float w2 = bfv_if(S.wt, 2 * HW + off, m2);
             float hn = fmaf(w1, h, inj);
             hn = fmaf(w0, from_left<kLaneRow>(h), hn);
             hn = fmaf(w2, from_right<kLaneRow>(h), hn);
@@ -253,6 +252,9 @@ __device__ __forceinline__ void fwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
             yv[VERT ? l : 0] += c;
         else
             yh[VERT ? 0 : l] += c;
+        // the step's reads stay in the step: hoisted over several steps they
+        // were slower (27.1 against 21.0 us at 14 x 14, B = 32, C = 384)
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -400,6 +402,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
         }
         ah[i] = a;
         an = a;
+        __builtin_amdgcn_sched_barrier(0);   // (as in the forward)
     }
 
     // forward sweep: h_i again, local gradients, weight-gradient terms
@@ -446,6 +449,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
             if ((threadIdx.x & 63) < kLaneRow)
                 slw[(k * 16 + i) * 16 + t.j] = v;
         }
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
