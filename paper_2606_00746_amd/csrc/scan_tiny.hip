@@ -254,7 +254,7 @@ __device__ __forceinline__ void fwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
             yh[VERT ? 0 : l] += c;
         // the step's reads stay in the step: hoisted over several steps they
         // were slower (27.1 against 21.0 us at 14 x 14, B = 32, C = 384)
-        __builtin_amdgcn_sched_barrier(0);
+        step_fence();
     }
 }
 
@@ -402,7 +402,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
         }
         ah[i] = a;
         an = a;
-        __builtin_amdgcn_sched_barrier(0);   // (as in the forward)
+        step_fence();   // (as in the forward)
     }
 
     // forward sweep: h_i again, local gradients, weight-gradient terms
@@ -449,7 +449,7 @@ __device__ __forceinline__ void bwd_tiny_dir(const TinyLds<H, W> &S, const TinyL
             if ((threadIdx.x & 63) < kLaneRow)
                 slw[(k * 16 + i) * 16 + t.j] = v;
         }
-        __builtin_amdgcn_sched_barrier(0);
+        step_fence();
     }
 }
 
