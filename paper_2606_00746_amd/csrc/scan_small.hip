@@ -66,30 +66,32 @@ __global__ __launch_bounds__(256) void fwd_small_kernel(
         const bool m0 = active && j > 0;
         const bool m2 = active && j + 1 < P;
         float h = 0.f;
+        // Steps past the line's end (T > L) repeat its last step's reads and
+        // leave results that the merge never reads: no branch per step, so
+        // the compiler can issue the loads of later steps early.
 #pragma unroll
         for (int i = 0; i < T; ++i) {
-            if (i < f.L) {
-                const int e = f.e0 + i * f.es;   // pixel (x)
-                const int q = f.lm(i);           // per-direction planes (lam, u, w)
-                float inj = load_f(lp + q) * load_f(xp + e);
-                inj = active ? inj : 0.f;
-                float hn = inj;
-                if (i > 0) {
-                    float w0 = load_f(wp + q);
-                    float w1 = load_f(wp + HW + q);
-                    float w2 = load_f(wp + 2 * HW + q);
-                    w0 = m0 ? w0 : 0.f;
-                    w1 = active ? w1 : 0.f;
-                    w2 = m2 ? w2 : 0.f;
-                    const float hl = from_left<T>(h);
-                    const float hr = from_right<T>(h);
-                    hn = fmaf(w1, h, hn);
-                    hn = fmaf(w0, hl, hn);
-                    hn = fmaf(w2, hr, hn);
-                }
-                h = hn;
-                yr[i] = load_f(up + q) * h;
+            const int ic = i < f.L ? i : f.L - 1;
+            const int e = f.e0 + ic * f.es;      // pixel (x)
+            const int q = f.lm(ic);              // per-direction planes (lam, u, w)
+            float inj = load_f(lp + q) * load_f(xp + e);
+            inj = active ? inj : 0.f;
+            float hn = inj;
+            if (i > 0) {
+                float w0 = load_f(wp + q);
+                float w1 = load_f(wp + HW + q);
+                float w2 = load_f(wp + 2 * HW + q);
+                w0 = m0 ? w0 : 0.f;
+                w1 = active ? w1 : 0.f;
+                w2 = m2 ? w2 : 0.f;
+                const float hl = from_left<T>(h);
+                const float hr = from_right<T>(h);
+                hn = fmaf(w1, h, hn);
+                hn = fmaf(w0, hl, hn);
+                hn = fmaf(w2, hr, hn);
             }
+            h = hn;
+            yr[i] = load_f(up + q) * h;
         }
     }
 
