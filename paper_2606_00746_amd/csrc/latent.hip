@@ -93,6 +93,13 @@ __device__ __forceinline__ void bst16(rsrc_t r, uint32_t voff, uint32_t soff, ui
     __builtin_amdgcn_raw_buffer_store_b16(v, r, voff, soff, 0);
 }
 
+// A byte offset beyond the range of every store descriptor of these kernels
+// (each covers one image's maps or less, which the entry points keep under
+// 2 GiB): the buffer's range check discards the store.  Stores of padding pixels and absent rows go there
+// instead of under a branch, which would split the code and make the
+// compiler wait for every earlier store before the next tile's products.
+constexpr uint32_t kDrop = 0x80000000u;
+
 __device__ __forceinline__ uint16_t bf16_bits(float v)
 {
     return __builtin_bit_cast(uint16_t, static_cast<__bf16>(v));
@@ -365,18 +372,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             load_a(rn, an);
 #pragma unroll
         for (int ct = 0; ct < 4; ++ct) {
-            if (ppix[ct] < 0)
-                continue;
+            const bool pv = ppix[ct] >= 0;     // a pixel of the image (not padding)
             if (MODE == Mode::Plain) {
                 // the lane's part of the offset in a register, the row's in soffset
                 const uint32_t vo = 2u * (uint32_t)(ppix[ct] + 4 * h * A.HW);
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int m = 32 * rt + 8 * (r >> 2) + (r & 3);
-                    if (m + 4 * h < A.M)
-                        bst16(yd, vo, 2u * (uint32_t)(m * A.HW), bf16_bits(acc[ct][r]));
+                    bst16(yd, pv && m + 4 * h < A.M ? vo : kDrop, 2u * (uint32_t)(m * A.HW),
+                          bf16_bits(acc[ct][r]));
                 }
             } else if (!fast) {
+                if (!pv)
+                    continue;
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
                     store_params(A, b, 32 * rt + 8 * g + 4 * h, prow[ct], pcol[ct],
@@ -385,7 +393,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void p
             } else {
                 // row 8 g + 4 h + e of the tile: plane 8 g + e (scalar) plus
                 // 4 h (u, lambda) or channel 2 g + h, tap e: plane 6 g + e plus 3 h (w)
-                const uint32_t vo = po[ct] + 2u * (uint32_t)((is_w ? 3 : 4) * h * A.HW);
+                const uint32_t vo =
+                    pv ? po[ct] + 2u * (uint32_t)((is_w ? 3 : 4) * h * A.HW) : kDrop;
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
                     float o[4] = {acc[ct][4 * g], acc[ct][4 * g + 1], acc[ct][4 * g + 2],
