@@ -95,9 +95,10 @@ __device__ __forceinline__ void bst16(rsrc_t r, uint32_t voff, uint32_t soff, ui
 
 // A byte offset beyond the range of every store descriptor of these kernels
 // (each covers one image's maps or less, which the entry points keep under
-// 2 GiB): the buffer's range check discards the store.  Stores of padding pixels and absent rows go there
-// instead of under a branch, which would split the code and make the
-// compiler wait for every earlier store before the next tile's products.
+// 2 GiB): the buffer's range check discards the store.  Stores of padding
+// pixels and absent rows go there instead of under a branch, which would
+// split the code and make the compiler wait for every earlier store before
+// the next tile's products.
 constexpr uint32_t kDrop = 0x80000000u;
 
 __device__ __forceinline__ uint16_t bf16_bits(float v)
