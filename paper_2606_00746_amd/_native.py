@@ -413,8 +413,11 @@ def _train_fwd(op, x, w, lam, u, direction, y, reserve, stream, workspace):
     n = reserve_size(x, w, direction, norm=op == OP_FWD_NORM_TRAIN)
     if n == 0:
         reserve = None
-    elif reserve is None or reserve.numel() < n:
+    elif reserve is None:
         reserve = torch.empty(n, dtype=torch.uint8, device=x.device)
+    elif reserve.numel() < n:
+        raise ValueError(f"reserve of {reserve.numel()} bytes, smaller than the {n} bytes "
+                         "reserve_size gives for these tensors")
     _scan(op, x, w, lam, u, direction, (y,), stream=stream, workspace=workspace,
           reserve=reserve)
     return y, reserve

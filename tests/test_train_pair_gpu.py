@@ -157,6 +157,9 @@ def test_front_end_checks_the_reserve():
         gspn.scan_bwd_reserve(*args, rs[: rs.numel() - 1], wl.dirs)
     with pytest.raises(gspn.GspnError, match="workspace"):
         gspn.scan_bwd_reserve(*args, None, wl.dirs)
+    # a caller's reserve that is too small is refused, not replaced
+    with pytest.raises(ValueError, match="reserve"):
+        gspn.scan_fwd_train(t["x"], t["w"], t["lam"], t["u"], wl.dirs, reserve=rs[:-1])
     torch.cuda.synchronize()
 
 
