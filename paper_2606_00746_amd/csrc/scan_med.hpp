@@ -326,12 +326,19 @@ struct BwdArgs {
 // Horizontal
 // directions read x and dy from the staged plane `stg` and add their dx
 // terms to dxr (this lane's row); vertical directions read x and dy rows from
-// global memory and add dx into the LDS dx plane.
-template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false>
+// global memory and add dx into the LDS dx plane.  When both vertical
+// directions run, the first (SH 1) leaves the column's dy and x packed two
+// rows to a dword in vdy and vx (rows 2k, 2k+1 in the low, high halves), and
+// the second (SH 2) takes them from there instead of reading the rows again.
+template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false,
+          int SH = 0>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
-                                        float (&dxr)[64], bool dx_first)
+                                        float (&dxr)[64], bool dx_first, uint32_t (&vdy)[H / 2],
+                                        uint32_t (&vx)[H / 2])
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
+    static_assert(SH == 0 || (SH == 1 && D == 0) || (SH == 2 && D == 1), "vertical pair only");
+    constexpr bool KEEP = SH == 2;                      // dy and x come from vdy, vx
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;
     constexpr uint32_t PL2 = 2 * H * W;                 // bytes of one bf16 plane
@@ -353,6 +360,8 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
     auto line_of = [](int i) { return REV ? L - 1 - i : i; };   // storage line of step i
     auto rowoff = [&](int i) -> uint32_t { return 2u * (uint32_t)(line_of(i) * W); };
     auto stg_at = [&](int i) { return lds_u32(stg, 4u * (uint32_t)pidx(jj, line_of(i))); };
+    // the kept value of storage line l
+    auto kept = [](const uint32_t *a, int l) { return (l & 1) ? bf_hi(a[l >> 1]) : bf_lo(a[l >> 1]); };
 
     // the forward sweep's pieces: its first two blocks are loaded during the
     // reverse sweep's last two, so that they arrive while it ends
@@ -369,7 +378,9 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 
     // --- reverse sweep: adjoint a_i -------------------------------------
     float ahist[L];
-    uint32_t pdy[VERT ? L / 2 : 1];
+    // dy of the column packed by pairs: storage rows for the first vertical
+    // direction (its steps are the rows), steps otherwise
+    uint32_t (&pdy)[H / 2] = vdy;
     {
         uint4 ru[NB], q0[NB], q1[NB], q2[NB];
         uint32_t rd[VERT ? L : 1];
@@ -384,7 +395,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         RLOAD(NB - 1);
         if (NB > 1)
             RLOAD(NB - 2);
-        if (VERT) {
+        if (VERT && !KEEP) {
 #pragma unroll
             for (int i = L - 1; i >= L - kPrefetch; --i)
                 rd[VERT ? i : 0] = ld16(A.dy, vr, rowoff(i));
@@ -409,14 +420,14 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 #pragma unroll
             for (int t = 7; t >= 0; --t) {
                 const int i = 8 * fb + t;
-                if (VERT && i - kPrefetch >= 0)
+                if (VERT && !KEEP && i - kPrefetch >= 0)
                     rd[VERT ? i - kPrefetch : 0] = ld16(A.dy, vr, rowoff(i - kPrefetch));
-                else if (VERT)
+                else if (VERT && !KEEP)
                     rx[VERT ? kPrefetch - 1 - i : 0] =
                         ld16(A.x, vr, rowoff(kPrefetch - 1 - i));
                 float dyv;
                 if (VERT) {
-                    dyv = bf_lo(rd[VERT ? i : 0]);
+                    dyv = KEEP ? kept(pdy, line_of(i)) : bf_lo(rd[VERT ? i : 0]);
                 } else {
                     if (i - kLdsAhead >= 0)
                         xq[VERT ? 0 : i - kLdsAhead] = stg_at(i - kLdsAhead);
@@ -437,7 +448,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 }
                 ahist[i] = a;
                 an = a;
-                if (VERT && (i & 1) == 0)
+                if (VERT && !KEEP && (i & 1) == 0)
                     pdy[VERT ? i >> 1 : 0] =
                         __builtin_amdgcn_perm(rd[VERT ? i + 1 : 0], rd[VERT ? i : 0], 0x05040100u);
                 step_fence();
@@ -516,12 +527,18 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         for (int t = 0; t < 8; ++t) {
             const int i = 8 * fb + t;
             const int e = REV ? 7 - t : t;
-            if (VERT && i + kPrefetch < L)
+            if (VERT && !KEEP && i + kPrefetch < L)
                 rx[VERT ? i + kPrefetch : 0] = ld16(A.x, vr, rowoff(i + kPrefetch));
             float xv, dyv;
-            if (VERT) {
+            if (VERT && KEEP) {
+                xv = kept(vx, line_of(i));
+                dyv = kept(pdy, line_of(i));
+            } else if (VERT) {
                 xv = bf_lo(rx[VERT ? i : 0]);
                 dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
+                if (SH == 1 && (i & 1))
+                    vx[VERT ? i >> 1 : 0] =
+                        __builtin_amdgcn_perm(rx[VERT ? i : 0], rx[VERT ? i - 1 : 0], 0x05040100u);
             } else {
                 if (i + kLdsAhead < L)
                     xq[VERT ? 0 : i + kLdsAhead] = stg_at(i + kLdsAhead);
@@ -1060,10 +1077,14 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
 
     // horizontal directions first (x and dy staged), dx in registers
     float dxr[64];
+    // the column's dy and x, from T2B to B2T (not where the vertical weights
+    // are read in place as rows: those registers are not there to spare)
+    constexpr int kPair = WV ? 0 : 1;
+    uint32_t vdy[H / 2], vx[H / 2];
     A.first = false;
     if (mask & 4) {
         setup(2);
-        dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, true);
+        dir_bwd<H, W, 2, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, true, vdy, vx);
         lds_barrier();   // slot buffers are reused by the next direction
         if (PM) {
             flush_out();
@@ -1076,7 +1097,8 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
         if ((mask & 4) && H >= 64)
             dir_bwd_ck<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr);
         else
-            dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, (mask & 4) == 0);
+            dir_bwd<H, W, 3, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, (mask & 4) == 0,
+                                                      vdy, vx);
         lds_barrier();
         if (PM)
             flush_out();
@@ -1091,13 +1113,18 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false);
+        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM, WV, kPair>(A, lane, cvalid, stg, dxr, false, vdy,
+                                                          vx);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false);
+        if (kPair && (mask & 1))
+            dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV, kPair ? 2 : 0>(A, lane, cvalid, stg, dxr, false, vdy,
+                                                          vx);
+        else
+            dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false, vdy, vx);
         lds_barrier();
     }
 
