@@ -144,6 +144,11 @@ EDGE = [
     case("med48-ns4-cpg12", 1, 24, 2, 48, 48),
     case("med64-ns4-cpg4", 2, 16, 4, 64, 64),
     case("med40-ns4-cpg12-dirs6", 1, 12, 1, 40, 40, dirs=6),
+    # both vertical directions (the second takes x and dy from the first's
+    # registers) at the sides no other case runs them on: 9 channels per group
+    # (uneven chunks), and with a horizontal direction run before them
+    case("med40-vertical-pair-cpg9", 1, 18, 2, 40, 40, dirs=3),
+    case("med24-dirs11-cpg3", 2, 6, 2, 24, 24, dirs=11),
 ]
 
 
@@ -167,6 +172,7 @@ BLOCKED = [
     case("wide-72x136", 1, 4, 2, 72, 136),
     case("med64-G=C", 1, 16, 16, 64, 64),
     case("med56-T2B-cpg12", 2, 24, 2, 56, 56, dirs=1),
+    case("med40-vertical-pair-cpg9", 1, 18, 2, 40, 40, dirs=3),
     case("chunk-256x256-c8", 1, 8, 2, 256, 256, backward=False),
 ]
 
