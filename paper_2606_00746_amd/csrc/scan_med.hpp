@@ -329,7 +329,8 @@ struct BwdArgs {
 // global memory and add dx into the LDS dx plane.  When both vertical
 // directions run, the first (SH 1) leaves the column's dy and x packed two
 // rows to a dword in vdy and vx (rows 2k, 2k+1 in the low, high halves), and
-// the second (SH 2) takes them from there instead of reading the rows again.
+// the second (SH 2) takes them from there instead of reading the rows again
+// (dy only with WV).
 template <int H, int W, int D, bool IMM, bool PC, int NS, bool PM, bool WPM, bool WV = false,
           int SH = 0>
 __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, const uint8_t *stg,
@@ -338,7 +339,8 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
 {
     constexpr bool VERT = D < 2, REV = D == 1 || D == 3;
     static_assert(SH == 0 || (SH == 1 && D == 0) || (SH == 2 && D == 1), "vertical pair only");
-    constexpr bool KEEP = SH == 2;                      // dy and x come from vdy, vx
+    constexpr bool KEEP = SH == 2;                      // dy comes from vdy
+    constexpr bool KEEPX = KEEP && !WV;                 // and x from vx
     constexpr int L = VERT ? H : W, P = VERT ? W : H;
     constexpr int NB = L / 8;
     constexpr uint32_t PL2 = 2 * H * W;                 // bytes of one bf16 plane
@@ -422,7 +424,7 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
                 const int i = 8 * fb + t;
                 if (VERT && !KEEP && i - kPrefetch >= 0)
                     rd[VERT ? i - kPrefetch : 0] = ld16(A.dy, vr, rowoff(i - kPrefetch));
-                else if (VERT && !KEEP)
+                if (VERT && !KEEPX && i - kPrefetch < 0)
                     rx[VERT ? kPrefetch - 1 - i : 0] =
                         ld16(A.x, vr, rowoff(kPrefetch - 1 - i));
                 float dyv;
@@ -527,16 +529,14 @@ __device__ __forceinline__ void dir_bwd(const BwdArgs &A, int j, bool cvalid, co
         for (int t = 0; t < 8; ++t) {
             const int i = 8 * fb + t;
             const int e = REV ? 7 - t : t;
-            if (VERT && !KEEP && i + kPrefetch < L)
+            if (VERT && !KEEPX && i + kPrefetch < L)
                 rx[VERT ? i + kPrefetch : 0] = ld16(A.x, vr, rowoff(i + kPrefetch));
             float xv, dyv;
-            if (VERT && KEEP) {
-                xv = kept(vx, line_of(i));
-                dyv = kept(pdy, line_of(i));
-            } else if (VERT) {
-                xv = bf_lo(rx[VERT ? i : 0]);
-                dyv = (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
-                if (SH == 1 && (i & 1))
+            if (VERT) {
+                xv = KEEPX ? kept(vx, line_of(i)) : bf_lo(rx[VERT ? i : 0]);
+                dyv = KEEP ? kept(pdy, line_of(i))
+                           : (i & 1) ? bf_hi(pdy[VERT ? i >> 1 : 0]) : bf_lo(pdy[VERT ? i >> 1 : 0]);
+                if (SH == 1 && !WV && (i & 1))
                     vx[VERT ? i >> 1 : 0] =
                         __builtin_amdgcn_perm(rx[VERT ? i : 0], rx[VERT ? i - 1 : 0], 0x05040100u);
             } else {
@@ -1077,9 +1077,8 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
 
     // horizontal directions first (x and dy staged), dx in registers
     float dxr[64];
-    // the column's dy and x, from T2B to B2T (not where the vertical weights
-    // are read in place as rows: those registers are not there to spare)
-    constexpr int kPair = WV ? 0 : 1;
+    // the column's dy and x, from T2B to B2T (dy only where the vertical
+    // weights are read in place as rows: no registers to spare for x there)
     uint32_t vdy[H / 2], vx[H / 2];
     A.first = false;
     if (mask & 4) {
@@ -1113,15 +1112,14 @@ __global__ __launch_bounds__(512) void bwd_med_kernel(
     if (mask & 1) {
         setup(0);
         A.first = !horiz;
-        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM, WV, kPair>(A, lane, cvalid, stg, dxr, false, vdy,
-                                                          vx);
+        dir_bwd<H, W, 0, IMM, PC, NS, PM, WPM, WV, 1>(A, lane, cvalid, stg, dxr, false, vdy, vx);
         lds_barrier();
     }
     if (mask & 2) {
         setup(1);
         A.first = !horiz && (mask & 1) == 0;
-        if (kPair && (mask & 1))
-            dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV, kPair ? 2 : 0>(A, lane, cvalid, stg, dxr, false, vdy,
+        if (mask & 1)
+            dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV, 2>(A, lane, cvalid, stg, dxr, false, vdy,
                                                           vx);
         else
             dir_bwd<H, W, 1, IMM, PC, NS, PM, WPM, WV>(A, lane, cvalid, stg, dxr, false, vdy, vx);
